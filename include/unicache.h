@@ -1,0 +1,293 @@
+/*
+ * unicache.h -- C ABI of the mixed-policy KV-cache attention library for
+ * AMD Instinct MI355X (gfx950).
+ *
+ * The library implements the data-parallel hot path of UniCache
+ * ("UniCache: Task- and Type-Aware KV Cache Compression for Unified
+ * Multimodal Models"): attention over a KV cache split into typed segments,
+ * each segment stored under its own compression policy (Sec. 3.1, Sec. 3.4,
+ * App. E "Physical, type-aware KV storage").
+ *
+ *   uc_score_importance  attention-probability importance per cached token and
+ *                        attention mass per segment (Sec. 3.3, Eq. 1;
+ *                        App. E "Efficient attention-guided allocation")
+ *   uc_select_keep       per-KV-head top-k token eviction with compaction
+ *                        (App. E "Batched GQA token selection")
+ *   uc_quantize_segment  group-wise asymmetric low-bit quantization
+ *                        (App. E "Physical, type-aware KV storage")
+ *   uc_attend_mixed      one shared-softmax attention pass over dense,
+ *                        compacted and packed segments
+ *                        (App. E "Attention over heterogeneous cache segments")
+ *   uc_append_rows       decode-time write of new K/V rows into a protected
+ *                        dense segment (Sec. 3.1, protected objects)
+ *   host helpers         byte accounting and budget -> policy configuration
+ *                        (Sec. 3.3 Eq. 2 and Eq. 3, Sec. 3.4)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Tensors are row-major with the innermost dimension last.
+ * - Query head h attends through KV head h / (Hq / Hkv) (grouped-query
+ *   attention; the query heads of one KV head form its "group").
+ * - Device pointers are plain HIP device addresses; `stream` is a
+ *   hipStream_t passed as void* (NULL = the default stream).
+ * - Ownership: the caller allocates every input, output and workspace
+ *   buffer.  The library never allocates or frees device memory, never
+ *   synchronises the stream, and only enqueues work on `stream`.  Buffers
+ *   must stay valid until that work completes.
+ * - Errors: every argument check happens on the host before any launch; on
+ *   error nothing is written and no work is enqueued.  UC_E_INVALID covers
+ *   bad sizes, null required pointers and misaligned pointers,
+ *   UC_E_UNSUPPORTED a legal but unimplemented combination, UC_E_WORKSPACE
+ *   a workspace smaller than the matching *_workspace_size helper reports,
+ *   UC_E_DEVICE a HIP error reported at launch.  uc_last_error() returns a
+ *   thread-local text describing the last failure of the calling thread.
+ * - Values stored in device memory (codes, per-head bit widths, offsets)
+ *   are not inspected on the host.  Kernels bound every access by the
+ *   capacities given in the descriptors; a head whose device-side offsets
+ *   would leave those capacities is skipped and its outputs are set to NaN.
+ *   NaN or Inf inside K, V, Q or scores gives undefined (but in-bounds)
+ *   results.
+ */
+#ifndef UNICACHE_H
+#define UNICACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  UC_OK = 0,
+  UC_E_INVALID = 1,
+  UC_E_UNSUPPORTED = 2,
+  UC_E_WORKSPACE = 3,
+  UC_E_DEVICE = 4
+} uc_status;
+
+/* Element type of dense rows, residual-tail rows, queries and of the value a
+ * dequantised code is rounded to (round-to-nearest-even). */
+typedef enum { UC_F32 = 0, UC_F16 = 1, UC_BF16 = 2 } uc_dtype;
+
+/* Storage kind of one segment (App. E "Physical, type-aware KV storage"):
+ * UC_SEG_DENSE  rows kept in their original representation -- protected
+ *               segments, segments kept at full precision, and the compacted
+ *               survivors of an eviction policy (ascending token order);
+ * UC_SEG_PACKED low-bit codes with per-group scales and minima plus a short
+ *               residual tail of rows held in `dtype`. */
+typedef enum { UC_SEG_DENSE = 0, UC_SEG_PACKED = 1 } uc_seg_kind;
+
+/* Batch B, query heads Hq, KV heads Hkv (Hq % Hkv == 0), head dim D. */
+typedef struct {
+  int32_t B, Hq, Hkv, D;
+} uc_shape;
+
+#define UC_MAX_SEGMENTS 8
+
+/* One segment of the logical KV sequence.  Segments are passed as an array in
+ * logical token order; attention treats their rows as one sequence under one
+ * softmax (Sec. 3.4: compressed candidates and protected segments are
+ * reassembled in their original order).
+ *
+ * Dense segment (kind = UC_SEG_DENSE):
+ *   k, v      [B, Hkv, row_stride, D] elements of `dtype`; rows 0..n_rows-1 of
+ *             each (b, h_kv) are live.  row_stride = 0 means n_rows.
+ *   idx       optional int32 [B, Hkv, n_rows] logical positions of the rows
+ *             (an eviction policy's survivors); carried for the caller, never
+ *             read by attention (softmax is invariant to row order).
+ *
+ * Packed segment (kind = UC_SEG_PACKED), N = n_rows, G = group,
+ * n_full = G * floor(N / G), tail_len = N - n_full:
+ *   bits      uniform code width in {2, 4, 8} used when head_bits is NULL.
+ *   head_bits optional device uint8 [B*Hkv]: per-(b, h_kv) code width in
+ *             {2, 4, 8}; then code_off is required.
+ *   code_off  device int64 [B*Hkv]: byte offset of each (b, h_kv)'s codes in
+ *             codes_k / codes_v.  NULL (with head_bits NULL) means
+ *             (b*Hkv + h) * n_full * D * bits / 8.
+ *   codes_bytes  capacity in bytes of each of codes_k and codes_v.
+ *   codes_k, codes_v  row r of a head occupies D*bits/8 bytes at
+ *             offset + r*D*bits/8; channel c sits in byte c*bits/8 at bit
+ *             (c % (8/bits)) * bits (least significant bits first).
+ *   scale_k, min_k  float [B, Hkv, n_full/G, D]: keys are quantised per
+ *             channel over groups of G consecutive rows.
+ *   scale_v, min_v  float [B, Hkv, n_full, D/G]: values are quantised per
+ *             row over groups of G consecutive channels.
+ *   tail_k, tail_v  [B, Hkv, tail_len, D] of `dtype`: the last N - n_full rows,
+ *             unquantised.  May be NULL when tail_len == 0.
+ *   A code q of a group with scale s and minimum m stands for the value
+ *   round_to(dtype, fmaf((float)q, s, m)).
+ *
+ * All pointers of a packed segment must be 16-byte aligned; dense k/v must be
+ * 16-byte aligned and D * sizeof(dtype) is a multiple of 16 by construction
+ * (D in {64, 128}). */
+typedef struct {
+  int32_t kind;       /* uc_seg_kind */
+  int32_t dtype;      /* uc_dtype */
+  int32_t n_rows;     /* logical rows per (b, h_kv); may be 0 */
+  int32_t row_stride; /* dense only: allocated rows per (b, h_kv); 0 = n_rows */
+  void* k;
+  void* v;
+  const int32_t* idx;
+  int32_t group;
+  int32_t bits;
+  const uint8_t* head_bits;
+  const int64_t* code_off;
+  uint64_t codes_bytes;
+  uint8_t* codes_k;
+  uint8_t* codes_v;
+  float* scale_k;
+  float* min_k;
+  float* scale_v;
+  float* min_v;
+  void* tail_k;
+  void* tail_v;
+} uc_segment;
+
+/* ------------------------------------------------------------------------ */
+/* Importance scoring (Sec. 3.3 Eq. 1 and its attention probabilities P;
+ * App. E "Batched GQA token selection": scores are aggregated over the query
+ * heads that share a KV head).
+ *
+ * For every (b, h_kv) let Q be the G*W observation rows (g, w) -- query head
+ * h_kv*G + g, window position w -- of q_obs [B, Hq, W, D] (q_dt).  Each row's
+ * logits s_j = sm_scale * <q, k_j> run over every row j of every segment in
+ * logical order (packed rows dequantised), P = softmax over all of them, and
+ *   scores_out[s][b, h_kv, j] = sum over the G*W rows of P_j   (j in segment s)
+ *   mass_out[b, h_kv, s]       = sum over the G*W rows and j in s of P_j
+ * Sums are accumulated in double and rounded once to float.
+ * scores_out is a host array of n_segs device pointers; an entry (or the whole
+ * array) may be NULL to skip that segment's scores.  mass_out is device float
+ * [B, Hkv, n_segs] or NULL.  Dense segments may be fp32/fp16/bf16; a packed
+ * segment's dequantised rows are rounded to its dtype.  ws must hold
+ * uc_score_workspace_size(...) bytes. */
+uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs,
+                              int n_segs, const void* q_obs, uc_dtype q_dt,
+                              int W, float sm_scale, float* const* scores_out,
+                              float* mass_out, void* ws, size_t ws_bytes,
+                              void* stream);
+
+size_t uc_score_workspace_size(const uc_shape* shape, const uc_segment* segs,
+                               int n_segs, int W);
+
+/* ------------------------------------------------------------------------ */
+/* Top-k token selection and physical compaction for one eviction-managed
+ * segment (App. E "Batched GQA token selection" and "Physical, type-aware KV
+ * storage": heavy-hitter plus recent-token selection per KV head, then only
+ * the retained rows and their logical indices are stored).
+ *
+ * scores [BH, N] float (BH = B*Hkv rows).  For each row the last n_recent
+ * positions are always kept; of the other N - n_recent positions the
+ * k - n_recent with the largest (score, -index) are kept (equal scores: the
+ * lower index wins).  keep_idx [BH, k] int32 receives the kept positions in
+ * ascending order.  When k_src is non-NULL the kept rows of k_src/v_src
+ * [BH, N, D] (dtype dt) are gathered, in the same order, into k_dst/v_dst
+ * [BH, k, D].  0 <= n_recent <= k <= N.  ws must hold
+ * uc_select_workspace_size(BH, N) bytes. */
+uc_status uc_select_keep(const float* scores, int BH, int N, int k,
+                         int n_recent, int32_t* keep_idx, const void* k_src,
+                         const void* v_src, void* k_dst, void* v_dst,
+                         uc_dtype dt, int D, void* ws, size_t ws_bytes,
+                         void* stream);
+
+size_t uc_select_workspace_size(int BH, int N);
+
+/* ------------------------------------------------------------------------ */
+/* Group-wise asymmetric min/max quantization of one segment (App. E
+ * "Physical, type-aware KV storage": packed low-bit codes, scales, minima and
+ * a short residual tail).
+ *
+ * k, v [B, Hkv, N, D] of dtype dt are read; `out` (kind UC_SEG_PACKED,
+ * n_rows = N, dtype = dt) names the destination buffers, its bit widths and
+ * its group G.  For a group x_1..x_G (keys: one channel over G consecutive
+ * rows; values: G consecutive channels of one row), in IEEE binary32:
+ *   mn = min x,  mx = max x,  s = (mx - mn) / (2^bits - 1),
+ *   code = s > 0 ? clamp(rint((x - mn) / s), 0, 2^bits - 1) : 0
+ * (rint rounds half to even).  Rows n_full..N-1 are copied unchanged to the
+ * tail.  G must be a power of two in [8, 128] dividing D. */
+uc_status uc_quantize_segment(const uc_shape* shape, const void* k,
+                              const void* v, uc_dtype dt, int N,
+                              const uc_segment* out, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Attention over the mixed segments under one shared softmax (App. E
+ * "Attention over heterogeneous cache segments"; chunk outputs merged with
+ * log-sum-exp statistics).
+ *
+ * q [B, Hq, M, D] (q_dt) -> o float [B, Hq, M, D]:
+ *   o = sum_j softmax_j(sm_scale * <q, k_j>) v_j
+ * over every row j of every segment in logical order (packed rows
+ * dequantised as described for uc_segment).  No causal mask.
+ * lse     optional float [B, Hq, M]: natural-log log-sum-exp of the logits.
+ * seg_lse optional float [B, Hq, M, n_segs]: the same restricted to one
+ *         segment; -inf for a segment with no rows.
+ * M = 1 is decode; M > 1 is a query block (prefill / denoising step).  The
+ * sequence (sum of n_rows) must be non-empty.  ws must hold
+ * uc_attend_workspace_size(...) bytes. */
+uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs,
+                          int n_segs, const void* q, uc_dtype q_dt, int M,
+                          float sm_scale, float* o, float* lse, float* seg_lse,
+                          void* ws, size_t ws_bytes, void* stream);
+
+size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs,
+                                int n_segs, uc_dtype q_dt, int M);
+
+/* ------------------------------------------------------------------------ */
+/* Decode append (Sec. 3.1: newly produced K/V belong to a protected segment
+ * kept in its original representation).  Copies n_new rows of k_new / v_new
+ * [B, Hkv, n_new, D] (dtype of seg) into rows pos..pos+n_new-1 of every
+ * (b, h_kv) of the dense segment `seg`; requires pos + n_new <= row_stride.
+ * The caller then raises seg->n_rows itself. */
+uc_status uc_append_rows(const uc_shape* shape, const void* k_new,
+                         const void* v_new, int n_new, const uc_segment* seg,
+                         int pos, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Host helpers: storage accounting and budget -> policy configuration
+ * (Sec. 3.3 "S_a, the original storage cost"; Sec. 3.4: an eviction policy is
+ * configured by how many tokens it keeps, a quantization policy by its
+ * precision and grouping).  No device work. */
+
+/* Bytes of one (b, h_kv) of a segment kept dense: rows * 2 * D * elem. */
+int64_t uc_dense_bytes(int64_t rows, int D, uc_dtype dt);
+/* Bytes of one (b, h_kv) of a compacted eviction segment: kept rows plus one
+ * int32 logical index per row. */
+int64_t uc_evicted_bytes(int64_t rows, int D, uc_dtype dt);
+/* Bytes of one (b, h_kv) of a packed segment: codes, float scale/min of K and
+ * V, and the residual tail in dt.  Returns -1 for invalid arguments. */
+int64_t uc_packed_bytes(int64_t N, int D, int G, int bits, uc_dtype dt);
+/* Largest k with fixed_bytes + uc_evicted_bytes(k) <= budget_bytes, clamped
+ * to [0, N]. */
+int64_t uc_evict_rows_for_budget(double budget_bytes, double fixed_bytes,
+                                 int64_t N, int D, uc_dtype dt);
+/* Per-head code widths of one batch element's quantised segment under a byte
+ * budget: every head starts at 2 bits; heads are raised to 4 bits in
+ * descending order of `mass` (equal mass: lower head first) while
+ * fixed_bytes + the sum of packed bytes stays <= budget_bytes.
+ * bits_out[n_heads]. */
+uc_status uc_assign_bits(int n_heads, const float* mass, int64_t N, int D,
+                         int G, uc_dtype dt, double budget_bytes,
+                         double fixed_bytes, uint8_t* bits_out);
+
+/* Sec. 3.3 Eq. 2: b_next[a] = min(b_prev[a], m[a] / sum_j m[j] * B_total),
+ * with the budget a capped type cannot use redistributed proportionally to
+ * mass over the uncapped types with positive mass until none is left or
+ * every such type is capped.  n_types <= 64. */
+uc_status uc_type_budget(int n_types, const double* mass, const double* b_prev,
+                         double B_total, double* b_next);
+
+/* Sec. 3.3 Eq. 3: rho_next = min(rho, max(rho_min, rho_init * M_c / M_0)),
+ * requires 0 < rho_min <= rho_init <= 1 and M_0 > 0; returns NAN otherwise. */
+double uc_retention_next(double rho, double rho_init, double rho_min,
+                         double M_c, double M_0);
+
+/* ------------------------------------------------------------------------ */
+const char* uc_status_string(uc_status s);
+/* Thread-local description of the calling thread's last error ("" if none). */
+const char* uc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UNICACHE_H */
