@@ -103,8 +103,8 @@ typedef struct {
  *   head_bits optional device uint8 [B*Hkv]: per-(b, h_kv) code width in
  *             {2, 4, 8}; then code_off is required.
  *   code_off  device int64 [B*Hkv]: byte offset of each (b, h_kv)'s codes in
- *             codes_k / codes_v.  NULL (with head_bits NULL) means
- *             (b*Hkv + h) * n_full * D * bits / 8.
+ *             codes_k / codes_v, a multiple of 16.  NULL (with head_bits NULL)
+ *             means (b*Hkv + h) * n_full * D * bits / 8.
  *   codes_bytes  capacity in bytes of each of codes_k and codes_v.
  *   codes_k, codes_v  row r of a head occupies D*bits/8 bytes at
  *             offset + r*D*bits/8; channel c sits in byte c*bits/8 at bit
@@ -231,6 +231,17 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs,
 
 size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs,
                                 int n_segs, uc_dtype q_dt, int M);
+
+/* Per-segment attention mass from attention statistics (Sec. 3.3 Eq. 1: the
+ * bracket summed over the query heads of one KV head and the query rows).
+ * lse [B, Hq, M] and seg_lse [B, Hq, M, n_segs] as written by uc_attend_mixed;
+ * mass_out [B, Hkv, n_segs] float receives
+ *   sum over (g, m) of exp(seg_lse[b, h_kv*G + g, m, a] - lse[b, h_kv*G + g, m])
+ * accumulated in double.  Dividing by G*M gives the Mean over heads and
+ * queries of Eq. 1 for one layer and step. */
+uc_status uc_segment_mass(const uc_shape* shape, int M, int n_segs,
+                          const float* lse, const float* seg_lse,
+                          float* mass_out, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Decode append (Sec. 3.1: newly produced K/V belong to a protected segment

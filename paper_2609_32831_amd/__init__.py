@@ -1,0 +1,322 @@
+"""Python binding of libunicache (mixed-policy KV attention for MI355X).
+
+Argument marshalling only: every function forwards to the C ABI declared in
+``include/unicache.h`` under the same name; all device work runs in the
+library's HIP kernels.  PyTorch supplies device memory and the stream.  There
+is no fallback: importing this module fails if ``libunicache.so`` is missing,
+and a call raises ``UcError`` when the library returns an error status.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import List, Optional, Sequence
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libunicache.so")
+
+UC_OK, UC_E_INVALID, UC_E_UNSUPPORTED, UC_E_WORKSPACE, UC_E_DEVICE = range(5)
+UC_F32, UC_F16, UC_BF16 = 0, 1, 2
+UC_SEG_DENSE, UC_SEG_PACKED = 0, 1
+UC_MAX_SEGMENTS = 8
+
+TORCH_DT = {torch.float32: UC_F32, torch.float16: UC_F16, torch.bfloat16: UC_BF16}
+DT_TORCH = {v: k for k, v in TORCH_DT.items()}
+NAME_DT = {"f32": UC_F32, "f16": UC_F16, "bf16": UC_BF16}
+
+
+class UcError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where}: status {status} ({detail})")
+        self.status = status
+
+
+class uc_shape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int32), ("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32),
+                ("D", ctypes.c_int32)]
+
+
+class uc_segment(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("dtype", ctypes.c_int32), ("n_rows", ctypes.c_int32),
+                ("row_stride", ctypes.c_int32), ("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("idx", ctypes.c_void_p), ("group", ctypes.c_int32), ("bits", ctypes.c_int32),
+                ("head_bits", ctypes.c_void_p), ("code_off", ctypes.c_void_p),
+                ("codes_bytes", ctypes.c_uint64), ("codes_k", ctypes.c_void_p),
+                ("codes_v", ctypes.c_void_p), ("scale_k", ctypes.c_void_p),
+                ("min_k", ctypes.c_void_p), ("scale_v", ctypes.c_void_p),
+                ("min_v", ctypes.c_void_p), ("tail_k", ctypes.c_void_p),
+                ("tail_v", ctypes.c_void_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run paper_2609_32831_amd/build.py "
+                          "(or __graft_entry__.build())")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, u64, dbl, sz = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                  ctypes.c_uint64, ctypes.c_double, ctypes.c_size_t)
+    shp, segp = ctypes.POINTER(uc_shape), ctypes.POINTER(uc_segment)
+    sigs = {
+        "uc_score_importance": (i32, [shp, segp, i32, vp, i32, i32, ctypes.c_float, vp, vp, vp,
+                                      sz, vp]),
+        "uc_score_workspace_size": (sz, [shp, segp, i32, i32]),
+        "uc_select_keep": (i32, [vp, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, vp, sz,
+                                 vp]),
+        "uc_select_workspace_size": (sz, [i32, i32]),
+        "uc_quantize_segment": (i32, [shp, vp, vp, i32, i32, segp, vp]),
+        "uc_attend_mixed": (i32, [shp, segp, i32, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp,
+                                  sz, vp]),
+        "uc_attend_workspace_size": (sz, [shp, segp, i32, i32, i32]),
+        "uc_segment_mass": (i32, [shp, i32, i32, vp, vp, vp, vp]),
+        "uc_append_rows": (i32, [shp, vp, vp, i32, segp, i32, vp]),
+        "uc_dense_bytes": (i64, [i64, i32, i32]),
+        "uc_evicted_bytes": (i64, [i64, i32, i32]),
+        "uc_packed_bytes": (i64, [i64, i32, i32, i32, i32]),
+        "uc_evict_rows_for_budget": (i64, [dbl, dbl, i64, i32, i32]),
+        "uc_assign_bits": (i32, [i32, vp, i64, i32, i32, i32, dbl, dbl, vp]),
+        "uc_type_budget": (i32, [i32, vp, vp, dbl, vp]),
+        "uc_retention_next": (dbl, [dbl, dbl, dbl, dbl, dbl]),
+        "uc_status_string": (ctypes.c_char_p, [i32]),
+        "uc_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sigs.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    return L
+
+
+lib = _load()
+
+
+def _check(status: int, where: str):
+    if status != UC_OK:
+        raise UcError(status, where, lib.uc_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        if torch.cuda.is_available():
+            return torch.cuda.current_stream().cuda_stream
+        return None
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def make_shape(B: int, Hq: int, Hkv: int, D: int) -> uc_shape:
+    return uc_shape(B, Hq, Hkv, D)
+
+
+class Segment:
+    """One segment of the logical KV sequence plus the tensors it points into
+    (kept alive with the descriptor)."""
+
+    def __init__(self, desc: uc_segment, tensors: dict):
+        self.desc = desc
+        self.t = tensors
+
+    @property
+    def n_rows(self) -> int:
+        return self.desc.n_rows
+
+    @n_rows.setter
+    def n_rows(self, n: int):
+        self.desc.n_rows = n
+
+
+def dense_segment(k: torch.Tensor, v: torch.Tensor, n_rows: Optional[int] = None,
+                  idx: Optional[torch.Tensor] = None) -> Segment:
+    """k, v [B, Hkv, row_stride, D] (contiguous); rows 0..n_rows-1 live."""
+    assert k.is_contiguous() and v.is_contiguous() and k.shape == v.shape and k.dtype == v.dtype
+    stride = k.shape[2]
+    d = uc_segment(kind=UC_SEG_DENSE, dtype=TORCH_DT[k.dtype],
+                   n_rows=stride if n_rows is None else n_rows, row_stride=stride,
+                   k=k.data_ptr(), v=v.data_ptr(), idx=_ptr(idx))
+    return Segment(d, {"k": k, "v": v, "idx": idx})
+
+
+def packed_layout(BH: int, N: int, D: int, G: int, head_bits: Sequence[int]):
+    """Back-to-back per-head code offsets (16-byte aligned) and total bytes."""
+    n_full = G * (N // G)
+    off, pos = [], 0
+    for b in head_bits:
+        off.append(pos)
+        pos += (n_full * D * int(b) // 8 + 15) // 16 * 16
+    return off, pos
+
+
+def packed_segment(B: int, Hkv: int, N: int, D: int, G: int, dtype: torch.dtype,
+                   bits: int = 4, head_bits: Optional[Sequence[int]] = None,
+                   device="cuda") -> Segment:
+    """Allocate the buffers of a packed segment (to be filled by
+    uc_quantize_segment).  head_bits: optional per-(b, h_kv) code widths."""
+    BH = B * Hkv
+    n_full = G * (N // G)
+    tail = N - n_full
+    t = {}
+    if head_bits is not None:
+        off, total = packed_layout(BH, N, D, G, head_bits)
+        t["head_bits"] = torch.tensor(list(head_bits), dtype=torch.uint8, device=device)
+        t["code_off"] = torch.tensor(off, dtype=torch.int64, device=device)
+    else:
+        total = BH * n_full * D * bits // 8
+    t["codes_k"] = torch.zeros(max(total, 16), dtype=torch.uint8, device=device)
+    t["codes_v"] = torch.zeros(max(total, 16), dtype=torch.uint8, device=device)
+    t["scale_k"] = torch.zeros(B, Hkv, n_full // G, D, dtype=torch.float32, device=device)
+    t["min_k"] = torch.zeros_like(t["scale_k"])
+    t["scale_v"] = torch.zeros(B, Hkv, n_full, D // G, dtype=torch.float32, device=device)
+    t["min_v"] = torch.zeros_like(t["scale_v"])
+    t["tail_k"] = torch.zeros(B, Hkv, tail, D, dtype=dtype, device=device)
+    t["tail_v"] = torch.zeros_like(t["tail_k"])
+    d = uc_segment(kind=UC_SEG_PACKED, dtype=TORCH_DT[dtype], n_rows=N, row_stride=0,
+                   group=G, bits=bits if head_bits is None else int(max(head_bits)),
+                   head_bits=_ptr(t.get("head_bits")), code_off=_ptr(t.get("code_off")),
+                   codes_bytes=total, codes_k=t["codes_k"].data_ptr(),
+                   codes_v=t["codes_v"].data_ptr(), scale_k=t["scale_k"].data_ptr(),
+                   min_k=t["min_k"].data_ptr(), scale_v=t["scale_v"].data_ptr(),
+                   min_v=t["min_v"].data_ptr(),
+                   tail_k=t["tail_k"].data_ptr() if tail else None,
+                   tail_v=t["tail_v"].data_ptr() if tail else None)
+    return Segment(d, t)
+
+
+def _seg_array(segs: Sequence[Segment]):
+    arr = (uc_segment * len(segs))()
+    for i, s in enumerate(segs):
+        arr[i] = s.desc
+    return arr
+
+
+def _ws(nbytes: int, device) -> torch.Tensor:
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+# ---- the C ABI, one function per entry point -------------------------------
+
+def uc_attend_workspace_size(shape: uc_shape, segs: Sequence[Segment], q_dt: int, M: int) -> int:
+    return int(lib.uc_attend_workspace_size(ctypes.byref(shape), _seg_array(segs), len(segs),
+                                            q_dt, M))
+
+
+def uc_attend_mixed(shape: uc_shape, segs: Sequence[Segment], q: torch.Tensor, M: int,
+                    sm_scale: float, o: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                    seg_lse: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                    stream=None):
+    arr = _seg_array(segs)
+    q_dt = TORCH_DT[q.dtype]
+    if ws is None:
+        ws = _ws(lib.uc_attend_workspace_size(ctypes.byref(shape), arr, len(segs), q_dt, M),
+                 q.device)
+    _check(lib.uc_attend_mixed(ctypes.byref(shape), arr, len(segs), q.data_ptr(), q_dt, M,
+                               ctypes.c_float(sm_scale), o.data_ptr(), _ptr(lse), _ptr(seg_lse),
+                               ws.data_ptr(), ws.numel(), _stream(stream)), "uc_attend_mixed")
+    return o
+
+
+def uc_score_workspace_size(shape: uc_shape, segs: Sequence[Segment], W: int) -> int:
+    return int(lib.uc_score_workspace_size(ctypes.byref(shape), _seg_array(segs), len(segs), W))
+
+
+def uc_score_importance(shape: uc_shape, segs: Sequence[Segment], q_obs: torch.Tensor, W: int,
+                        sm_scale: float, scores_out: Sequence[Optional[torch.Tensor]],
+                        mass_out: Optional[torch.Tensor] = None,
+                        ws: Optional[torch.Tensor] = None, stream=None):
+    arr = _seg_array(segs)
+    if ws is None:
+        ws = _ws(lib.uc_score_workspace_size(ctypes.byref(shape), arr, len(segs), W),
+                 q_obs.device)
+    ptrs = (ctypes.c_void_p * len(segs))(*[_ptr(t) for t in scores_out])
+    _check(lib.uc_score_importance(ctypes.byref(shape), arr, len(segs), q_obs.data_ptr(),
+                                   TORCH_DT[q_obs.dtype], W, ctypes.c_float(sm_scale),
+                                   ctypes.cast(ptrs, ctypes.c_void_p), _ptr(mass_out),
+                                   ws.data_ptr(), ws.numel(), _stream(stream)),
+           "uc_score_importance")
+
+
+def uc_select_keep(scores: torch.Tensor, k: int, n_recent: int, keep_idx: torch.Tensor,
+                   k_src: Optional[torch.Tensor] = None, v_src: Optional[torch.Tensor] = None,
+                   k_dst: Optional[torch.Tensor] = None, v_dst: Optional[torch.Tensor] = None,
+                   stream=None):
+    """scores [BH, N] -> keep_idx [BH, k]; optional gather of [BH, N, D] rows."""
+    BH, N = scores.shape[0], scores.shape[-1]
+    dt = TORCH_DT[k_src.dtype] if k_src is not None else UC_BF16
+    D = k_src.shape[-1] if k_src is not None else 128
+    ws = _ws(lib.uc_select_workspace_size(BH, N), scores.device)
+    _check(lib.uc_select_keep(scores.data_ptr(), BH, N, k, n_recent, keep_idx.data_ptr(),
+                              _ptr(k_src), _ptr(v_src), _ptr(k_dst), _ptr(v_dst), dt, D,
+                              ws.data_ptr(), ws.numel(), _stream(stream)), "uc_select_keep")
+    return keep_idx
+
+
+def uc_quantize_segment(shape: uc_shape, k: torch.Tensor, v: torch.Tensor, N: int,
+                        out: Segment, stream=None):
+    _check(lib.uc_quantize_segment(ctypes.byref(shape), k.data_ptr(), v.data_ptr(),
+                                   TORCH_DT[k.dtype], N, ctypes.byref(out.desc),
+                                   _stream(stream)), "uc_quantize_segment")
+
+
+def uc_append_rows(shape: uc_shape, k_new: torch.Tensor, v_new: torch.Tensor, n_new: int,
+                   seg: Segment, pos: int, stream=None):
+    _check(lib.uc_append_rows(ctypes.byref(shape), k_new.data_ptr(), v_new.data_ptr(), n_new,
+                              ctypes.byref(seg.desc), pos, _stream(stream)), "uc_append_rows")
+
+
+def uc_segment_mass(shape: uc_shape, M: int, n_segs: int, lse: torch.Tensor,
+                    seg_lse: torch.Tensor, mass_out: torch.Tensor, stream=None):
+    _check(lib.uc_segment_mass(ctypes.byref(shape), M, n_segs, lse.data_ptr(),
+                               seg_lse.data_ptr(), mass_out.data_ptr(), _stream(stream)),
+           "uc_segment_mass")
+
+
+def uc_dense_bytes(rows: int, D: int, dt: int) -> int:
+    return int(lib.uc_dense_bytes(rows, D, dt))
+
+
+def uc_evicted_bytes(rows: int, D: int, dt: int) -> int:
+    return int(lib.uc_evicted_bytes(rows, D, dt))
+
+
+def uc_packed_bytes(N: int, D: int, G: int, bits: int, dt: int) -> int:
+    return int(lib.uc_packed_bytes(N, D, G, bits, dt))
+
+
+def uc_evict_rows_for_budget(budget: float, fixed: float, N: int, D: int, dt: int) -> int:
+    return int(lib.uc_evict_rows_for_budget(budget, fixed, N, D, dt))
+
+
+def uc_assign_bits(mass: Sequence[float], N: int, D: int, G: int, dt: int, budget: float,
+                   fixed: float) -> List[int]:
+    import numpy as np
+    m = np.ascontiguousarray(mass, np.float32)
+    out = np.zeros(m.shape[0], np.uint8)
+    _check(lib.uc_assign_bits(m.shape[0], m.ctypes.data, N, D, G, dt, budget, fixed,
+                              out.ctypes.data), "uc_assign_bits")
+    return [int(x) for x in out]
+
+
+def uc_type_budget(mass: Sequence[float], b_prev: Sequence[float], B_total: float):
+    import numpy as np
+    m = np.ascontiguousarray(mass, np.float64)
+    bp = np.ascontiguousarray(b_prev, np.float64)
+    out = np.zeros(m.shape[0])
+    _check(lib.uc_type_budget(m.shape[0], m.ctypes.data, bp.ctypes.data, B_total,
+                              out.ctypes.data), "uc_type_budget")
+    return out
+
+
+def uc_retention_next(rho: float, rho_init: float, rho_min: float, M_c: float,
+                      M_0: float) -> float:
+    return float(lib.uc_retention_next(rho, rho_init, rho_min, M_c, M_0))
+
+
+def uc_status_string(s: int) -> str:
+    return lib.uc_status_string(s).decode()
+
+
+def uc_last_error() -> str:
+    return lib.uc_last_error().decode()

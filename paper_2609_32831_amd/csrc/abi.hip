@@ -1,0 +1,442 @@
+// abi.hip -- the C ABI entry points of libunicache: argument validation,
+// work planning, workspace carving and kernel dispatch, plus the host-only
+// storage-accounting and budget helpers.  Every check runs before any launch,
+// so a failing call writes nothing and enqueues nothing.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "uc_common.h"
+
+using namespace uc;
+
+namespace uc {
+bool decode_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M);
+size_t decode_mfma_workspace(const uc_shape& sh, const KSegs& segs, int M);
+hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
+                              float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
+                              hipStream_t st);
+}  // namespace uc
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+uc_status fail(uc_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+uc_status ok() {
+  g_err[0] = 0;
+  return UC_OK;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+bool dtype_ok(int dt) { return dt == UC_F32 || dt == UC_F16 || dt == UC_BF16; }
+bool pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
+
+uc_status check_shape(const uc_shape* sh) {
+  if (!sh) return fail(UC_E_INVALID, "shape is NULL");
+  if (sh->B < 1 || sh->Hq < 1 || sh->Hkv < 1)
+    return fail(UC_E_INVALID, "B, Hq, Hkv must be >= 1 (got %d, %d, %d)", sh->B, sh->Hq, sh->Hkv);
+  if (sh->Hq % sh->Hkv) return fail(UC_E_INVALID, "Hq %% Hkv != 0 (%d, %d)", sh->Hq, sh->Hkv);
+  if (sh->D != 64 && sh->D != 128) return fail(UC_E_INVALID, "D must be 64 or 128 (got %d)", sh->D);
+  return UC_OK;
+}
+
+int64_t n_full_of(int N, int G) { return (int64_t)G * (N / G); }
+
+// Validate one segment descriptor against the shape; fill the kernel copy.
+uc_status check_segment(const uc_shape& sh, const uc_segment& s, int idx, KSeg& ks,
+                        bool require_packed_buffers) {
+  memset(&ks, 0, sizeof ks);
+  if (s.kind != UC_SEG_DENSE && s.kind != UC_SEG_PACKED)
+    return fail(UC_E_INVALID, "segment %d: bad kind %d", idx, s.kind);
+  if (!dtype_ok(s.dtype)) return fail(UC_E_INVALID, "segment %d: bad dtype %d", idx, s.dtype);
+  if (s.n_rows < 0) return fail(UC_E_INVALID, "segment %d: n_rows < 0", idx);
+  ks.kind = s.kind;
+  ks.dtype = s.dtype;
+  ks.n_rows = s.n_rows;
+  const int64_t BH = (int64_t)sh.B * sh.Hkv;
+  if (s.kind == UC_SEG_DENSE) {
+    ks.row_stride = s.row_stride ? s.row_stride : s.n_rows;
+    if (ks.row_stride < s.n_rows)
+      return fail(UC_E_INVALID, "segment %d: row_stride %d < n_rows %d", idx, ks.row_stride, s.n_rows);
+    if (s.n_rows > 0 && (!s.k || !s.v)) return fail(UC_E_INVALID, "segment %d: k/v NULL", idx);
+    if (!aligned16(s.k) || !aligned16(s.v))
+      return fail(UC_E_INVALID, "segment %d: k/v not 16-byte aligned", idx);
+    ks.k = s.k;
+    ks.v = s.v;
+    return UC_OK;
+  }
+  const int G = s.group;
+  if (!pow2(G) || G < 8 || G > 128 || sh.D % G)
+    return fail(UC_E_INVALID, "segment %d: group %d must be a power of two in [8,128] dividing D", idx, G);
+  if (!s.head_bits && s.bits != 2 && s.bits != 4 && s.bits != 8)
+    return fail(UC_E_INVALID, "segment %d: bits %d not in {2,4,8}", idx, s.bits);
+  if (s.head_bits && !s.code_off)
+    return fail(UC_E_INVALID, "segment %d: head_bits given without code_off", idx);
+  ks.group = G;
+  ks.bits = s.bits;
+  ks.n_full = (int)n_full_of(s.n_rows, G);
+  ks.tail_len = s.n_rows - ks.n_full;
+  ks.head_bits = s.head_bits;
+  ks.code_off = s.code_off;
+  ks.codes_bytes = s.codes_bytes;
+  if (!s.head_bits && !s.code_off) {
+    const uint64_t need = (uint64_t)BH * ks.n_full * sh.D * s.bits / 8;
+    if (s.codes_bytes < need)
+      return fail(UC_E_INVALID, "segment %d: codes_bytes %llu < %llu needed", idx,
+                  (unsigned long long)s.codes_bytes, (unsigned long long)need);
+  }
+  if (ks.n_full > 0 || require_packed_buffers) {
+    if (!s.codes_k || !s.codes_v || !s.scale_k || !s.min_k || !s.scale_v || !s.min_v)
+      return fail(UC_E_INVALID, "segment %d: packed buffer NULL", idx);
+  }
+  if (ks.tail_len > 0 && (!s.tail_k || !s.tail_v))
+    return fail(UC_E_INVALID, "segment %d: tail of %d rows but tail_k/tail_v NULL", idx, ks.tail_len);
+  const void* ptrs[] = {s.codes_k, s.codes_v, s.scale_k, s.min_k, s.scale_v, s.min_v, s.tail_k, s.tail_v};
+  for (const void* p : ptrs)
+    if (!aligned16(p)) return fail(UC_E_INVALID, "segment %d: packed pointer not 16-byte aligned", idx);
+  ks.codes_k = s.codes_k;
+  ks.codes_v = s.codes_v;
+  ks.scale_k = s.scale_k;
+  ks.min_k = s.min_k;
+  ks.scale_v = s.scale_v;
+  ks.min_v = s.min_v;
+  ks.tail_k = s.tail_k;
+  ks.tail_v = s.tail_v;
+  return UC_OK;
+}
+
+uc_status check_segments(const uc_shape* sh, const uc_segment* segs, int n, KSegs& ks) {
+  uc_status st = check_shape(sh);
+  if (st) return st;
+  if (!segs) return fail(UC_E_INVALID, "segs is NULL");
+  if (n < 1 || n > kMaxSeg) return fail(UC_E_INVALID, "n_segs %d not in [1,%d]", n, kMaxSeg);
+  memset(&ks, 0, sizeof ks);
+  ks.n = n;
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    st = check_segment(*sh, segs[i], i, ks.s[i], false);
+    if (st) return st;
+    total += segs[i].n_rows;
+  }
+  if (total <= 0) return fail(UC_E_INVALID, "all segments are empty");
+  if (total > INT32_MAX) return fail(UC_E_UNSUPPORTED, "more than 2^31-1 rows");
+  return UC_OK;
+}
+
+// Chunk plan: rows per chunk for every segment (empty segments get no chunk).
+ChunkPlan make_plan(const KSegs& ks, int rows_min, int max_chunks_per_seg) {
+  ChunkPlan p{};
+  int c = 0;
+  for (int i = 0; i < ks.n; ++i) {
+    const int n = ks.s[i].n_rows;
+    int rows = std::max(rows_min, (n + max_chunks_per_seg - 1) / max_chunks_per_seg);
+    p.first[i] = c;
+    p.rows[i] = rows;
+    c += n > 0 ? (n + rows - 1) / rows : 0;
+  }
+  for (int i = ks.n; i <= kMaxSeg; ++i) p.first[i] = c;
+  p.n_chunks = c;
+  return p;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// generic attention: partial stride per (query row, chunk)
+size_t generic_ws(const uc_shape& sh, const ChunkPlan& p, int M, bool want_o) {
+  const size_t stride = want_o ? (size_t)sh.D + 2 : 2;
+  return align256((size_t)sh.B * sh.Hq * M * p.n_chunks * stride * sizeof(float));
+}
+
+ChunkPlan attend_plan(const KSegs& ks) { return make_plan(ks, 256, 64); }
+ChunkPlan score_lse_plan(const KSegs& ks) { return make_plan(ks, 512, 32); }
+ChunkPlan score_col_plan(const KSegs& ks) { return make_plan(ks, 256, 1 << 20); }
+
+uc_status launched(hipError_t e) {
+  if (e != hipSuccess) return fail(UC_E_DEVICE, "HIP launch error: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* uc_status_string(uc_status s) {
+  switch (s) {
+    case UC_OK: return "UC_OK";
+    case UC_E_INVALID: return "UC_E_INVALID: invalid argument";
+    case UC_E_UNSUPPORTED: return "UC_E_UNSUPPORTED: unsupported combination";
+    case UC_E_WORKSPACE: return "UC_E_WORKSPACE: workspace too small";
+    case UC_E_DEVICE: return "UC_E_DEVICE: HIP error";
+  }
+  return "unknown uc_status";
+}
+
+const char* uc_last_error(void) { return g_err; }
+
+// ---------------------------------------------------------------- attention
+size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs, int n_segs,
+                                uc_dtype q_dt, int M) {
+  KSegs ks;
+  if (check_segments(shape, segs, n_segs, ks) || M < 1 || !dtype_ok(q_dt)) return 0;
+  if (decode_mfma_eligible(*shape, ks, q_dt, M)) return decode_mfma_workspace(*shape, ks, M);
+  return generic_ws(*shape, attend_plan(ks), M, true);
+}
+
+uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_segs,
+                          const void* q, uc_dtype q_dt, int M, float sm_scale, float* o,
+                          float* lse, float* seg_lse, void* ws, size_t ws_bytes, void* stream) {
+  KSegs ks;
+  uc_status st = check_segments(shape, segs, n_segs, ks);
+  if (st) return st;
+  if (!q || !o) return fail(UC_E_INVALID, "q or o is NULL");
+  if (!dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad q dtype %d", q_dt);
+  if (M < 1) return fail(UC_E_INVALID, "M must be >= 1 (got %d)", M);
+  if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
+  if ((int64_t)shape->B * shape->Hq * M > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
+  hipStream_t s = (hipStream_t)stream;
+  if (decode_mfma_eligible(*shape, ks, q_dt, M)) {
+    const size_t need = decode_mfma_workspace(*shape, ks, M);
+    if (ws_bytes < need || (need && !ws))
+      return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+    return launched(launch_decode_mfma(*shape, ks, q, M, sm_scale, o, lse, seg_lse, ws, s));
+  }
+  const ChunkPlan p = attend_plan(ks);
+  const size_t need = generic_ws(*shape, p, M, true);
+  if (ws_bytes < need || !ws) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  float* partial = (float*)ws;
+  hipError_t e = launch_attend_generic(*shape, ks, p, q, q_dt, M, sm_scale, partial, true, s);
+  if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, M, partial, o, lse, seg_lse, s);
+  return launched(e);
+}
+
+// ---------------------------------------------------------------- scoring
+static void score_ws_parts(const uc_shape& sh, const KSegs& ks, int W, size_t& part1,
+                           size_t& lse_b, size_t& mass_b) {
+  part1 = generic_ws(sh, score_lse_plan(ks), W, false);
+  lse_b = align256((size_t)sh.B * sh.Hq * W * sizeof(float));
+  mass_b = align256((size_t)sh.B * sh.Hkv * score_col_plan(ks).n_chunks * sizeof(double));
+}
+
+size_t uc_score_workspace_size(const uc_shape* shape, const uc_segment* segs, int n_segs, int W) {
+  KSegs ks;
+  if (check_segments(shape, segs, n_segs, ks) || W < 1) return 0;
+  size_t a, b, c;
+  score_ws_parts(*shape, ks, W, a, b, c);
+  return a + b + c;
+}
+
+uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int n_segs,
+                              const void* q_obs, uc_dtype q_dt, int W, float sm_scale,
+                              float* const* scores_out, float* mass_out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  KSegs ks;
+  uc_status st = check_segments(shape, segs, n_segs, ks);
+  if (st) return st;
+  if (!q_obs) return fail(UC_E_INVALID, "q_obs is NULL");
+  if (!dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad q dtype %d", q_dt);
+  if (W < 1) return fail(UC_E_INVALID, "W must be >= 1 (got %d)", W);
+  if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
+  size_t a, b, c;
+  score_ws_parts(*shape, ks, W, a, b, c);
+  if (!ws || ws_bytes < a + b + c) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, a + b + c);
+  hipStream_t s = (hipStream_t)stream;
+  float* partial = (float*)ws;
+  float* lse = (float*)((char*)ws + a);
+  double* mpart = (double*)((char*)ws + a + b);
+  const ChunkPlan p1 = score_lse_plan(ks), p2 = score_col_plan(ks);
+  hipError_t e = launch_attend_generic(*shape, ks, p1, q_obs, q_dt, W, sm_scale, partial, false, s);
+  if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p1, W, partial, nullptr, lse, nullptr, s);
+  float* sp[kMaxSeg] = {};
+  if (scores_out)
+    for (int i = 0; i < n_segs; ++i) sp[i] = scores_out[i];
+  if (e == hipSuccess)
+    e = launch_score_colsum(*shape, ks, p2, q_obs, q_dt, W, sm_scale, lse, sp, mpart, s);
+  if (e == hipSuccess && mass_out)
+    e = launch_mass_finalize(p2, shape->B * shape->Hkv, n_segs, mpart, mass_out, s);
+  return launched(e);
+}
+
+uc_status uc_segment_mass(const uc_shape* shape, int M, int n_segs, const float* lse,
+                          const float* seg_lse, float* mass_out, void* stream) {
+  uc_status st = check_shape(shape);
+  if (st) return st;
+  if (M < 1 || n_segs < 1 || n_segs > kMaxSeg) return fail(UC_E_INVALID, "bad M or n_segs");
+  if (!lse || !seg_lse || !mass_out) return fail(UC_E_INVALID, "NULL pointer");
+  return launched(launch_segment_mass(*shape, M, n_segs, lse, seg_lse, mass_out, (hipStream_t)stream));
+}
+
+// ---------------------------------------------------------------- selection
+size_t uc_select_workspace_size(int BH, int N) {
+  (void)BH;
+  (void)N;
+  return 0;
+}
+
+uc_status uc_select_keep(const float* scores, int BH, int N, int k, int n_recent,
+                         int32_t* keep_idx, const void* k_src, const void* v_src, void* k_dst,
+                         void* v_dst, uc_dtype dt, int D, void* ws, size_t ws_bytes,
+                         void* stream) {
+  (void)ws;
+  (void)ws_bytes;
+  if (BH < 1 || N < 0) return fail(UC_E_INVALID, "BH must be >= 1 and N >= 0");
+  if (k < 0 || k > N) return fail(UC_E_INVALID, "k=%d not in [0, N=%d]", k, N);
+  if (n_recent < 0 || n_recent > k) return fail(UC_E_INVALID, "n_recent=%d not in [0, k=%d]", n_recent, k);
+  if (k > 0 && !keep_idx) return fail(UC_E_INVALID, "keep_idx is NULL");
+  if (N > 0 && k > n_recent && !scores) return fail(UC_E_INVALID, "scores is NULL");
+  if (k_src) {
+    if (!v_src || !k_dst || !v_dst) return fail(UC_E_INVALID, "gather buffers NULL");
+    if (!dtype_ok(dt)) return fail(UC_E_INVALID, "bad dtype %d", dt);
+    if (D != 64 && D != 128) return fail(UC_E_INVALID, "D must be 64 or 128");
+    if (!aligned16(k_src) || !aligned16(v_src) || !aligned16(k_dst) || !aligned16(v_dst))
+      return fail(UC_E_INVALID, "gather pointers not 16-byte aligned");
+  }
+  if (k == 0) return ok();
+  hipStream_t s = (hipStream_t)stream;
+  hipError_t e = launch_select(scores, BH, N, k, n_recent, keep_idx, s);
+  if (e == hipSuccess && k_src)
+    e = launch_gather(keep_idx, BH, N, k, k_src, v_src, k_dst, v_dst, dtype_bytes(dt), D, s);
+  return launched(e);
+}
+
+// ---------------------------------------------------------------- quantize
+uc_status uc_quantize_segment(const uc_shape* shape, const void* k, const void* v, uc_dtype dt,
+                              int N, const uc_segment* out, void* stream) {
+  uc_status st = check_shape(shape);
+  if (st) return st;
+  if (!out) return fail(UC_E_INVALID, "out is NULL");
+  if (!dtype_ok(dt)) return fail(UC_E_INVALID, "bad dtype %d", dt);
+  if (N < 0) return fail(UC_E_INVALID, "N < 0");
+  if (out->kind != UC_SEG_PACKED) return fail(UC_E_INVALID, "out must be a packed segment");
+  if (out->n_rows != N) return fail(UC_E_INVALID, "out->n_rows %d != N %d", out->n_rows, N);
+  if (out->dtype != dt) return fail(UC_E_INVALID, "out->dtype != dt");
+  KSeg ks;
+  st = check_segment(*shape, *out, 0, ks, false);
+  if (st) return st;
+  if (N > 0 && (!k || !v)) return fail(UC_E_INVALID, "k or v is NULL");
+  if (!aligned16(k) || !aligned16(v)) return fail(UC_E_INVALID, "k/v not 16-byte aligned");
+  if (N == 0) return ok();
+  return launched(launch_quantize(*shape, k, v, dt, N, ks, (hipStream_t)stream));
+}
+
+// ---------------------------------------------------------------- append
+uc_status uc_append_rows(const uc_shape* shape, const void* k_new, const void* v_new, int n_new,
+                         const uc_segment* seg, int pos, void* stream) {
+  uc_status st = check_shape(shape);
+  if (st) return st;
+  if (!seg || seg->kind != UC_SEG_DENSE) return fail(UC_E_INVALID, "seg must be a dense segment");
+  KSeg ks;
+  st = check_segment(*shape, *seg, 0, ks, false);
+  if (st) return st;
+  if (n_new < 0 || pos < 0) return fail(UC_E_INVALID, "n_new and pos must be >= 0");
+  if ((int64_t)pos + n_new > ks.row_stride)
+    return fail(UC_E_INVALID, "pos + n_new = %lld > row_stride %d", (long long)pos + n_new, ks.row_stride);
+  if (n_new == 0) return ok();
+  if (!k_new || !v_new || !seg->k || !seg->v) return fail(UC_E_INVALID, "NULL pointer");
+  if (!aligned16(k_new) || !aligned16(v_new)) return fail(UC_E_INVALID, "k_new/v_new not 16-byte aligned");
+  ks.k = seg->k;
+  ks.v = seg->v;
+  return launched(launch_append(*shape, k_new, v_new, n_new, ks, pos, (hipStream_t)stream));
+}
+
+// ---------------------------------------------------------------- host helpers
+int64_t uc_dense_bytes(int64_t rows, int D, uc_dtype dt) {
+  return rows * 2 * (int64_t)D * dtype_bytes(dt);
+}
+
+int64_t uc_evicted_bytes(int64_t rows, int D, uc_dtype dt) {
+  return rows * (2 * (int64_t)D * dtype_bytes(dt) + (int64_t)sizeof(int32_t));
+}
+
+int64_t uc_packed_bytes(int64_t N, int D, int G, int bits, uc_dtype dt) {
+  if (N < 0 || D < 1 || G < 1 || D % G || !(bits == 2 || bits == 4 || bits == 8) || !dtype_ok(dt))
+    return -1;
+  const int64_t nf = (int64_t)G * (N / G);
+  const int64_t codes = 2 * nf * D * bits / 8;
+  const int64_t kmeta = (nf / G) * D * 2 * (int64_t)sizeof(float);
+  const int64_t vmeta = nf * (D / G) * 2 * (int64_t)sizeof(float);
+  return codes + kmeta + vmeta + uc_dense_bytes(N - nf, D, dt);
+}
+
+int64_t uc_evict_rows_for_budget(double budget_bytes, double fixed_bytes, int64_t N, int D,
+                                 uc_dtype dt) {
+  const double per = (double)uc_evicted_bytes(1, D, dt);
+  const double k = floor((budget_bytes - fixed_bytes) / per);
+  if (!(k > 0.0)) return 0;
+  return k >= (double)N ? N : (int64_t)k;
+}
+
+uc_status uc_assign_bits(int n_heads, const float* mass, int64_t N, int D, int G, uc_dtype dt,
+                         double budget_bytes, double fixed_bytes, uint8_t* bits_out) {
+  if (n_heads < 1 || !mass || !bits_out) return fail(UC_E_INVALID, "bad arguments");
+  const int64_t b2 = uc_packed_bytes(N, D, G, 2, dt), b4 = uc_packed_bytes(N, D, G, 4, dt);
+  if (b2 < 0) return fail(UC_E_INVALID, "bad packed geometry");
+  std::vector<int> order(n_heads);
+  for (int i = 0; i < n_heads; ++i) order[i] = i;
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return mass[a] > mass[b]; });
+  double total = fixed_bytes + (double)b2 * n_heads;
+  for (int i = 0; i < n_heads; ++i) bits_out[i] = 2;
+  for (int i = 0; i < n_heads; ++i) {
+    if (total + (double)(b4 - b2) > budget_bytes) break;
+    total += (double)(b4 - b2);
+    bits_out[order[i]] = 4;
+  }
+  return ok();
+}
+
+uc_status uc_type_budget(int n_types, const double* mass, const double* b_prev, double B_total,
+                         double* b_next) {
+  if (n_types < 1 || n_types > 64 || !mass || !b_prev || !b_next)
+    return fail(UC_E_INVALID, "bad arguments");
+  bool active[64], done = false;
+  for (int a = 0; a < n_types; ++a) {
+    b_next[a] = 0.0;
+    active[a] = mass[a] > 0.0;
+  }
+  double remaining = B_total;
+  while (!done) {
+    double msum = 0.0;
+    int n_active = 0;
+    for (int a = 0; a < n_types; ++a)
+      if (active[a]) {
+        msum += mass[a];
+        ++n_active;
+      }
+    if (n_active == 0) break;
+    bool capped_any = false;
+    bool capped[64] = {};
+    for (int a = 0; a < n_types; ++a)
+      if (active[a] && mass[a] / msum * remaining >= b_prev[a]) capped[a] = capped_any = true;
+    if (!capped_any) {
+      for (int a = 0; a < n_types; ++a)
+        if (active[a]) b_next[a] = mass[a] / msum * remaining;
+      done = true;
+    } else {
+      for (int a = 0; a < n_types; ++a)
+        if (capped[a]) {
+          b_next[a] = b_prev[a];
+          remaining -= b_prev[a];
+          active[a] = false;
+        }
+    }
+  }
+  return ok();
+}
+
+double uc_retention_next(double rho, double rho_init, double rho_min, double M_c, double M_0) {
+  if (!(rho_min > 0.0 && rho_min <= rho_init && rho_init <= 1.0 && M_0 > 0.0)) return NAN;
+  return std::min(rho, std::max(rho_min, rho_init * M_c / M_0));
+}
+
+}  // extern "C"

@@ -1,0 +1,400 @@
+// attend_generic.hip -- shared-softmax attention over heterogeneous segments
+// for any element type (fp32 / fp16 / bf16 rows and queries), plus the
+// log-sum-exp merge of chunk results (App. E, "Attention over heterogeneous
+// cache segments": one softmax normalisation across all segments; results of
+// separately evaluated chunks merged with log-sum-exp statistics).
+//
+// Work split: every segment's rows are cut into chunks (ChunkPlan); one
+// workgroup handles one (chunk, query head, query row).  Its four waves take
+// interleaved rows of the chunk; a lane owns D/64 dimensions, so a logit is a
+// lane-partial dot product reduced with wave shuffles.  Each chunk leaves an
+// unnormalised partial (running max m, sum l, accumulator o) in the
+// workspace, in base-2 units (logits pre-multiplied by log2(e)); the combine
+// kernel merges them into o, lse and the per-segment lse.
+//
+// This path runs on VALU only.  It serves queries and rows that are not bf16
+// (the bf16 path uses matrix cores) and cross-checks the fast kernels.
+#include <math.h>
+
+#include "uc_common.h"
+
+namespace uc {
+namespace {
+
+template <int D>
+struct RowLoader {
+  static constexpr int PER = D / 64;
+  // K and V values of row r for dims lane + 64*i
+  __device__ static inline void load(const KSeg& s, int bh, int r, int lane, int bits, int64_t off,
+                                     float (&kv)[PER], float (&vv)[PER]) {
+    if (s.kind == UC_SEG_DENSE) {
+      const int64_t base = ((int64_t)bh * s.row_stride + r) * D + lane;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        kv[i] = load_elem(s.k, s.dtype, base + 64 * i);
+        vv[i] = load_elem(s.v, s.dtype, base + 64 * i);
+      }
+    } else if (r < s.n_full) {
+      const int rb = D * bits / 8, G = s.group, ngk = s.n_full / G;
+      const uint8_t* ck = s.codes_k + off + (int64_t)r * rb;
+      const uint8_t* cv = s.codes_v + off + (int64_t)r * rb;
+      const int mask = (1 << bits) - 1, per_byte = 8 / bits;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int d = lane + 64 * i;
+        const int sh = (d % per_byte) * bits, by = d / per_byte;
+        const int qk = (ck[by] >> sh) & mask, qv = (cv[by] >> sh) & mask;
+        const int64_t ik = ((int64_t)bh * ngk + r / G) * D + d;
+        const int64_t iv = ((int64_t)bh * s.n_full + r) * (D / G) + d / G;
+        kv[i] = round_to(fmaf((float)qk, s.scale_k[ik], s.min_k[ik]), s.dtype);
+        vv[i] = round_to(fmaf((float)qv, s.scale_v[iv], s.min_v[iv]), s.dtype);
+      }
+    } else {
+      const int64_t base = ((int64_t)bh * s.tail_len + (r - s.n_full)) * D + lane;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        kv[i] = load_elem(s.tail_k, s.dtype, base + 64 * i);
+        vv[i] = load_elem(s.tail_v, s.dtype, base + 64 * i);
+      }
+    }
+  }
+};
+
+__device__ inline int chunk_segment(const ChunkPlan& plan, int nseg, int c) {
+  int si = 0;
+  while (si + 1 < nseg && c >= plan.first[si + 1]) ++si;
+  return si;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void attend_generic_kernel(KSegs segs, ChunkPlan plan,
+                                                             const void* __restrict__ q, int q_dt,
+                                                             int Hq, int Hkv, int M,
+                                                             float scale_log2, float* partial,
+                                                             int want_o, int ps) {
+  constexpr int PER = D / 64;
+  __shared__ float red_m[4], red_l[4];
+  __shared__ float red_o[4][D];
+  const int c = blockIdx.x, bq = blockIdx.y, m = blockIdx.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int si = chunk_segment(plan, segs.n, c);
+  const KSeg& s = segs.s[si];
+  const int r0 = (c - plan.first[si]) * plan.rows[si];
+  const int r1 = min(r0 + plan.rows[si], s.n_rows);
+  const int G = Hq / Hkv, b = bq / Hq, hq = bq % Hq, bh = b * Hkv + hq / G;
+
+  int bits = 0;
+  int64_t off = 0;
+  const bool ok = s.kind == UC_SEG_DENSE || head_codes(s, bh, D, bits, off);
+
+  float qv[PER];
+  const int64_t qbase = ((int64_t)bq * M + m) * D + lane;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) qv[i] = load_elem(q, q_dt, qbase + 64 * i) * scale_log2;
+
+  float mx = -INFINITY, l = 0.0f, acc[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) acc[i] = 0.0f;
+  if (ok) {
+    for (int r = r0 + wave; r < r1; r += 4) {
+      float kv[PER], vv[PER];
+      RowLoader<D>::load(s, bh, r, lane, bits, off, kv, vv);
+      float d = 0.0f;
+#pragma unroll
+      for (int i = 0; i < PER; ++i) d = fmaf(qv[i], kv[i], d);
+      d = wave_sum(d);
+      const float mn = fmaxf(mx, d);
+      const float alpha = exp2f(mx - mn), p = exp2f(d - mn);
+      l = l * alpha + p;
+      if (want_o) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) acc[i] = fmaf(p, vv[i], acc[i] * alpha);
+      }
+      mx = mn;
+    }
+  }
+  if (lane == 0) {
+    red_m[wave] = mx;
+    red_l[wave] = l;
+  }
+#pragma unroll
+  for (int i = 0; i < PER; ++i) red_o[wave][lane + 64 * i] = acc[i];
+  __syncthreads();
+  if (wave != 0) return;
+  float M_ = fmaxf(fmaxf(red_m[0], red_m[1]), fmaxf(red_m[2], red_m[3]));
+  float w[4], L = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    w[j] = red_m[j] == -INFINITY ? 0.0f : exp2f(red_m[j] - M_);
+    L += w[j] * red_l[j];
+  }
+  const int C = plan.n_chunks;
+  float* out = partial + (((int64_t)bq * M + m) * C + c) * ps;
+  if (lane == 0) {
+    out[0] = ok ? M_ : 0.0f;
+    out[1] = ok ? L : __builtin_nanf("");
+  }
+  if (want_o) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int d = lane + 64 * i;
+      out[2 + d] = w[0] * red_o[0][d] + w[1] * red_o[1][d] + w[2] * red_o[2][d] + w[3] * red_o[3][d];
+    }
+  }
+}
+
+// One wave per query row: merge the chunk partials of that row.
+template <int D>
+__global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int nseg, int ps,
+                                                            const float* __restrict__ partial,
+                                                            float* o, float* lse, float* seg_lse) {
+  constexpr int PER = D / 64;
+  const int64_t qi = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int C = plan.n_chunks;
+  const float* P = partial + qi * C * ps;
+  float mall = -INFINITY;
+  for (int c = lane; c < C; c += 64) mall = fmaxf(mall, P[(int64_t)c * ps]);
+  mall = wave_max(mall);
+  float L = 0.0f;
+  for (int c = lane; c < C; c += 64) {
+    const float* pc = P + (int64_t)c * ps;
+    L += pc[1] * exp2f(pc[0] - mall);
+  }
+  L = wave_sum(L);
+  if (lse && lane == 0) lse[qi] = (mall + log2f(L)) * kLn2;
+  if (seg_lse) {
+    for (int a = 0; a < nseg; ++a) {
+      float ma = -INFINITY, la = 0.0f;
+      for (int c = plan.first[a] + lane; c < plan.first[a + 1]; c += 64)
+        ma = fmaxf(ma, P[(int64_t)c * ps]);
+      ma = wave_max(ma);
+      for (int c = plan.first[a] + lane; c < plan.first[a + 1]; c += 64) {
+        const float* pc = P + (int64_t)c * ps;
+        la += pc[1] * exp2f(pc[0] - ma);
+      }
+      la = wave_sum(la);
+      if (lane == 0) seg_lse[qi * nseg + a] = la > 0.0f ? (ma + log2f(la)) * kLn2 : -INFINITY;
+    }
+  }
+  if (o) {
+    float acc[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) acc[i] = 0.0f;
+    for (int c = 0; c < C; ++c) {
+      const float* pc = P + (int64_t)c * ps;
+      const float w = exp2f(pc[0] - mall);
+#pragma unroll
+      for (int i = 0; i < PER; ++i) acc[i] = fmaf(w, pc[2 + lane + 64 * i], acc[i]);
+    }
+    const float inv = 1.0f / L;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) o[qi * D + lane + 64 * i] = acc[i] * inv;
+  }
+}
+
+// Importance scores, second pass: one thread per key row.  For every
+// observation row (g, w) of the KV head, p = exp(s - lse) with lse from the
+// first pass; the column sums run in double.  Per-chunk segment masses go to
+// mass_partial[bh, chunk].
+struct ScorePtrs {
+  float* p[kMaxSeg];
+};
+
+template <int D>
+__global__ __launch_bounds__(256) void score_colsum_kernel(KSegs segs, ChunkPlan plan,
+                                                           const void* __restrict__ q, int q_dt,
+                                                           int Hq, int Hkv, int W,
+                                                           float scale_log2,
+                                                           const float* __restrict__ lse,
+                                                           ScorePtrs scores,
+                                                           double* mass_partial) {
+  constexpr int QB = 16;  // query rows staged per round
+  __shared__ float qs[QB][D];
+  __shared__ float ls[QB];
+  __shared__ double red[4];
+  const int c = blockIdx.x, bh = blockIdx.y;
+  const int si = chunk_segment(plan, segs.n, c);
+  const KSeg& s = segs.s[si];
+  const int r = (c - plan.first[si]) * plan.rows[si] + threadIdx.x;
+  const int r_end = min((c - plan.first[si] + 1) * plan.rows[si], s.n_rows);
+  const bool live = r < r_end;
+  const int G = Hq / Hkv, b = bh / Hkv, hkv = bh % Hkv;
+  int bits = 0;
+  int64_t off = 0;
+  const bool ok = s.kind == UC_SEG_DENSE || head_codes(s, bh, D, bits, off);
+
+  // the key row, dequantised, in registers
+  float kr[D];
+  if (live && ok) {
+    if (s.kind == UC_SEG_DENSE) {
+      const int64_t base = ((int64_t)bh * s.row_stride + r) * D;
+#pragma unroll
+      for (int d = 0; d < D; ++d) kr[d] = load_elem(s.k, s.dtype, base + d);
+    } else if (r < s.n_full) {
+      const int rb = D * bits / 8, Gq = s.group, ngk = s.n_full / Gq;
+      const uint8_t* ck = s.codes_k + off + (int64_t)r * rb;
+      const int mask = (1 << bits) - 1, per_byte = 8 / bits;
+#pragma unroll
+      for (int d = 0; d < D; ++d) {
+        const int qk = (ck[d / per_byte] >> ((d % per_byte) * bits)) & mask;
+        const int64_t ik = ((int64_t)bh * ngk + r / Gq) * D + d;
+        kr[d] = round_to(fmaf((float)qk, s.scale_k[ik], s.min_k[ik]), s.dtype);
+      }
+    } else {
+      const int64_t base = ((int64_t)bh * s.tail_len + (r - s.n_full)) * D;
+#pragma unroll
+      for (int d = 0; d < D; ++d) kr[d] = load_elem(s.tail_k, s.dtype, base + d);
+    }
+  } else {
+#pragma unroll
+    for (int d = 0; d < D; ++d) kr[d] = 0.0f;
+  }
+
+  double acc = 0.0;
+  const int nq = G * W;
+  for (int q0 = 0; q0 < nq; q0 += QB) {
+    __syncthreads();
+    for (int e = threadIdx.x; e < QB * D; e += blockDim.x) {
+      const int j = e / D, d = e % D, qr = q0 + j;
+      float val = 0.0f;
+      if (qr < nq) {
+        const int g = qr / W, w = qr % W;
+        val = load_elem(q, q_dt, (((int64_t)b * Hq + hkv * G + g) * W + w) * D + d) * scale_log2;
+      }
+      qs[j][d] = val;
+    }
+    if (threadIdx.x < QB) {
+      const int qr = q0 + threadIdx.x;
+      float lv = 0.0f;
+      if (qr < nq) {
+        const int g = qr / W, w = qr % W;
+        lv = lse[((int64_t)b * Hq + hkv * G + g) * W + w] * kLog2e;
+      }
+      ls[threadIdx.x] = lv;
+    }
+    __syncthreads();
+    const int jn = min(QB, nq - q0);
+    for (int j = 0; j < jn; ++j) {
+      float d = 0.0f;
+#pragma unroll
+      for (int e = 0; e < D; ++e) d = fmaf(qs[j][e], kr[e], d);
+      acc += (double)exp2f(d - ls[j]);
+    }
+  }
+  if (!ok) acc = __builtin_nan("");
+  if (live) {
+    float* sp = scores.p[si];
+    if (sp) sp[(int64_t)bh * s.n_rows + r] = (float)acc;
+  }
+  // chunk mass (fixed-order reduction: deterministic)
+  double part = live ? acc : 0.0;
+  part = wave_sum_d(part);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = part;
+  __syncthreads();
+  if (threadIdx.x == 0 && mass_partial)
+    mass_partial[(int64_t)bh * plan.n_chunks + c] = red[0] + red[1] + red[2] + red[3];
+}
+
+__global__ void mass_finalize_kernel(ChunkPlan plan, int nseg, const double* __restrict__ part,
+                                     float* mass) {
+  const int bh = blockIdx.x, a = threadIdx.x;
+  if (a >= nseg) return;
+  double s = 0.0;
+  for (int c = plan.first[a]; c < plan.first[a + 1]; ++c) s += part[(int64_t)bh * plan.n_chunks + c];
+  mass[(int64_t)bh * nseg + a] = (float)s;
+}
+
+// Eq. 1 bracket from attention statistics: sum over the query heads of a KV
+// head and the query rows of P mass per segment = exp(seg_lse - lse).
+__global__ __launch_bounds__(256) void segment_mass_kernel(int Hq, int Hkv, int M, int nseg,
+                                                           const float* __restrict__ lse,
+                                                           const float* __restrict__ seg_lse,
+                                                           float* mass) {
+  __shared__ double red[4][kMaxSeg];
+  const int bh = blockIdx.x, b = bh / Hkv, hkv = bh % Hkv, G = Hq / Hkv;
+  double acc[kMaxSeg];
+  for (int a = 0; a < kMaxSeg; ++a) acc[a] = 0.0;
+  const int n = G * M;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    const int g = i / M, m = i % M;
+    const int64_t qi = ((int64_t)b * Hq + hkv * G + g) * M + m;
+    const double L = lse[qi];
+    for (int a = 0; a < nseg; ++a) {
+      const float sl = seg_lse[qi * nseg + a];
+      if (sl != -INFINITY) acc[a] += exp((double)sl - L);
+    }
+  }
+  for (int a = 0; a < nseg; ++a) {
+    double v = wave_sum_d(acc[a]);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6][a] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < nseg) {
+    const int a = threadIdx.x;
+    mass[(int64_t)bh * nseg + a] = (float)(red[0][a] + red[1][a] + red[2][a] + red[3][a]);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attend_generic(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
+                                 const void* q, int q_dt, int M, float sm_scale, float* partial,
+                                 bool want_o, hipStream_t st) {
+  dim3 grid(plan.n_chunks, sh.B * sh.Hq, M);
+  const float sl2 = sm_scale * kLog2e;
+  const int ps = want_o ? sh.D + 2 : 2;
+  if (sh.D == 64)
+    hipLaunchKernelGGL(attend_generic_kernel<64>, grid, dim3(256), 0, st, segs, plan, q, q_dt,
+                       sh.Hq, sh.Hkv, M, sl2, partial, (int)want_o, ps);
+  else
+    hipLaunchKernelGGL(attend_generic_kernel<128>, grid, dim3(256), 0, st, segs, plan, q, q_dt,
+                       sh.Hq, sh.Hkv, M, sl2, partial, (int)want_o, ps);
+  return hipGetLastError();
+}
+
+hipError_t launch_attend_combine(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
+                                 int M, const float* partial, float* o, float* lse, float* seg_lse,
+                                 hipStream_t st) {
+  const int64_t Q = (int64_t)sh.B * sh.Hq * M;
+  const int ps = o ? sh.D + 2 : 2;
+  if (sh.D == 64)
+    hipLaunchKernelGGL(attend_combine_kernel<64>, dim3((unsigned)Q), dim3(64), 0, st, plan, segs.n,
+                       ps, partial, o, lse, seg_lse);
+  else
+    hipLaunchKernelGGL(attend_combine_kernel<128>, dim3((unsigned)Q), dim3(64), 0, st, plan,
+                       segs.n, ps, partial, o, lse, seg_lse);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_colsum(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
+                               const void* q, int q_dt, int W, float sm_scale, const float* lse,
+                               float* const* scores, double* mass_partial, hipStream_t st) {
+  ScorePtrs sp{};
+  for (int i = 0; i < segs.n; ++i) sp.p[i] = scores ? scores[i] : nullptr;
+  dim3 grid(plan.n_chunks, sh.B * sh.Hkv);
+  const float sl2 = sm_scale * kLog2e;
+  if (sh.D == 64)
+    hipLaunchKernelGGL(score_colsum_kernel<64>, grid, dim3(256), 0, st, segs, plan, q, q_dt, sh.Hq,
+                       sh.Hkv, W, sl2, lse, sp, mass_partial);
+  else
+    hipLaunchKernelGGL(score_colsum_kernel<128>, grid, dim3(256), 0, st, segs, plan, q, q_dt,
+                       sh.Hq, sh.Hkv, W, sl2, lse, sp, mass_partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_mass_finalize(const ChunkPlan& plan, int BH, int n_segs,
+                                const double* mass_partial, float* mass, hipStream_t st) {
+  hipLaunchKernelGGL(mass_finalize_kernel, dim3(BH), dim3(64), 0, st, plan, n_segs, mass_partial,
+                     mass);
+  return hipGetLastError();
+}
+
+hipError_t launch_segment_mass(const uc_shape& sh, int M, int n_segs, const float* lse,
+                               const float* seg_lse, float* mass, hipStream_t st) {
+  hipLaunchKernelGGL(segment_mass_kernel, dim3(sh.B * sh.Hkv), dim3(256), 0, st, sh.Hq, sh.Hkv, M,
+                     n_segs, lse, seg_lse, mass);
+  return hipGetLastError();
+}
+
+}  // namespace uc

@@ -1,0 +1,153 @@
+// quantize.hip -- group-wise asymmetric min/max quantization of one segment
+// into packed low-bit codes, float scales/minima and a residual tail
+// (App. E, "Physical, type-aware KV storage").
+//
+//   keys:   one channel over G consecutive rows     (per-channel groups)
+//   values: G consecutive channels of one row       (per-token groups)
+//   mn = min, mx = max, s = (mx - mn) / (2^b - 1)
+//   code = s > 0 ? clamp(rint((x - mn) / s), 0, 2^b - 1) : 0
+// All in IEEE binary32 with correctly rounded division and no contraction, so
+// codes and scales are reproducible bit for bit.
+//
+// Layout of the output (see unicache.h): row r of a head's codes occupies
+// D*b/8 bytes; channel c sits in byte c*b/8 at bit (c % (8/b))*b.  One lane
+// owns one channel; lanes of one 32-bit word (32/b consecutive channels)
+// OR their shifted codes together with cross-lane shuffles and the first lane
+// of the word stores it, so each row's codes leave as coalesced 32-bit stores.
+#pragma clang fp contract(off)
+
+#include "uc_common.h"
+
+namespace uc {
+namespace {
+
+__device__ inline int quant_code(float x, float mn, float s, int qmax) {
+  if (!(s > 0.0f)) return 0;
+  float t = __fdiv_rn(x - mn, s);
+  int c = (int)rintf(t);
+  return min(max(c, 0), qmax);
+}
+
+// OR-combine the shifted codes of the 32/b lanes that share a word; returns
+// the word in every lane of the group.
+__device__ inline uint32_t pack_word(int code, int c, int b) {
+  const int cpw = 32 / b;
+  uint32_t w = (uint32_t)code << ((c % cpw) * b);
+  for (int o = 1; o < cpw; o <<= 1) w |= (uint32_t)__shfl_xor((int)w, o, 64);
+  return w;
+}
+
+// Keys: block = D threads (one per channel), one block per (row group, bh).
+__global__ void quantize_k_kernel(KSeg seg, const void* __restrict__ k, int dt, int N, int D) {
+  const int g = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
+  const int G = seg.group;
+  const int ngk = seg.n_full / G;
+  int b;
+  int64_t off;
+  float* scale = const_cast<float*>(seg.scale_k) + ((int64_t)bh * ngk + g) * D + c;
+  float* mnp = const_cast<float*>(seg.min_k) + ((int64_t)bh * ngk + g) * D + c;
+  if (!head_codes(seg, bh, D, b, off) || (off & 15)) {
+    *scale = __builtin_nanf("");
+    return;
+  }
+  const int qmax = (1 << b) - 1;
+  const int64_t base = ((int64_t)bh * N + (int64_t)g * G) * D + c;
+  float mn = load_elem(k, dt, base), mx = mn;
+  for (int r = 1; r < G; ++r) {
+    float x = load_elem(k, dt, base + (int64_t)r * D);
+    mn = fminf(mn, x);
+    mx = fmaxf(mx, x);
+  }
+  const float s = __fdiv_rn(mx - mn, (float)qmax);
+  *scale = s;
+  *mnp = mn;
+  const int row_bytes = D * b / 8;
+  uint8_t* codes = const_cast<uint8_t*>(seg.codes_k) + off + (int64_t)g * G * row_bytes;
+  const int cpw = 32 / b;
+  for (int r = 0; r < G; ++r) {
+    int code = quant_code(load_elem(k, dt, base + (int64_t)r * D), mn, s, qmax);
+    uint32_t w = pack_word(code, c, b);
+    if (c % cpw == 0) *reinterpret_cast<uint32_t*>(codes + (int64_t)r * row_bytes + c * b / 8) = w;
+  }
+}
+
+// Values: block = 256 threads = (256 / D) rows x D channels; group min/max
+// through LDS.
+__global__ void quantize_v_kernel(KSeg seg, const void* __restrict__ v, int dt, int N, int D) {
+  __shared__ float xs[256];
+  __shared__ float ss[256], ms[256];
+  const int rows_per_block = 256 / D;
+  const int lr = threadIdx.x / D, c = threadIdx.x % D;
+  const int r = blockIdx.x * rows_per_block + lr, bh = blockIdx.y;
+  const int G = seg.group, ngv = D / G;
+  int b;
+  int64_t off;
+  const bool ok = head_codes(seg, bh, D, b, off) && !(off & 15);
+  const bool live = r < seg.n_full;
+  float x = live ? load_elem(v, dt, ((int64_t)bh * N + r) * D + c) : 0.0f;
+  xs[threadIdx.x] = x;
+  __syncthreads();
+  if (live && c % G == 0) {
+    float mn = xs[threadIdx.x], mx = mn;
+    for (int i = 1; i < G; ++i) {
+      float y = xs[threadIdx.x + i];
+      mn = fminf(mn, y);
+      mx = fmaxf(mx, y);
+    }
+    const float s = ok ? __fdiv_rn(mx - mn, (float)((1 << b) - 1)) : __builtin_nanf("");
+    ss[threadIdx.x] = s;
+    ms[threadIdx.x] = mn;
+    const int64_t mi = ((int64_t)bh * seg.n_full + r) * ngv + c / G;
+    const_cast<float*>(seg.scale_v)[mi] = s;
+    const_cast<float*>(seg.min_v)[mi] = mn;
+  }
+  __syncthreads();
+  if (!ok) return;  // uniform over the block: bh is per block
+  const int gl = threadIdx.x - (c % G);
+  const int code = live ? quant_code(x, ms[gl], ss[gl], (1 << b) - 1) : 0;
+  const uint32_t w = pack_word(code, c, b);
+  const int cpw = 32 / b;
+  if (live && c % cpw == 0) {
+    const int row_bytes = D * b / 8;
+    uint8_t* codes = const_cast<uint8_t*>(seg.codes_v) + off + (int64_t)r * row_bytes;
+    *reinterpret_cast<uint32_t*>(codes + c * b / 8) = w;
+  }
+}
+
+// Residual tail: rows n_full..N-1 copied unchanged (16 bytes per lane).
+__global__ void copy_tail_kernel(KSeg seg, const void* __restrict__ k, const void* __restrict__ v,
+                                 int N, int row_bytes) {
+  const int bh = blockIdx.y;
+  const int64_t tail_bytes = (int64_t)seg.tail_len * row_bytes;
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 16;
+  if (i >= tail_bytes) return;
+  const int64_t src = ((int64_t)bh * N + seg.n_full) * row_bytes + i;
+  const int64_t dst = (int64_t)bh * tail_bytes + i;
+  *reinterpret_cast<uint4*>((char*)seg.tail_k + dst) =
+      *reinterpret_cast<const uint4*>((const char*)k + src);
+  *reinterpret_cast<uint4*>((char*)seg.tail_v + dst) =
+      *reinterpret_cast<const uint4*>((const char*)v + src);
+}
+
+}  // namespace
+
+hipError_t launch_quantize(const uc_shape& sh, const void* k, const void* v, int dt, int N,
+                           const KSeg& out, hipStream_t st) {
+  const int BH = sh.B * sh.Hkv, D = sh.D;
+  if (out.n_full > 0) {
+    hipLaunchKernelGGL(quantize_k_kernel, dim3(out.n_full / out.group, BH), dim3(D), 0, st, out,
+                       k, dt, N, D);
+    const int rpb = 256 / D;
+    hipLaunchKernelGGL(quantize_v_kernel, dim3((out.n_full + rpb - 1) / rpb, BH), dim3(256), 0,
+                       st, out, v, dt, N, D);
+  }
+  if (out.tail_len > 0) {
+    const int row_bytes = D * dtype_bytes(dt);
+    const int64_t lanes = ((int64_t)out.tail_len * row_bytes + 15) / 16;
+    hipLaunchKernelGGL(copy_tail_kernel, dim3((unsigned)((lanes + 255) / 256), BH), dim3(256), 0,
+                       st, out, k, v, N, row_bytes);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace uc

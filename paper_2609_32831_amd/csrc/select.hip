@@ -1,0 +1,186 @@
+// select.hip -- per-KV-head top-k token selection, ordered compaction and
+// row gather (App. E, "Batched GQA token selection" and "Physical, type-aware
+// KV storage": heavy-hitter plus recent-token selection per KV head; only the
+// retained rows and their logical indices are stored, in token order).
+//
+// One 1024-thread workgroup per (b, h_kv) row of scores:
+//  1. radix select, 8 bits per pass over order-preserving 32-bit keys of the
+//     float scores, finds the exact k'-th largest key tau (k' = k - n_recent)
+//     and how many rows equal to tau must be taken;
+//  2. ordered compaction: each thread owns a contiguous run of positions,
+//     counts rows above tau and rows equal to tau, a block-wide exclusive scan
+//     gives every run its output offset, and ties are taken lowest position
+//     first -- the result is the unique set of the (score, -index) order,
+//     written in ascending position;
+//  3. the last n_recent positions follow unconditionally.
+// The gather kernel then copies the kept K/V rows with 16-byte lanes.
+#include "uc_common.h"
+
+namespace uc {
+namespace {
+
+constexpr int kSelThreads = 1024;
+
+__device__ inline uint32_t order_key(float f) {
+  uint32_t u = __float_as_uint(f);
+  if (u == 0x80000000u) u = 0u;  // -0 ranks as +0
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+// exclusive scan of one uint32 per thread over the block (16 waves)
+__device__ inline uint32_t block_exclusive_scan(uint32_t x, uint32_t* wave_tot) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t inc = x;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t y = __shfl_up(inc, o, 64);
+    if (lane >= o) inc += y;
+  }
+  if (lane == 63) wave_tot[wave] = inc;
+  __syncthreads();
+  if (wave == 0) {
+    uint32_t t = lane < kSelThreads / 64 ? wave_tot[lane] : 0u;
+    uint32_t ti = t;
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) {
+      uint32_t y = __shfl_up(ti, o, 64);
+      if (lane >= o) ti += y;
+    }
+    if (lane < kSelThreads / 64) wave_tot[lane] = ti - t;
+  }
+  __syncthreads();
+  uint32_t r = wave_tot[wave] + inc - x;
+  __syncthreads();
+  return r;
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores, int N,
+                                                             int k, int n_recent,
+                                                             int32_t* __restrict__ keep) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t wave_tot[kSelThreads / 64];
+  __shared__ uint32_t sh_digit, sh_need;
+  const int bh = blockIdx.x, tid = threadIdx.x;
+  const float* s = scores + (int64_t)bh * N;
+  int32_t* out = keep + (int64_t)bh * k;
+  const int Nc = N - n_recent, kc = k - n_recent;
+
+  uint32_t prefix = 0, need = (uint32_t)kc;
+  if (kc > 0) {
+    for (int pass = 0; pass < 4; ++pass) {
+      const int shift = 24 - 8 * pass;
+      const uint32_t hi_mask = pass == 0 ? 0u : (0xFFFFFFFFu << (32 - 8 * pass));
+      for (int t = tid; t < 256; t += kSelThreads) hist[t] = 0u;
+      __syncthreads();
+      for (int i = tid; i < Nc; i += kSelThreads) {
+        const uint32_t key = order_key(s[i]);
+        if ((key & hi_mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+      }
+      __syncthreads();
+      if (tid == 0) {
+        uint32_t cum = 0;
+        for (int d = 255; d >= 0; --d) {
+          if (cum + hist[d] >= need) {
+            sh_digit = (uint32_t)d;
+            sh_need = need - cum;
+            break;
+          }
+          cum += hist[d];
+        }
+      }
+      __syncthreads();
+      prefix |= sh_digit << shift;
+      need = sh_need;
+      __syncthreads();
+    }
+  }
+  // prefix is the k'-th largest key; `need` rows equal to it are kept
+  const int per = (Nc + kSelThreads - 1) / kSelThreads;
+  const int i0 = min(tid * per, Nc), i1 = min(i0 + per, Nc);
+  uint32_t cgt = 0, ceq = 0;
+  if (kc > 0) {
+    for (int i = i0; i < i1; ++i) {
+      const uint32_t key = order_key(s[i]);
+      cgt += key > prefix;
+      ceq += key == prefix;
+    }
+  }
+  const uint32_t gt_ex = block_exclusive_scan(cgt, wave_tot);
+  const uint32_t eq_ex = block_exclusive_scan(ceq, wave_tot);
+  if (kc > 0) {
+    uint32_t pos = gt_ex + min(eq_ex, need), eq_seen = eq_ex;
+    for (int i = i0; i < i1; ++i) {
+      const uint32_t key = order_key(s[i]);
+      if (key > prefix) {
+        out[pos++] = i;
+      } else if (key == prefix) {
+        if (eq_seen < need) out[pos++] = i;
+        ++eq_seen;
+      }
+    }
+  }
+  for (int j = tid; j < n_recent; j += kSelThreads) out[kc + j] = Nc + j;
+}
+
+// Copy kept rows: 16 bytes per lane; grid.y = (b, h_kv).
+__global__ void gather_kernel(const int32_t* __restrict__ keep, int N, int k, const char* ksrc,
+                              const char* vsrc, char* kdst, char* vdst, int row_bytes) {
+  const int bh = blockIdx.y;
+  const int lanes_per_row = row_bytes / 16;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= (int64_t)k * lanes_per_row) return;
+  const int j = (int)(e / lanes_per_row), piece = (int)(e % lanes_per_row);
+  const int src_row = keep[(int64_t)bh * k + j];
+  if (src_row < 0 || src_row >= N) return;
+  const int64_t so = ((int64_t)bh * N + src_row) * row_bytes + piece * 16;
+  const int64_t dof = ((int64_t)bh * k + j) * row_bytes + piece * 16;
+  *reinterpret_cast<uint4*>(kdst + dof) = *reinterpret_cast<const uint4*>(ksrc + so);
+  *reinterpret_cast<uint4*>(vdst + dof) = *reinterpret_cast<const uint4*>(vsrc + so);
+}
+
+// Decode append: rows pos..pos+n_new-1 of a dense segment.
+__global__ void append_kernel(const char* knew, const char* vnew, int n_new, char* kd, char* vd,
+                              int row_stride, int pos, int row_bytes) {
+  const int bh = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t per_bh = (int64_t)n_new * row_bytes / 16;
+  if (e >= per_bh) return;
+  const int64_t src = (int64_t)bh * n_new * row_bytes + e * 16;
+  const int64_t dst = ((int64_t)bh * row_stride + pos) * row_bytes + e * 16;
+  *reinterpret_cast<uint4*>(kd + dst) = *reinterpret_cast<const uint4*>(knew + src);
+  *reinterpret_cast<uint4*>(vd + dst) = *reinterpret_cast<const uint4*>(vnew + src);
+}
+
+}  // namespace
+
+hipError_t launch_select(const float* scores, int BH, int N, int k, int n_recent, int32_t* keep,
+                         hipStream_t st) {
+  hipLaunchKernelGGL(select_kernel, dim3(BH), dim3(kSelThreads), 0, st, scores, N, k, n_recent,
+                     keep);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather(const int32_t* keep, int BH, int N, int k, const void* ksrc,
+                         const void* vsrc, void* kdst, void* vdst, int elem_bytes, int D,
+                         hipStream_t st) {
+  const int row_bytes = D * elem_bytes;
+  const int64_t lanes = (int64_t)k * (row_bytes / 16);
+  if (lanes == 0) return hipSuccess;
+  hipLaunchKernelGGL(gather_kernel, dim3((unsigned)((lanes + 255) / 256), BH), dim3(256), 0, st,
+                     keep, N, k, (const char*)ksrc, (const char*)vsrc, (char*)kdst, (char*)vdst,
+                     row_bytes);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const uc_shape& sh, const void* knew, const void* vnew, int n_new,
+                         const KSeg& seg, int pos, hipStream_t st) {
+  const int row_bytes = sh.D * dtype_bytes(seg.dtype);
+  const int64_t lanes = (int64_t)n_new * row_bytes / 16;
+  if (lanes == 0) return hipSuccess;
+  hipLaunchKernelGGL(append_kernel, dim3((unsigned)((lanes + 255) / 256), sh.B * sh.Hkv), dim3(256),
+                     0, st, (const char*)knew, (const char*)vnew, n_new, (char*)seg.k,
+                     (char*)seg.v, seg.row_stride, pos, row_bytes);
+  return hipGetLastError();
+}
+
+}  // namespace uc

@@ -1,0 +1,273 @@
+"""Per-call GPU parity against the CPU oracle (stage-isolated: both sides get
+identical input bytes).  Bars: codes, scales, minima, tails and kept indices
+bit-exact; attention within 2e-3 max-abs and 1e-3 relative L2 in fp32."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():  # collected on CPU-only hosts, never run there
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import oracle as ref  # noqa: E402
+import paper_2609_32831_amd as uc  # noqa: E402
+import workloads as gen  # noqa: E402
+from gpu_util import (TORCH, UCDT, check_attention, dev, host_bytes, packed_from_oracle,  # noqa: E402
+                      rand_rows, sm_scale)
+
+
+def _print_case(**kw):
+    print("CASE", " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+# ------------------------------------------------------------------ quantize
+
+QCASES = [
+    # dtype, B, Hkv, N, D, G, bits (int or per-head list)
+    ("f32", 1, 1, 256, 64, 32, 4),
+    ("bf16", 2, 4, 4096 + 37, 128, 64, 4),
+    ("bf16", 2, 4, 1000, 128, 64, [4, 2, 4, 4, 2, 4, 4, 2]),
+    ("f16", 1, 2, 500, 128, 32, 2),
+    ("bf16", 1, 3, 77, 64, 8, 8),
+    ("bf16", 1, 2, 100, 128, 128, 4),   # shorter than one group: all tail
+    ("bf16", 1, 1, 64, 128, 64, 2),     # exactly one group, no tail
+]
+
+
+@pytest.mark.parametrize("case", QCASES, ids=[f"q{i}" for i in range(len(QCASES))])
+def test_quantize_bit_exact(case):
+    dtype, B, Hkv, N, D, G, bits = case
+    _print_case(test="quantize", dtype=dtype, B=B, Hkv=Hkv, N=N, D=D, G=G, bits=bits)
+    BH = B * Hkv
+    per_head = isinstance(bits, list)
+    hb = bits if per_head else [bits] * BH
+    k = rand_rows(11, BH, N, D, dtype, 2.0, outliers=(3, 40))
+    v = rand_rows(12, BH, N, D, dtype)
+    pk = ref.quantize(k, v, dtype, G, hb)
+    seg = uc.packed_segment(B, Hkv, N, D, G, TORCH[dtype], bits=hb[0],
+                            head_bits=hb if per_head else None)
+    shape = uc.make_shape(B, Hkv, Hkv, D)
+    kd = dev(k, dtype).reshape(B, Hkv, N, D)
+    vd = dev(v, dtype).reshape(B, Hkv, N, D)
+    uc.uc_quantize_segment(shape, kd, vd, N, seg)
+    torch.cuda.synchronize()
+    n = pk["codes_k"].shape[0]
+    assert np.array_equal(seg.t["codes_k"].cpu().numpy()[:n], pk["codes_k"])
+    assert np.array_equal(seg.t["codes_v"].cpu().numpy()[:n], pk["codes_v"])
+    for name in ("scale_k", "min_k", "scale_v", "min_v"):
+        got = seg.t[name].cpu().numpy().reshape(pk[name].shape)
+        assert np.array_equal(got.view(np.uint32), pk[name].view(np.uint32)), name
+    if pk["tail_k"].shape[1]:
+        assert np.array_equal(host_bytes(seg.t["tail_k"]).reshape(pk["tail_k"].shape), pk["tail_k"])
+        assert np.array_equal(host_bytes(seg.t["tail_v"]).reshape(pk["tail_v"].shape), pk["tail_v"])
+
+
+# ------------------------------------------------------------------ select
+
+@pytest.mark.parametrize("N,k,nr", [(1, 1, 0), (100, 37, 0), (100, 37, 5), (4099, 1024, 0),
+                                    (4099, 4099, 0), (61440, 11735, 0), (300, 10, 10),
+                                    (1500, 0, 0)])
+def test_select_bit_exact(N, k, nr):
+    _print_case(test="select", N=N, k=k, n_recent=nr)
+    BH, D = 6, 128
+    rng = np.random.default_rng(N + k)
+    s = rng.integers(0, 50, (BH, N)).astype(np.float32) / 13.0  # many exact ties
+    s[0] = rng.random(N).astype(np.float32)
+    s[1, : N // 2] = 0.0
+    want = ref.select(s, k, nr)
+    sd = torch.from_numpy(s).cuda()
+    keep = torch.full((BH, max(k, 1)), -7, dtype=torch.int32, device="cuda")
+    kv = rand_rows(5, BH, N, D, "bf16")
+    ksrc = dev(kv, "bf16")
+    vsrc = dev(kv[:, ::-1].copy(), "bf16")
+    kdst = torch.zeros(BH, max(k, 1), D, dtype=torch.bfloat16, device="cuda")
+    vdst = torch.zeros_like(kdst)
+    uc.uc_select_keep(sd, k, nr, keep, ksrc, vsrc, kdst, vdst)
+    torch.cuda.synchronize()
+    if k == 0:
+        return
+    got = keep.cpu().numpy()
+    assert np.array_equal(got, want)
+    kb = host_bytes(kdst)
+    vb = host_bytes(vdst)
+    for bh in range(BH):
+        assert np.array_equal(kb[bh], kv[bh][want[bh]])
+        assert np.array_equal(vb[bh], kv[bh, ::-1][want[bh]])
+
+
+# ------------------------------------------------------------------ attention
+
+def _mixed_case(B, Hq, Hkv, D, dtype, sizes, seed=0, G=64, bits=4, per_head=False):
+    """Segments: dense 'text', compacted 'vit' (rows chosen at random, with
+    their logical positions), packed 'vae' with tail, dense tail segment with
+    spare capacity.  Returns GPU segments and the oracle's logical K/V."""
+    n_text, n_vit_full, n_vit_keep, n_pack, n_tail, cap = sizes
+    BH = B * Hkv
+    segs, kh, vh, seg_id = [], [], [], []
+    # text (dense)
+    kt = rand_rows(seed + 1, BH, n_text, D, dtype, outliers=(5,))
+    vt = rand_rows(seed + 2, BH, n_text, D, dtype)
+    segs.append(uc.dense_segment(dev(kt, dtype).reshape(B, Hkv, n_text, D),
+                                 dev(vt, dtype).reshape(B, Hkv, n_text, D)))
+    kh.append(ref.widen(kt, dtype)); vh.append(ref.widen(vt, dtype))
+    # compacted eviction survivors
+    kv_full = rand_rows(seed + 3, BH, n_vit_full, D, dtype, outliers=(5,))
+    vv_full = rand_rows(seed + 4, BH, n_vit_full, D, dtype)
+    rng = np.random.default_rng(seed)
+    idx = np.sort(np.stack([rng.choice(n_vit_full, n_vit_keep, replace=False) for _ in range(BH)]), 1)
+    kc = np.stack([kv_full[i][idx[i]] for i in range(BH)])
+    vc = np.stack([vv_full[i][idx[i]] for i in range(BH)])
+    segs.append(uc.dense_segment(dev(kc, dtype).reshape(B, Hkv, n_vit_keep, D),
+                                 dev(vc, dtype).reshape(B, Hkv, n_vit_keep, D),
+                                 idx=torch.from_numpy(idx.astype(np.int32)).cuda()))
+    kh.append(ref.widen(kc, dtype)); vh.append(ref.widen(vc, dtype))
+    # packed
+    kp = rand_rows(seed + 5, BH, n_pack, D, dtype, 2.0, outliers=(5,))
+    vp = rand_rows(seed + 6, BH, n_pack, D, dtype)
+    hb = [bits] * BH if not per_head else [4 if (i % 3) else 2 for i in range(BH)]
+    pk = ref.quantize(kp, vp, dtype, G, hb)
+    segs.append(packed_from_oracle(B, Hkv, n_pack, D, G, dtype, pk, per_head=per_head))
+    khp, vhp = ref.dequant(pk, n_pack, D, G, dtype)
+    kh.append(khp); vh.append(vhp)
+    # dense tail with spare capacity
+    ktl = rand_rows(seed + 7, BH, cap, D, dtype)
+    vtl = rand_rows(seed + 8, BH, cap, D, dtype)
+    segs.append(uc.dense_segment(dev(ktl, dtype).reshape(B, Hkv, cap, D),
+                                 dev(vtl, dtype).reshape(B, Hkv, cap, D), n_rows=n_tail))
+    kh.append(ref.widen(ktl[:, :n_tail], dtype)); vh.append(ref.widen(vtl[:, :n_tail], dtype))
+    for a, n in enumerate([n_text, n_vit_keep, n_pack, n_tail]):
+        seg_id += [a] * n
+    K = np.concatenate(kh, axis=1).reshape(B, Hkv, -1, D)
+    V = np.concatenate(vh, axis=1).reshape(B, Hkv, -1, D)
+    return segs, K, V, np.asarray(seg_id, np.int32)
+
+
+ACASES = [
+    # B, Hq, Hkv, D, dtype, q dtype, M, sizes
+    (1, 4, 1, 64, "f32", "f32", 1, (64, 256, 51, 256, 0, 4)),
+    (2, 28, 4, 128, "bf16", "bf16", 1, (512, 4096, 406, 4096 + 17, 5, 16)),
+    (2, 28, 4, 128, "bf16", "bf16", 7, (100, 900, 300, 1000, 3, 8)),
+    (1, 8, 2, 64, "f16", "f16", 3, (33, 200, 77, 130, 1, 2)),
+    (1, 14, 2, 128, "bf16", "bf16", 1, (0, 700, 1, 63, 2, 2)),   # empty text, tail-only pack
+]
+
+
+@pytest.mark.parametrize("case", ACASES, ids=[f"a{i}" for i in range(len(ACASES))])
+def test_attend_parity(case):
+    B, Hq, Hkv, D, dtype, qdt, M, sizes = case
+    _print_case(test="attend", B=B, Hq=Hq, Hkv=Hkv, D=D, dtype=dtype, M=M, sizes=sizes)
+    segs, K, V, seg_id = _mixed_case(B, Hq, Hkv, D, dtype, sizes, seed=D + M)
+    q = rand_rows(99, B * Hq, M, D, qdt).reshape(B, Hq, M, D)
+    sm = sm_scale(D)
+    o_ref, lse_ref, sl_ref, _ = ref.attend(ref.widen(q, qdt), K, V, None, seg_id, 4, sm)
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    qd = dev(q, qdt)
+    o = torch.empty(B, Hq, M, D, device="cuda")
+    lse = torch.empty(B, Hq, M, device="cuda")
+    sl = torch.empty(B, Hq, M, 4, device="cuda")
+    uc.uc_attend_mixed(shape, segs, qd, M, sm, o, lse, sl)
+    torch.cuda.synchronize()
+    check_attention(o.cpu().numpy(), o_ref, "o")
+    assert np.allclose(lse.cpu().numpy(), lse_ref, rtol=1e-5, atol=1e-4)
+    slg = sl.cpu().numpy()
+    fin = np.isfinite(sl_ref)
+    assert np.array_equal(np.isfinite(slg), fin)
+    assert np.allclose(slg[fin], sl_ref[fin], rtol=1e-5, atol=1e-4)
+
+
+def test_attend_full_budget_equals_uncompressed():
+    """A 100%-budget eviction segment (all rows kept) plus 16-bit rows is exact
+    attention over the original sequence."""
+    B, Hq, Hkv, D, N = 2, 28, 4, 128, 1000
+    BH = B * Hkv
+    k = rand_rows(1, BH, N, D, "bf16", outliers=(7,))
+    v = rand_rows(2, BH, N, D, "bf16")
+    q = rand_rows(3, B * Hq, 1, D, "bf16").reshape(B, Hq, 1, D)
+    scores = torch.rand(BH, N, device="cuda")
+    keep = torch.empty(BH, N, dtype=torch.int32, device="cuda")
+    kd, vd = dev(k, "bf16"), dev(v, "bf16")
+    kc, vc = torch.empty_like(kd), torch.empty_like(vd)
+    uc.uc_select_keep(scores, N, 0, keep, kd, vd, kc, vc)
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    o1 = torch.empty(B, Hq, 1, D, device="cuda")
+    o2 = torch.empty_like(o1)
+    uc.uc_attend_mixed(shape, [uc.dense_segment(kd.reshape(B, Hkv, N, D), vd.reshape(B, Hkv, N, D))],
+                       dev(q, "bf16"), 1, sm_scale(D), o1)
+    uc.uc_attend_mixed(shape, [uc.dense_segment(kc.reshape(B, Hkv, N, D), vc.reshape(B, Hkv, N, D))],
+                       dev(q, "bf16"), 1, sm_scale(D), o2)
+    torch.cuda.synchronize()
+    assert np.array_equal(keep.cpu().numpy(), np.tile(np.arange(N, dtype=np.int32), (BH, 1)))
+    assert torch.equal(o1, o2)
+    o_ref = ref.attend(ref.widen(q, "bf16"), ref.widen(k, "bf16").reshape(B, Hkv, N, D),
+                       ref.widen(v, "bf16").reshape(B, Hkv, N, D), None, np.zeros(N, np.int32), 1,
+                       sm_scale(D))[0]
+    check_attention(o1.cpu().numpy(), o_ref, "full budget")
+
+
+# ------------------------------------------------------------------ scoring
+
+@pytest.mark.parametrize("B,Hq,Hkv,D,dtype,W,sizes", [
+    (1, 4, 1, 64, "f32", 16, (64, 256, 256)),
+    (2, 28, 4, 128, "bf16", 32, (512, 4096, 0)),
+    (1, 14, 2, 128, "bf16", 5, (100, 333, 70)),
+])
+def test_score_parity(B, Hq, Hkv, D, dtype, W, sizes):
+    _print_case(test="score", B=B, Hq=Hq, Hkv=Hkv, D=D, dtype=dtype, W=W, sizes=sizes)
+    BH = B * Hkv
+    ks, vs, segs, seg_id = [], [], [], []
+    for a, n in enumerate(sizes):
+        k = rand_rows(20 + a, BH, n, D, dtype, outliers=(2, 9))
+        v = rand_rows(30 + a, BH, n, D, dtype)
+        ks.append(k); vs.append(v)
+        segs.append(uc.dense_segment(dev(k, dtype).reshape(B, Hkv, n, D),
+                                     dev(v, dtype).reshape(B, Hkv, n, D)))
+        seg_id += [a] * n
+    q = rand_rows(40, B * Hq, W, D, dtype).reshape(B, Hq, W, D)
+    K = np.concatenate([ref.widen(k, dtype) for k in ks], axis=1).reshape(B, Hkv, -1, D)
+    sc_ref, ms_ref = ref.score64(ref.widen(q, dtype), K, np.asarray(seg_id, np.int32), len(sizes),
+                                 sm_scale(D))
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    outs = [torch.empty(B, Hkv, n, device="cuda") for n in sizes]
+    mass = torch.empty(B, Hkv, len(sizes), device="cuda")
+    uc.uc_score_importance(shape, segs, dev(q, dtype), W, sm_scale(D), outs, mass)
+    torch.cuda.synchronize()
+    got = np.concatenate([o.cpu().numpy().reshape(B, Hkv, -1) for o in outs], axis=2).astype(np.float64)
+    rel = np.abs(got - sc_ref) / np.maximum(sc_ref, 1e-12)
+    tot = Hq // Hkv * W
+    # per-row probability mass is resolved to ~1e-6 of the row total
+    assert np.all(np.abs(got - sc_ref) <= 2e-5 * sc_ref + 1e-7 * tot), rel.max()
+    assert np.allclose(mass.cpu().numpy(), ms_ref, rtol=2e-5, atol=1e-6 * tot)
+    assert np.allclose(got.sum(axis=2), tot, rtol=1e-5)
+
+
+def test_segment_mass_from_attention():
+    B, Hq, Hkv, D, M = 2, 28, 4, 128, 9
+    segs, K, V, seg_id = _mixed_case(B, Hq, Hkv, D, "bf16", (64, 400, 100, 256, 3, 8), seed=3)
+    q = rand_rows(7, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+    _, _, _, smass = ref.attend(ref.widen(q, "bf16"), K, V, None, seg_id, 4, sm_scale(D))
+    want = smass.reshape(B, Hkv, Hq // Hkv, M, 4).sum(axis=(2, 3))
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    o = torch.empty(B, Hq, M, D, device="cuda")
+    lse = torch.empty(B, Hq, M, device="cuda")
+    sl = torch.empty(B, Hq, M, 4, device="cuda")
+    uc.uc_attend_mixed(shape, segs, dev(q, "bf16"), M, sm_scale(D), o, lse, sl)
+    mass = torch.empty(B, Hkv, 4, device="cuda")
+    uc.uc_segment_mass(shape, M, 4, lse, sl, mass)
+    torch.cuda.synchronize()
+    assert np.allclose(mass.cpu().numpy(), want, rtol=1e-4, atol=1e-5)
+
+
+def test_append_rows():
+    B, Hkv, D, cap = 2, 4, 128, 8
+    shape = uc.make_shape(B, 28, Hkv, D)
+    k = torch.zeros(B, Hkv, cap, D, dtype=torch.bfloat16, device="cuda")
+    v = torch.zeros_like(k)
+    seg = uc.dense_segment(k, v, n_rows=0)
+    for t in range(3):
+        kn = torch.randn(B, Hkv, 1, D, device="cuda").to(torch.bfloat16)
+        vn = torch.randn(B, Hkv, 1, D, device="cuda").to(torch.bfloat16)
+        uc.uc_append_rows(shape, kn, vn, 1, seg, t)
+        torch.cuda.synchronize()
+        assert torch.equal(k[:, :, t], kn[:, :, 0]) and torch.equal(v[:, :, t], vn[:, :, 0])
+    assert not k[:, :, 3:].any()
