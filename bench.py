@@ -1,0 +1,246 @@
+"""Benchmark: mixed-policy KV decode attention at 64k context on one MI355X.
+
+One timed step is one pass of the whole hot path over one batch of the
+64k-context long-document workload (batch 16, 28 query / 4 KV heads, head dim
+128, bf16; 4096 text + 15 x 4096 ViT tokens under a 5x storage budget):
+  importance scoring over the full context (observation window 32),
+  top-k eviction + compaction of the ViT segment (11735 rows per KV head),
+  4-bit group quantization of the text segment (group 64),
+  512 decode steps, each appending the step's K/V to the protected tail and
+  attending over text (packed) + ViT (compacted) + tail.
+value = decoded tokens per second of that whole job (B * 512 per step).
+Inputs are synthetic (seeded), resident in HBM before timing starts.
+
+The roofline object covers the decode attention call (the dominant kernel
+pair: matrix-core split-K pass + log-sum-exp combine), timed with HIP events
+on the stream it runs on, against the 8 TB/s HBM peak; cpu_baseline times the
+CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "mixed-policy KV decode attention tokens/s and achieved HBM GB/s @64k ctx"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5, help="timed jobs")
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--decode-steps", type=int, default=None,
+                    help="decode steps per job (default: the workload's 512)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-heads", type=int, default=16)
+    ap.add_argument("--cpu-sample-steps", type=int, default=8)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="after the run, copy a 1 GiB device buffer 3 times (a plain copy "
+                         "kernel of known size, for scaling HBM byte counters)")
+    return ap.parse_args()
+
+
+def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
+    """Time the CPU oracle on n_heads KV heads (full 64k context, full
+    compression) and n_steps decode steps; extrapolate linearly to the whole
+    job (all B*Hkv heads, T steps) and express it in decode tokens/s."""
+    import numpy as np
+
+    import oracle as ref
+    import workloads as gen
+
+    cores = ref.set_threads(0)
+    D, G = w.D, w.group_size
+    nb = max(1, n_heads // w.Hkv)
+    BHs = nb * w.Hkv
+    sm = float(np.float32(1.0 / np.sqrt(D)))
+    pols = None
+    import oracle.pipeline as op
+    pols = op.plan(w)
+    text, vit = 0, 1
+    t0 = time.perf_counter()
+    kt = gen.segment_kv(w, text, "k", 0, BHs)
+    vt = gen.segment_kv(w, text, "v", 0, BHs)
+    kv_ = gen.segment_kv(w, vit, "k", 0, BHs)
+    vv_ = gen.segment_kv(w, vit, "v", 0, BHs)
+    q_obs = gen.queries(w, gen.T_QOBS, w.W, bh0=0, nbh=nb * w.Hq)
+    qd = gen.queries(w, gen.T_QDEC, n_steps, bh0=0, nbh=nb * w.Hq)
+    kd = gen.decode_kv(w, "k", 0, n_steps, 0, BHs)
+    vd = gen.decode_kv(w, "v", 0, n_steps, 0, BHs)
+    t_gen = time.perf_counter() - t0
+
+    t0 = time.perf_counter()
+    n_t, n_v = w.segments[text].n, w.segments[vit].n
+    K = np.concatenate([ref.widen(kt, "bf16"), ref.widen(kv_, "bf16")], axis=1).reshape(nb, w.Hkv, -1, D)
+    seg = np.concatenate([np.zeros(n_t, np.int32), np.ones(n_v, np.int32)])
+    sc, _ = ref.score(ref.widen(q_obs, "bf16").reshape(nb, w.Hq, w.W, D), K, seg, 2, sm)
+    keep = ref.select(sc.reshape(BHs, -1)[:, n_t:], pols[vit]["k"], 0)
+    pk = ref.quantize(kt, vt, "bf16", pols[text]["group"], [pols[text]["bits"]] * BHs)
+    kh, vh = ref.dequant(pk, n_t, D, pols[text]["group"], "bf16")
+    t_compress = time.perf_counter() - t0
+
+    present = np.zeros((BHs, n_v), np.uint8)
+    for i in range(BHs):
+        present[i, keep[i]] = 1
+    Kl = np.concatenate([kh, ref.widen(kv_, "bf16")], axis=1)
+    Vl = np.concatenate([vh, ref.widen(vv_, "bf16")], axis=1)
+    del K
+    t_att = 0.0
+    for t in range(n_steps):
+        Kt = np.concatenate([Kl, ref.widen(kd[:, : t + 1], "bf16")], axis=1).reshape(nb, w.Hkv, -1, D)
+        Vt = np.concatenate([Vl, ref.widen(vd[:, : t + 1], "bf16")], axis=1).reshape(nb, w.Hkv, -1, D)
+        pr = np.concatenate([np.ones((BHs, n_t), np.uint8), present, np.ones((BHs, t + 1), np.uint8)],
+                            axis=1).reshape(nb, w.Hkv, -1)
+        segs = np.concatenate([seg, np.full(t + 1, 2, np.int32)])
+        q = ref.widen(qd[:, t:t + 1], "bf16").reshape(nb, w.Hq, 1, D)
+        t0 = time.perf_counter()
+        ref.attend(q, Kt, Vt, pr, segs, 3, sm)
+        t_att += time.perf_counter() - t0
+    scale = (w.B * w.Hkv) / BHs
+    t_job = (t_compress + t_att / n_steps * T) * scale
+    return {
+        "value": round(w.B * T / t_job, 3),
+        "unit": "tokens/s",
+        "cores": int(cores),
+        "kind": "oracle",
+        "sample": (f"{BHs} of {w.B * w.Hkv} KV heads at full 65536-token context: "
+                   f"scoring + selection + quantization ({t_compress:.2f} s) and "
+                   f"{n_steps} of {T} decode steps ({t_att:.2f} s), extrapolated "
+                   f"linearly to all heads and steps"),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the path would shard over (b, h_kv) with no exchange, see the design notes)",
+              file=sys.stderr, flush=True)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import paper_2609_32831_amd as uc
+    import workloads as gen
+    from paper_2609_32831_amd.runner import Run
+    from workloads.device import device_inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    w = gen.CFG5
+    T = w.steps if args.decode_steps is None else args.decode_steps
+    t0 = time.perf_counter()
+    inp = device_inputs(w, "cuda", steps=T)
+    run = Run(w, inp)
+    torch.cuda.synchronize()
+    print(f"# inputs ready in {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    o = torch.empty(T, w.B, w.Hq, 1, w.D, device="cuda")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(T)]
+    ev_c = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+
+    def job(record: bool):
+        if record:
+            ev_c[0].record(stream)
+        run.compress()
+        if record:
+            ev_c[1].record(stream)
+        for t in range(T):
+            uc.uc_append_rows(run.shape, inp["k_dec"][t], inp["v_dec"][t], 1, run.tail, t)
+            run.tail.n_rows = t + 1
+            if record:
+                ev[t][0].record(stream)
+            uc.uc_attend_mixed(run.shape, run.mixed, inp["q_dec"][t], 1, run.sm, o[t],
+                               ws=run.ws_attend)
+            if record:
+                ev[t][1].record(stream)
+
+    for _ in range(args.warmup):
+        job(False)
+    torch.cuda.synchronize()
+    print("# warmup done", file=sys.stderr, flush=True)
+    attend_ms = 0.0
+    compress_ms = 0.0
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record(stream)
+    for k in range(args.steps):
+        job(True)
+        torch.cuda.synchronize()
+        attend_ms += sum(a.elapsed_time(b) for a, b in ev)
+        compress_ms += ev_c[0].elapsed_time(ev_c[1])
+        print(f"# job {k + 1}/{args.steps} done", file=sys.stderr, flush=True)
+    end.record(stream)
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(end)
+    ms_per_step = total_ms / args.steps
+    tokens = w.B * T
+    value = tokens / (ms_per_step / 1e3)
+    att_us = attend_ms / (args.steps * T) * 1e3
+    # algorithmic bytes per attend call, averaged over the tail lengths 1..T
+    avg_bytes = sum(run.attended_bytes(t + 1) for t in range(T)) / T
+    achieved = avg_bytes / (att_us * 1e-6) / 1e9
+    traffic = None
+    tp = os.path.join(ROOT, "profiles", "decode_attend_64k_traffic.json")
+    if os.path.exists(tp):
+        try:
+            with open(tp) as f:
+                tr = json.load(f)
+            from paper_2609_32831_amd.build import source_digest
+            if tr.get("source_digest") == source_digest():
+                traffic = tr.get("traffic_bytes_per_launch")
+        except Exception:  # stale or unreadable counters: report none
+            traffic = None
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "long_context_64k", "batch": w.B, "q_heads": w.Hq,
+                   "kv_heads": w.Hkv, "head_dim": w.D, "context": w.n_context,
+                   "segments": "text 4096 int4 g64 | vit 61440 -> 11735 kept per kv head | "
+                               "protected decode tail", "budget": "5x",
+                   "decode_steps": T, "observation_window": w.W},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": traffic,
+                     "kernel": "uc_attend_mixed decode (decode_mfma_kernel + attend_combine_kernel)",
+                     "avg_launch_us": round(att_us, 2),
+                     "algorithmic_bytes_per_launch": int(avg_bytes)},
+        "decode_only_tokens_per_s": round(w.B / (att_us * 1e-6), 1),
+        "compress_ms": round(compress_ms / args.steps, 3),
+    }
+    if args.calibrate_copy:
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    if not args.no_cpu_baseline:
+        t0 = time.perf_counter()
+        out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_heads, args.cpu_sample_steps, T)
+        print(f"# cpu baseline took {time.perf_counter() - t0:.1f} s", file=sys.stderr, flush=True)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

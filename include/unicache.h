@@ -229,6 +229,9 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs,
                           float sm_scale, float* o, float* lse, float* seg_lse,
                           void* ws, size_t ws_bytes, void* stream);
 
+/* Workspace bytes for uc_attend_mixed.  The value never decreases when a
+ * segment gains rows, so a workspace sized for the largest row counts (say a
+ * decode tail at full capacity) serves every call with fewer rows. */
 size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs,
                                 int n_segs, uc_dtype q_dt, int M);
 
@@ -291,6 +294,16 @@ uc_status uc_type_budget(int n_types, const double* mass, const double* b_prev,
  * requires 0 < rho_min <= rho_init <= 1 and M_0 > 0; returns NAN otherwise. */
 double uc_retention_next(double rho, double rho_init, double rho_min,
                          double M_c, double M_0);
+
+/* ------------------------------------------------------------------------ */
+/* Kernel path selection for uc_attend_mixed (process-wide; for cross-checks):
+ * UC_PATH_AUTO (default) uses the matrix-core kernels where the inputs allow
+ * (bf16 rows and queries, D = 128, at most 16 query rows per KV head for
+ * decode), UC_PATH_VALU forces the vector-ALU kernels for every input.
+ * Returns the previous setting, or -1 for an unknown value. */
+#define UC_PATH_AUTO 0
+#define UC_PATH_VALU 1
+int uc_set_path(int path);
 
 /* ------------------------------------------------------------------------ */
 const char* uc_status_string(uc_status s);

@@ -21,6 +21,7 @@ UC_OK, UC_E_INVALID, UC_E_UNSUPPORTED, UC_E_WORKSPACE, UC_E_DEVICE = range(5)
 UC_F32, UC_F16, UC_BF16 = 0, 1, 2
 UC_SEG_DENSE, UC_SEG_PACKED = 0, 1
 UC_MAX_SEGMENTS = 8
+UC_PATH_AUTO, UC_PATH_VALU = 0, 1
 
 TORCH_DT = {torch.float32: UC_F32, torch.float16: UC_F16, torch.bfloat16: UC_BF16}
 DT_TORCH = {v: k for k, v in TORCH_DT.items()}
@@ -80,6 +81,7 @@ def _load():
         "uc_retention_next": (dbl, [dbl, dbl, dbl, dbl, dbl]),
         "uc_status_string": (ctypes.c_char_p, [i32]),
         "uc_last_error": (ctypes.c_char_p, []),
+        "uc_set_path": (i32, [i32]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -320,3 +322,9 @@ def uc_status_string(s: int) -> str:
 
 def uc_last_error() -> str:
     return lib.uc_last_error().decode()
+
+
+def uc_set_path(path: int) -> int:
+    """UC_PATH_AUTO (matrix cores where eligible) or UC_PATH_VALU; returns the
+    previous setting."""
+    return int(lib.uc_set_path(path))

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <vector>
 
 #include "uc_common.h"
@@ -25,6 +26,7 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
 namespace {
 
 thread_local char g_err[512] = "";
+std::atomic<int> g_path{UC_PATH_AUTO};
 
 uc_status fail(uc_status s, const char* fmt, ...) {
   va_list ap;
@@ -153,14 +155,23 @@ ChunkPlan make_plan(const KSegs& ks, int rows_min, int max_chunks_per_seg) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// generic attention: partial stride per (query row, chunk)
-size_t generic_ws(const uc_shape& sh, const ChunkPlan& p, int M, bool want_o) {
+// Generic attention partials: one (m, l[, o]) per (query row, chunk).  The
+// size is a bound on the chunks of any plan for these segments or for
+// segments with fewer rows (min(max_chunks, ceil(n / rows_min)) per segment),
+// so a workspace sized at the largest row counts serves smaller ones.
+constexpr int kAttRows = 256, kAttMaxChunks = 64, kLseRows = 512, kLseMaxChunks = 32;
+
+size_t generic_ws(const uc_shape& sh, const KSegs& ks, int rows_min, int max_chunks, int M,
+                  bool want_o) {
+  size_t chunks = 0;
+  for (int i = 0; i < ks.n; ++i)
+    chunks += std::min<size_t>(max_chunks, (ks.s[i].n_rows + rows_min - 1) / rows_min);
   const size_t stride = want_o ? (size_t)sh.D + 2 : 2;
-  return align256((size_t)sh.B * sh.Hq * M * p.n_chunks * stride * sizeof(float));
+  return align256((size_t)sh.B * sh.Hq * M * chunks * stride * sizeof(float));
 }
 
-ChunkPlan attend_plan(const KSegs& ks) { return make_plan(ks, 256, 64); }
-ChunkPlan score_lse_plan(const KSegs& ks) { return make_plan(ks, 512, 32); }
+ChunkPlan attend_plan(const KSegs& ks) { return make_plan(ks, kAttRows, kAttMaxChunks); }
+ChunkPlan score_lse_plan(const KSegs& ks) { return make_plan(ks, kLseRows, kLseMaxChunks); }
 ChunkPlan score_col_plan(const KSegs& ks) { return make_plan(ks, 256, 1 << 20); }
 
 uc_status launched(hipError_t e) {
@@ -185,13 +196,19 @@ const char* uc_status_string(uc_status s) {
 
 const char* uc_last_error(void) { return g_err; }
 
+int uc_set_path(int path) {
+  if (path != UC_PATH_AUTO && path != UC_PATH_VALU) return -1;
+  return g_path.exchange(path);
+}
+
 // ---------------------------------------------------------------- attention
 size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs, int n_segs,
                                 uc_dtype q_dt, int M) {
   KSegs ks;
   if (check_segments(shape, segs, n_segs, ks) || M < 1 || !dtype_ok(q_dt)) return 0;
-  if (decode_mfma_eligible(*shape, ks, q_dt, M)) return decode_mfma_workspace(*shape, ks, M);
-  return generic_ws(*shape, attend_plan(ks), M, true);
+  if (g_path.load() == UC_PATH_AUTO && decode_mfma_eligible(*shape, ks, q_dt, M))
+    return decode_mfma_workspace(*shape, ks, M);
+  return generic_ws(*shape, ks, kAttRows, kAttMaxChunks, M, true);
 }
 
 uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_segs,
@@ -206,14 +223,14 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
   if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
   if ((int64_t)shape->B * shape->Hq * M > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
   hipStream_t s = (hipStream_t)stream;
-  if (decode_mfma_eligible(*shape, ks, q_dt, M)) {
+  if (g_path.load() == UC_PATH_AUTO && decode_mfma_eligible(*shape, ks, q_dt, M)) {
     const size_t need = decode_mfma_workspace(*shape, ks, M);
     if (ws_bytes < need || (need && !ws))
       return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
     return launched(launch_decode_mfma(*shape, ks, q, M, sm_scale, o, lse, seg_lse, ws, s));
   }
   const ChunkPlan p = attend_plan(ks);
-  const size_t need = generic_ws(*shape, p, M, true);
+  const size_t need = generic_ws(*shape, ks, kAttRows, kAttMaxChunks, M, true);
   if (ws_bytes < need || !ws) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   float* partial = (float*)ws;
   hipError_t e = launch_attend_generic(*shape, ks, p, q, q_dt, M, sm_scale, partial, true, s);
@@ -224,7 +241,7 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
 // ---------------------------------------------------------------- scoring
 static void score_ws_parts(const uc_shape& sh, const KSegs& ks, int W, size_t& part1,
                            size_t& lse_b, size_t& mass_b) {
-  part1 = generic_ws(sh, score_lse_plan(ks), W, false);
+  part1 = generic_ws(sh, ks, kLseRows, kLseMaxChunks, W, false);
   lse_b = align256((size_t)sh.B * sh.Hq * W * sizeof(float));
   mass_b = align256((size_t)sh.B * sh.Hkv * score_col_plan(ks).n_chunks * sizeof(double));
 }

@@ -143,12 +143,16 @@ __global__ __launch_bounds__(256) void attend_generic_kernel(KSegs segs, ChunkPl
   }
 }
 
-// One wave per query row: merge the chunk partials of that row.
+// One wave per query row: merge the chunk partials (m, l, o) of that row by
+// log-sum-exp.  Lane = (record group rg = lane / 16, dims (lane % 16) * D/16
+// ...): a lane reads every fourth record's slice of o with independent
+// loads, and the four record groups are summed with cross-lane exchanges.
+// Records with m = -inf hold no rows (their o is not read).
 template <int D>
 __global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int nseg, int ps,
                                                             const float* __restrict__ partial,
                                                             float* o, float* lse, float* seg_lse) {
-  constexpr int PER = D / 64;
+  constexpr int PD = D / 16;  // dims per lane
   const int64_t qi = blockIdx.x;
   const int lane = threadIdx.x;
   const int C = plan.n_chunks;
@@ -159,7 +163,7 @@ __global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int 
   float L = 0.0f;
   for (int c = lane; c < C; c += 64) {
     const float* pc = P + (int64_t)c * ps;
-    L += pc[1] * exp2f(pc[0] - mall);
+    if (pc[0] != -INFINITY) L += pc[1] * exp2f(pc[0] - mall);
   }
   L = wave_sum(L);
   if (lse && lane == 0) lse[qi] = (mall + log2f(L)) * kLn2;
@@ -171,25 +175,38 @@ __global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int 
       ma = wave_max(ma);
       for (int c = plan.first[a] + lane; c < plan.first[a + 1]; c += 64) {
         const float* pc = P + (int64_t)c * ps;
-        la += pc[1] * exp2f(pc[0] - ma);
+        if (pc[0] != -INFINITY) la += pc[1] * exp2f(pc[0] - ma);
       }
       la = wave_sum(la);
       if (lane == 0) seg_lse[qi * nseg + a] = la > 0.0f ? (ma + log2f(la)) * kLn2 : -INFINITY;
     }
   }
   if (o) {
-    float acc[PER];
+    const int rg = lane >> 4, d0 = (lane & 15) * PD;
+    float acc[PD];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) acc[i] = 0.0f;
-    for (int c = 0; c < C; ++c) {
+    for (int i = 0; i < PD; ++i) acc[i] = 0.0f;
+#pragma unroll 4
+    for (int c = rg; c < C; c += 4) {
       const float* pc = P + (int64_t)c * ps;
-      const float w = exp2f(pc[0] - mall);
+      const float m = pc[0];
+      if (m == -INFINITY) continue;
+      const float w = exp2f(m - mall);
 #pragma unroll
-      for (int i = 0; i < PER; ++i) acc[i] = fmaf(w, pc[2 + lane + 64 * i], acc[i]);
+      for (int i = 0; i < PD; ++i) acc[i] = fmaf(w, pc[2 + d0 + i], acc[i]);
     }
     const float inv = 1.0f / L;
 #pragma unroll
-    for (int i = 0; i < PER; ++i) o[qi * D + lane + 64 * i] = acc[i] * inv;
+    for (int i = 0; i < PD; ++i) {
+      float v = acc[i];
+      v += __shfl_xor(v, 16, 64);
+      v += __shfl_xor(v, 32, 64);
+      acc[i] = v;
+    }
+    if (rg == 0) {
+#pragma unroll
+      for (int i = 0; i < PD; ++i) o[qi * D + d0 + i] = acc[i] * inv;
+    }
   }
 }
 

@@ -1,0 +1,153 @@
+"""Chained end-to-end parity on the five workloads: the GPU runs the whole
+hot path (scoring -> budget -> top-k eviction + compaction -> quantization ->
+decode append + attention, or prefill attention) at the workload's real
+sizes in the launch configuration the benchmark times; the oracle recomputes
+sampled KV heads and steps from the same seeded inputs.
+
+Bars: codes, scales and minima bit-exact; kept sets equal except rows whose
+oracle score lies within 1e-6 * max(1, tau) of the cut tau (their count must
+still be exact); scores within the double-accumulation tolerance; attention
+within 2e-3 max-abs and 1e-3 relative L2 (fp32 output)."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import oracle.pipeline as op  # noqa: E402
+import workloads as gen  # noqa: E402
+from gpu_util import check_attention, host_bytes  # noqa: E402
+from paper_2609_32831_amd.runner import Run  # noqa: E402
+from workloads.device import device_inputs  # noqa: E402
+
+
+def _case(name, **kw):
+    print("CASE", name, " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+def _check_keep(gpu_keep, ref_keep, score64, k):
+    """Kept sets agree outside the tie band around the oracle's cut."""
+    assert gpu_keep.shape == (k,) and np.all(np.diff(gpu_keep) > 0)
+    s = np.asarray(score64, np.float64)
+    tau = np.sort(s)[::-1][k - 1] if k > 0 else np.inf
+    band = 1e-6 * max(1.0, abs(tau))
+    diff = np.setxor1d(gpu_keep, ref_keep)
+    assert np.all(np.abs(s[diff] - tau) <= band), (len(diff), np.abs(s[diff] - tau).max())
+    return len(diff)
+
+
+def _check_scores(gpu, ref64, total):
+    assert np.all(np.abs(gpu - ref64) <= 2e-5 * ref64 + 1e-7 * total), \
+        np.max(np.abs(gpu - ref64) / np.maximum(ref64, 1e-12))
+
+
+def _packed_equal(seg, pk, bh):
+    """Codes/scales/minima of one head of a GPU packed segment vs the oracle's."""
+    t = seg.t
+    n = pk["codes_k"].shape[0]
+    codes_per_head = n  # oracle quantised one head
+    off = bh * codes_per_head
+    assert np.array_equal(t["codes_k"][off:off + n].cpu().numpy(), pk["codes_k"])
+    assert np.array_equal(t["codes_v"][off:off + n].cpu().numpy(), pk["codes_v"])
+    B, Hkv = t["scale_k"].shape[:2]
+    for name in ("scale_k", "min_k", "scale_v", "min_v"):
+        g = t[name].reshape(B * Hkv, *t[name].shape[2:])[bh].cpu().numpy()
+        assert np.array_equal(g.view(np.uint32), pk[name][0].view(np.uint32)), name
+
+
+def _decode_chain(w, heads, steps):
+    inp = device_inputs(w, "cuda", steps=w.steps)
+    run = Run(w, inp)
+    run.compress()
+    T = w.steps
+    o = torch.empty(T, w.B, w.Hq, 1, w.D, device="cuda")
+    for t in range(T):
+        run.decode_step(t, o[t])
+    torch.cuda.synchronize()
+    pols = op.plan(w)
+    G = w.group_size
+    for (b, h) in heads:
+        _case(w.name, b=b, h=h)
+        bh = b * w.Hkv + h
+        hi = op.head_inputs(w, b, h, steps=T)
+        comp = op.compress_head(w, hi, pols)
+        start = 0
+        tot = G * w.W
+        for i, (s, p) in enumerate(zip(w.segments, pols)):
+            if p["kind"] == "evict":
+                gs = run.scores[i].reshape(w.B * w.Hkv, -1)[bh].cpu().numpy().astype(np.float64)
+                _check_scores(gs, comp["score64"][start:start + s.n], tot)
+                gk = run.keep[i][bh].cpu().numpy()[: p["k"]]
+                nd = _check_keep(gk, comp["keep"][i], comp["score64"][start:start + s.n], p["k"])
+                if nd:  # attend over the GPU's (equally valid) kept set
+                    pres = np.zeros(s.n, np.uint8)
+                    pres[gk] = 1
+                    comp["present"][i] = pres
+                # compacted rows are the kept rows, in order
+                rows = host_bytes(run.mixed[i].t["k"]).reshape(w.B * w.Hkv, -1, w.D)[bh, : p["k"]]
+                assert np.array_equal(rows, hi["seg_k"][i][gk])
+            elif p["kind"] == "quant":
+                _packed_equal(run.mixed[i], comp["packed"][i], bh)
+            start += s.n
+        gm = run.mass.reshape(w.B * w.Hkv, -1)[bh].cpu().numpy()
+        assert np.allclose(gm, comp["mass"], rtol=2e-5, atol=1e-6 * tot)
+        for t in steps:
+            o_ref, _, _, _ = op.attend_head(w, comp, hi["q_dec"][:, t:t + 1], w.q_dtype,
+                                            hi["k_dec"][: t + 1] if run.tail is not None else None,
+                                            hi["v_dec"][: t + 1] if run.tail is not None else None)
+            og = o[t, b, h * G:(h + 1) * G, 0].cpu().numpy()
+            check_attention(og, o_ref[:, 0], f"{w.name} b={b} h={h} t={t}")
+
+
+def test_cfg1_tiny_understanding():
+    _decode_chain(gen.CFG1, [(0, 0)], [0])
+
+
+def test_cfg2_understanding_7b():
+    _decode_chain(gen.CFG2, [(0, 0), (3, 3)], [0, 1, 255])
+
+
+def test_cfg5_long_context_64k():
+    _decode_chain(gen.CFG5, [(0, 0), (7, 2), (15, 3)], [0, 1, 200, 511])
+
+
+def test_cfg3_image_editing_prefill():
+    """Editing workload at full context sizes with a 512-query block (scoring
+    window = the block, as at the first full-KV step)."""
+    w = gen.scaled(gen.CFG3, W=512, M=512, steps=2)
+    inp = device_inputs(w, "cuda")
+    run = Run(w, inp)
+    q0 = inp["q_pre"](0)
+    run.score(q_obs=q0, W=w.M)
+    run.select()
+    run.quantize()
+    outs = []
+    for t in range(w.steps):
+        o = torch.empty(w.B, w.Hq, w.M, w.D, device="cuda")
+        run.prefill_step(inp["q_pre"](t), o)
+        outs.append(o)
+    torch.cuda.synchronize()
+    pols = op.plan(w)
+    G = w.group_size
+    for (b, h) in [(0, 0), (1, 3)]:
+        _case(w.name, b=b, h=h)
+        bh = b * w.Hkv + h
+        hi = op.head_inputs(w, b, h)
+        hi["q_obs"] = gen.queries(w, gen.T_QPRE, w.M, bh0=b * w.Hq + h * G, nbh=G, step=0)
+        comp = op.compress_head(w, hi, pols)
+        vit = 1
+        gk = run.keep[vit][bh].cpu().numpy()[: pols[vit]["k"]]
+        s64 = comp["score64"][w.segments[0].n: w.segments[0].n + w.segments[1].n]
+        if _check_keep(gk, comp["keep"][vit], s64, pols[vit]["k"]):
+            pres = np.zeros(w.segments[1].n, np.uint8)
+            pres[gk] = 1
+            comp["present"][vit] = pres
+        _packed_equal(run.mixed[2], comp["packed"][2], bh)
+        for t in range(w.steps):
+            q = gen.queries(w, gen.T_QPRE, w.M, bh0=b * w.Hq + h * G, nbh=G, step=t)
+            o_ref, _, _, _ = op.attend_head(w, comp, q, w.q_dtype)
+            og = outs[t][b, h * G:(h + 1) * G].cpu().numpy()
+            check_attention(og, o_ref, f"{w.name} b={b} h={h} t={t}")

@@ -271,3 +271,52 @@ def test_append_rows():
         torch.cuda.synchronize()
         assert torch.equal(k[:, :, t], kn[:, :, 0]) and torch.equal(v[:, :, t], vn[:, :, 0])
     assert not k[:, :, 3:].any()
+
+
+# ------------------------------------------------------------------ matrix-core decode
+
+DCASES = [
+    # B, Hq, Hkv, M, G, bits, per_head, sizes (text, vit_full, vit_keep, pack, tail, cap)
+    (2, 28, 4, 1, 64, 4, False, (512, 4096, 406, 4096, 7, 16)),
+    (2, 28, 4, 2, 32, 4, False, (77, 3000, 1111, 4096 + 33, 1, 4)),
+    (1, 28, 4, 1, 16, 2, True, (300, 900, 333, 1000, 3, 8)),
+    (1, 28, 4, 1, 128, 8, False, (31, 700, 129, 5000, 2, 2)),
+    (1, 16, 1, 1, 8, 4, True, (1, 64, 33, 520, 1, 1)),
+    (2, 14, 2, 1, 64, 4, False, (4096, 61440 // 8, 1467, 4096, 511, 512)),
+    (2, 28, 4, 1, 64, 2, False, (300, 2000, 512, 1000, 17, 32)),
+    (1, 28, 4, 2, 128, 4, False, (0, 100, 3, 130, 0, 4)),
+]
+
+
+@pytest.mark.parametrize("case", DCASES, ids=[f"d{i}" for i in range(len(DCASES))])
+def test_decode_mfma_parity(case):
+    B, Hq, Hkv, M, G, bits, per_head, sizes = case
+    _print_case(test="decode_mfma", B=B, Hq=Hq, Hkv=Hkv, M=M, G=G, bits=bits, sizes=sizes)
+    D = 128
+    segs, K, V, seg_id = _mixed_case(B, Hq, Hkv, D, "bf16", sizes, seed=G + bits, G=G,
+                                     bits=bits, per_head=per_head)
+    q = rand_rows(77, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+    sm = sm_scale(D)
+    o_ref, lse_ref, sl_ref, _ = ref.attend(ref.widen(q, "bf16"), K, V, None, seg_id, 4, sm)
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    qd = dev(q, "bf16")
+    outs = {}
+    for path in (uc.UC_PATH_AUTO, uc.UC_PATH_VALU):
+        prev = uc.uc_set_path(path)
+        try:
+            o = torch.empty(B, Hq, M, D, device="cuda")
+            lse = torch.empty(B, Hq, M, device="cuda")
+            sl = torch.empty(B, Hq, M, 4, device="cuda")
+            uc.uc_attend_mixed(shape, segs, qd, M, sm, o, lse, sl)
+            torch.cuda.synchronize()
+            outs[path] = (o.cpu().numpy(), lse.cpu().numpy(), sl.cpu().numpy())
+        finally:
+            uc.uc_set_path(prev)
+    for path, (o, lse, sl) in outs.items():
+        check_attention(o, o_ref, f"path {path}")
+        assert np.allclose(lse, lse_ref, rtol=1e-5, atol=1e-4)
+        fin = np.isfinite(sl_ref)
+        assert np.array_equal(np.isfinite(sl), fin)
+        assert np.allclose(sl[fin], sl_ref[fin], rtol=1e-5, atol=1e-4)
+    # the two kernel paths agree far inside the bar
+    assert np.abs(outs[0][0] - outs[1][0]).max() < 5e-4
