@@ -44,7 +44,93 @@ def parse():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the run, copy a 1 GiB device buffer 3 times (a plain copy "
                          "kernel of known size, for scaling HBM byte counters)")
+    ap.add_argument("--summarize-profiles", metavar="DIR", default=None,
+                    help="no benchmark: read rocprofv3 output under DIR/trace (kernel trace "
+                         "stats), DIR/fetch and DIR/write (FETCH_SIZE / WRITE_SIZE counters of "
+                         "runs with --calibrate-copy) and write the summaries under profiles/")
+    ap.add_argument("--profile-command", default="",
+                    help="with --summarize-profiles: the commands that produced DIR (recorded)")
     return ap.parse_args()
+
+
+DECODE_KERNELS = ("decode_mfma_kernel", "attend_combine_kernel")
+COPY_BYTES = 1 << 30
+
+
+def _csv(path_glob):
+    import csv
+    import glob
+    files = sorted(glob.glob(path_glob, recursive=True))
+    if not files:
+        raise FileNotFoundError(path_glob)
+    with open(files[0]) as f:
+        return list(csv.DictReader(f))
+
+
+def summarize_profiles(d: str, command: str):
+    """Per-dispatch HBM bytes of the decode attention call from FETCH_SIZE /
+    WRITE_SIZE (KiB per dispatch), each scaled by the factor that makes the
+    counter read exactly 1 GiB for a plain 1 GiB device copy; plus the kernel
+    trace statistics.  Writes profiles/decode_attend_64k_traffic.json (read by
+    the benchmark while the library sources are unchanged) and a text summary."""
+    from paper_2609_32831_amd.build import source_digest
+
+    def per_kernel(rows, counter):
+        acc = {}
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return acc
+
+    out = {"source_digest": source_digest(), "command": command}
+    for counter, sub in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write")):
+        acc = per_kernel(_csv(os.path.join(d, sub, "**", "*counter_collection.csv")), counter)
+        copies = [max(v) for k, v in acc.items() if "copy" in k.lower()]
+        if not copies:
+            raise RuntimeError(f"{sub}: no copy kernel found (run with --calibrate-copy)")
+        factor = (COPY_BYTES / 1024.0) / max(copies)
+        out[f"{counter.lower()}_copy_kib"] = max(copies)
+        out[f"{counter.lower()}_factor"] = factor
+        for kn in DECODE_KERNELS:
+            vals = [v for k, vs in acc.items() if kn in k for v in vs]
+            out[f"{kn}_{counter.lower()}_kib_avg"] = sum(vals) / len(vals)
+            out[f"{kn}_dispatches"] = len(vals)
+    traffic = 0.0
+    for kn in DECODE_KERNELS:
+        traffic += (out[f"{kn}_fetch_size_kib_avg"] * out["fetch_size_factor"] +
+                    out[f"{kn}_write_size_kib_avg"] * out["write_size_factor"]) * 1024.0
+    out["traffic_bytes_per_launch"] = int(round(traffic))
+    stats = _csv(os.path.join(d, "trace", "**", "*kernel_stats.csv"))
+    lines = ["# Kernel statistics and HBM traffic of the 64k-context decode benchmark", "",
+             "Commands (rocprofv3 on one MI355X):", "", "```", command, "```", "",
+             "| kernel | calls | avg us | min us | max us | % |", "|---|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:10]:
+        name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0]
+        name = name.replace("void ", "").replace("uc::", "")
+        lines.append(f"| {name[:80]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.2f} |")
+    avg = {kn: next(float(r["AverageNs"]) / 1e3 for r in stats if kn in r["Name"])
+           for kn in DECODE_KERNELS}
+    out["avg_us"] = avg
+    lines += ["", f"decode attention call (sum of the two kernels' averages): "
+                  f"{sum(avg.values()):.2f} us", "",
+              "HBM bytes per dispatch (FETCH_SIZE x {:.4f}, WRITE_SIZE x {:.4f}; the factors make a "
+              "plain 1 GiB copy read 1 GiB):".format(out["fetch_size_factor"],
+                                                     out["write_size_factor"])]
+    for kn in DECODE_KERNELS:
+        fb = out[f"{kn}_fetch_size_kib_avg"] * out["fetch_size_factor"] * 1024
+        wb = out[f"{kn}_write_size_kib_avg"] * out["write_size_factor"] * 1024
+        lines.append(f"- {kn}: read {fb / 1e6:.2f} MB, written {wb / 1e6:.2f} MB "
+                     f"({out[f'{kn}_dispatches']} dispatches)")
+    lines.append(f"- per call: {out['traffic_bytes_per_launch'] / 1e6:.2f} MB")
+    os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
+    with open(os.path.join(ROOT, "profiles", "decode_attend_64k_traffic.json"), "w") as f:
+        json.dump(out, f, indent=1)
+    with open(os.path.join(ROOT, "profiles", "decode_attend_64k.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
@@ -119,6 +205,9 @@ def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
 
 def main():
     args = parse()
+    if args.summarize_profiles:
+        summarize_profiles(args.summarize_profiles, args.profile_command)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
               "(the path would shard over (b, h_kv) with no exchange, see the design notes)",

@@ -99,9 +99,12 @@ typedef struct {
  *
  * Packed segment (kind = UC_SEG_PACKED), N = n_rows, G = group,
  * n_full = G * floor(N / G), tail_len = N - n_full:
- *   bits      uniform code width in {2, 4, 8} used when head_bits is NULL.
+ *   bits      code width in {2, 4, 8}: the uniform width when head_bits is
+ *             NULL, else an upper bound on the per-head widths (the library
+ *             picks kernels from it).
  *   head_bits optional device uint8 [B*Hkv]: per-(b, h_kv) code width in
- *             {2, 4, 8}; then code_off is required.
+ *             {2, 4, 8}, at most bits; then code_off is required.  Heads
+ *             whose entry breaks this get NaN attention outputs.
  *   code_off  device int64 [B*Hkv]: byte offset of each (b, h_kv)'s codes in
  *             codes_k / codes_v, a multiple of 16.  NULL (with head_bits NULL)
  *             means (b*Hkv + h) * n_full * D * bits / 8.

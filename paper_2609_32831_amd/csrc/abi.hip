@@ -82,7 +82,7 @@ uc_status check_segment(const uc_shape& sh, const uc_segment& s, int idx, KSeg& 
   const int G = s.group;
   if (!pow2(G) || G < 8 || G > 128 || sh.D % G)
     return fail(UC_E_INVALID, "segment %d: group %d must be a power of two in [8,128] dividing D", idx, G);
-  if (!s.head_bits && s.bits != 2 && s.bits != 4 && s.bits != 8)
+  if (s.bits != 2 && s.bits != 4 && s.bits != 8)
     return fail(UC_E_INVALID, "segment %d: bits %d not in {2,4,8}", idx, s.bits);
   if (s.head_bits && !s.code_off)
     return fail(UC_E_INVALID, "segment %d: head_bits given without code_off", idx);

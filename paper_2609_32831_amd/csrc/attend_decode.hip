@@ -4,12 +4,11 @@
 // softmax across all segments, chunk results merged by log-sum-exp).
 //
 // Work item: W workgroups per (b, h_kv) -- two per CU, one round -- each
-// taking the same share of every segment (so every CU mixes bandwidth-bound
-// dense tiles with dequantisation-bound packed tiles).  Each of the four
+// taking the same tile-aligned share of every segment.  Each of the four
 // waves takes every fourth 32-row tile of its share with two register sets
-// (A/B): while tile t is computed, the
-// loads of tiles t+1 and t+2 are outstanding.  A tile is consumed in two
-// halves so its registers are refilled as early as possible:
+// (A/B): while tile t is computed, the loads of tiles t+1 and t+2 are
+// outstanding.  A tile is consumed in two halves so its registers are
+// refilled as early as possible:
 //   head: V (or dequantised K and V for packed rows) goes to the wave's LDS
 //         tile; S^T = K Q^T runs on v_mfma_f32_16x16x32_bf16 with the 32 keys
 //         as two 16-row A blocks and the query block (padded to 16 rows) as
@@ -25,14 +24,16 @@
 // wave-wide ballot; otherwise the tile skips the cross-lane maximum and the
 // rescale.  l and O always share the same reference, so the result is the
 // same softmax; probabilities stay below 2^8 before normalisation.
-// Dense rows are read with raw buffer loads whose descriptor ends at the
-// chunk's last row (reads past it return zeros); packed rows of the last,
-// partial tile are clamped to the last valid row.  Either way the loads need
-// no branches, and rows past the chunk are masked out of the softmax.
+// All loads are raw buffer loads whose descriptor ends at the range's last
+// row (reads past it return zeros), so they need no clamping or branches;
+// only a range's last tile can be partial, and only the epilogue tiles of the
+// loop mask rows past the end.  Packed segments: whole row groups are packed
+// and the key row groups span whole tiles, so packed tiles are always full;
+// the residual tail rows (stored at the segment dtype) take the dense path.
 // LDS rows are padded by 32 bytes, which keeps the transposing reads free of
-// bank conflicts and their addresses affine in the head dimension.  The four waves merge through LDS and the workgroup writes
-// one unnormalised partial (m, l, o) per query row and segment touched; the
-// combine kernel merges them.
+// bank conflicts and their addresses affine in the head dimension.  The four
+// waves merge through LDS and the workgroup writes unnormalised partials
+// (m, l, o) per query row; the combine kernel merges them.
 #include "uc_common.h"
 
 namespace uc {
@@ -85,31 +86,50 @@ struct State {
   f4 acc[8];
 };
 
-// softmax over one tile's scores + O^T += V^T P (V from the wave's LDS tile)
+__device__ inline void state_init(State& st) {
+  st.m = -INFINITY;
+  st.l = 0.0f;
+#pragma unroll
+  for (int d = 0; d < 8; ++d) st.acc[d] = f4{0.f, 0.f, 0.f, 0.f};
+}
+
+// softmax over one tile's scores + O^T += V^T P (V from the wave's LDS tile).
+// MASK: the tile may reach past r_end (only a chunk's last tile does).
+template <bool MASK>
 __device__ inline void softmax_pv(State& st, const f4& s0, const f4& s1, float scale_log2,
                                   int row0, int r_end, const char* lv, int i16, int g4) {
   float p[8];
-  float mx = -INFINITY;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    p[j] = row0 + g4 * 4 + j < r_end ? s0[j] * scale_log2 : -INFINITY;
-    p[4 + j] = row0 + 16 + g4 * 4 + j < r_end ? s1[j] * scale_log2 : -INFINITY;
-    mx = fmaxf(mx, fmaxf(p[j], p[4 + j]));
+    p[j] = s0[j];
+    p[4 + j] = s1[j];
   }
+  if (MASK) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (row0 + g4 * 4 + j >= r_end) p[j] = -INFINITY;
+      if (row0 + 16 + g4 * 4 + j >= r_end) p[4 + j] = -INFINITY;
+    }
+  }
+  // the scale is positive, so the maximum of the raw logits gives the maximum
+  float mx = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])),
+                   fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7]))) * scale_log2;
   if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazy)) {  // rare: raise the reference max
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(st.m, mx);
-    const float alpha = exp2f(st.m - m_new);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
     st.l *= alpha;
 #pragma unroll
     for (int d = 0; d < 8; ++d) st.acc[d] *= alpha;
     st.m = m_new;
   }
+  // exponents are at most kLazy, so v_exp_f32 needs no range reduction; tiny
+  // probabilities may flush to zero
   float e[8], psum = 0.0f;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
-    e[j] = exp2f(p[j] - st.m);
+    e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
     psum += e[j];
   }
   uint32_t hi[4], lo[4];
@@ -135,23 +155,27 @@ __device__ inline void softmax_pv(State& st, const f4& s0, const f4& s1, float s
   }
 }
 
-// ---------------------------------------------------------------- dense rows
-struct DenseSet {
-  u4 k[8];  // A operands: k[blk*4 + t] = row blk*16 + i16, dims t*32 + g4*8 .. +7
-  u4 v[8];  // v[i] = row lane/16 + 4*i, 16-byte chunk lane%16
-};
-
-// Buffer descriptor over rows [0, n_rows) of one (b, h_kv) of a dense segment:
-// loads past the end return zeros (raw buffer, stride 0), so the partial last
-// tile needs no clamping and each load needs one 32-bit offset register.
-__device__ inline __amdgpu_buffer_rsrc_t rows_rsrc(const uint16_t* base, int n_rows) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, n_rows * ROWB,
-                                           0x00020000);
+// Raw buffer descriptor over `bytes` bytes from `base`: loads at or past the
+// end return zeros, and each load needs one 32-bit offset register.
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
 }
 
 __device__ inline u4 bload(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
   return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
+
+// a value the compiler cannot see through (keeps byte-extract conversions)
+__device__ inline uint32_t opaque(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+
+// ---------------------------------------------------------------- dense rows
+struct DenseSet {
+  u4 k[8];  // A operands: k[blk*4 + t] = row blk*16 + i16, dims t*32 + g4*8 .. +7
+  u4 v[8];  // v[i] = row lane/16 + 4*i, 16-byte chunk lane%16
+};
 
 __device__ inline void dense_issue(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int row0,
                                    int lane, DenseSet& S) {
@@ -181,17 +205,22 @@ __device__ inline void dense_head(const DenseSet& S, char* lv, const u4 (&qop)[4
   }
 }
 
-__device__ inline void dense_loop(State& st, const KSeg& ks, int bh, int r0, int r1, int n_mine,
+// Rows [r0, r1) of one head's dense rows at kb / vb (row-major, D per row).
+// The wave takes tiles wave, wave + WAVES, ...; only the last tile of the
+// range can be partial, and it is always one of the epilogue tiles.
+__device__ inline void dense_loop(State& st, const uint16_t* kb, const uint16_t* vb, int r0, int r1,
                                   int wave, int lane, const u4 (&qop)[4], float scale_log2,
                                   char* lv) {
+  const int n_tiles = (r1 - r0 + TILE - 1) / TILE;
+  const int n_mine = n_tiles > wave ? (n_tiles - wave + WAVES - 1) / WAVES : 0;
+  if (n_mine == 0) return;
   const int i16 = lane & 15, g4 = lane >> 4;
-  const int64_t base = (int64_t)bh * ks.row_stride * D;
-  const __amdgpu_buffer_rsrc_t rk = rows_rsrc((const uint16_t*)ks.k + base, r1);
-  const __amdgpu_buffer_rsrc_t rv = rows_rsrc((const uint16_t*)ks.v + base, r1);
+  const __amdgpu_buffer_rsrc_t rk = rsrc(kb, (uint32_t)r1 * ROWB);
+  const __amdgpu_buffer_rsrc_t rv = rsrc(vb, (uint32_t)r1 * ROWB);
   auto row_of = [&](int k) { return r0 + (wave + k * WAVES) * TILE; };
   DenseSet A, B;
   f4 s0, s1;
-  if (n_mine > 0) dense_issue(rk, rv, row_of(0), lane, A);
+  dense_issue(rk, rv, row_of(0), lane, A);
   if (n_mine > 1) dense_issue(rk, rv, row_of(1), lane, B);
   int k = 0;
   // steady state without branches, so the compiler's wait counts keep the
@@ -199,167 +228,126 @@ __device__ inline void dense_loop(State& st, const KSeg& ks, int bh, int r0, int
   for (; k + 3 < n_mine; k += 2) {
     dense_head(A, lv, qop, lane, s0, s1);
     dense_issue(rk, rv, row_of(k + 2), lane, A);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
+    softmax_pv<false>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
     dense_head(B, lv, qop, lane, s0, s1);
     dense_issue(rk, rv, row_of(k + 3), lane, B);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
+    softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
-  const int left = n_mine - k;  // 0..3 tiles; A holds tile k, B tile k+1
-  if (left >= 1) {
-    dense_head(A, lv, qop, lane, s0, s1);
-    if (left == 3) dense_issue(rk, rv, row_of(k + 2), lane, A);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
-  }
+  const int left = n_mine - k;  // 1..3 tiles; A holds tile k, B tile k+1
+  dense_head(A, lv, qop, lane, s0, s1);
+  if (left == 3) dense_issue(rk, rv, row_of(k + 2), lane, A);
+  softmax_pv<true>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
   if (left >= 2) {
     dense_head(B, lv, qop, lane, s0, s1);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
+    softmax_pv<true>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
   if (left == 3) {
     dense_head(A, lv, qop, lane, s0, s1);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k + 2), r1, lv, i16, g4);
+    softmax_pv<true>(st, s0, s1, scale_log2, row_of(k + 2), r1, lv, i16, g4);
   }
 }
 
 // ---------------------------------------------------------------- packed rows
-// lane owns channels c8*8 .. c8*8+7 of rows lane/16 + 4*i (i < 8); BITS-bit
-// codes of those 8 channels fill BITS bytes (one or two 32-bit words)
+// Only whole row groups are packed and groups span whole 32-row tiles, so a
+// packed tile is always full and lies in one key row group.  Lane (c8, g4)
+// owns channels c8*8 .. c8*8+7 of rows g4 + 4*i (i < 8); the BITS-bit codes of
+// those 8 channels fill BITS bytes.
 template <int BITS>
 struct PackedSet {
-  static constexpr int W = BITS == 8 ? 2 : 1;
-  uint32_t ck[8][W], cv[8][W];
-  float sv[8], mv[8];  // value scale/min of the lane's channel group, per row
-  float sk[8], mk[8];  // key scale/min of the lane's 8 channels (the tile's row group:
-                       // groups span at least one 32-row tile)
+  // 128-bit groups throughout (element [i] is row g4 + 4*i): this keeps the
+  // two register sets of the pipelined loop in whole register tuples
+  u4 ck[2], cv[2];  // code words (the low 16 bits at 2 bits per code)
+  u4 sv[2], mv[2];  // value scale/min bits of the lane's channel group, per row
+  u4 sk[2], mk[2];  // key scale/min bits of the lane's 8 channels (the tile's row group)
 };
 
 struct PackedSeg {
-  const uint8_t* ck;
-  const uint8_t* cv;
-  const float* sk;
-  const float* mk;
-  const float* sv;
-  const float* mv;
-  const uint16_t* tk;
-  const uint16_t* tv;
-  int64_t off;
-  int lgG, n_full, tail_len, bh;  // group size as a power of two
+  __amdgpu_buffer_rsrc_t ck, cv, sk, mk, sv, mv;  // one head's codes and scales
+  int lgG, ngv;                                   // log2(group), value groups per row
 };
 
-// the 8 codes of a lane's channels as floats (channel e of the lane -> c[e])
+// the 8 codes of a lane's channels as floats (channel e of the lane -> c[e]);
+// the masks are opaque so each code is one v_cvt_f32_ubyteN
 template <int BITS>
-__device__ inline void codes8(const uint32_t (&w)[BITS == 8 ? 2 : 1], float (&c)[8]) {
+__device__ inline void codes8(uint32_t w0, float (&c)[8]) {
   if constexpr (BITS == 4) {
-    const uint32_t lo = w[0] & 0x0F0F0F0Fu, hi = (w[0] >> 4) & 0x0F0F0F0Fu;
+    const uint32_t m = opaque(0x0F0F0F0Fu);
+    const uint32_t lo = w0 & m, hi = (w0 >> 4) & m;
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       c[2 * b] = (float)((lo >> (8 * b)) & 0xFFu);
       c[2 * b + 1] = (float)((hi >> (8 * b)) & 0xFFu);
     }
-  } else if constexpr (BITS == 8) {
-#pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      c[b] = (float)((w[0] >> (8 * b)) & 0xFFu);
-      c[4 + b] = (float)((w[1] >> (8 * b)) & 0xFFu);
-    }
-  } else {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) c[e] = (float)((w[0] >> (2 * e)) & 3u);
-  }
-}
-
-template <int BITS>
-__device__ inline void load_codes(const uint8_t* p, uint32_t (&w)[BITS == 8 ? 2 : 1]) {
-  if constexpr (BITS == 8) {
-    const uint2 a = *reinterpret_cast<const uint2*>(p);
-    w[0] = a.x;
-    w[1] = a.y;
-  } else if constexpr (BITS == 4) {
-    w[0] = *reinterpret_cast<const uint32_t*>(p);
-  } else {
-    w[0] = *reinterpret_cast<const uint16_t*>(p);
-  }
-}
-
-template <int BITS>
-__device__ inline void packed_issue(const PackedSeg& P, int row0, int last, int lane,
-                                    PackedSet<BITS>& S) {
-  const int c8 = lane & 15, g4 = lane >> 4;
-  constexpr int RB = D * BITS / 8;  // bytes per row
-  const int ngk = P.n_full >> P.lgG, lgGv = P.lgG;  // key row groups; value groups of G channels
-  const bool any_full = row0 < P.n_full;
-  if (any_full) {  // key scales of the tile's first row group
-    const int64_t si = ((int64_t)P.bh * ngk + (row0 >> P.lgG)) * D + c8 * 8;
-    const u4 a = *reinterpret_cast<const u4*>(P.sk + si);
-    const u4 b = *reinterpret_cast<const u4*>(P.sk + si + 4);
-    const u4 c = *reinterpret_cast<const u4*>(P.mk + si);
-    const u4 d = *reinterpret_cast<const u4*>(P.mk + si + 4);
+  } else {  // channel e at bits 2e: masks pick channels e and e + 4 into bytes 0 and 1
+    const uint32_t m = opaque(0x0303u);
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      S.sk[e] = __uint_as_float(a[e]);
-      S.sk[4 + e] = __uint_as_float(b[e]);
-      S.mk[e] = __uint_as_float(c[e]);
-      S.mk[4 + e] = __uint_as_float(d[e]);
-    }
-    const int ngv_lg = 7 - lgGv;  // log2(D / G)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int r = min(row0 + g4 + 4 * i, last);
-      const int rq = min(r, P.n_full - 1);  // a valid code row even where r is a tail row
-      load_codes<BITS>(P.ck + P.off + (int64_t)rq * RB + c8 * BITS, S.ck[i]);
-      load_codes<BITS>(P.cv + P.off + (int64_t)rq * RB + c8 * BITS, S.cv[i]);
-      const int64_t vi = (((int64_t)P.bh * P.n_full + rq) << ngv_lg) + ((c8 * 8) >> lgGv);
-      S.sv[i] = P.sv[vi];
-      S.mv[i] = P.mv[vi];
+      const uint32_t t = (w0 >> (2 * e)) & m;
+      c[e] = (float)(t & 0xFFu);
+      c[4 + e] = (float)((t >> 8) & 0xFFu);
     }
   }
 }
 
-// dequantise one row's 8 channels of K and V into packed bf16 (4 x u32 each)
+__device__ inline uint32_t bload32(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
+
+template <int BITS>
+__device__ inline void packed_issue(const PackedSeg& P, int row0, int lane, PackedSet<BITS>& S) {
+  const int c8 = lane & 15, g4 = lane >> 4;
+  constexpr int RB = D * BITS / 8;  // code bytes per row
+  const int so = ((row0 >> P.lgG) * D + c8 * 8) * 4;
+  S.sk[0] = bload(P.sk, so, 0);
+  S.sk[1] = bload(P.sk, so, 16);
+  S.mk[0] = bload(P.mk, so, 0);
+  S.mk[1] = bload(P.mk, so, 16);
+  const int co = (row0 + g4) * RB + c8 * BITS;
+  const int vo = ((row0 + g4) * P.ngv + ((c8 * 8) >> P.lgG)) * 4;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    if constexpr (BITS == 4) {
+      S.ck[i >> 2][i & 3] = bload32(P.ck, co, i * 4 * RB);
+      S.cv[i >> 2][i & 3] = bload32(P.cv, co, i * 4 * RB);
+    } else {
+      S.ck[i >> 2][i & 3] = __builtin_amdgcn_raw_buffer_load_b16(P.ck, co, i * 4 * RB, 0);
+      S.cv[i >> 2][i & 3] = __builtin_amdgcn_raw_buffer_load_b16(P.cv, co, i * 4 * RB, 0);
+    }
+    S.sv[i >> 2][i & 3] = bload32(P.sv, vo, i * 16 * P.ngv);
+    S.mv[i >> 2][i & 3] = bload32(P.mv, vo, i * 16 * P.ngv);
+  }
+}
+
+// dequantise one row's 8 channels of K and V into packed bf16 (4 x u32 each):
+// round_to_bf16(fmaf(code, scale, min)), the stored-value definition
 template <int BITS>
 __device__ inline void dequant_row(const PackedSet<BITS>& S, int i, u4& kk, u4& vv) {
   float qk[8], qv[8];
-  codes8<BITS>(S.ck[i], qk);
-  codes8<BITS>(S.cv[i], qv);
+  codes8<BITS>(S.ck[i >> 2][i & 3], qk);
+  codes8<BITS>(S.cv[i >> 2][i & 3], qv);
+  const float sv = __uint_as_float(S.sv[i >> 2][i & 3]), mv = __uint_as_float(S.mv[i >> 2][i & 3]);
   float xk[8], xv[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
-    xk[e] = fmaf(qk[e], S.sk[e], S.mk[e]);
-    xv[e] = fmaf(qv[e], S.sv[i], S.mv[i]);
+    xk[e] = fmaf(qk[e], __uint_as_float(S.sk[e >> 2][e & 3]), __uint_as_float(S.mk[e >> 2][e & 3]));
+    xv[e] = fmaf(qv[e], sv, mv);
   }
   kk = u4{bf2(xk[0], xk[1]), bf2(xk[2], xk[3]), bf2(xk[4], xk[5]), bf2(xk[6], xk[7])};
   vv = u4{bf2(xv[0], xv[1]), bf2(xv[2], xv[3]), bf2(xv[4], xv[5]), bf2(xv[6], xv[7])};
 }
 
 template <int BITS>
-__device__ inline void packed_head(const PackedSeg& P, const PackedSet<BITS>& S, int row0, int last,
-                                   char* lk, char* lv, const u4 (&qop)[4], int lane, f4& s0,
-                                   f4& s1) {
+__device__ inline void packed_head(const PackedSet<BITS>& S, char* lk, char* lv,
+                                   const u4 (&qop)[4], int lane, f4& s0, f4& s1) {
   const int c8 = lane & 15, g4 = lane >> 4;
-  if (row0 + TILE <= P.n_full) {  // whole tile quantised: no per-row branches
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int rr = g4 + 4 * i;
-      u4 kk, vv;
-      dequant_row<BITS>(S, i, kk, vv);
-      *reinterpret_cast<u4*>(lk + toff(rr, c8)) = kk;
-      *reinterpret_cast<u4*>(lv + toff(rr, c8)) = vv;
-    }
-  } else {  // the tile reaches the residual tail (at most once per head)
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int rr = g4 + 4 * i;
-      const int r = min(row0 + rr, last);
-      u4 kk, vv;
-      if (r < P.n_full) {
-        dequant_row<BITS>(S, i, kk, vv);
-      } else {
-        const int64_t e = ((int64_t)P.bh * P.tail_len + (r - P.n_full)) * D + c8 * 8;
-        kk = *reinterpret_cast<const u4*>(P.tk + e);
-        vv = *reinterpret_cast<const u4*>(P.tv + e);
-      }
-      *reinterpret_cast<u4*>(lk + toff(rr, c8)) = kk;
-      *reinterpret_cast<u4*>(lv + toff(rr, c8)) = vv;
-    }
+  for (int i = 0; i < 8; ++i) {
+    const int rr = g4 + 4 * i;
+    u4 kk, vv;
+    dequant_row<BITS>(S, i, kk, vv);
+    *reinterpret_cast<u4*>(lk + toff(rr, c8)) = kk;
+    *reinterpret_cast<u4*>(lv + toff(rr, c8)) = vv;
+    __builtin_amdgcn_sched_barrier(0);  // one row's temporaries at a time
   }
   const int i16 = lane & 15;
   s0 = f4{0.f, 0.f, 0.f, 0.f};
@@ -373,52 +361,62 @@ __device__ inline void packed_head(const PackedSeg& P, const PackedSet<BITS>& S,
   }
 }
 
+// Rows [r0, r1) of one head's packed rows; both ends are multiples of TILE.
 template <int BITS>
-__device__ inline void packed_loop(State& st, const PackedSeg& P, int r0, int r1, int n_mine,
-                                   int wave, int lane, const u4 (&qop)[4], float scale_log2,
-                                   char* lk, char* lv) {
+__device__ inline void packed_loop(State& st, const PackedSeg& P, int r0, int r1, int wave,
+                                   int lane, const u4 (&qop)[4], float scale_log2, char* lk,
+                                   char* lv) {
+  const int n_tiles = (r1 - r0) / TILE;
+  const int n_mine = n_tiles > wave ? (n_tiles - wave + WAVES - 1) / WAVES : 0;
+  if (n_mine == 0) return;
   const int i16 = lane & 15, g4 = lane >> 4;
-  const int last = r1 - 1;
   auto row_of = [&](int k) { return r0 + (wave + k * WAVES) * TILE; };
   PackedSet<BITS> A, B;
   f4 s0, s1;
-  if (n_mine > 0) packed_issue<BITS>(P, row_of(0), last, lane, A);
-  if (n_mine > 1) packed_issue<BITS>(P, row_of(1), last, lane, B);
+  packed_issue<BITS>(P, row_of(0), lane, A);
+  if (n_mine > 1) packed_issue<BITS>(P, row_of(1), lane, B);
   int k = 0;
+  // the scheduling barriers keep the refill loads behind the dequantisation
+  // that frees their registers (hoisting them would need a third set)
   for (; k + 3 < n_mine; k += 2) {
-    packed_head<BITS>(P, A, row_of(k), last, lk, lv, qop, lane, s0, s1);
-    packed_issue<BITS>(P, row_of(k + 2), last, lane, A);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
-    packed_head<BITS>(P, B, row_of(k + 1), last, lk, lv, qop, lane, s0, s1);
-    packed_issue<BITS>(P, row_of(k + 3), last, lane, B);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
+    packed_head<BITS>(A, lk, lv, qop, lane, s0, s1);
+    __builtin_amdgcn_sched_barrier(0);
+    packed_issue<BITS>(P, row_of(k + 2), lane, A);
+    __builtin_amdgcn_sched_barrier(0);
+    softmax_pv<false>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
+    __builtin_amdgcn_sched_barrier(0);
+    packed_head<BITS>(B, lk, lv, qop, lane, s0, s1);
+    __builtin_amdgcn_sched_barrier(0);
+    packed_issue<BITS>(P, row_of(k + 3), lane, B);
+    __builtin_amdgcn_sched_barrier(0);
+    softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
+    __builtin_amdgcn_sched_barrier(0);
   }
   const int left = n_mine - k;
-  if (left >= 1) {
-    packed_head<BITS>(P, A, row_of(k), last, lk, lv, qop, lane, s0, s1);
-    if (left == 3) packed_issue<BITS>(P, row_of(k + 2), last, lane, A);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
-  }
+  packed_head<BITS>(A, lk, lv, qop, lane, s0, s1);
+  if (left == 3) packed_issue<BITS>(P, row_of(k + 2), lane, A);
+  softmax_pv<false>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
   if (left >= 2) {
-    packed_head<BITS>(P, B, row_of(k + 1), last, lk, lv, qop, lane, s0, s1);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
+    packed_head<BITS>(B, lk, lv, qop, lane, s0, s1);
+    softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
   if (left == 3) {
-    packed_head<BITS>(P, A, row_of(k + 2), last, lk, lv, qop, lane, s0, s1);
-    softmax_pv(st, s0, s1, scale_log2, row_of(k + 2), r1, lv, i16, g4);
+    packed_head<BITS>(A, lk, lv, qop, lane, s0, s1);
+    softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 2), r1, lv, i16, g4);
   }
 }
 
 // ---------------------------------------------------------------- kernel
 // Work split: W workgroups per (b, h_kv) (two per CU, one round).  Workgroup
-// w takes the w-th of W equal tile-aligned shares of every segment, so each
-// CU mixes bandwidth-bound dense tiles with dequantisation-bound packed
-// tiles.  Each workgroup writes one partial record (m, l, o) per segment for
-// its query rows (slot s*W + w; m = -inf for an empty share); the combine
-// kernel merges them.
+// w takes the w-th of W equal tile-aligned shares of every segment.  With
+// per-segment statistics requested, each workgroup writes one partial record
+// (m, l, o) per segment for its query rows (slot s*W + w; m = -inf for an
+// empty share); otherwise one running state spans all segments and one record
+// per workgroup (slot w) is written.  The combine kernel merges the records.
 struct DecodePlan {
-  int W;      // workgroups per (b, h_kv)
+  int W;        // workgroups per (b, h_kv)
   int n_seg;
+  int per_seg;  // 1: one record per segment and workgroup
 };
 
 // tile-aligned share w of n rows among W workgroups
@@ -437,7 +435,8 @@ __device__ inline int64_t qrow_of(const Ctx& c, int qs) {
   return ((int64_t)c.b * c.Hq + c.hkv * c.G + qs / c.M) * c.M + qs % c.M;
 }
 
-// merge the four waves' state through LDS and write one partial record
+// merge the four waves' state through LDS and write one partial record;
+// ok = false marks the record invalid (l = NaN)
 __device__ inline void flush(State& st, char* lds, const Ctx& c, int slot, bool ok, int lane,
                              int wave) {
   const int i16 = lane & 15, g4 = lane >> 4;
@@ -481,6 +480,54 @@ __device__ inline void flush(State& st, char* lds, const Ctx& c, int slot, bool 
   __syncthreads();  // LDS free again
 }
 
+// one workgroup's share [r0, r1) of segment ks for head bh
+__device__ inline bool segment_share(State& st, const KSeg& ks, int bh, int r0, int r1, int wave,
+                                     int lane, const u4 (&qop)[4], float scale_log2, char* lk,
+                                     char* lv) {
+  if (r1 <= r0) return true;
+  if (ks.kind == UC_SEG_DENSE) {
+    const int64_t base = (int64_t)bh * ks.row_stride * D;
+    dense_loop(st, (const uint16_t*)ks.k + base, (const uint16_t*)ks.v + base, r0, r1, wave, lane,
+               qop, scale_log2, lv);
+    return true;
+  }
+  int bits = 0;
+  int64_t off = 0;
+  // code widths of 2 and 4 bits only (ks.bits bounds the per-head widths)
+  if (!head_codes(ks, bh, D, bits, off) || bits > 4) return false;
+  // the per-head entries are the same in every lane: keep them in scalar
+  // registers so the buffer descriptors built from them stay scalar
+  bits = __builtin_amdgcn_readfirstlane(bits);
+  off = (int64_t)(((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)(off >> 32)) << 32) |
+                  (uint32_t)__builtin_amdgcn_readfirstlane((int)off));
+  // packed rows [0, n_full), then the residual tail rows as dense rows
+  const int p1 = min(r1, ks.n_full);
+  if (p1 > r0) {
+    const int lgG = __builtin_ctz((unsigned)ks.group);
+    const int ngk = ks.n_full >> lgG, ngv = D >> lgG;
+    const uint32_t cbytes = (uint32_t)ks.n_full * (D * bits / 8);
+    PackedSeg P;
+    P.ck = rsrc(ks.codes_k + off, cbytes);
+    P.cv = rsrc(ks.codes_v + off, cbytes);
+    const int64_t sko = (int64_t)bh * ngk * D, svo = (int64_t)bh * ks.n_full * ngv;
+    P.sk = rsrc(ks.scale_k + sko, (uint32_t)ngk * D * 4);
+    P.mk = rsrc(ks.min_k + sko, (uint32_t)ngk * D * 4);
+    P.sv = rsrc(ks.scale_v + svo, (uint32_t)ks.n_full * ngv * 4);
+    P.mv = rsrc(ks.min_v + svo, (uint32_t)ks.n_full * ngv * 4);
+    P.lgG = lgG;
+    P.ngv = ngv;
+    if (bits == 4) packed_loop<4>(st, P, r0, p1, wave, lane, qop, scale_log2, lk, lv);
+    else packed_loop<2>(st, P, r0, p1, wave, lane, qop, scale_log2, lk, lv);
+  }
+  const int t0 = max(r0, ks.n_full);
+  if (r1 > t0) {
+    const int64_t base = (int64_t)bh * ks.tail_len * D;
+    dense_loop(st, (const uint16_t*)ks.tail_k + base, (const uint16_t*)ks.tail_v + base,
+               t0 - ks.n_full, r1 - ks.n_full, wave, lane, qop, scale_log2, lv);
+  }
+  return true;
+}
+
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodePlan pl,
                                                              const uint16_t* __restrict__ q,
                                                              int Hq, int Hkv, int M,
@@ -504,48 +551,23 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
   }
   char* lk = lds + wave * 2 * TILEB;
   char* lv = lk + TILEB;
-  Ctx c{partial, pl.n_seg * W, nq, M, Hq, G, b, hkv};
+  Ctx c{partial, pl.per_seg ? pl.n_seg * W : W, nq, M, Hq, G, b, hkv};
 
+  State st;
+  state_init(st);
+  bool ok = true;
   for (int si = 0; si < pl.n_seg; ++si) {
     const KSeg& ks = segs.s[si];
     const int r0 = share_row(ks.n_rows, w, W);
     const int r1 = share_row(ks.n_rows, w + 1, W);
-    State st;
-    st.m = -INFINITY;
-    st.l = 0.0f;
-#pragma unroll
-    for (int d = 0; d < 8; ++d) st.acc[d] = f4{0.f, 0.f, 0.f, 0.f};
-    bool ok = true;
-    if (r1 > r0) {
-      int bits = 0;
-      int64_t off = 0;
-      if (ks.kind == UC_SEG_PACKED) ok = head_codes(ks, bh, D, bits, off);
-      const int n_tiles = ok ? (r1 - r0 + TILE - 1) / TILE : 0;
-      const int n_mine = n_tiles > wave ? (n_tiles - wave + WAVES - 1) / WAVES : 0;
-      if (ks.kind == UC_SEG_DENSE) {
-        dense_loop(st, ks, bh, r0, r1, n_mine, wave, lane, qop, scale_log2, lv);
-      } else if (n_mine > 0) {
-        PackedSeg P;
-        P.ck = ks.codes_k;
-        P.cv = ks.codes_v;
-        P.sk = ks.scale_k;
-        P.mk = ks.min_k;
-        P.sv = ks.scale_v;
-        P.mv = ks.min_v;
-        P.tk = (const uint16_t*)ks.tail_k;
-        P.tv = (const uint16_t*)ks.tail_v;
-        P.off = off;
-        P.lgG = __builtin_ctz((unsigned)ks.group);
-        P.n_full = ks.n_full;
-        P.tail_len = ks.tail_len;
-        P.bh = bh;
-        if (bits == 4) packed_loop<4>(st, P, r0, r1, n_mine, wave, lane, qop, scale_log2, lk, lv);
-        else packed_loop<2>(st, P, r0, r1, n_mine, wave, lane, qop, scale_log2, lk, lv);
-      }
+    ok &= segment_share(st, ks, bh, r0, r1, wave, lane, qop, scale_log2, lk, lv);
+    if (pl.per_seg) {
+      flush(st, lds, c, si * W + w, ok, lane, wave);
+      state_init(st);
+      ok = true;
     }
-    flush(st, lds, c, si * W + w, ok, lane, wave);
   }
-
+  if (!pl.per_seg) flush(st, lds, c, w, ok, lane, wave);
 }
 
 int device_cus() {
@@ -574,10 +596,10 @@ bool decode_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M
   if ((sh.Hq / sh.Hkv) * M > 16) return false;
   for (int i = 0; i < segs.n; ++i) {
     if (segs.s[i].dtype != UC_BF16) return false;
-    // packed: 2- or 4-bit codes of uniform width, key row groups covering
-    // whole 32-row tiles (one scale set per tile)
-    if (segs.s[i].kind == UC_SEG_PACKED &&
-        (segs.s[i].group < TILE || segs.s[i].head_bits || segs.s[i].bits == 8))
+    // packed: 2- or 4-bit codes (bits is the uniform width, or the bound of
+    // the per-head widths); key row groups must cover whole 32-row tiles (one
+    // scale set per tile; groups are powers of two)
+    if (segs.s[i].kind == UC_SEG_PACKED && (segs.s[i].group < TILE || segs.s[i].bits > 4))
       return false;
   }
   return true;
@@ -597,15 +619,18 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   DecodePlan p{};
   p.W = decode_w(sh);
   p.n_seg = segs.n;
+  p.per_seg = seg_lse != nullptr;
   float* partial = (float*)ws;
   hipLaunchKernelGGL(decode_mfma_kernel, dim3(p.W, sh.B * sh.Hkv), dim3(256), 0, st, segs, p,
                      (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  // records are segment-major: segment s owns slots [s*W, (s+1)*W)
+  // per-segment records are segment-major (segment s owns slots [s*W, (s+1)*W));
+  // otherwise all W records are attributed to the first segment (no seg_lse)
   ChunkPlan cp{};
-  cp.n_chunks = segs.n * p.W;
-  for (int i = 0; i <= kMaxSeg; ++i) cp.first[i] = min(i, segs.n) * p.W;
+  cp.n_chunks = p.per_seg ? segs.n * p.W : p.W;
+  for (int i = 0; i <= kMaxSeg; ++i)
+    cp.first[i] = p.per_seg ? min(i, segs.n) * p.W : (i == 0 ? 0 : p.W);
   return launch_attend_combine(sh, segs, cp, M, partial, o, lse, seg_lse, st);
 }
 

@@ -144,10 +144,12 @@ __global__ __launch_bounds__(256) void attend_generic_kernel(KSegs segs, ChunkPl
 }
 
 // One wave per query row: merge the chunk partials (m, l, o) of that row by
-// log-sum-exp.  Lane = (record group rg = lane / 16, dims (lane % 16) * D/16
-// ...): a lane reads every fourth record's slice of o with independent
-// loads, and the four record groups are summed with cross-lane exchanges.
-// Records with m = -inf hold no rows (their o is not read).
+// log-sum-exp in a single pass.  Lane = (record group rg = lane / 16, dims
+// (lane % 16) * D/16 ...): each record group merges every fourth record
+// online (independent loads, running maximum), then the four groups are
+// merged with cross-lane exchanges.  Records with m = -inf hold no rows
+// (nothing of them is read but m).  Per-segment log-sum-exps take one more
+// pass over m and l only.
 template <int D>
 __global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int nseg, int ps,
                                                             const float* __restrict__ partial,
@@ -157,55 +159,65 @@ __global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int 
   const int lane = threadIdx.x;
   const int C = plan.n_chunks;
   const float* P = partial + qi * C * ps;
-  float mall = -INFINITY;
-  for (int c = lane; c < C; c += 64) mall = fmaxf(mall, P[(int64_t)c * ps]);
-  mall = wave_max(mall);
-  float L = 0.0f;
-  for (int c = lane; c < C; c += 64) {
+  const int rg = lane >> 4, d0 = (lane & 15) * PD;
+  float m = -INFINITY, l = 0.0f, acc[PD];
+#pragma unroll
+  for (int i = 0; i < PD; ++i) acc[i] = 0.0f;
+#pragma unroll 2
+  for (int c = rg; c < C; c += 4) {
     const float* pc = P + (int64_t)c * ps;
-    if (pc[0] != -INFINITY) L += pc[1] * exp2f(pc[0] - mall);
-  }
-  L = wave_sum(L);
-  if (lse && lane == 0) lse[qi] = (mall + log2f(L)) * kLn2;
-  if (seg_lse) {
-    for (int a = 0; a < nseg; ++a) {
-      float ma = -INFINITY, la = 0.0f;
-      for (int c = plan.first[a] + lane; c < plan.first[a + 1]; c += 64)
-        ma = fmaxf(ma, P[(int64_t)c * ps]);
-      ma = wave_max(ma);
-      for (int c = plan.first[a] + lane; c < plan.first[a + 1]; c += 64) {
-        const float* pc = P + (int64_t)c * ps;
-        if (pc[0] != -INFINITY) la += pc[1] * exp2f(pc[0] - ma);
-      }
-      la = wave_sum(la);
-      if (lane == 0) seg_lse[qi * nseg + a] = la > 0.0f ? (ma + log2f(la)) * kLn2 : -INFINITY;
+    const float mc = pc[0];
+    if (mc == -INFINITY) continue;
+    const float lc = pc[1];
+    float oc[PD];
+    if (o) {
+#pragma unroll
+      for (int i = 0; i < PD; ++i) oc[i] = pc[2 + d0 + i];
     }
+    const float mn = fmaxf(m, mc);
+    const float a = exp2f(m - mn), b = exp2f(mc - mn);
+    l = fmaf(l, a, lc * b);
+    if (o) {
+#pragma unroll
+      for (int i = 0; i < PD; ++i) acc[i] = fmaf(acc[i], a, oc[i] * b);
+    }
+    m = mn;
   }
+  float M = fmaxf(m, __shfl_xor(m, 16, 64));
+  M = fmaxf(M, __shfl_xor(M, 32, 64));
+  const float sc = m == -INFINITY ? 0.0f : exp2f(m - M);
+  l *= sc;
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (lse && lane == 0) lse[qi] = (M + log2f(l)) * kLn2;
   if (o) {
-    const int rg = lane >> 4, d0 = (lane & 15) * PD;
-    float acc[PD];
-#pragma unroll
-    for (int i = 0; i < PD; ++i) acc[i] = 0.0f;
-#pragma unroll 4
-    for (int c = rg; c < C; c += 4) {
-      const float* pc = P + (int64_t)c * ps;
-      const float m = pc[0];
-      if (m == -INFINITY) continue;
-      const float w = exp2f(m - mall);
-#pragma unroll
-      for (int i = 0; i < PD; ++i) acc[i] = fmaf(w, pc[2 + d0 + i], acc[i]);
-    }
-    const float inv = 1.0f / L;
+    const float inv = 1.0f / l;
 #pragma unroll
     for (int i = 0; i < PD; ++i) {
-      float v = acc[i];
+      float v = acc[i] * sc;
       v += __shfl_xor(v, 16, 64);
       v += __shfl_xor(v, 32, 64);
-      acc[i] = v;
+      acc[i] = v * inv;
     }
     if (rg == 0) {
 #pragma unroll
-      for (int i = 0; i < PD; ++i) o[qi * D + d0 + i] = acc[i] * inv;
+      for (int i = 0; i < PD; ++i) o[qi * D + d0 + i] = acc[i];
+    }
+  }
+  if (seg_lse) {
+    for (int a = 0; a < nseg; ++a) {
+      float ma = -INFINITY, la = 0.0f;
+      for (int c = plan.first[a] + lane; c < plan.first[a + 1]; c += 64) {
+        const float* pc = P + (int64_t)c * ps;
+        const float mc = pc[0];
+        if (mc == -INFINITY) continue;
+        const float mn = fmaxf(ma, mc);
+        la = fmaf(la, exp2f(ma - mn), pc[1] * exp2f(mc - mn));
+        ma = mn;
+      }
+      const float mw = wave_max(ma);
+      la = wave_sum(ma == -INFINITY ? 0.0f : la * exp2f(ma - mw));
+      if (lane == 0) seg_lse[qi * nseg + a] = la > 0.0f ? (mw + log2f(la)) * kLn2 : -INFINITY;
     }
   }
 }

@@ -94,7 +94,9 @@ __device__ inline bool head_codes(const KSeg& s, int bh, int D, int& bits, int64
     bits = s.bits;
     off = s.code_off ? s.code_off[bh] : (int64_t)bh * s.n_full * D * s.bits / 8;
   }
+  // per-head widths are bounded by the segment's bits (kernels are chosen by it)
   if (bits != 2 && bits != 4 && bits != 8) return false;
+  if (s.head_bits && bits > s.bits) return false;
   int64_t need = (int64_t)s.n_full * D * bits / 8;
   return off >= 0 && (uint64_t)(off + need) <= s.codes_bytes;
 }

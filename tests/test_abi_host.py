@@ -86,6 +86,8 @@ def test_attend_validation(uc):
     assert _attend(uc, good, [_packed(uc, 100, tail_k=None)]) == E  # tail rows, no tail
     assert _attend(uc, good, [_packed(uc, 128, scale_v=None)]) == E
     assert _attend(uc, good, [_packed(uc, 128, head_bits=FAKE)]) == E  # no code_off
+    # with per-head widths, bits is their bound and must still be a valid width
+    assert _attend(uc, good, [_packed(uc, 128, bits=5, head_bits=FAKE, code_off=FAKE)]) == E
     # a workspace that is too small is its own status
     assert _attend(uc, good, [_dense(uc, 8)], ws_bytes=16) == uc.UC_E_WORKSPACE
     assert uc.uc_status_string(uc.UC_E_WORKSPACE).startswith("UC_E_WORKSPACE")

@@ -285,6 +285,8 @@ DCASES = [
     (2, 14, 2, 1, 64, 4, False, (4096, 61440 // 8, 1467, 4096, 511, 512)),
     (2, 28, 4, 1, 64, 2, False, (300, 2000, 512, 1000, 17, 32)),
     (1, 28, 4, 2, 128, 4, False, (0, 100, 3, 130, 0, 4)),
+    (2, 28, 4, 1, 64, 4, True, (128, 1000, 257, 2048 + 40, 5, 8)),   # int2/int4 per head
+    (1, 28, 4, 1, 32, 4, False, (0, 0, 0, 31, 1, 1)),                # tail-only packed rows
 ]
 
 
@@ -301,22 +303,30 @@ def test_decode_mfma_parity(case):
     shape = uc.make_shape(B, Hq, Hkv, D)
     qd = dev(q, "bf16")
     outs = {}
-    for path in (uc.UC_PATH_AUTO, uc.UC_PATH_VALU):
+    # matrix-core path with per-segment statistics (one record per segment),
+    # matrix-core path with o only (one running state across segments), and
+    # the VALU path
+    for name, path, want_sl in (("mfma", uc.UC_PATH_AUTO, True), ("mfma_o", uc.UC_PATH_AUTO, False),
+                                ("valu", uc.UC_PATH_VALU, True)):
         prev = uc.uc_set_path(path)
         try:
             o = torch.empty(B, Hq, M, D, device="cuda")
-            lse = torch.empty(B, Hq, M, device="cuda")
-            sl = torch.empty(B, Hq, M, 4, device="cuda")
+            lse = torch.empty(B, Hq, M, device="cuda") if want_sl else None
+            sl = torch.empty(B, Hq, M, 4, device="cuda") if want_sl else None
             uc.uc_attend_mixed(shape, segs, qd, M, sm, o, lse, sl)
             torch.cuda.synchronize()
-            outs[path] = (o.cpu().numpy(), lse.cpu().numpy(), sl.cpu().numpy())
+            outs[name] = (o.cpu().numpy(), None if lse is None else lse.cpu().numpy(),
+                          None if sl is None else sl.cpu().numpy())
         finally:
             uc.uc_set_path(prev)
-    for path, (o, lse, sl) in outs.items():
-        check_attention(o, o_ref, f"path {path}")
+    for name, (o, lse, sl) in outs.items():
+        check_attention(o, o_ref, f"path {name}")
+        if lse is None:
+            continue
         assert np.allclose(lse, lse_ref, rtol=1e-5, atol=1e-4)
         fin = np.isfinite(sl_ref)
         assert np.array_equal(np.isfinite(sl), fin)
         assert np.allclose(sl[fin], sl_ref[fin], rtol=1e-5, atol=1e-4)
-    # the two kernel paths agree far inside the bar
-    assert np.abs(outs[0][0] - outs[1][0]).max() < 5e-4
+    # the kernel paths agree far inside the bar
+    assert np.abs(outs["mfma"][0] - outs["valu"][0]).max() < 5e-4
+    assert np.abs(outs["mfma_o"][0] - outs["valu"][0]).max() < 5e-4
