@@ -17,6 +17,14 @@ using namespace uc;
 
 namespace uc {
 bool decode_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M);
+bool score_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt);
+int score_mfma_chunk_rows();
+hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
+                                 const void* q, int W, float sm_scale, float* partial,
+                                 hipStream_t st);
+hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
+                                 const void* q, int W, float sm_scale, const float* lse,
+                                 float* const* scores, double* mass_partial, hipStream_t st);
 size_t decode_mfma_workspace(const uc_shape& sh, const KSegs& segs, int M);
 hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
@@ -239,19 +247,40 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
 }
 
 // ---------------------------------------------------------------- scoring
-static void score_ws_parts(const uc_shape& sh, const KSegs& ks, int W, size_t& part1,
+static bool score_fast(const uc_shape& sh, const KSegs& ks, int q_dt) {
+  return g_path.load() == UC_PATH_AUTO && score_mfma_eligible(sh, ks, q_dt);
+}
+
+// matrix-core scoring: both passes use one plan of score_mfma_chunk_rows()
+// keys per chunk
+static ChunkPlan score_mfma_plan(const KSegs& ks) {
+  return make_plan(ks, score_mfma_chunk_rows(), 1 << 30);
+}
+
+// workspace parts: pass-1 records, row log-sum-exps, chunk masses (fp64);
+// every part grows monotonically with the row counts
+static void score_ws_parts(const uc_shape& sh, const KSegs& ks, int W, bool fast, size_t& part1,
                            size_t& lse_b, size_t& mass_b) {
-  part1 = generic_ws(sh, ks, kLseRows, kLseMaxChunks, W, false);
   lse_b = align256((size_t)sh.B * sh.Hq * W * sizeof(float));
+  if (fast) {
+    const int C = score_mfma_plan(ks).n_chunks;
+    part1 = align256((size_t)sh.B * sh.Hq * W * C * 2 * sizeof(float));
+    mass_b = align256((size_t)sh.B * sh.Hkv * C * sizeof(double));
+    return;
+  }
+  part1 = generic_ws(sh, ks, kLseRows, kLseMaxChunks, W, false);
   mass_b = align256((size_t)sh.B * sh.Hkv * score_col_plan(ks).n_chunks * sizeof(double));
 }
 
 size_t uc_score_workspace_size(const uc_shape* shape, const uc_segment* segs, int n_segs, int W) {
   KSegs ks;
   if (check_segments(shape, segs, n_segs, ks) || W < 1) return 0;
-  size_t a, b, c;
-  score_ws_parts(*shape, ks, W, a, b, c);
-  return a + b + c;
+  // the larger of the two paths' needs, so the size does not depend on the
+  // query dtype or the selected path
+  size_t a, b, c, a2, b2, c2;
+  score_ws_parts(*shape, ks, W, false, a, b, c);
+  score_ws_parts(*shape, ks, W, true, a2, b2, c2);
+  return std::max(a + b + c, a2 + b2 + c2);
 }
 
 uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int n_segs,
@@ -265,21 +294,34 @@ uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int
   if (!dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad q dtype %d", q_dt);
   if (W < 1) return fail(UC_E_INVALID, "W must be >= 1 (got %d)", W);
   if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
+  if ((int64_t)shape->B * shape->Hq * W > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
+  const bool fast = score_fast(*shape, ks, q_dt);
   size_t a, b, c;
-  score_ws_parts(*shape, ks, W, a, b, c);
+  score_ws_parts(*shape, ks, W, fast, a, b, c);
   if (!ws || ws_bytes < a + b + c) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, a + b + c);
   hipStream_t s = (hipStream_t)stream;
   float* partial = (float*)ws;
   float* lse = (float*)((char*)ws + a);
   double* mpart = (double*)((char*)ws + a + b);
-  const ChunkPlan p1 = score_lse_plan(ks), p2 = score_col_plan(ks);
-  hipError_t e = launch_attend_generic(*shape, ks, p1, q_obs, q_dt, W, sm_scale, partial, false, s);
-  if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p1, W, partial, nullptr, lse, nullptr, s);
   float* sp[kMaxSeg] = {};
   if (scores_out)
     for (int i = 0; i < n_segs; ++i) sp[i] = scores_out[i];
-  if (e == hipSuccess)
-    e = launch_score_colsum(*shape, ks, p2, q_obs, q_dt, W, sm_scale, lse, sp, mpart, s);
+  hipError_t e;
+  ChunkPlan p2;
+  if (fast) {
+    const ChunkPlan p = score_mfma_plan(ks);
+    e = launch_score_lse_mfma(*shape, ks, p, q_obs, W, sm_scale, partial, s);
+    if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, W, partial, nullptr, lse, nullptr, s);
+    if (e == hipSuccess) e = launch_score_col_mfma(*shape, ks, p, q_obs, W, sm_scale, lse, sp, mpart, s);
+    p2 = p;
+  } else {
+    const ChunkPlan p1 = score_lse_plan(ks);
+    p2 = score_col_plan(ks);
+    e = launch_attend_generic(*shape, ks, p1, q_obs, q_dt, W, sm_scale, partial, false, s);
+    if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p1, W, partial, nullptr, lse, nullptr, s);
+    if (e == hipSuccess)
+      e = launch_score_colsum(*shape, ks, p2, q_obs, q_dt, W, sm_scale, lse, sp, mpart, s);
+  }
   if (e == hipSuccess && mass_out)
     e = launch_mass_finalize(p2, shape->B * shape->Hkv, n_segs, mpart, mass_out, s);
   return launched(e);

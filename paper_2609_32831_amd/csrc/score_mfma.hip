@@ -1,0 +1,354 @@
+// score_mfma.hip -- attention-guided importance scores on the CDNA4 matrix
+// cores (Sec. 3.2, Eq. 1 and App. E, "Batched GQA token selection": the
+// attention probability each cached token receives from the observation
+// queries, summed over the query heads that share its KV head).
+//
+// For one KV head the observation block is the G*W query rows of its query
+// heads (row g*W + w is head h_kv*G + g, position w; these rows are
+// contiguous in q).  Softmax normalises each query row over every key of
+// every segment, so the scores take two passes over the keys:
+//   pass 1  per (key chunk, query block of <= 256 rows, b*h_kv): running
+//           maximum and sum of exp2 per query row over the chunk's keys, one
+//           (m, l) record per (row, chunk); the attention combine kernel
+//           merges the records into the row log-sum-exps.
+//   pass 2  per (key chunk, b*h_kv): p = exp2(s - lse) for every query row,
+//           summed over the rows per key (column sums), for all query blocks
+//           of the head; the per-key sums are written as the scores and
+//           their total is the chunk's probability mass (Eq. 1 bracket).
+// Both passes compute S^T = K Q^T with v_mfma_f32_16x16x32_bf16: a wave
+// takes 32-key tiles of the chunk (keys straight from HBM into the A-operand
+// layout, two register sets in flight) and runs them against every 16-row
+// query tile of the block, whose B operands it reads from the block staged
+// in LDS.  Logits are in base 2 (q.k times scale*log2(e)).
+// Column sums: a lane sums its key's probabilities over the query tiles in
+// fp32, the 16 query columns of a tile are added by a butterfly, and the
+// query blocks are accumulated in fp64 in LDS; chunk masses are fp64.
+#include "uc_common.h"
+
+namespace uc {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+
+constexpr int D = 128;
+constexpr int TILE = 32;             // keys per tile
+constexpr int WAVES = 4;
+constexpr int TPW = 4;               // key tiles per wave and sub-chunk
+constexpr int SUB = WAVES * TPW * TILE;  // 512 keys per sub-chunk (K held in registers)
+constexpr int CHUNK = 2 * SUB;       // keys per workgroup
+constexpr int QB = 256;              // query rows per block (16 tiles)
+constexpr int QT = QB / 16;
+constexpr int QROW = D * 2 + 16;     // bytes of one staged query row (16 B padding)
+constexpr int ROWB = D * 2;
+constexpr float kLazy = 8.0f;
+
+__device__ inline f4 mfma(const u4& a, const u4& b, const f4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
+}
+
+__device__ inline u4 bload(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// A wave's TPW key tiles of a sub-chunk as A operands: k[i][blk*4 + t] =
+// row (tile i) blk*16 + i16, dims t*32 + g4*8 .. +7.  Rows past the
+// descriptor's end read as zeros.
+struct KTiles {
+  u4 k[TPW][8];
+};
+
+__device__ inline void k_issue(__amdgpu_buffer_rsrc_t rk, int row0, int lane, u4 (&k)[8]) {
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int ko = (row0 + i16) * ROWB + g4 * 16;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    k[t] = bload(rk, ko, t * 64);
+    k[4 + t] = bload(rk, ko, 16 * ROWB + t * 64);
+  }
+}
+
+// S^T of a key tile against query tile qt: s0 = keys 0..15, s1 = keys 16..31;
+// lane (i16, g4) holds keys g4*4 + j (+16) of query column i16
+__device__ inline void s_tile(const u4 (&k)[8], const char* qs, int qt, int lane, f4& s0, f4& s1) {
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const char* qrow = qs + (qt * 16 + i16) * QROW + g4 * 16;
+  s0 = f4{0.f, 0.f, 0.f, 0.f};
+  s1 = s0;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const u4 b = *reinterpret_cast<const u4*>(qrow + t * 64);
+    s0 = mfma(k[t], b, s0);
+    s1 = mfma(k[4 + t], b, s1);
+  }
+}
+
+// stage query rows [q0, q0 + QB) of the head's observation block (rows past nq
+// are zero) into LDS
+__device__ inline void stage_q(char* qs, const uint16_t* qh, int q0, int nq) {
+  for (int e = threadIdx.x; e < QB * (D / 8); e += blockDim.x) {
+    const int r = e / (D / 8), c = e % (D / 8);
+    u4 v = u4{0, 0, 0, 0};
+    if (q0 + r < nq) v = *reinterpret_cast<const u4*>(qh + (int64_t)(q0 + r) * D + c * 8);
+    *reinterpret_cast<u4*>(qs + r * QROW + c * 16) = v;
+  }
+}
+
+// chunk c of the plan -> segment and row range
+__device__ inline int chunk_rows(const ChunkPlan& p, const KSegs& segs, int c, int& r0, int& r1) {
+  int si = 0;
+  while (si + 1 < segs.n && c >= p.first[si + 1]) ++si;
+  r0 = (c - p.first[si]) * p.rows[si];
+  r1 = min(r0 + p.rows[si], segs.s[si].n_rows);
+  return si;
+}
+
+// base-2 logits of one lane: 8 keys (tile rows g4*4 + j and 16 + g4*4 + j),
+// keys at or past r1 masked out
+__device__ inline void logits(const f4& s0, const f4& s1, float scale_log2, int row0, int r1,
+                              int g4, float (&x)[8]) {
+  if (row0 + TILE <= r1) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = s0[j] * scale_log2;
+      x[4 + j] = s1[j] * scale_log2;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[j] = row0 + g4 * 4 + j < r1 ? s0[j] * scale_log2 : -INFINITY;
+      x[4 + j] = row0 + 16 + g4 * 4 + j < r1 ? s1[j] * scale_log2 : -INFINITY;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- pass 1
+// grid (chunks, query blocks, b*h_kv); one (m, l) record per (row, chunk)
+__global__ __launch_bounds__(256, 2) void score_lse_kernel(KSegs segs, ChunkPlan plan,
+                                                           const uint16_t* __restrict__ q, int Hq,
+                                                           int Hkv, int W, float scale_log2,
+                                                           float* __restrict__ partial) {
+  __shared__ __attribute__((aligned(16))) char qs[QB * QROW];
+  __shared__ float red_m[WAVES][QB], red_l[WAVES][QB];
+  const int c = blockIdx.x, qb = blockIdx.y, bh = blockIdx.z;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int G = Hq / Hkv, nq = G * W, b = bh / Hkv, hkv = bh % Hkv;
+  int r0, r1;
+  const int si = chunk_rows(plan, segs, c, r0, r1);
+  const KSeg& ks = segs.s[si];
+  const uint16_t* qh = q + ((int64_t)b * Hq + hkv * G) * W * D;
+  const int q0 = qb * QB;
+  const int nqt = min(QT, (nq - q0 + 15) / 16);
+  stage_q(qs, qh, q0, nq);
+  for (int e = threadIdx.x; e < WAVES * QB; e += blockDim.x) {
+    red_m[e / QB][e % QB] = -INFINITY;
+    red_l[e / QB][e % QB] = 0.0f;
+  }
+  __syncthreads();
+
+  const int64_t base = (int64_t)bh * ks.row_stride * D;
+  const __amdgpu_buffer_rsrc_t rk = rsrc((const uint16_t*)ks.k + base, (uint32_t)r1 * ROWB);
+  for (int sc = r0; sc < r1; sc += SUB) {
+    // the wave's tiles of this sub-chunk: rows sc + (wave + i*WAVES)*TILE
+    KTiles K;
+#pragma unroll
+    for (int i = 0; i < TPW; ++i) k_issue(rk, sc + (wave + i * WAVES) * TILE, lane, K.k[i]);
+    for (int t = 0; t < nqt; ++t) {
+      // the wave's state so far enters through one of the four key-row lanes
+      float m = g4 == 0 ? red_m[wave][t * 16 + i16] : -INFINITY;
+      float l = g4 == 0 ? red_l[wave][t * 16 + i16] : 0.0f;
+#pragma unroll
+      for (int i = 0; i < TPW; ++i) {
+        const int row0 = sc + (wave + i * WAVES) * TILE;
+        if (row0 < r1) {
+          f4 s0, s1;
+          s_tile(K.k[i], qs, t, lane, s0, s1);
+          float x[8];
+          logits(s0, s1, scale_log2, row0, r1, g4, x);
+          const float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
+                                 fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+          if (mx > m + kLazy) {  // per-lane state: raise the reference maximum
+            l *= exp2f(m - mx);
+            m = mx;
+          }
+          float e = 0.0f;
+#pragma unroll
+          for (int j = 0; j < 8; ++j) e += exp2f(x[j] - m);
+          l += e;
+        }
+      }
+      // merge the four key-row lanes (g4) of each query column
+#pragma unroll
+      for (int o = 16; o <= 32; o <<= 1) {
+        const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(l, o, 64);
+        const float mn = fmaxf(m, m2);
+        l = (m == -INFINITY ? 0.0f : l * exp2f(m - mn)) +
+            (m2 == -INFINITY ? 0.0f : l2 * exp2f(m2 - mn));
+        m = mn;
+      }
+      if (g4 == 0) {  // the four lanes now agree; one keeps the wave's state
+        red_m[wave][t * 16 + i16] = m;
+        red_l[wave][t * 16 + i16] = l;
+      }
+    }
+  }
+  __syncthreads();
+  const int C = plan.n_chunks;
+  for (int r = threadIdx.x; r < nqt * 16; r += blockDim.x) {
+    if (q0 + r >= nq) continue;
+    float mm = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w) mm = fmaxf(mm, red_m[w][r]);
+    float ll = 0.0f;
+#pragma unroll
+    for (int w = 0; w < WAVES; ++w)
+      if (red_m[w][r] != -INFINITY) ll += red_l[w][r] * exp2f(red_m[w][r] - mm);
+    const int64_t qi = ((int64_t)b * Hq + hkv * G) * W + q0 + r;  // global query row
+    partial[(qi * C + c) * 2] = mm;
+    partial[(qi * C + c) * 2 + 1] = ll;
+  }
+}
+
+// ---------------------------------------------------------------- pass 2
+struct ScoreOut {
+  float* p[kMaxSeg];
+};
+
+// grid (chunks, b*h_kv); every query block of the head
+__global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan plan,
+                                                           const uint16_t* __restrict__ q, int Hq,
+                                                           int Hkv, int W, float scale_log2,
+                                                           const float* __restrict__ lse,
+                                                           ScoreOut out,
+                                                           double* __restrict__ mass_partial) {
+  __shared__ __attribute__((aligned(16))) char qs[QB * QROW];
+  __shared__ float ls[QB];
+  __shared__ double colsum[CHUNK];
+  __shared__ double red[WAVES];
+  const int c = blockIdx.x, bh = blockIdx.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int G = Hq / Hkv, nq = G * W, b = bh / Hkv, hkv = bh % Hkv;
+  int r0, r1;
+  const int si = chunk_rows(plan, segs, c, r0, r1);
+  const KSeg& ks = segs.s[si];
+  const uint16_t* qh = q + ((int64_t)b * Hq + hkv * G) * W * D;
+  const float* lh = lse + ((int64_t)b * Hq + hkv * G) * W;
+  for (int e = threadIdx.x; e < CHUNK; e += blockDim.x) colsum[e] = 0.0;
+
+  const int64_t base = (int64_t)bh * ks.row_stride * D;
+  const __amdgpu_buffer_rsrc_t rk = rsrc((const uint16_t*)ks.k + base, (uint32_t)r1 * ROWB);
+  for (int q0 = 0; q0 < nq; q0 += QB) {
+    const int nqt = min(QT, (nq - q0 + 15) / 16);
+    __syncthreads();  // the previous block's readers are done
+    stage_q(qs, qh, q0, nq);
+    for (int r = threadIdx.x; r < QB; r += blockDim.x)
+      ls[r] = q0 + r < nq ? lh[q0 + r] * kLog2e : INFINITY;  // padded rows: p = 0
+    __syncthreads();
+    for (int sc = r0; sc < r1; sc += SUB) {
+      KTiles K;
+#pragma unroll
+      for (int i = 0; i < TPW; ++i) k_issue(rk, sc + (wave + i * WAVES) * TILE, lane, K.k[i]);
+      float cs[TPW][8];
+#pragma unroll
+      for (int i = 0; i < TPW; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) cs[i][j] = 0.0f;
+      for (int t = 0; t < nqt; ++t) {
+        const float lq = ls[t * 16 + i16];
+#pragma unroll
+        for (int i = 0; i < TPW; ++i) {
+          if (sc + (wave + i * WAVES) * TILE < r1) {
+            f4 s0, s1;
+            s_tile(K.k[i], qs, t, lane, s0, s1);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              cs[i][j] += exp2f(fmaf(s0[j], scale_log2, -lq));
+              cs[i][4 + j] += exp2f(fmaf(s1[j], scale_log2, -lq));
+            }
+          }
+        }
+      }
+      // sum the 16 query columns (lanes i16), then add to the chunk's sums
+#pragma unroll
+      for (int i = 0; i < TPW; ++i) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          float v = cs[i][j];
+          v += __shfl_xor(v, 1, 64);
+          v += __shfl_xor(v, 2, 64);
+          v += __shfl_xor(v, 4, 64);
+          v += __shfl_xor(v, 8, 64);
+          cs[i][j] = v;
+        }
+        if (i16 == 0) {
+          const int kt = sc - r0 + (wave + i * WAVES) * TILE;  // tile offset in the chunk
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            colsum[kt + g4 * 4 + j] += (double)cs[i][j];
+            colsum[kt + 16 + g4 * 4 + j] += (double)cs[i][4 + j];
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // scores (rows past r1 were masked by never being written) and the
+  // chunk's mass (fixed-order reduction: deterministic)
+  float* sp = out.p[si];
+  double part = 0.0;
+  for (int e = threadIdx.x; e < CHUNK; e += blockDim.x) {
+    if (r0 + e < r1) {
+      if (sp) sp[(int64_t)bh * ks.n_rows + r0 + e] = (float)colsum[e];
+      part += colsum[e];
+    }
+  }
+  part = wave_sum_d(part);
+  if (lane == 0) red[wave] = part;
+  __syncthreads();
+  if (threadIdx.x == 0 && mass_partial)
+    mass_partial[(int64_t)bh * plan.n_chunks + c] = red[0] + red[1] + red[2] + red[3];
+}
+
+}  // namespace
+
+bool score_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt) {
+  if (sh.D != D || q_dt != UC_BF16) return false;
+  for (int i = 0; i < segs.n; ++i)
+    if (segs.s[i].kind != UC_SEG_DENSE || segs.s[i].dtype != UC_BF16) return false;
+  return true;
+}
+
+int score_mfma_chunk_rows() { return CHUNK; }
+
+int score_mfma_qblocks(int nq) { return (nq + QB - 1) / QB; }
+
+hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
+                                 const void* q, int W, float sm_scale, float* partial,
+                                 hipStream_t st) {
+  const int nq = (sh.Hq / sh.Hkv) * W;
+  dim3 grid(plan.n_chunks, score_mfma_qblocks(nq), sh.B * sh.Hkv);
+  hipLaunchKernelGGL(score_lse_kernel, grid, dim3(256), 0, st, segs, plan, (const uint16_t*)q,
+                     sh.Hq, sh.Hkv, W, sm_scale * kLog2e, partial);
+  return hipGetLastError();
+}
+
+hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
+                                 const void* q, int W, float sm_scale, const float* lse,
+                                 float* const* scores, double* mass_partial, hipStream_t st) {
+  ScoreOut so{};
+  for (int i = 0; i < segs.n; ++i) so.p[i] = scores ? scores[i] : nullptr;
+  dim3 grid(plan.n_chunks, sh.B * sh.Hkv);
+  hipLaunchKernelGGL(score_col_kernel, grid, dim3(256), 0, st, segs, plan, (const uint16_t*)q,
+                     sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so, mass_partial);
+  return hipGetLastError();
+}
+
+}  // namespace uc

@@ -211,6 +211,8 @@ def test_attend_full_budget_equals_uncompressed():
     (1, 4, 1, 64, "f32", 16, (64, 256, 256)),
     (2, 28, 4, 128, "bf16", 32, (512, 4096, 0)),
     (1, 14, 2, 128, "bf16", 5, (100, 333, 70)),
+    (1, 28, 4, 128, "bf16", 40, (300, 1500)),        # 280 query rows: two query blocks
+    (1, 14, 2, 128, "bf16", 600, (1030, 2100, 1)),   # 4200 query rows, ragged chunks
 ])
 def test_score_parity(B, Hq, Hkv, D, dtype, W, sizes):
     _print_case(test="score", B=B, Hq=Hq, Hkv=Hkv, D=D, dtype=dtype, W=W, sizes=sizes)
@@ -228,17 +230,25 @@ def test_score_parity(B, Hq, Hkv, D, dtype, W, sizes):
     sc_ref, ms_ref = ref.score64(ref.widen(q, dtype), K, np.asarray(seg_id, np.int32), len(sizes),
                                  sm_scale(D))
     shape = uc.make_shape(B, Hq, Hkv, D)
-    outs = [torch.empty(B, Hkv, n, device="cuda") for n in sizes]
-    mass = torch.empty(B, Hkv, len(sizes), device="cuda")
-    uc.uc_score_importance(shape, segs, dev(q, dtype), W, sm_scale(D), outs, mass)
-    torch.cuda.synchronize()
-    got = np.concatenate([o.cpu().numpy().reshape(B, Hkv, -1) for o in outs], axis=2).astype(np.float64)
-    rel = np.abs(got - sc_ref) / np.maximum(sc_ref, 1e-12)
     tot = Hq // Hkv * W
-    # per-row probability mass is resolved to ~1e-6 of the row total
-    assert np.all(np.abs(got - sc_ref) <= 2e-5 * sc_ref + 1e-7 * tot), rel.max()
-    assert np.allclose(mass.cpu().numpy(), ms_ref, rtol=2e-5, atol=1e-6 * tot)
-    assert np.allclose(got.sum(axis=2), tot, rtol=1e-5)
+    # bf16 / head dim 128 takes the matrix-core kernels; the VALU path is
+    # checked on the same inputs
+    for path in (uc.UC_PATH_AUTO, uc.UC_PATH_VALU):
+        prev = uc.uc_set_path(path)
+        try:
+            outs = [torch.empty(B, Hkv, n, device="cuda") for n in sizes]
+            mass = torch.empty(B, Hkv, len(sizes), device="cuda")
+            uc.uc_score_importance(shape, segs, dev(q, dtype), W, sm_scale(D), outs, mass)
+            torch.cuda.synchronize()
+        finally:
+            uc.uc_set_path(prev)
+        got = np.concatenate([o.cpu().numpy().reshape(B, Hkv, -1) for o in outs],
+                             axis=2).astype(np.float64)
+        rel = np.abs(got - sc_ref) / np.maximum(sc_ref, 1e-12)
+        # per-row probability mass is resolved to ~1e-6 of the row total
+        assert np.all(np.abs(got - sc_ref) <= 2e-5 * sc_ref + 1e-7 * tot), (path, rel.max())
+        assert np.allclose(mass.cpu().numpy(), ms_ref, rtol=2e-5, atol=1e-6 * tot), path
+        assert np.allclose(got.sum(axis=2), tot, rtol=1e-5), path
 
 
 def test_segment_mass_from_attention():
