@@ -18,6 +18,11 @@ using namespace uc;
 namespace uc {
 bool decode_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M);
 bool score_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt);
+bool prefill_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M);
+size_t prefill_mfma_workspace(const uc_shape& sh, const KSegs& segs);
+hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
+                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
+                               hipStream_t st);
 int score_mfma_chunk_rows();
 hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
                                  const void* q, int W, float sm_scale, float* partial,
@@ -216,6 +221,8 @@ size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs, i
   if (check_segments(shape, segs, n_segs, ks) || M < 1 || !dtype_ok(q_dt)) return 0;
   if (g_path.load() == UC_PATH_AUTO && decode_mfma_eligible(*shape, ks, q_dt, M))
     return decode_mfma_workspace(*shape, ks, M);
+  if (g_path.load() == UC_PATH_AUTO && prefill_mfma_eligible(*shape, ks, q_dt, M))
+    return prefill_mfma_workspace(*shape, ks);
   return generic_ws(*shape, ks, kAttRows, kAttMaxChunks, M, true);
 }
 
@@ -236,6 +243,12 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
     if (ws_bytes < need || (need && !ws))
       return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
     return launched(launch_decode_mfma(*shape, ks, q, M, sm_scale, o, lse, seg_lse, ws, s));
+  }
+  if (g_path.load() == UC_PATH_AUTO && prefill_mfma_eligible(*shape, ks, q_dt, M)) {
+    const size_t need = prefill_mfma_workspace(*shape, ks);
+    if (ws_bytes < need || (need && !ws))
+      return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+    return launched(launch_prefill_mfma(*shape, ks, q, M, sm_scale, o, lse, seg_lse, ws, s));
   }
   const ChunkPlan p = attend_plan(ks);
   const size_t need = generic_ws(*shape, ks, kAttRows, kAttMaxChunks, M, true);

@@ -34,51 +34,16 @@
 // bank conflicts and their addresses affine in the head dimension.  The four
 // waves merge through LDS and the workgroup writes unnormalised partials
 // (m, l, o) per query row; the combine kernel merges them.
+#include "mfma_util.h"
 #include "uc_common.h"
 
 namespace uc {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef float f2 __attribute__((ext_vector_type(2)));
-typedef short s4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+using namespace mf;
 
-constexpr int D = 128;
-constexpr int TILE = 32;          // rows per tile
 constexpr int WAVES = 4;
-constexpr int ROWB = D * 2;       // bytes of one bf16 row
-constexpr int LROW = ROWB + 32;   // bytes of one staged row in LDS (32 B padding)
-constexpr int TILEB = TILE * LROW;
-constexpr float kLazy = 8.0f;        // base-2 headroom before the reference max is raised
-
-// byte offset of 16-byte chunk c of row r inside a staged tile.  The 32-byte
-// row padding puts row r at bank 8r (mod 64): the eight rows a half-wave
-// reads in one transposing load land in disjoint 8-bank groups.
-__device__ inline int toff(int r, int c) { return r * LROW + (c << 4); }
-
-// two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32)
-__device__ inline uint32_t bf2(float a, float b) {
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, bf16x2));
-}
-
-__device__ inline f4 mfma(const u4& a, const u4& b, const f4& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-
-typedef __attribute__((address_space(3))) s4 lds_s4;
-
-__device__ inline u4 ds_tr(const char* p0, const char* p1) {
-  s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p0));
-  s4 b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p1));
-  return u4{(uint32_t)(uint16_t)a[0] | ((uint32_t)(uint16_t)a[1] << 16),
-            (uint32_t)(uint16_t)a[2] | ((uint32_t)(uint16_t)a[3] << 16),
-            (uint32_t)(uint16_t)b[0] | ((uint32_t)(uint16_t)b[1] << 16),
-            (uint32_t)(uint16_t)b[2] | ((uint32_t)(uint16_t)b[3] << 16)};
-}
+constexpr float kLazy = 8.0f;  // base-2 headroom before the reference max is raised
 
 // running softmax state of the lane's query (i16) and its O^T accumulators
 struct State {
@@ -132,43 +97,15 @@ __device__ inline void softmax_pv(State& st, const f4& s0, const f4& s1, float s
     e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
     psum += e[j];
   }
-  uint32_t hi[4], lo[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    hi[j] = bf2(e[2 * j], e[2 * j + 1]);
-    const float h0 = __uint_as_float(hi[j] << 16), h1 = __uint_as_float(hi[j] & 0xFFFF0000u);
-    lo[j] = bf2(e[2 * j] - h0, e[2 * j + 1] - h1);
-  }
-  const u4 phi = u4{hi[0], hi[1], hi[2], hi[3]};
-  const u4 plo = u4{lo[0], lo[1], lo[2], lo[3]};
+  u4 phi, plo;
+  split_p(e, phi, plo);
   st.l += psum;
-  // lane (i16, g4) reads, for dim tile d, rows g4*4 + i16/4 (+16) at dims d*16 + 4*(i16%4)
-  const int rr = g4 * 4 + (i16 >> 2);
-  const int cb = (i16 & 3) >> 1, hb8 = (i16 & 1) * 8;
 #pragma unroll
   for (int d = 0; d < 8; ++d) {
-    const char* a0 = lv + toff(rr, 2 * d + cb) + hb8;
-    const char* a1 = lv + toff(rr + 16, 2 * d + cb) + hb8;
-    const u4 vt = ds_tr(a0, a1);
+    const u4 vt = vt_operand(lv, d, i16, g4);
     st.acc[d] = mfma(vt, phi, st.acc[d]);
     st.acc[d] = mfma(vt, plo, st.acc[d]);
   }
-}
-
-// Raw buffer descriptor over `bytes` bytes from `base`: loads at or past the
-// end return zeros, and each load needs one 32-bit offset register.
-__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
-}
-
-__device__ inline u4 bload(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
-}
-
-// a value the compiler cannot see through (keeps byte-extract conversions)
-__device__ inline uint32_t opaque(uint32_t x) {
-  asm volatile("" : "+v"(x));
-  return x;
 }
 
 // ---------------------------------------------------------------- dense rows
@@ -287,10 +224,6 @@ __device__ inline void codes8(uint32_t w0, float (&c)[8]) {
       c[4 + e] = (float)((t >> 8) & 0xFFu);
     }
   }
-}
-
-__device__ inline uint32_t bload32(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
 }
 
 template <int BITS>

@@ -1,0 +1,391 @@
+// attend_prefill.hip -- multi-query (prefill / denoising) attention over
+// bf16 segments on the CDNA4 matrix cores (App. E, "Attention over
+// heterogeneous cache segments": one softmax across all segments; packed
+// segments are dequantised into a reusable workspace before attention).
+//
+// Work item: 128 query rows of one (b, h_kv) -- the rows of its G query heads
+// are contiguous in q -- in one workgroup of four waves; each wave owns two
+// 16-row query tiles.  The workgroup walks every key tile (32 rows) of every
+// segment once: the four waves stage the K and V rows of tile i+2 through
+// registers into a three-deep ring of padded LDS tiles while the waves
+// compute tile i.  Per tile and wave:
+//   S^T = K Q^T    v_mfma_f32_16x16x32_bf16, K rows read from LDS as the A
+//                  operand (shared by both query tiles), Q^T in registers;
+//   softmax        base 2, lazy reference maximum (one ballot per tile and
+//                  query tile), running per-segment sums for seg_lse;
+//   O^T += V^T P   V^T by transposing LDS reads (shared by both query
+//                  tiles), P as bf16 hi + lo parts.
+// Outputs (normalised O, lse, per-segment lse) are written directly; no
+// split over keys.  Workgroups are mapped so that those of one (b, h_kv) run
+// on the same XCD and share its L2 copy of the head's rows.
+//
+// Packed segments first go through dequant_kernel: codes -> round_to_bf16(
+// fmaf(code, scale, min)) into a [B, Hkv, n_full, D] bf16 workspace; their
+// residual tails are read in place.
+#include "mfma_util.h"
+#include "uc_common.h"
+
+namespace uc {
+namespace {
+
+using namespace mf;
+
+constexpr int WAVES = 4;
+constexpr int QTW = 2;                     // query tiles per wave
+constexpr int QROWS = WAVES * QTW * 16;    // query rows per workgroup
+constexpr int STAGES = 3;                  // key/value tiles staged in LDS
+constexpr int STAGEB = 2 * TILEB;          // K tile + V tile
+constexpr float kLazy = 8.0f;
+constexpr int kMaxViews = 2 * kMaxSeg;
+
+// dense row views of the logical sequence, in order; seg = logical segment
+struct View {
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t bh_stride;  // elements between consecutive (b, h_kv)
+  int n;              // rows
+  int seg;
+};
+
+struct Views {
+  View v[kMaxViews];
+  int n;
+  int tiles;  // total key tiles
+};
+
+struct QState {
+  float m, l, ls;  // reference max (base 2), row sum, running sum of the current segment
+  f4 acc[8];       // O^T, dims d*16 + g4*4 + j of query column i16
+};
+
+// tile t of the sequence -> view index and first row
+__device__ inline int tile_view(const Views& vs, int t, int& row0) {
+  int i = 0;
+  while (i + 1 < vs.n && t >= (vs.v[i].n + TILE - 1) / TILE) {
+    t -= (vs.v[i].n + TILE - 1) / TILE;
+    ++i;
+  }
+  row0 = t * TILE;
+  return i;
+}
+
+// one thread's share of staging a tile: rows tid/16 and tid/16 + 16, chunk tid%16
+struct Stage {
+  u4 k[2], v[2];
+};
+
+__device__ inline void stage_load(const Views& vs, int t, int bh, Stage& S) {
+  int row0;
+  const View& w = vs.v[tile_view(vs, t, row0)];
+  const __amdgpu_buffer_rsrc_t rk = rsrc(w.k + bh * w.bh_stride, (uint32_t)w.n * ROWB);
+  const __amdgpu_buffer_rsrc_t rv = rsrc(w.v + bh * w.bh_stride, (uint32_t)w.n * ROWB);
+  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+  const int off = (row0 + r) * ROWB + c * 16;
+  S.k[0] = bload(rk, off, 0);
+  S.k[1] = bload(rk, off, 16 * ROWB);
+  S.v[0] = bload(rv, off, 0);
+  S.v[1] = bload(rv, off, 16 * ROWB);
+}
+
+__device__ inline void stage_store(char* buf, const Stage& S) {
+  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+  *reinterpret_cast<u4*>(buf + toff(r, c)) = S.k[0];
+  *reinterpret_cast<u4*>(buf + toff(r + 16, c)) = S.k[1];
+  *reinterpret_cast<u4*>(buf + TILEB + toff(r, c)) = S.v[0];
+  *reinterpret_cast<u4*>(buf + TILEB + toff(r + 16, c)) = S.v[1];
+}
+
+// softmax of one query tile's 8 logits per lane; returns the bf16 hi/lo
+// probability operands.  n_valid < TILE masks the tile's last rows.
+__device__ inline void tile_softmax(QState& st, const f4& s0, const f4& s1, float scale_log2,
+                                    int n_valid, int g4, u4& phi, u4& plo) {
+  float p[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    p[j] = s0[j];
+    p[4 + j] = s1[j];
+  }
+  if (n_valid < TILE) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      if (g4 * 4 + j >= n_valid) p[j] = -INFINITY;
+      if (16 + g4 * 4 + j >= n_valid) p[4 + j] = -INFINITY;
+    }
+  }
+  float mx = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])),
+                   fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7]))) * scale_log2;
+  if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazy)) {  // rare: raise the reference max
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float m_new = fmaxf(st.m, mx);
+    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+    st.l *= alpha;
+    st.ls *= alpha;
+#pragma unroll
+    for (int d = 0; d < 8; ++d) st.acc[d] *= alpha;
+    st.m = m_new;
+  }
+  float e[8], psum = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
+    psum += e[j];
+  }
+  st.l += psum;
+  st.ls += psum;
+  split_p(e, phi, plo);
+}
+
+// sum of a lane-partial value over the four key-row lanes of a query column
+__device__ inline float col_sum(float x) {
+  x += __shfl_xor(x, 16, 64);
+  x += __shfl_xor(x, 32, 64);
+  return x;
+}
+
+__global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const uint16_t* __restrict__ q,
+                                                              int Hq, int Hkv, int M, int nseg,
+                                                              int n_qblocks, int n_work,
+                                                              float scale_log2, float* __restrict__ o,
+                                                              float* __restrict__ lse,
+                                                              float* __restrict__ seg_lse) {
+  __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGEB];
+  // XCD-aware work mapping: consecutive work items (the query blocks of one
+  // head, which share its K/V rows) go to the same XCD
+  const int per_xcd = (n_work + 7) / 8;
+  const int work = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (work >= n_work) return;
+  const int qb = work % n_qblocks, bh = work / n_qblocks;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int G = Hq / Hkv, nq = G * M, b = bh / Hkv, hkv = bh % Hkv;
+  const int64_t qbase = ((int64_t)b * Hq + hkv * G) * M;  // first query row of the head
+  const int r_wave = qb * QROWS + wave * QTW * 16;        // first row of the wave
+
+  u4 qop[QTW][4];
+  QState st[QTW];
+#pragma unroll
+  for (int t = 0; t < QTW; ++t) {
+    const int r = r_wave + t * 16 + i16;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      qop[t][k] = r < nq ? *reinterpret_cast<const u4*>(q + (qbase + r) * D + k * 32 + g4 * 8)
+                         : u4{0, 0, 0, 0};
+    st[t].m = -INFINITY;
+    st[t].l = 0.0f;
+    st[t].ls = 0.0f;
+#pragma unroll
+    for (int d = 0; d < 8; ++d) st[t].acc[d] = f4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // segments without rows never see a tile: their log-sum-exp stays -inf
+  if (seg_lse && g4 == 0) {
+#pragma unroll
+    for (int t = 0; t < QTW; ++t) {
+      const int r = r_wave + t * 16 + i16;
+      if (r < nq)
+        for (int a = 0; a < nseg; ++a) seg_lse[(qbase + r) * nseg + a] = -INFINITY;
+    }
+  }
+  const int T = vs.tiles;
+  {
+    Stage S;
+    stage_load(vs, 0, bh, S);
+    stage_store(lds, S);
+    if (T > 1) {
+      stage_load(vs, 1, bh, S);
+      stage_store(lds + STAGEB, S);
+    }
+  }
+  __syncthreads();
+  int cur_view = -1;
+  for (int t = 0; t < T; ++t) {
+    Stage S;
+    const bool pre = t + 2 < T;
+    if (pre) stage_load(vs, t + 2, bh, S);
+    const char* lk = lds + (t % STAGES) * STAGEB;
+    const char* lv = lk + TILEB;
+    int row0;
+    const int vi = tile_view(vs, t, row0);
+    const int n_valid = min(TILE, vs.v[vi].n - row0);
+    if (seg_lse && vi != cur_view && cur_view >= 0 && vs.v[vi].seg != vs.v[cur_view].seg) {
+      // the previous logical segment ended: its log-sum-exp per query row
+#pragma unroll
+      for (int qt = 0; qt < QTW; ++qt) {
+        const float ls = col_sum(st[qt].ls);
+        const int r = r_wave + qt * 16 + i16;
+        if (g4 == 0 && r < nq)
+          seg_lse[(qbase + r) * nseg + vs.v[cur_view].seg] =
+              ls > 0.0f ? (st[qt].m + __log2f(ls)) * kLn2 : -INFINITY;
+        st[qt].ls = 0.0f;
+      }
+    }
+    cur_view = vi;
+    // K rows of the tile as A operands, shared by the query tiles
+    u4 ka[8];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      ka[k] = *reinterpret_cast<const u4*>(lk + toff(i16, k * 4 + g4));
+      ka[4 + k] = *reinterpret_cast<const u4*>(lk + toff(16 + i16, k * 4 + g4));
+    }
+    u4 phi[QTW], plo[QTW];
+#pragma unroll
+    for (int qt = 0; qt < QTW; ++qt) {
+      f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        s0 = mfma(ka[k], qop[qt][k], s0);
+        s1 = mfma(ka[4 + k], qop[qt][k], s1);
+      }
+      tile_softmax(st[qt], s0, s1, scale_log2, n_valid, g4, phi[qt], plo[qt]);
+    }
+#pragma unroll
+    for (int d = 0; d < 8; ++d) {
+      const u4 vt = vt_operand(lv, d, i16, g4);
+#pragma unroll
+      for (int qt = 0; qt < QTW; ++qt) {
+        st[qt].acc[d] = mfma(vt, phi[qt], st[qt].acc[d]);
+        st[qt].acc[d] = mfma(vt, plo[qt], st[qt].acc[d]);
+      }
+    }
+    if (pre) stage_store(lds + ((t + 2) % STAGES) * STAGEB, S);
+    __syncthreads();
+  }
+  // outputs
+#pragma unroll
+  for (int qt = 0; qt < QTW; ++qt) {
+    const int r = r_wave + qt * 16 + i16;
+    const float l = col_sum(st[qt].l);
+    const float ls = col_sum(st[qt].ls);
+    if (r < nq) {
+      const float inv = 1.0f / l;
+      float* orow = o + (qbase + r) * D;
+#pragma unroll
+      for (int d = 0; d < 8; ++d) *reinterpret_cast<f4*>(orow + d * 16 + g4 * 4) = st[qt].acc[d] * inv;
+      if (g4 == 0) {
+        if (lse) lse[qbase + r] = (st[qt].m + __log2f(l)) * kLn2;
+        if (seg_lse && cur_view >= 0)
+          seg_lse[(qbase + r) * nseg + vs.v[cur_view].seg] =
+              ls > 0.0f ? (st[qt].m + __log2f(ls)) * kLn2 : -INFINITY;
+      }
+    }
+  }
+}
+
+// codes -> bf16 values of one packed segment's whole row groups:
+// out[b, h, r, c] = round_to_bf16(fmaf(code, scale, min)); one thread per
+// 8 channels of one row, K and V
+__global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
+                               uint16_t* __restrict__ vout) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (bh, row, c8)
+  const int c8 = (int)(e % (D / 8));
+  const int64_t rr = e / (D / 8);
+  const int r = (int)(rr % s.n_full), bh = (int)(rr / s.n_full);
+  if (bh >= BH) return;
+  int bits;
+  int64_t off;
+  u4 ko, vo;
+  if (!head_codes(s, bh, D, bits, off)) {
+    const uint32_t nan2 = 0x7FC07FC0u;
+    ko = u4{nan2, nan2, nan2, nan2};
+    vo = ko;
+  } else {
+    const int rb = D * bits / 8, G = s.group, ngk = s.n_full / G;
+    const uint8_t* ck = s.codes_k + off + (int64_t)r * rb + c8 * bits;  // 8 channels = bits bytes
+    const uint8_t* cv = s.codes_v + off + (int64_t)r * rb + c8 * bits;
+    uint64_t wk = 0, wv = 0;
+    for (int i = 0; i < bits; ++i) {
+      wk |= (uint64_t)ck[i] << (8 * i);
+      wv |= (uint64_t)cv[i] << (8 * i);
+    }
+    const int mask = (1 << bits) - 1;
+    const float* sk = s.scale_k + ((int64_t)bh * ngk + r / G) * D + c8 * 8;
+    const float* mk = s.min_k + ((int64_t)bh * ngk + r / G) * D + c8 * 8;
+    // value groups: G consecutive channels of the row (G may be below 8)
+    const int64_t vrow = ((int64_t)bh * s.n_full + r) * (D / G);
+    uint32_t kw[4], vw[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int c0 = 2 * j, c1 = 2 * j + 1;
+      const int64_t v0i = vrow + (c8 * 8 + c0) / G, v1i = vrow + (c8 * 8 + c1) / G;
+      const float k0 = fmaf((float)((wk >> (c0 * bits)) & mask), sk[c0], mk[c0]);
+      const float k1 = fmaf((float)((wk >> (c1 * bits)) & mask), sk[c1], mk[c1]);
+      const float v0 = fmaf((float)((wv >> (c0 * bits)) & mask), s.scale_v[v0i], s.min_v[v0i]);
+      const float v1 = fmaf((float)((wv >> (c1 * bits)) & mask), s.scale_v[v1i], s.min_v[v1i]);
+      kw[j] = bf2(k0, k1);
+      vw[j] = bf2(v0, v1);
+    }
+    ko = u4{kw[0], kw[1], kw[2], kw[3]};
+    vo = u4{vw[0], vw[1], vw[2], vw[3]};
+  }
+  const int64_t oi = ((int64_t)bh * s.n_full + r) * D + c8 * 8;
+  *reinterpret_cast<u4*>(kout + oi) = ko;
+  *reinterpret_cast<u4*>(vout + oi) = vo;
+}
+
+}  // namespace
+
+bool prefill_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M) {
+  if (sh.D != D || q_dt != UC_BF16) return false;
+  if ((sh.Hq / sh.Hkv) * M <= 16) return false;  // the decode kernel's range
+  for (int i = 0; i < segs.n; ++i)
+    if (segs.s[i].dtype != UC_BF16) return false;
+  return true;
+}
+
+// Workspace: bf16 K and V of every packed segment's whole row groups.
+size_t prefill_mfma_workspace(const uc_shape& sh, const KSegs& segs) {
+  size_t bytes = 0;
+  for (int i = 0; i < segs.n; ++i)
+    if (segs.s[i].kind == UC_SEG_PACKED)
+      bytes += (((size_t)sh.B * sh.Hkv * segs.s[i].n_full * D * 2 * 2) + 255) & ~(size_t)255;
+  return bytes;
+}
+
+hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
+                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
+                               hipStream_t st) {
+  const int BH = sh.B * sh.Hkv;
+  Views vs{};
+  char* wp = (char*)ws;
+  int tiles = 0;
+  for (int i = 0; i < segs.n; ++i) {
+    const KSeg& s = segs.s[i];
+    if (s.kind == UC_SEG_DENSE) {
+      vs.v[vs.n++] = View{(const uint16_t*)s.k, (const uint16_t*)s.v, (int64_t)s.row_stride * D,
+                          s.n_rows, i};
+      continue;
+    }
+    if (s.n_full > 0) {
+      uint16_t* kd = (uint16_t*)wp;
+      uint16_t* vd = kd + (size_t)BH * s.n_full * D;
+      wp += (((size_t)BH * s.n_full * D * 2 * 2) + 255) & ~(size_t)255;
+      const int64_t n_thr = (int64_t)BH * s.n_full * (D / 8);
+      hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)((n_thr + 255) / 256)), dim3(256), 0, st,
+                         s, BH, kd, vd);
+      vs.v[vs.n++] = View{kd, vd, (int64_t)s.n_full * D, s.n_full, i};
+    }
+    if (s.tail_len > 0)
+      vs.v[vs.n++] = View{(const uint16_t*)s.tail_k, (const uint16_t*)s.tail_v,
+                          (int64_t)s.tail_len * D, s.tail_len, i};
+  }
+  // drop empty views (their tiles would be empty); keep the order
+  int n = 0;
+  for (int i = 0; i < vs.n; ++i)
+    if (vs.v[i].n > 0) vs.v[n++] = vs.v[i];
+  vs.n = n;
+  for (int i = 0; i < n; ++i) tiles += (vs.v[i].n + TILE - 1) / TILE;
+  vs.tiles = tiles;
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nq = (sh.Hq / sh.Hkv) * M;
+  const int n_qblocks = (nq + QROWS - 1) / QROWS;
+  const int n_work = n_qblocks * BH;
+  const int grid = (n_work + 7) / 8 * 8;
+  hipLaunchKernelGGL(prefill_mfma_kernel, dim3(grid), dim3(256), 0, st, vs, (const uint16_t*)q,
+                     sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sm_scale * kLog2e, o, lse,
+                     seg_lse);
+  return hipGetLastError();
+}
+
+}  // namespace uc

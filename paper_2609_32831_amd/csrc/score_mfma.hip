@@ -23,17 +23,14 @@
 // Column sums: a lane sums its key's probabilities over the query tiles in
 // fp32, the 16 query columns of a tile are added by a butterfly, and the
 // query blocks are accumulated in fp64 in LDS; chunk masses are fp64.
+#include "mfma_util.h"
 #include "uc_common.h"
 
 namespace uc {
 namespace {
 
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+using namespace mf;
 
-constexpr int D = 128;
-constexpr int TILE = 32;             // keys per tile
 constexpr int WAVES = 4;
 constexpr int TPW = 4;               // key tiles per wave and sub-chunk
 constexpr int SUB = WAVES * TPW * TILE;  // 512 keys per sub-chunk (K held in registers)
@@ -41,21 +38,7 @@ constexpr int CHUNK = 2 * SUB;       // keys per workgroup
 constexpr int QB = 256;              // query rows per block (16 tiles)
 constexpr int QT = QB / 16;
 constexpr int QROW = D * 2 + 16;     // bytes of one staged query row (16 B padding)
-constexpr int ROWB = D * 2;
 constexpr float kLazy = 8.0f;
-
-__device__ inline f4 mfma(const u4& a, const u4& b, const f4& c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
-                                                 __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
-
-__device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
-}
-
-__device__ inline u4 bload(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
-}
 
 // A wave's TPW key tiles of a sub-chunk as A operands: k[i][blk*4 + t] =
 // row (tile i) blk*16 + i16, dims t*32 + g4*8 .. +7.  Rows past the

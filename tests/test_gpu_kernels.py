@@ -340,3 +340,49 @@ def test_decode_mfma_parity(case):
     # the kernel paths agree far inside the bar
     assert np.abs(outs["mfma"][0] - outs["valu"][0]).max() < 5e-4
     assert np.abs(outs["mfma_o"][0] - outs["valu"][0]).max() < 5e-4
+
+
+# ------------------------------------------------------------------ matrix-core prefill
+
+PCASES = [
+    # B, Hq, Hkv, M, G, bits, per_head, sizes (text, vit_full, vit_keep, pack, tail, cap)
+    (1, 28, 4, 64, 64, 4, False, (100, 900, 300, 1000 + 17, 5, 8)),   # 448 rows per KV head
+    (2, 14, 2, 37, 16, 2, True, (33, 200, 77, 130, 1, 2)),            # ragged block, group 16
+    (1, 28, 4, 3, 128, 8, False, (0, 100, 3, 130, 0, 4)),             # 21 rows, 8-bit, empty text
+    (1, 16, 1, 2, 32, 4, False, (1, 64, 33, 520, 1, 1)),              # 32 rows, 16 heads per KV
+    (1, 28, 4, 40, 64, 4, False, (0, 0, 0, 31, 0, 1)),                # tail-only packed rows
+]
+
+
+@pytest.mark.parametrize("case", PCASES, ids=[f"p{i}" for i in range(len(PCASES))])
+def test_prefill_mfma_parity(case):
+    B, Hq, Hkv, M, G, bits, per_head, sizes = case
+    _print_case(test="prefill_mfma", B=B, Hq=Hq, Hkv=Hkv, M=M, G=G, bits=bits, sizes=sizes)
+    D = 128
+    segs, K, V, seg_id = _mixed_case(B, Hq, Hkv, D, "bf16", sizes, seed=3 * G + bits, G=G,
+                                     bits=bits, per_head=per_head)
+    q = rand_rows(55, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+    sm = sm_scale(D)
+    o_ref, lse_ref, sl_ref, _ = ref.attend(ref.widen(q, "bf16"), K, V, None, seg_id, 4, sm)
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    qd = dev(q, "bf16")
+    outs = {}
+    for name, path in (("mfma", uc.UC_PATH_AUTO), ("valu", uc.UC_PATH_VALU)):
+        prev = uc.uc_set_path(path)
+        try:
+            o = torch.empty(B, Hq, M, D, device="cuda")
+            lse = torch.empty(B, Hq, M, device="cuda")
+            sl = torch.empty(B, Hq, M, 4, device="cuda")
+            uc.uc_attend_mixed(shape, segs, qd, M, sm, o, lse, sl)
+            torch.cuda.synchronize()
+            outs[name] = (o.cpu().numpy(), lse.cpu().numpy(), sl.cpu().numpy())
+        finally:
+            uc.uc_set_path(prev)
+    for name, (o, lse, sl) in outs.items():
+        check_attention(o, o_ref, f"path {name}")
+        assert np.allclose(lse, lse_ref, rtol=1e-5, atol=1e-4), name
+        fin = np.isfinite(sl_ref)
+        assert np.array_equal(np.isfinite(sl), fin), name
+        assert np.allclose(sl[fin], sl_ref[fin], rtol=1e-5, atol=1e-4), name
+    assert np.abs(outs["mfma"][0] - outs["valu"][0]).max() < 5e-4
+
