@@ -123,3 +123,98 @@ def attend_head(w, comp: Dict, q: np.ndarray, q_dtype: str, tail_k=None, tail_v=
     o, lse, sl, smass = attend(widen(q, q_dtype)[None], K, V, P, np.concatenate(seg_id), n_segs,
                                sm_scale(w.D))
     return o[0], lse[0], sl[0], smass[0]
+
+
+def denoise_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
+                  bits_given: Optional[Dict[int, List[int]]] = None) -> Dict:
+    """Oracle chain of a denoising workload with drifting latent keys and
+    queries and per-head latent code widths (text-to-image), for batch
+    element b and its Hkv KV heads.
+
+    Timestep t: the latent keys and the query block take the random-walk
+    step (t >= 1); the latent is attended dense until widths exist (t = 0,
+    the first full-KV step), afterwards fake-quantised with the widths in
+    force; at every rescore_every-th step the per-head latent mass of that
+    step's attention (Eq. 1 bracket at head granularity) sets the widths for
+    the following steps: all heads at 2 bits, raised to 4 bits in descending
+    mass order within the batch element's storage budget.
+
+    steps: timesteps whose attention is returned (rows: optional query rows
+    of every query head, default all).  bits_given[t]: widths decided at step
+    t to use instead of the oracle's own decision (for runs where only sampled
+    rows can be attended and the full masses are not computed).
+    Returns {"bits": {t: widths}, "mass": {t: [Hkv] latent masses},
+    "att": {t: (o, lse, seg_lse) per KV head}, "packed": {t: quantised latent
+    per KV head (steps with widths in force)}}."""
+    G, Hq, Hkv, D, M = w.group_size, w.Hq, w.Hkv, w.D, w.M
+    lat = next(i for i, s in enumerate(w.segments) if s.policy == "quant")
+    ls = w.segments[lat]
+    N, Gq = ls.n, ls.group
+    bh0 = b * Hkv
+    seg_k = [None] * len(w.segments)
+    seg_v = []
+    for i, s in enumerate(w.segments):
+        seg_v.append(gen.segment_kv(w, i, "v", bh0=bh0, nbh=Hkv))
+        if i != lat:
+            seg_k[i] = gen.segment_kv(w, i, "k", bh0=bh0, nbh=Hkv)
+    lk, mk = gen.segment_kv(w, lat, "k", bh0=bh0, nbh=Hkv, master=True)
+    dk = gen.Drift(w, gen.T_DRIFT_K, mk, ls.dtype, start=bh0 * N * D)
+    q, mq = gen.queries(w, gen.T_QPRE, M, bh0=b * Hq, nbh=Hq, step=0, master=True)
+    dq = gen.Drift(w, gen.T_DRIFT_Q, mq, w.q_dtype, start=b * Hq * M * D)
+    orig = sum(dense_bytes(s.n, D, w.q_dtype) for s in w.segments)
+    fixed = sum(dense_bytes(s.n, D, s.dtype) for i, s in enumerate(w.segments) if i != lat)
+    budget_b, fixed_b = Hkv * orig / w.budget_ratio, Hkv * fixed
+    seg_id = np.concatenate([np.full(s.n, i, np.int32) for i, s in enumerate(w.segments)])
+    nseg = len(w.segments)
+    sm = sm_scale(D)
+    bits = None
+    out = {"bits": {}, "mass": {}, "att": {}, "packed": {}}
+    last = max(steps)
+    for t in range(last + 1):
+        if t > 0:
+            lk = dk.step()
+            q = dq.step()
+        rescore = t % w.rescore_every == 0
+        if not (t in steps or (rescore and (bits_given is None or t not in bits_given))):
+            if rescore:
+                bits = list(bits_given[t])
+            continue
+        need_mass = rescore and (bits_given is None or t not in bits_given)
+        att, mass = [], []
+        for h in range(Hkv):
+            ks, vs = [], []
+            for i, s in enumerate(w.segments):
+                if i != lat:
+                    ks.append(widen(seg_k[i][h], s.dtype))
+                    vs.append(widen(seg_v[i][h], s.dtype))
+                elif bits is None:
+                    ks.append(widen(lk[h], s.dtype))
+                    vs.append(widen(seg_v[i][h], s.dtype))
+                else:
+                    pk = quantize(lk[h][None], seg_v[i][h][None], s.dtype, Gq, [bits[h]])
+                    if t in steps:
+                        out["packed"].setdefault(t, []).append(pk)
+                    kh, vh = dequant(pk, N, D, Gq, s.dtype)
+                    ks.append(kh[0])
+                    vs.append(vh[0])
+            K = np.concatenate(ks)[None, None]
+            V = np.concatenate(vs)[None, None]
+            qh = widen(q[h * G:(h + 1) * G], w.q_dtype)          # [G, M, D]
+            if need_mass or rows is None:
+                o, lse, sl, smass = attend(qh[None], K, V, None, seg_id, nseg, sm)
+                mass.append(float(smass[0, :, :, lat].sum()))  # over the G heads and M rows
+                if rows is not None:
+                    o, lse, sl = o[:, :, rows], lse[:, :, rows], sl[:, :, rows]
+            else:
+                o, lse, sl, _ = attend(qh[:, rows][None], K, V, None, seg_id, nseg, sm)
+            att.append((o[0], lse[0], sl[0]))
+        if t in steps:
+            out["att"][t] = att
+        if rescore:
+            if need_mass:
+                out["mass"][t] = np.asarray(mass, np.float64)
+                bits = [int(x) for x in assign_bits(mass, N, D, Gq, ls.dtype, budget_b, fixed_b)]
+            else:
+                bits = list(bits_given[t])
+            out["bits"][t] = list(bits)
+    return out

@@ -16,9 +16,9 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (NAME_DT, TORCH_DT, dense_segment, make_shape, packed_segment, uc_append_rows,
-               uc_assign_bits, uc_attend_mixed, uc_attend_workspace_size, uc_dense_bytes,
-               uc_evict_rows_for_budget, uc_packed_bytes, uc_quantize_segment,
+from . import (NAME_DT, TORCH_DT, dense_segment, make_shape, packed_layout, packed_segment,
+               uc_append_rows, uc_assign_bits, uc_attend_mixed, uc_attend_workspace_size,
+               uc_dense_bytes, uc_evict_rows_for_budget, uc_packed_bytes, uc_quantize_segment,
                uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep)
 
 TORCH = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
@@ -201,3 +201,95 @@ class Run:
         qb = 4 if w.q_dtype == "f32" else 2
         M = w.M if w.mode == "prefill" else 1
         return BH * per + w.B * w.Hq * M * w.D * (qb + 4)
+
+
+class DenoiseRun:
+    """A denoising workload whose quantised latent gets per-head code widths
+    from its attention mass (text-to-image): a kept text segment plus one
+    latent segment under a shared storage budget per batch element.
+
+    Timestep t: at t = 0 (no widths yet) the latent is attended dense, as the
+    first full-KV step that initialises the statistics (Sec. 3.3); afterwards
+    the current latent keys are re-quantised with the current widths
+    (int2/int4 per KV head) and attended packed.  Every rescore_every steps
+    the step's per-segment log-sum-exps give each KV head's latent mass
+    (Eq. 1 bracket at head granularity), and the widths for the next steps are
+    assigned greedily: all heads at 2 bits, heads raised to 4 bits in
+    descending mass order while the batch element's stored bytes stay within
+    its budget.  Host-side control flow only."""
+
+    def __init__(self, w, seg_k, seg_v, device="cuda"):
+        self.w, self.device = w, device
+        B, Hkv, D = w.B, w.Hkv, w.D
+        self.BH = B * Hkv
+        self.shape = make_shape(w.B, w.Hq, w.Hkv, D)
+        self.sm = sm_scale(D)
+        self.lat = next(i for i, s in enumerate(w.segments) if s.policy == "quant")
+        ls = w.segments[self.lat]
+        self.G, self.N = ls.group, ls.n
+        self.dt = NAME_DT[ls.dtype]
+        self.dense = [dense_segment(seg_k[i], seg_v[i]) for i in range(len(w.segments))]
+        self.packed = packed_segment(B, Hkv, self.N, D, self.G, TORCH[ls.dtype], bits=4,
+                                     head_bits=[4] * self.BH, device=device)
+        self.bits = None
+        io = NAME_DT[w.q_dtype]
+        orig = sum(uc_dense_bytes(s.n, D, io) for s in w.segments)
+        fixed = sum(uc_dense_bytes(s.n, D, NAME_DT[s.dtype]) for i, s in enumerate(w.segments)
+                    if i != self.lat)
+        self.budget_b = Hkv * orig / w.budget_ratio   # per batch element
+        self.fixed_b = Hkv * fixed
+        q_dt = NAME_DT[w.q_dtype]
+        ws = max(uc_attend_workspace_size(self.shape, self.dense, q_dt, w.M),
+                 uc_attend_workspace_size(self.shape, self._segs_packed(), q_dt, w.M))
+        self.ws = torch.empty(max(ws, 256), dtype=torch.uint8, device=device)
+        nseg = len(w.segments)
+        self.lse = torch.empty(B, w.Hq, w.M, device=device)
+        self.seg_lse = torch.empty(B, w.Hq, w.M, nseg, device=device)
+        self.mass = torch.empty(B, Hkv, nseg, device=device)
+
+    def _segs_packed(self):
+        return [self.packed if i == self.lat else d for i, d in enumerate(self.dense)]
+
+    def set_bits(self, bits):
+        """Per-(b, h_kv) code widths; codes of consecutive heads are packed
+        back to back."""
+        off, total = packed_layout(self.BH, self.N, self.w.D, self.G, bits)
+        t = self.packed.t
+        assert total <= t["codes_k"].numel()
+        t["head_bits"].copy_(torch.tensor(bits, dtype=torch.uint8))
+        t["code_off"].copy_(torch.tensor(off, dtype=torch.int64))
+        self.packed.desc.bits = max(bits)
+        self.bits = list(bits)
+
+    def assign(self, mass_latent):
+        """Greedy int2/int4 widths of every batch element from [B, Hkv] masses."""
+        w = self.w
+        out = []
+        for b in range(w.B):
+            out += uc_assign_bits(list(mass_latent[b]), self.N, w.D, self.G, self.dt,
+                                  self.budget_b, self.fixed_b)
+        return out
+
+    def step(self, t: int, q: torch.Tensor, o: torch.Tensor, want_stats: bool = False):
+        """One timestep over the current latent keys (already in seg_k).  With
+        want_stats (and at every rescoring step) lse / seg_lse are produced;
+        at a rescoring step the widths for the following steps are assigned
+        and returned."""
+        w = self.w
+        if self.bits is None:
+            segs = self.dense
+        else:
+            segs = self._segs_packed()
+            uc_quantize_segment(self.shape, self.dense[self.lat].t["k"],
+                                self.dense[self.lat].t["v"], self.N, self.packed)
+        rescore = w.rescore_every and t % w.rescore_every == 0
+        stats = want_stats or rescore
+        uc_attend_mixed(self.shape, segs, q, w.M, self.sm, o, self.lse if stats else None,
+                        self.seg_lse if stats else None, ws=self.ws)
+        if not rescore:
+            return None
+        uc_segment_mass(self.shape, w.M, len(w.segments), self.lse, self.seg_lse, self.mass)
+        m = self.mass[:, :, self.lat].cpu().numpy()
+        new = self.assign(m)
+        self.set_bits(new)
+        return new

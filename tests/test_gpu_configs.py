@@ -20,8 +20,8 @@ if not torch.cuda.is_available():
 import oracle.pipeline as op  # noqa: E402
 import workloads as gen  # noqa: E402
 from gpu_util import check_attention, host_bytes  # noqa: E402
-from paper_2609_32831_amd.runner import Run  # noqa: E402
-from workloads.device import device_inputs  # noqa: E402
+from paper_2609_32831_amd.runner import DenoiseRun, Run  # noqa: E402
+from workloads.device import DenoiseInputs, device_inputs  # noqa: E402
 
 
 def _case(name, **kw):
@@ -151,3 +151,92 @@ def test_cfg3_image_editing_prefill():
             o_ref, _, _, _ = op.attend_head(w, comp, q, w.q_dtype)
             og = outs[t][b, h * G:(h + 1) * G].cpu().numpy()
             check_attention(og, o_ref, f"{w.name} b={b} h={h} t={t}")
+
+
+def _denoise_gpu(w, check):
+    """All timesteps of a drifting denoising workload on the GPU; returns the
+    width decisions, the latent masses at rescoring steps, outputs and
+    statistics at the check steps, and the packed codes at the last step."""
+    inp = DenoiseInputs(w, "cuda")
+    run = DenoiseRun(w, inp.seg_k, inp.seg_v)
+    bits, mass, outs = {}, {}, {}
+    for t in range(w.steps):
+        if t > 0:
+            inp.advance()
+        o = torch.empty(w.B, w.Hq, w.M, w.D, device="cuda")
+        nb = run.step(t, inp.q, o, want_stats=t in check)
+        if nb is not None:
+            bits[t] = nb
+            mass[t] = run.mass[:, :, run.lat].cpu().numpy().astype(np.float64)
+        if t in check:
+            outs[t] = (o.cpu().numpy(), run.lse.cpu().numpy(), run.seg_lse.cpu().numpy())
+    torch.cuda.synchronize()
+    return run, bits, mass, outs
+
+
+def _check_denoise_outputs(w, b, ref, outs, steps, rows=None):
+    G = w.group_size
+    for t in steps:
+        o, lse, sl = outs[t]
+        for h in range(w.Hkv):
+            ro, rl, rs = ref["att"][t][h]
+            og, lg, sg = o[b, h * G:(h + 1) * G], lse[b, h * G:(h + 1) * G], sl[b, h * G:(h + 1) * G]
+            if rows is not None:
+                og, lg, sg = og[:, rows], lg[:, rows], sg[:, rows]
+            check_attention(og, ro, f"{w.name} b={b} h={h} t={t}")
+            assert np.allclose(lg, rl, rtol=1e-5, atol=1e-4), (t, h)
+            assert np.allclose(sg, rs, rtol=1e-5, atol=1e-4), (t, h)
+
+
+def test_cfg4_text_to_image_chain():
+    """Text-to-image at its full context (768 text + 4096 latent rows per KV
+    head, batch 8) with a 128-query block per query head, all 50 timesteps:
+    drift of latent keys and queries, per-step requantisation, rescoring every
+    10 steps with per-head int2/int4 widths under the 2.5x budget.  The oracle
+    follows batch elements 0 and 5 through every decision."""
+    w = gen.scaled(gen.CFG4, M=128)
+    check = [0, 1, 10, 11, 49]
+    run, bits, mass, outs = _denoise_gpu(w, check)
+    Hkv = w.Hkv
+    for b in (0, 5):
+        _case(w.name, b=b, M=w.M)
+        ref = op.denoise_chain(w, b, check)
+        for t, rb in ref["bits"].items():
+            assert np.allclose(mass[t][b], ref["mass"][t], rtol=2e-5), (t, mass[t][b], ref["mass"][t])
+            gb = bits[t][b * Hkv:(b + 1) * Hkv]
+            if gb != rb:  # only a near tie of the deciding masses may differ
+                m = np.sort(ref["mass"][t])
+                gaps = np.abs(np.diff(m)) / m[1:]
+                assert gaps.min() <= 1e-6, (t, gb, rb, ref["mass"][t])
+        assert sorted(bits[40][b * Hkv:(b + 1) * Hkv]) == [2, 4, 4, 4]  # the 2.5x budget
+        _check_denoise_outputs(w, b, ref, outs, check)
+        # codes of the last step, bit for bit
+        t = w.steps - 1
+        off = run.packed.t["code_off"].cpu().numpy()
+        ck = run.packed.t["codes_k"].cpu().numpy()
+        cv = run.packed.t["codes_v"].cpu().numpy()
+        for h, pk in enumerate(ref["packed"][t]):
+            bh = b * Hkv + h
+            n = pk["codes_k"].shape[0]
+            assert np.array_equal(ck[off[bh]:off[bh] + n], pk["codes_k"]), (b, h)
+            assert np.array_equal(cv[off[bh]:off[bh] + n], pk["codes_v"]), (b, h)
+
+
+def test_cfg4_text_to_image_full_sampled():
+    """Text-to-image at full size (4096-query blocks, batch 8, 50 timesteps).
+    The oracle attends sampled query rows of batch element 0 with the widths
+    the GPU chose; the per-row latent mass that drives the choice is checked
+    on the same rows, and the widths follow from the GPU's masses by the
+    budget rule."""
+    w = gen.CFG4
+    check = [0, 10, 49]
+    run, bits, mass, outs = _denoise_gpu(w, check)
+    b, Hkv, G = 0, w.Hkv, w.group_size
+    for t, bt in bits.items():
+        assert bt == run.assign(mass[t]), t
+        assert all(sorted(bt[i * Hkv:(i + 1) * Hkv]) == [2, 4, 4, 4] for i in range(w.B)), t
+    rows = np.arange(3, w.M, 271)
+    _case(w.name, b=b, rows=len(rows))
+    ref = op.denoise_chain(w, b, check, rows=rows,
+                           bits_given={t: bt[b * Hkv:(b + 1) * Hkv] for t, bt in bits.items()})
+    _check_denoise_outputs(w, b, ref, outs, check, rows=rows)

@@ -406,3 +406,22 @@ def test_generator_pins(gen):
     kf = kw.view(np.float32)
     std = kf.std(axis=0)
     assert set(np.argsort(std)[-2:]) == set(ch.tolist()) and len(ch) == 2
+
+
+def test_generator_drift(gen):
+    """Random-walk drift: a slice of a tensor drifts exactly as inside the
+    whole, each step adds sigma * N(0,1) to the fp64 master, and the stored
+    copy is the master rounded to the storage dtype."""
+    w = gen.scaled(gen.CFG4, M=8)
+    k, m = gen.segment_kv(w, 1, "k", bh0=0, nbh=3, row0=0, n=64, master=True)
+    whole = gen.Drift(w, gen.T_DRIFT_K, m.copy(), "bf16")
+    part = gen.Drift(w, gen.T_DRIFT_K, m[2].copy(), "bf16", start=2 * 64 * w.D)
+    prev = m.copy()
+    for _ in range(3):
+        a, b = whole.step(), part.step()
+        assert np.array_equal(a[2], b)
+        step = (whole.master - prev) / w.drift_sigma
+        assert abs(step.mean()) < 0.02 and abs(step.std() - 1) < 0.02
+        prev = whole.master.copy()
+    rounded = torch.from_numpy(whole.master).to(torch.bfloat16).view(torch.int16).numpy()
+    assert np.array_equal(a.view(np.int16), rounded)

@@ -64,7 +64,7 @@ def lib():
         L.ucgen_rows.restype = None
         L.ucgen_rows.argtypes = [u64, i64, i32, i64, i32, i64, vp, vp, vp, i32, vp, vp]
         L.ucgen_drift.restype = None
-        L.ucgen_drift.argtypes = [u64, u64, ctypes.c_double, i64, vp, i32, vp]
+        L.ucgen_drift.argtypes = [u64, u64, ctypes.c_double, i64, i64, vp, i32, vp]
         _lib = L
     return _lib
 
@@ -319,19 +319,21 @@ def decode_kv(w: Workload, which: str, row0: int, n: int, bh0: int = 0,
 
 class Drift:
     """Random walk X_t = X_{t-1} + sigma * eps_t on an fp64 master copy, rounded
-    to the storage dtype after every step (text-to-image timesteps)."""
+    to the storage dtype after every step (text-to-image timesteps).  The
+    master holds elements start .. start + size - 1 of the whole tensor (a
+    slice drifts exactly as inside the whole tensor)."""
 
-    def __init__(self, w: Workload, tensor: int, master: np.ndarray, dtype: str):
-        self.w, self.tensor, self.master, self.dtype = w, tensor, master, dtype
+    def __init__(self, w: Workload, tensor: int, master: np.ndarray, dtype: str, start: int = 0):
+        self.w, self.tensor, self.dtype, self.start = w, tensor, dtype, start
+        self.master = np.ascontiguousarray(master, np.float64)
         self.t = 0
 
     def step(self) -> np.ndarray:
         self.t += 1
         out = np.empty(self.master.shape, NP_STORAGE[self.dtype])
         base = stream(self.w.seed, self.w.cfg_id, self.tensor)
-        lib().ucgen_drift(base, self.t, self.w.drift_sigma, self.master.size,
-                          self.master.ctypes.data, DTYPE_CODE[self.dtype],
-                          out.ctypes.data)
+        lib().ucgen_drift(base, self.t, self.w.drift_sigma, self.start, self.master.size,
+                          self.master.ctypes.data, DTYPE_CODE[self.dtype], out.ctypes.data)
         return out
 
 

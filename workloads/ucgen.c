@@ -141,14 +141,16 @@ void ucgen_rows(uint64_t base, int64_t bh0, int BH, int64_t N, int D, int64_t ro
   }
 }
 
-/* Random-walk drift of an fp64 master copy: x += sigma * z (z from
- * ucgen_stream(base, {step}) element k), then the rounded copy is stored. */
-void ucgen_drift(uint64_t base, uint64_t step, double sigma, int64_t n,
+/* Random-walk drift of an fp64 master copy: x += sigma * z, then the rounded
+ * copy is stored.  master[k] is element start + k of the whole tensor and z
+ * is element start + k of the stream ucgen_stream(base, {step}), so any slice
+ * of a tensor drifts exactly as it does inside the whole. */
+void ucgen_drift(uint64_t base, uint64_t step, double sigma, int64_t start, int64_t n,
                  double* master, int dtype, void* out) {
   uint64_t seed = ucgen_stream(base, &step, 1);
 #pragma omp parallel for schedule(static)
   for (int64_t k = 0; k < n; ++k) {
-    master[k] += sigma * ucgen_normal_at(seed, (uint64_t)k);
+    master[k] += sigma * ucgen_normal_at(seed, (uint64_t)(start + k));
     store(out, k, master[k], dtype);
   }
 }
