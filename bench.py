@@ -48,6 +48,10 @@ def parse():
                     help="no benchmark: read rocprofv3 output under DIR/trace (kernel trace "
                          "stats), DIR/fetch and DIR/write (FETCH_SIZE / WRITE_SIZE counters of "
                          "runs with --calibrate-copy) and write the summaries under profiles/")
+    ap.add_argument("--prefill", action="store_true",
+                    help="instead of the decode job: time the multi-query attention of the "
+                         "image-editing (cfg3) and text-to-image (cfg4) workloads and report "
+                         "matrix-core utilisation (one JSON line each)")
     ap.add_argument("--profile-command", default="",
                     help="with --summarize-profiles: the commands that produced DIR (recorded)")
     return ap.parse_args()
@@ -203,10 +207,81 @@ def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
     }
 
 
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def prefill_bench(args):
+    """Multi-query attention steps of the editing (4096-query blocks against
+    text + compacted ViT + int4 VAE, fixed cache, fresh queries) and
+    text-to-image (4096-query blocks against text + int2/int4 latent that is
+    requantised every step) workloads.  Utilisation = algorithmic flops
+    4 * M * N_attended * D * Hq * B per step over the bf16 dense peak."""
+    import torch
+
+    import workloads as gen
+    from paper_2609_32831_amd import uc_attend_mixed
+    from paper_2609_32831_amd.runner import DenoiseRun, Run
+    from workloads.device import DenoiseInputs, device_inputs
+
+    def timed(fn, n):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(max(1, args.warmup)):
+            fn(0)
+        torch.cuda.synchronize()
+        a.record()
+        for i in range(n):
+            fn(i)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / n
+
+    n = max(1, args.steps)
+    # image editing: scoring on the first latent block, 25% ViT, int4 VAE
+    w = gen.CFG3
+    inp = device_inputs(w, "cuda")
+    run = Run(w, inp)
+    qs = [inp["q_pre"](t) for t in range(2)]
+    torch.cuda.synchronize()
+    t_c = timed(lambda i: (run.score(q_obs=qs[0], W=w.M), run.select(), run.quantize()), 1)
+    o = torch.empty(w.B, w.Hq, w.M, w.D, device="cuda")
+    t_p = timed(lambda i: run.prefill_step(qs[i % 2], o), n)
+    n_att = sum(p.k if p.kind == "evict" else s.n for s, p in zip(w.segments, run.pol))
+    fl = 4.0 * w.M * n_att * w.D * w.Hq * w.B
+    print(json.dumps({"metric": "prefill attention step (matrix cores)", "workload": w.name,
+                      "ms_per_step": round(t_p, 4), "tflops": round(fl / t_p / 1e9, 1),
+                      "frac_of_bf16_peak": round(fl / t_p / 1e9 / BF16_PEAK_TFLOPS, 4),
+                      "gflop_per_step": round(fl / 1e9, 1), "attended_rows": n_att,
+                      "compress_ms": round(t_c, 3), "steps": n}), flush=True)
+    del run, inp, qs, o
+    torch.cuda.empty_cache()
+    # text-to-image: widths from the first (dense) step, then requantise + attend
+    w = gen.CFG4
+    di = DenoiseInputs(w, "cuda")
+    run = DenoiseRun(w, di.seg_k, di.seg_v)
+    o = torch.empty(w.B, w.Hq, w.M, w.D, device="cuda")
+    run.step(0, di.q, o)
+    torch.cuda.synchronize()
+    segs = run._segs_packed()
+    t_s = timed(lambda i: run.step(1 + i, di.q, o), n)  # requantise + attend (no rescoring)
+    t_a = timed(lambda i: uc_attend_mixed(run.shape, segs, di.q, w.M, run.sm, o, ws=run.ws), n)
+    fl = 4.0 * w.M * w.n_context * w.D * w.Hq * w.B
+    print(json.dumps({"metric": "prefill attention step (matrix cores)", "workload": w.name,
+                      "ms_per_step": round(t_a, 4), "tflops": round(fl / t_a / 1e9, 1),
+                      "frac_of_bf16_peak": round(fl / t_a / 1e9 / BF16_PEAK_TFLOPS, 4),
+                      "gflop_per_step": round(fl / 1e9, 1), "attended_rows": w.n_context,
+                      "step_with_requantise_ms": round(t_s, 4), "bits": run.bits[:8],
+                      "steps": n}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_profiles:
         summarize_profiles(args.summarize_profiles, args.profile_command)
+        return
+    if args.prefill:
+        if args.gpus != 1:
+            sys.exit(2)
+        prefill_bench(args)
         return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "

@@ -145,7 +145,7 @@ __device__ inline void dense_head(const DenseSet& S, char* lv, const u4 (&qop)[4
 // Rows [r0, r1) of one head's dense rows at kb / vb (row-major, D per row).
 // The wave takes tiles wave, wave + WAVES, ...; only the last tile of the
 // range can be partial, and it is always one of the epilogue tiles.
-__device__ inline void dense_loop(State& st, const uint16_t* kb, const uint16_t* vb, int r0, int r1,
+__device__ __attribute__((always_inline)) inline void dense_loop(State& st, const uint16_t* kb, const uint16_t* vb, int r0, int r1,
                                   int wave, int lane, const u4 (&qop)[4], float scale_log2,
                                   char* lv) {
   const int n_tiles = (r1 - r0 + TILE - 1) / TILE;
@@ -296,7 +296,7 @@ __device__ inline void packed_head(const PackedSet<BITS>& S, char* lk, char* lv,
 
 // Rows [r0, r1) of one head's packed rows; both ends are multiples of TILE.
 template <int BITS>
-__device__ inline void packed_loop(State& st, const PackedSeg& P, int r0, int r1, int wave,
+__device__ __attribute__((always_inline)) inline void packed_loop(State& st, const PackedSeg& P, int r0, int r1, int wave,
                                    int lane, const u4 (&qop)[4], float scale_log2, char* lk,
                                    char* lv) {
   const int n_tiles = (r1 - r0) / TILE;
@@ -370,7 +370,7 @@ __device__ inline int64_t qrow_of(const Ctx& c, int qs) {
 
 // merge the four waves' state through LDS and write one partial record;
 // ok = false marks the record invalid (l = NaN)
-__device__ inline void flush(State& st, char* lds, const Ctx& c, int slot, bool ok, int lane,
+__device__ __attribute__((always_inline)) inline void flush(State& st, char* lds, const Ctx& c, int slot, bool ok, int lane,
                              int wave) {
   const int i16 = lane & 15, g4 = lane >> 4;
   // full row sums: the four lanes of one query hold partial sums
@@ -414,7 +414,7 @@ __device__ inline void flush(State& st, char* lds, const Ctx& c, int slot, bool 
 }
 
 // one workgroup's share [r0, r1) of segment ks for head bh
-__device__ inline bool segment_share(State& st, const KSeg& ks, int bh, int r0, int r1, int wave,
+__device__ __attribute__((always_inline)) inline bool segment_share(State& st, const KSeg& ks, int bh, int r0, int r1, int wave,
                                      int lane, const u4 (&qop)[4], float scale_log2, char* lk,
                                      char* lv) {
   if (r1 <= r0) return true;

@@ -14,7 +14,9 @@
 //   softmax        base 2, lazy reference maximum (one ballot per tile and
 //                  query tile), running per-segment sums for seg_lse;
 //   O^T += V^T P   V^T by transposing LDS reads (shared by both query
-//                  tiles), P as bf16 hi + lo parts.
+//                  tiles); fp16 P and V on v_mfma_f32_16x16x32_f16 when every
+//                  V value of the call fits fp16 (a range pass sets a flag the
+//                  kernel reads), else bf16 V with P as bf16 hi + lo parts.
 // Outputs (normalised O, lse, per-segment lse) are written directly; no
 // split over keys.  Workgroups are mapped so that those of one (b, h_kv) run
 // on the same XCD and share its L2 copy of the head's rows.
@@ -87,16 +89,28 @@ __device__ inline void stage_load(const Views& vs, int t, int bh, Stage& S) {
   S.v[1] = bload(rv, off, 16 * ROWB);
 }
 
+// F16: V is staged as fp16 (the range check found every value in range)
+template <bool F16>
 __device__ inline void stage_store(char* buf, const Stage& S) {
   const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
   *reinterpret_cast<u4*>(buf + toff(r, c)) = S.k[0];
   *reinterpret_cast<u4*>(buf + toff(r + 16, c)) = S.k[1];
-  *reinterpret_cast<u4*>(buf + TILEB + toff(r, c)) = S.v[0];
-  *reinterpret_cast<u4*>(buf + TILEB + toff(r + 16, c)) = S.v[1];
+  u4 v0 = S.v[0], v1 = S.v[1];
+  if (F16) {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      v0[e] = bf2_to_h2(v0[e]);
+      v1[e] = bf2_to_h2(v1[e]);
+    }
+  }
+  *reinterpret_cast<u4*>(buf + TILEB + toff(r, c)) = v0;
+  *reinterpret_cast<u4*>(buf + TILEB + toff(r + 16, c)) = v1;
 }
 
-// softmax of one query tile's 8 logits per lane; returns the bf16 hi/lo
-// probability operands.  n_valid < TILE masks the tile's last rows.
+// softmax of one query tile's 8 logits per lane; returns the probability
+// operands: fp16 P (F16) or bf16 hi/lo parts.  n_valid < TILE masks the
+// tile's last rows.
+template <bool F16>
 __device__ inline void tile_softmax(QState& st, const f4& s0, const f4& s1, float scale_log2,
                                     int n_valid, int g4, u4& phi, u4& plo) {
   float p[8];
@@ -133,7 +147,12 @@ __device__ inline void tile_softmax(QState& st, const f4& s0, const f4& s1, floa
   }
   st.l += psum;
   st.ls += psum;
-  split_p(e, phi, plo);
+  if (F16) {
+    // probabilities stay below 2^kLazy, well inside fp16
+    phi = u4{h2(e[0], e[1]), h2(e[2], e[3]), h2(e[4], e[5]), h2(e[6], e[7])};
+  } else {
+    split_p(e, phi, plo);
+  }
 }
 
 // sum of a lane-partial value over the four key-row lanes of a query column
@@ -143,62 +162,25 @@ __device__ inline float col_sum(float x) {
   return x;
 }
 
-__global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const uint16_t* __restrict__ q,
-                                                              int Hq, int Hkv, int M, int nseg,
-                                                              int n_qblocks, int n_work,
-                                                              float scale_log2, float* __restrict__ o,
-                                                              float* __restrict__ lse,
-                                                              float* __restrict__ seg_lse) {
-  __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGEB];
-  // XCD-aware work mapping: consecutive work items (the query blocks of one
-  // head, which share its K/V rows) go to the same XCD
-  const int per_xcd = (n_work + 7) / 8;
-  const int work = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-  if (work >= n_work) return;
-  const int qb = work % n_qblocks, bh = work / n_qblocks;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i16 = lane & 15, g4 = lane >> 4;
-  const int G = Hq / Hkv, nq = G * M, b = bh / Hkv, hkv = bh % Hkv;
-  const int64_t qbase = ((int64_t)b * Hq + hkv * G) * M;  // first query row of the head
-  const int r_wave = qb * QROWS + wave * QTW * 16;        // first row of the wave
-
-  u4 qop[QTW][4];
-  QState st[QTW];
-#pragma unroll
-  for (int t = 0; t < QTW; ++t) {
-    const int r = r_wave + t * 16 + i16;
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      qop[t][k] = r < nq ? *reinterpret_cast<const u4*>(q + (qbase + r) * D + k * 32 + g4 * 8)
-                         : u4{0, 0, 0, 0};
-    st[t].m = -INFINITY;
-    st[t].l = 0.0f;
-    st[t].ls = 0.0f;
-#pragma unroll
-    for (int d = 0; d < 8; ++d) st[t].acc[d] = f4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  // segments without rows never see a tile: their log-sum-exp stays -inf
-  if (seg_lse && g4 == 0) {
-#pragma unroll
-    for (int t = 0; t < QTW; ++t) {
-      const int r = r_wave + t * 16 + i16;
-      if (r < nq)
-        for (int a = 0; a < nseg; ++a) seg_lse[(qbase + r) * nseg + a] = -INFINITY;
-    }
-  }
+// the key-tile loop of one workgroup (see the file comment); returns the
+// view of the last tile
+template <bool F16>
+__device__ __attribute__((always_inline)) inline int tile_loop(
+    const Views& vs, int bh, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW],
+    float scale_log2, int r_wave, int nq, int64_t qbase, int nseg, float* seg_lse, int i16,
+    int g4) {
+  int cur_view = -1;
   const int T = vs.tiles;
   {
     Stage S;
     stage_load(vs, 0, bh, S);
-    stage_store(lds, S);
+    stage_store<F16>(lds, S);
     if (T > 1) {
       stage_load(vs, 1, bh, S);
-      stage_store(lds + STAGEB, S);
+      stage_store<F16>(lds + STAGEB, S);
     }
   }
   __syncthreads();
-  int cur_view = -1;
   for (int t = 0; t < T; ++t) {
     Stage S;
     const bool pre = t + 2 < T;
@@ -237,20 +219,77 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const ui
         s0 = mfma(ka[k], qop[qt][k], s0);
         s1 = mfma(ka[4 + k], qop[qt][k], s1);
       }
-      tile_softmax(st[qt], s0, s1, scale_log2, n_valid, g4, phi[qt], plo[qt]);
+      tile_softmax<F16>(st[qt], s0, s1, scale_log2, n_valid, g4, phi[qt], plo[qt]);
     }
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
       const u4 vt = vt_operand(lv, d, i16, g4);
 #pragma unroll
       for (int qt = 0; qt < QTW; ++qt) {
-        st[qt].acc[d] = mfma(vt, phi[qt], st[qt].acc[d]);
-        st[qt].acc[d] = mfma(vt, plo[qt], st[qt].acc[d]);
+        if (F16) {
+          st[qt].acc[d] = mfma_f16(vt, phi[qt], st[qt].acc[d]);
+        } else {
+          st[qt].acc[d] = mfma(vt, phi[qt], st[qt].acc[d]);
+          st[qt].acc[d] = mfma(vt, plo[qt], st[qt].acc[d]);
+        }
       }
     }
-    if (pre) stage_store(lds + ((t + 2) % STAGES) * STAGEB, S);
+    if (pre) stage_store<F16>(lds + ((t + 2) % STAGES) * STAGEB, S);
     __syncthreads();
   }
+  return cur_view;
+}
+
+__global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const uint16_t* __restrict__ q,
+                                                              int Hq, int Hkv, int M, int nseg,
+                                                              int n_qblocks, int n_work,
+                                                              float scale_log2, float* __restrict__ o,
+                                                              float* __restrict__ lse,
+                                                              float* __restrict__ seg_lse,
+                                                              const int* __restrict__ v_unsafe) {
+  __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGEB];
+  // XCD-aware work mapping: consecutive work items (the query blocks of one
+  // head, which share its K/V rows) go to the same XCD
+  const int per_xcd = (n_work + 7) / 8;
+  const int work = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+  if (work >= n_work) return;
+  const int qb = work % n_qblocks, bh = work / n_qblocks;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i16 = lane & 15, g4 = lane >> 4;
+  const int G = Hq / Hkv, nq = G * M, b = bh / Hkv, hkv = bh % Hkv;
+  const int64_t qbase = ((int64_t)b * Hq + hkv * G) * M;  // first query row of the head
+  const int r_wave = qb * QROWS + wave * QTW * 16;        // first row of the wave
+
+  u4 qop[QTW][4];
+  QState st[QTW];
+#pragma unroll
+  for (int t = 0; t < QTW; ++t) {
+    const int r = r_wave + t * 16 + i16;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      qop[t][k] = r < nq ? *reinterpret_cast<const u4*>(q + (qbase + r) * D + k * 32 + g4 * 8)
+                         : u4{0, 0, 0, 0};
+    st[t].m = -INFINITY;
+    st[t].l = 0.0f;
+    st[t].ls = 0.0f;
+#pragma unroll
+    for (int d = 0; d < 8; ++d) st[t].acc[d] = f4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // segments without rows never see a tile: their log-sum-exp stays -inf
+  if (seg_lse && g4 == 0) {
+#pragma unroll
+    for (int t = 0; t < QTW; ++t) {
+      const int r = r_wave + t * 16 + i16;
+      if (r < nq)
+        for (int a = 0; a < nseg; ++a) seg_lse[(qbase + r) * nseg + a] = -INFINITY;
+    }
+  }
+  const bool f16 = *v_unsafe == 0;
+  const int cur_view = f16 ? tile_loop<true>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
+                                             nseg, seg_lse, i16, g4)
+                           : tile_loop<false>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
+                                              nseg, seg_lse, i16, g4);
   // outputs
 #pragma unroll
   for (int qt = 0; qt < QTW; ++qt) {
@@ -276,7 +315,7 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const ui
 // out[b, h, r, c] = round_to_bf16(fmaf(code, scale, min)); one thread per
 // 8 channels of one row, K and V
 __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
-                               uint16_t* __restrict__ vout) {
+                               uint16_t* __restrict__ vout, int* __restrict__ v_unsafe) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (bh, row, c8)
   const int c8 = (int)(e % (D / 8));
   const int64_t rr = e / (D / 8);
@@ -321,7 +360,21 @@ __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
   const int64_t oi = ((int64_t)bh * s.n_full + r) * D + c8 * 8;
   *reinterpret_cast<u4*>(kout + oi) = ko;
   *reinterpret_cast<u4*>(vout + oi) = vo;
+  if (bf2_over_f16(vo[0]) || bf2_over_f16(vo[1]) || bf2_over_f16(vo[2]) || bf2_over_f16(vo[3]))
+    atomicOr(v_unsafe, 1);
 }
+
+// V rows of a dense view: flag values that fp16 cannot hold
+__global__ void vrange_kernel(const uint16_t* __restrict__ v, int64_t bh_stride, int n_rows,
+                              int* __restrict__ v_unsafe) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // 8 elements each
+  if (e >= (int64_t)n_rows * (D / 8)) return;
+  const u4 x = *reinterpret_cast<const u4*>(v + blockIdx.y * bh_stride + e * 8);
+  if (bf2_over_f16(x[0]) || bf2_over_f16(x[1]) || bf2_over_f16(x[2]) || bf2_over_f16(x[3]))
+    atomicOr(v_unsafe, 1);
+}
+
+__global__ void flag_clear_kernel(int* flag) { *flag = 0; }
 
 }  // namespace
 
@@ -333,9 +386,10 @@ bool prefill_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int 
   return true;
 }
 
-// Workspace: bf16 K and V of every packed segment's whole row groups.
+// Workspace: a flag word (some V value outside fp16's range), then bf16 K
+// and V of every packed segment's whole row groups.
 size_t prefill_mfma_workspace(const uc_shape& sh, const KSegs& segs) {
-  size_t bytes = 0;
+  size_t bytes = 256;
   for (int i = 0; i < segs.n; ++i)
     if (segs.s[i].kind == UC_SEG_PACKED)
       bytes += (((size_t)sh.B * sh.Hkv * segs.s[i].n_full * D * 2 * 2) + 255) & ~(size_t)255;
@@ -347,8 +401,12 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
                                hipStream_t st) {
   const int BH = sh.B * sh.Hkv;
   Views vs{};
-  char* wp = (char*)ws;
+  int* v_unsafe = (int*)ws;
+  char* wp = (char*)ws + 256;
   int tiles = 0;
+  // the PV product runs in fp16 when every V value fits fp16 (checked here,
+  // decided in the kernel); otherwise in bf16 hi + lo parts
+  hipLaunchKernelGGL(flag_clear_kernel, dim3(1), dim3(1), 0, st, v_unsafe);
   for (int i = 0; i < segs.n; ++i) {
     const KSeg& s = segs.s[i];
     if (s.kind == UC_SEG_DENSE) {
@@ -362,7 +420,7 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
       wp += (((size_t)BH * s.n_full * D * 2 * 2) + 255) & ~(size_t)255;
       const int64_t n_thr = (int64_t)BH * s.n_full * (D / 8);
       hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)((n_thr + 255) / 256)), dim3(256), 0, st,
-                         s, BH, kd, vd);
+                         s, BH, kd, vd, v_unsafe);
       vs.v[vs.n++] = View{kd, vd, (int64_t)s.n_full * D, s.n_full, i};
     }
     if (s.tail_len > 0)
@@ -374,7 +432,14 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   for (int i = 0; i < vs.n; ++i)
     if (vs.v[i].n > 0) vs.v[n++] = vs.v[i];
   vs.n = n;
-  for (int i = 0; i < n; ++i) tiles += (vs.v[i].n + TILE - 1) / TILE;
+  for (int i = 0; i < n; ++i) {
+    tiles += (vs.v[i].n + TILE - 1) / TILE;
+    if (segs.s[vs.v[i].seg].kind == UC_SEG_PACKED && vs.v[i].v != (const uint16_t*)segs.s[vs.v[i].seg].tail_v)
+      continue;  // dequantised rows were checked by the dequant kernel
+    const int64_t per = (int64_t)vs.v[i].n * (D / 8);
+    hipLaunchKernelGGL(vrange_kernel, dim3((unsigned)((per + 255) / 256), BH), dim3(256), 0, st,
+                       vs.v[i].v, vs.v[i].bh_stride, vs.v[i].n, v_unsafe);
+  }
   vs.tiles = tiles;
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -384,7 +449,7 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   const int grid = (n_work + 7) / 8 * 8;
   hipLaunchKernelGGL(prefill_mfma_kernel, dim3(grid), dim3(256), 0, st, vs, (const uint16_t*)q,
                      sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sm_scale * kLog2e, o, lse,
-                     seg_lse);
+                     seg_lse, v_unsafe);
   return hipGetLastError();
 }
 

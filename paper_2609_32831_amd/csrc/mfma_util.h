@@ -43,6 +43,32 @@ __device__ inline f4 mfma(const u4& a, const u4& b, const f4& c) {
                                                  __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline f4 mfma_f16(const u4& a, const u4& b, const f4& c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8, a),
+                                                __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+}
+
+// two floats -> packed fp16 pair, round to nearest even (v_cvt_pk_f16_f32)
+__device__ inline uint32_t h2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f2{a, b}, f16x2));
+}
+
+// packed bf16 pair -> packed fp16 pair (exact for magnitudes in fp16's
+// normal range; callers check the range)
+__device__ inline uint32_t bf2_to_h2(uint32_t w) {
+  return h2(__uint_as_float(w << 16), __uint_as_float(w & 0xFFFF0000u));
+}
+
+// true if some bf16 of the packed word reaches 2^16 in magnitude (or is
+// inf/NaN): such a value has no fp16 counterpart (fp16's largest is 65504 and
+// the bf16 value below 2^16 is 65280)
+__device__ inline bool bf2_over_f16(uint32_t w) {
+  return (w & 0x7FFFu) >= 0x4780u || ((w >> 16) & 0x7FFFu) >= 0x4780u;
+}
+
 // two transposing 64-bit LDS reads -> one 8 x bf16 operand
 __device__ inline u4 ds_tr(const char* p0, const char* p1) {
   s4 a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4*)(p0));

@@ -384,5 +384,33 @@ def test_prefill_mfma_parity(case):
         fin = np.isfinite(sl_ref)
         assert np.array_equal(np.isfinite(sl), fin), name
         assert np.allclose(sl[fin], sl_ref[fin], rtol=1e-5, atol=1e-4), name
-    assert np.abs(outs["mfma"][0] - outs["valu"][0]).max() < 5e-4
+    # fp16 probabilities (11 significant bits) on the matrix-core path
+    assert np.abs(outs["mfma"][0] - outs["valu"][0]).max() < 1.5e-3
 
+
+
+def test_prefill_value_outside_fp16_range():
+    """A value row holding 70000 (beyond fp16's 65504) switches the prefill
+    PV product from fp16 to bf16 hi + lo parts; the result still matches.  The
+    row's key is zero so its probability is moderate and the output finite."""
+    B, Hq, Hkv, D, M = 1, 28, 4, 128, 9
+    segs, K, V, seg_id = _mixed_case(B, Hq, Hkv, D, "bf16", (64, 300, 100, 256, 3, 8), seed=11)
+    kt, vt = segs[0].t["k"], segs[0].t["v"]          # dense text segment [B, Hkv, 64, D]
+    kt[:, :, 5] = 0
+    vt[:, :, 5, 3] = 70000.0
+    torch.cuda.synchronize()
+    K = K.copy()
+    V = V.copy()
+    K[:, :, 5] = 0.0
+    V[:, :, 5, 3] = float(torch.tensor(70000.0, dtype=torch.bfloat16))
+    q = rand_rows(12, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+    o_ref, lse_ref, _, _ = ref.attend(ref.widen(q, "bf16"), K, V, None, seg_id, 4, sm_scale(D))
+    o = torch.empty(B, Hq, M, D, device="cuda")
+    lse = torch.empty(B, Hq, M, device="cuda")
+    uc.uc_attend_mixed(uc.make_shape(B, Hq, Hkv, D), segs, dev(q, "bf16"), M, sm_scale(D), o, lse)
+    torch.cuda.synchronize()
+    og = o.cpu().numpy()
+    assert np.isfinite(og).all() and np.abs(og).max() > 10.0
+    err = np.abs(og - o_ref)
+    assert err.max() <= 2e-3 + 2e-5 * np.abs(o_ref).max(), err.max()
+    assert np.allclose(lse.cpu().numpy(), lse_ref, rtol=1e-5, atol=1e-4)
