@@ -108,6 +108,15 @@ __device__ inline void softmax_pv(State& st, const f4& s0, const f4& s1, float s
   }
 }
 
+// The query block's B operands (Q^T, four 32-dim steps) live in LDS, shared
+// by the workgroup's waves: reloading them per tile is cheaper than holding
+// 16 more registers in the streaming loops.
+constexpr int QOPB = 4 * 64 * 16;
+
+__device__ inline u4 q_operand(const char* lq, int t, int lane) {
+  return *reinterpret_cast<const u4*>(lq + (t * 64 + lane) * 16);
+}
+
 // ---------------------------------------------------------------- dense rows
 struct DenseSet {
   u4 k[8];  // A operands: k[blk*4 + t] = row blk*16 + i16, dims t*32 + g4*8 .. +7
@@ -128,7 +137,7 @@ __device__ inline void dense_issue(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rs
   for (int i = 0; i < 8; ++i) S.v[i] = bload(rv, vo, i * 4 * ROWB);
 }
 
-__device__ inline void dense_head(const DenseSet& S, char* lv, const u4 (&qop)[4], int lane,
+__device__ inline void dense_head(const DenseSet& S, char* lv, const char* lq, int lane,
                                   f4& s0, f4& s1) {
   const int i16 = lane & 15, g4 = lane >> 4;
 #pragma unroll
@@ -137,8 +146,9 @@ __device__ inline void dense_head(const DenseSet& S, char* lv, const u4 (&qop)[4
   s1 = s0;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    s0 = mfma(S.k[t], qop[t], s0);
-    s1 = mfma(S.k[4 + t], qop[t], s1);
+    const u4 qb = q_operand(lq, t, lane);
+    s0 = mfma(S.k[t], qb, s0);
+    s1 = mfma(S.k[4 + t], qb, s1);
   }
 }
 
@@ -146,7 +156,7 @@ __device__ inline void dense_head(const DenseSet& S, char* lv, const u4 (&qop)[4
 // The wave takes tiles wave, wave + WAVES, ...; only the last tile of the
 // range can be partial, and it is always one of the epilogue tiles.
 __device__ __attribute__((always_inline)) inline void dense_loop(State& st, const uint16_t* kb, const uint16_t* vb, int r0, int r1,
-                                  int wave, int lane, const u4 (&qop)[4], float scale_log2,
+                                  int wave, int lane, const char* lq, float scale_log2,
                                   char* lv) {
   const int n_tiles = (r1 - r0 + TILE - 1) / TILE;
   const int n_mine = n_tiles > wave ? (n_tiles - wave + WAVES - 1) / WAVES : 0;
@@ -157,29 +167,32 @@ __device__ __attribute__((always_inline)) inline void dense_loop(State& st, cons
   auto row_of = [&](int k) { return r0 + (wave + k * WAVES) * TILE; };
   DenseSet A, B;
   f4 s0, s1;
+  // both sets are issued unconditionally (rows past r1 read as zeros without
+  // touching memory), so the loop is entered with exactly the outstanding
+  // loads of its back edge and the compiler's wait counts stay loose
   dense_issue(rk, rv, row_of(0), lane, A);
-  if (n_mine > 1) dense_issue(rk, rv, row_of(1), lane, B);
+  dense_issue(rk, rv, row_of(1), lane, B);
   int k = 0;
   // steady state without branches, so the compiler's wait counts keep the
   // other set's loads in flight: consume A, refill A, consume B, refill B
   for (; k + 3 < n_mine; k += 2) {
-    dense_head(A, lv, qop, lane, s0, s1);
+    dense_head(A, lv, lq, lane, s0, s1);
     dense_issue(rk, rv, row_of(k + 2), lane, A);
     softmax_pv<false>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
-    dense_head(B, lv, qop, lane, s0, s1);
+    dense_head(B, lv, lq, lane, s0, s1);
     dense_issue(rk, rv, row_of(k + 3), lane, B);
     softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
   const int left = n_mine - k;  // 1..3 tiles; A holds tile k, B tile k+1
-  dense_head(A, lv, qop, lane, s0, s1);
+  dense_head(A, lv, lq, lane, s0, s1);
   if (left == 3) dense_issue(rk, rv, row_of(k + 2), lane, A);
   softmax_pv<true>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
   if (left >= 2) {
-    dense_head(B, lv, qop, lane, s0, s1);
+    dense_head(B, lv, lq, lane, s0, s1);
     softmax_pv<true>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
   if (left == 3) {
-    dense_head(A, lv, qop, lane, s0, s1);
+    dense_head(A, lv, lq, lane, s0, s1);
     softmax_pv<true>(st, s0, s1, scale_log2, row_of(k + 2), r1, lv, i16, g4);
   }
 }
@@ -271,7 +284,7 @@ __device__ inline void dequant_row(const PackedSet<BITS>& S, int i, u4& kk, u4& 
 
 template <int BITS>
 __device__ inline void packed_head(const PackedSet<BITS>& S, char* lk, char* lv,
-                                   const u4 (&qop)[4], int lane, f4& s0, f4& s1) {
+                                   const char* lq, int lane, f4& s0, f4& s1) {
   const int c8 = lane & 15, g4 = lane >> 4;
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
@@ -289,15 +302,16 @@ __device__ inline void packed_head(const PackedSet<BITS>& S, char* lk, char* lv,
   for (int t = 0; t < 4; ++t) {
     const u4 k0 = *reinterpret_cast<const u4*>(lk + toff(i16, t * 4 + g4));
     const u4 k1 = *reinterpret_cast<const u4*>(lk + toff(16 + i16, t * 4 + g4));
-    s0 = mfma(k0, qop[t], s0);
-    s1 = mfma(k1, qop[t], s1);
+    const u4 qb = q_operand(lq, t, lane);
+    s0 = mfma(k0, qb, s0);
+    s1 = mfma(k1, qb, s1);
   }
 }
 
 // Rows [r0, r1) of one head's packed rows; both ends are multiples of TILE.
 template <int BITS>
 __device__ __attribute__((always_inline)) inline void packed_loop(State& st, const PackedSeg& P, int r0, int r1, int wave,
-                                   int lane, const u4 (&qop)[4], float scale_log2, char* lk,
+                                   int lane, const char* lq, float scale_log2, char* lk,
                                    char* lv) {
   const int n_tiles = (r1 - r0) / TILE;
   const int n_mine = n_tiles > wave ? (n_tiles - wave + WAVES - 1) / WAVES : 0;
@@ -307,18 +321,18 @@ __device__ __attribute__((always_inline)) inline void packed_loop(State& st, con
   PackedSet<BITS> A, B;
   f4 s0, s1;
   packed_issue<BITS>(P, row_of(0), lane, A);
-  if (n_mine > 1) packed_issue<BITS>(P, row_of(1), lane, B);
+  packed_issue<BITS>(P, row_of(1), lane, B);  // past the range: zeros, as above
   int k = 0;
   // the scheduling barriers keep the refill loads behind the dequantisation
   // that frees their registers (hoisting them would need a third set)
   for (; k + 3 < n_mine; k += 2) {
-    packed_head<BITS>(A, lk, lv, qop, lane, s0, s1);
+    packed_head<BITS>(A, lk, lv, lq, lane, s0, s1);
     __builtin_amdgcn_sched_barrier(0);
     packed_issue<BITS>(P, row_of(k + 2), lane, A);
     __builtin_amdgcn_sched_barrier(0);
     softmax_pv<false>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
     __builtin_amdgcn_sched_barrier(0);
-    packed_head<BITS>(B, lk, lv, qop, lane, s0, s1);
+    packed_head<BITS>(B, lk, lv, lq, lane, s0, s1);
     __builtin_amdgcn_sched_barrier(0);
     packed_issue<BITS>(P, row_of(k + 3), lane, B);
     __builtin_amdgcn_sched_barrier(0);
@@ -326,15 +340,15 @@ __device__ __attribute__((always_inline)) inline void packed_loop(State& st, con
     __builtin_amdgcn_sched_barrier(0);
   }
   const int left = n_mine - k;
-  packed_head<BITS>(A, lk, lv, qop, lane, s0, s1);
+  packed_head<BITS>(A, lk, lv, lq, lane, s0, s1);
   if (left == 3) packed_issue<BITS>(P, row_of(k + 2), lane, A);
   softmax_pv<false>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
   if (left >= 2) {
-    packed_head<BITS>(B, lk, lv, qop, lane, s0, s1);
+    packed_head<BITS>(B, lk, lv, lq, lane, s0, s1);
     softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
   if (left == 3) {
-    packed_head<BITS>(A, lk, lv, qop, lane, s0, s1);
+    packed_head<BITS>(A, lk, lv, lq, lane, s0, s1);
     softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 2), r1, lv, i16, g4);
   }
 }
@@ -415,13 +429,13 @@ __device__ __attribute__((always_inline)) inline void flush(State& st, char* lds
 
 // one workgroup's share [r0, r1) of segment ks for head bh
 __device__ __attribute__((always_inline)) inline bool segment_share(State& st, const KSeg& ks, int bh, int r0, int r1, int wave,
-                                     int lane, const u4 (&qop)[4], float scale_log2, char* lk,
+                                     int lane, const char* lq, float scale_log2, char* lk,
                                      char* lv) {
   if (r1 <= r0) return true;
   if (ks.kind == UC_SEG_DENSE) {
     const int64_t base = (int64_t)bh * ks.row_stride * D;
     dense_loop(st, (const uint16_t*)ks.k + base, (const uint16_t*)ks.v + base, r0, r1, wave, lane,
-               qop, scale_log2, lv);
+               lq, scale_log2, lv);
     return true;
   }
   int bits = 0;
@@ -449,14 +463,14 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
     P.mv = rsrc(ks.min_v + svo, (uint32_t)ks.n_full * ngv * 4);
     P.lgG = lgG;
     P.ngv = ngv;
-    if (bits == 4) packed_loop<4>(st, P, r0, p1, wave, lane, qop, scale_log2, lk, lv);
-    else packed_loop<2>(st, P, r0, p1, wave, lane, qop, scale_log2, lk, lv);
+    if (bits == 4) packed_loop<4>(st, P, r0, p1, wave, lane, lq, scale_log2, lk, lv);
+    else packed_loop<2>(st, P, r0, p1, wave, lane, lq, scale_log2, lk, lv);
   }
   const int t0 = max(r0, ks.n_full);
   if (r1 > t0) {
     const int64_t base = (int64_t)bh * ks.tail_len * D;
     dense_loop(st, (const uint16_t*)ks.tail_k + base, (const uint16_t*)ks.tail_v + base,
-               t0 - ks.n_full, r1 - ks.n_full, wave, lane, qop, scale_log2, lv);
+               t0 - ks.n_full, r1 - ks.n_full, wave, lane, lq, scale_log2, lv);
   }
   return true;
 }
@@ -466,7 +480,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
                                                              int Hq, int Hkv, int M,
                                                              float scale_log2,
                                                              float* __restrict__ partial) {
-  __shared__ __attribute__((aligned(16))) char lds[WAVES * 2 * TILEB];
+  __shared__ __attribute__((aligned(16))) char lds[WAVES * 2 * TILEB + QOPB];
   const int w = blockIdx.x, bh = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i16 = lane & 15, g4 = lane >> 4;
@@ -484,6 +498,12 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
   }
   char* lk = lds + wave * 2 * TILEB;
   char* lv = lk + TILEB;
+  char* lq = lds + WAVES * 2 * TILEB;  // outside the area the record merge reuses
+  if (wave == 0) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) *reinterpret_cast<u4*>(lq + (t * 64 + lane) * 16) = qop[t];
+  }
+  __syncthreads();
   Ctx c{partial, pl.per_seg ? pl.n_seg * W : W, nq, M, Hq, G, b, hkv};
 
   State st;
@@ -493,7 +513,7 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
     const KSeg& ks = segs.s[si];
     const int r0 = share_row(ks.n_rows, w, W);
     const int r1 = share_row(ks.n_rows, w + 1, W);
-    ok &= segment_share(st, ks, bh, r0, r1, wave, lane, qop, scale_log2, lk, lv);
+    ok &= segment_share(st, ks, bh, r0, r1, wave, lane, lq, scale_log2, lk, lv);
     if (pl.per_seg) {
       flush(st, lds, c, si * W + w, ok, lane, wave);
       state_init(st);
