@@ -429,13 +429,14 @@ __device__ __attribute__((always_inline)) inline void flush(State& st, char* lds
 
 // one workgroup's share [r0, r1) of segment ks for head bh
 __device__ __attribute__((always_inline)) inline bool segment_share(State& st, const KSeg& ks, int bh, int r0, int r1, int wave,
-                                     int lane, const char* lq, float scale_log2, char* lk,
-                                     char* lv) {
+                                     int& rot, int lane, const char* lq, float scale_log2,
+                                     char* lk, char* lv) {
   if (r1 <= r0) return true;
   if (ks.kind == UC_SEG_DENSE) {
     const int64_t base = (int64_t)bh * ks.row_stride * D;
-    dense_loop(st, (const uint16_t*)ks.k + base, (const uint16_t*)ks.v + base, r0, r1, wave, lane,
-               lq, scale_log2, lv);
+    dense_loop(st, (const uint16_t*)ks.k + base, (const uint16_t*)ks.v + base, r0, r1,
+               (wave - rot) & (WAVES - 1), lane, lq, scale_log2, lv);
+    rot += (r1 - r0 + TILE - 1) / TILE;
     return true;
   }
   int bits = 0;
@@ -463,14 +464,18 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
     P.mv = rsrc(ks.min_v + svo, (uint32_t)ks.n_full * ngv * 4);
     P.lgG = lgG;
     P.ngv = ngv;
-    if (bits == 4) packed_loop<4>(st, P, r0, p1, wave, lane, lq, scale_log2, lk, lv);
-    else packed_loop<2>(st, P, r0, p1, wave, lane, lq, scale_log2, lk, lv);
+    const int ew = (wave - rot) & (WAVES - 1);
+    if (bits == 4) packed_loop<4>(st, P, r0, p1, ew, lane, lq, scale_log2, lk, lv);
+    else packed_loop<2>(st, P, r0, p1, ew, lane, lq, scale_log2, lk, lv);
+    rot += (p1 - r0) / TILE;
   }
   const int t0 = max(r0, ks.n_full);
   if (r1 > t0) {
     const int64_t base = (int64_t)bh * ks.tail_len * D;
     dense_loop(st, (const uint16_t*)ks.tail_k + base, (const uint16_t*)ks.tail_v + base,
-               t0 - ks.n_full, r1 - ks.n_full, wave, lane, lq, scale_log2, lv);
+               t0 - ks.n_full, r1 - ks.n_full, (wave - rot) & (WAVES - 1), lane, lq, scale_log2,
+               lv);
+    rot += (r1 - t0 + TILE - 1) / TILE;
   }
   return true;
 }
@@ -509,11 +514,15 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
   State st;
   state_init(st);
   bool ok = true;
+  // tiles go to the waves round-robin, continuing across segments (and from
+  // a packed segment's codes into its tail), so no wave collects every
+  // segment's remainder tile
+  int rot = 0;
   for (int si = 0; si < pl.n_seg; ++si) {
     const KSeg& ks = segs.s[si];
     const int r0 = share_row(ks.n_rows, w, W);
     const int r1 = share_row(ks.n_rows, w + 1, W);
-    ok &= segment_share(st, ks, bh, r0, r1, wave, lane, lq, scale_log2, lk, lv);
+    ok &= segment_share(st, ks, bh, r0, r1, wave, rot, lane, lq, scale_log2, lk, lv);
     if (pl.per_seg) {
       flush(st, lds, c, si * W + w, ok, lane, wave);
       state_init(st);
