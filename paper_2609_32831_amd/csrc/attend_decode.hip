@@ -129,12 +129,12 @@ __device__ inline void dense_issue(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rs
   const int ko = (row0 + i16) * ROWB + g4 * 16;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    S.k[t] = bload(rk, ko, t * 64);
-    S.k[4 + t] = bload(rk, ko, 16 * ROWB + t * 64);
+    S.k[t] = bload<kNT>(rk, ko, t * 64);
+    S.k[4 + t] = bload<kNT>(rk, ko, 16 * ROWB + t * 64);
   }
   const int vo = (row0 + g4) * ROWB + i16 * 16;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) S.v[i] = bload(rv, vo, i * 4 * ROWB);
+  for (int i = 0; i < 8; ++i) S.v[i] = bload<kNT>(rv, vo, i * 4 * ROWB);
 }
 
 __device__ inline void dense_head(const DenseSet& S, char* lv, const char* lq, int lane,
@@ -253,14 +253,14 @@ __device__ inline void packed_issue(const PackedSeg& P, int row0, int lane, Pack
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     if constexpr (BITS == 4) {
-      S.ck[i >> 2][i & 3] = bload32(P.ck, co, i * 4 * RB);
-      S.cv[i >> 2][i & 3] = bload32(P.cv, co, i * 4 * RB);
+      S.ck[i >> 2][i & 3] = bload32<kNT>(P.ck, co, i * 4 * RB);
+      S.cv[i >> 2][i & 3] = bload32<kNT>(P.cv, co, i * 4 * RB);
     } else {
-      S.ck[i >> 2][i & 3] = __builtin_amdgcn_raw_buffer_load_b16(P.ck, co, i * 4 * RB, 0);
-      S.cv[i >> 2][i & 3] = __builtin_amdgcn_raw_buffer_load_b16(P.cv, co, i * 4 * RB, 0);
+      S.ck[i >> 2][i & 3] = __builtin_amdgcn_raw_buffer_load_b16(P.ck, co, i * 4 * RB, kNT);
+      S.cv[i >> 2][i & 3] = __builtin_amdgcn_raw_buffer_load_b16(P.cv, co, i * 4 * RB, kNT);
     }
-    S.sv[i >> 2][i & 3] = bload32(P.sv, vo, i * 16 * P.ngv);
-    S.mv[i >> 2][i & 3] = bload32(P.mv, vo, i * 16 * P.ngv);
+    S.sv[i >> 2][i & 3] = bload32<kNT>(P.sv, vo, i * 16 * P.ngv);
+    S.mv[i >> 2][i & 3] = bload32<kNT>(P.mv, vo, i * 16 * P.ngv);
   }
 }
 

@@ -107,12 +107,19 @@ __device__ inline __amdgpu_buffer_rsrc_t rsrc(const void* base, uint32_t bytes) 
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes, 0x00020000);
 }
 
+// Cache policy of a load: 0 = default; kNT = non-temporal, for data read
+// once per launch (the caches are not filled with it, which keeps a long
+// stream from evicting lines that are reused)
+constexpr int kNT = 2;
+
+template <int AUX = 0>
 __device__ inline u4 bload(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+  return __builtin_bit_cast(u4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, AUX));
 }
 
+template <int AUX = 0>
 __device__ inline uint32_t bload32(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
-  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, AUX);
 }
 
 // a value the compiler cannot see through (keeps byte-extract conversions)
