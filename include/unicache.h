@@ -309,6 +309,19 @@ double uc_retention_next(double rho, double rho_init, double rho_min,
 int uc_set_path(int path);
 
 /* ------------------------------------------------------------------------ */
+/* Timing hook (instrumentation, for measuring the attention kernel on its
+ * own).  The next uc_attend_mixed call made on the calling thread records
+ * `start` on its stream immediately before the kernel that reads the
+ * segments and `stop` immediately after it, so the pair brackets that kernel
+ * alone: the merge of partial results and the prefill path's dequantisation
+ * pass fall outside it.  Both are hipEvent_t handles passed as void*,
+ * created and owned by the caller; either may be NULL.  The setting is per
+ * thread and applies to exactly one uc_attend_mixed call, which clears it
+ * (also when that call fails validation, in which case nothing is recorded).
+ * An event-record failure makes that call return UC_E_DEVICE. */
+uc_status uc_set_kernel_events(void* start, void* stop);
+
+/* ------------------------------------------------------------------------ */
 const char* uc_status_string(uc_status s);
 /* Thread-local description of the calling thread's last error ("" if none). */
 const char* uc_last_error(void);

@@ -82,6 +82,7 @@ def _load():
         "uc_status_string": (ctypes.c_char_p, [i32]),
         "uc_last_error": (ctypes.c_char_p, []),
         "uc_set_path": (i32, [i32]),
+        "uc_set_kernel_events": (i32, [vp, vp]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -322,6 +323,17 @@ def uc_status_string(s: int) -> str:
 
 def uc_last_error() -> str:
     return lib.uc_last_error().decode()
+
+
+def uc_set_kernel_events(start, stop) -> None:
+    """Bracket the attention kernel of the next uc_attend_mixed call on this
+    thread with two events (torch.cuda.Event objects that have been recorded
+    once, so that their handles exist; or raw hipEvent_t values; or None)."""
+    def handle(ev):
+        if ev is None:
+            return None
+        return ctypes.c_void_p(ev.cuda_event if hasattr(ev, "cuda_event") else int(ev))
+    _check(lib.uc_set_kernel_events(handle(start), handle(stop)), "uc_set_kernel_events")
 
 
 def uc_set_path(path: int) -> int:

@@ -41,6 +41,20 @@ namespace {
 thread_local char g_err[512] = "";
 std::atomic<int> g_path{UC_PATH_AUTO};
 
+// timing events: pending (set by uc_set_kernel_events) and active (taken by
+// one uc_attend_mixed call for its duration)
+thread_local hipEvent_t g_ev_pending[2] = {nullptr, nullptr};
+thread_local hipEvent_t g_ev_active[2] = {nullptr, nullptr};
+
+struct TimerScope {
+  TimerScope() {
+    g_ev_active[0] = g_ev_pending[0];
+    g_ev_active[1] = g_ev_pending[1];
+    g_ev_pending[0] = g_ev_pending[1] = nullptr;
+  }
+  ~TimerScope() { g_ev_active[0] = g_ev_active[1] = nullptr; }
+};
+
 uc_status fail(uc_status s, const char* fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -194,7 +208,22 @@ uc_status launched(hipError_t e) {
 
 }  // namespace
 
+namespace uc {
+hipError_t kernel_timer_begin(hipStream_t st) {
+  return g_ev_active[0] ? hipEventRecord(g_ev_active[0], st) : hipSuccess;
+}
+hipError_t kernel_timer_end(hipStream_t st) {
+  return g_ev_active[1] ? hipEventRecord(g_ev_active[1], st) : hipSuccess;
+}
+}  // namespace uc
+
 extern "C" {
+
+uc_status uc_set_kernel_events(void* start, void* stop) {
+  g_ev_pending[0] = (hipEvent_t)start;
+  g_ev_pending[1] = (hipEvent_t)stop;
+  return ok();
+}
 
 const char* uc_status_string(uc_status s) {
   switch (s) {
@@ -229,6 +258,7 @@ size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs, i
 uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_segs,
                           const void* q, uc_dtype q_dt, int M, float sm_scale, float* o,
                           float* lse, float* seg_lse, void* ws, size_t ws_bytes, void* stream) {
+  TimerScope timer;
   KSegs ks;
   uc_status st = check_segments(shape, segs, n_segs, ks);
   if (st) return st;
@@ -254,7 +284,9 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
   const size_t need = generic_ws(*shape, ks, kAttRows, kAttMaxChunks, M, true);
   if (ws_bytes < need || !ws) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   float* partial = (float*)ws;
-  hipError_t e = launch_attend_generic(*shape, ks, p, q, q_dt, M, sm_scale, partial, true, s);
+  hipError_t e = kernel_timer_begin(s);
+  if (e == hipSuccess) e = launch_attend_generic(*shape, ks, p, q, q_dt, M, sm_scale, partial, true, s);
+  if (e == hipSuccess) e = kernel_timer_end(s);
   if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, M, partial, o, lse, seg_lse, s);
   return launched(e);
 }

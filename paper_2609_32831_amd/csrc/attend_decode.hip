@@ -583,9 +583,12 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   p.n_seg = segs.n;
   p.per_seg = seg_lse != nullptr;
   float* partial = (float*)ws;
+  hipError_t e = kernel_timer_begin(st);
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(decode_mfma_kernel, dim3(p.W, sh.B * sh.Hkv), dim3(256), 0, st, segs, p,
                      (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
+  if (e == hipSuccess) e = kernel_timer_end(st);
   if (e != hipSuccess) return e;
   // per-segment records are segment-major (segment s owns slots [s*W, (s+1)*W));
   // otherwise all W records are attributed to the first segment (no seg_lse)

@@ -447,10 +447,12 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   const int n_qblocks = (nq + QROWS - 1) / QROWS;
   const int n_work = n_qblocks * BH;
   const int grid = (n_work + 7) / 8 * 8;
+  if ((e = kernel_timer_begin(st)) != hipSuccess) return e;
   hipLaunchKernelGGL(prefill_mfma_kernel, dim3(grid), dim3(256), 0, st, vs, (const uint16_t*)q,
                      sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sm_scale * kLog2e, o, lse,
                      seg_lse, v_unsafe);
-  return hipGetLastError();
+  e = hipGetLastError();
+  return e == hipSuccess ? kernel_timer_end(st) : e;
 }
 
 }  // namespace uc

@@ -125,6 +125,12 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 // ---- launchers implemented in the kernel translation units -------------------
 namespace uc {
+// Events bracketing the attention kernel of the current uc_attend_mixed call
+// (null when timing was not requested); the launchers call these around the
+// kernel that reads the segments.
+hipError_t kernel_timer_begin(hipStream_t st);
+hipError_t kernel_timer_end(hipStream_t st);
+
 hipError_t launch_quantize(const uc_shape& sh, const void* k, const void* v, int dt, int N,
                            const KSeg& out, hipStream_t st);
 hipError_t launch_attend_generic(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,

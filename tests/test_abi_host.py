@@ -116,6 +116,13 @@ def test_select_quantize_append_validation(uc):
     assert L.uc_segment_mass(ctypes.byref(sh), 0, 1, FAKE, FAKE, FAKE, None) == E
 
 
+def test_kernel_events_setting(uc):
+    # null events are accepted and mean "record nothing"; the setting is
+    # cleared by the next attention call even when that call fails validation
+    uc.uc_set_kernel_events(None, None)
+    uc.uc_set_kernel_events(None, None)
+
+
 def test_workspace_size_helpers(uc):
     sh = uc.uc_shape(2, 8, 2, 128)
     segs = [_dense(uc, 300), _packed(uc, 200, BH=4)]

@@ -414,3 +414,39 @@ def test_prefill_value_outside_fp16_range():
     err = np.abs(og - o_ref)
     assert err.max() <= 2e-3 + 2e-5 * np.abs(o_ref).max(), err.max()
     assert np.allclose(lse.cpu().numpy(), lse_ref, rtol=1e-5, atol=1e-4)
+
+
+# ------------------------------------------------------------------ timing hook
+
+@pytest.mark.parametrize("M", [1, 40], ids=["decode", "prefill"])
+def test_kernel_events_bracket_attention_kernel(M):
+    """uc_set_kernel_events: the pair lies inside the call's own pair, the
+    outputs are unchanged, and the setting lasts exactly one call."""
+    B, Hq, Hkv, D = 1, 28, 4, 128
+    _print_case(test="kernel_events", M=M)
+    segs, K, V, seg_id = _mixed_case(B, Hq, Hkv, D, "bf16", (100, 900, 300, 1000 + 17, 5, 8),
+                                     seed=3, G=64, bits=4, per_head=False)
+    q = dev(rand_rows(5, B * Hq, M, D, "bf16").reshape(B, Hq, M, D), "bf16")
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    sm = sm_scale(D)
+    o0 = torch.empty(B, Hq, M, D, device="cuda")
+    uc.uc_attend_mixed(shape, segs, q, M, sm, o0)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for e in ev:
+        e.record()
+    torch.cuda.synchronize()
+    o1 = torch.empty_like(o0)
+    ev[0].record()
+    uc.uc_set_kernel_events(ev[2], ev[3])
+    uc.uc_attend_mixed(shape, segs, q, M, sm, o1)
+    ev[1].record()
+    torch.cuda.synchronize()
+    call_ms, kern_ms = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+    assert 0.0 < kern_ms <= call_ms
+    assert ev[0].elapsed_time(ev[2]) >= 0.0 and ev[3].elapsed_time(ev[1]) >= 0.0
+    assert torch.equal(o0, o1)
+    # the next call records nothing: the kernel pair keeps its timestamps
+    uc.uc_attend_mixed(shape, segs, q, M, sm, o1)
+    torch.cuda.synchronize()
+    assert ev[2].elapsed_time(ev[3]) == kern_ms
+    assert ev[0].elapsed_time(ev[2]) <= call_ms
