@@ -50,7 +50,7 @@ def parse():
                          "runs with --calibrate-copy) and write the summaries under profiles/")
     ap.add_argument("--prefill", action="store_true",
                     help="instead of the decode job: time the multi-query attention of the "
-                         "image-editing (cfg3) and text-to-image (cfg4) workloads and report "
+                         "image-editing and text-to-image workloads and report "
                          "matrix-core utilisation (one JSON line each)")
     ap.add_argument("--profile-command", default="",
                     help="with --summarize-profiles: the commands that produced DIR (recorded)")
@@ -290,7 +290,7 @@ def prefill_bench(args):
 
     n = max(1, args.steps)
     # image editing: scoring on the first latent block, 25% ViT, int4 VAE
-    w = gen.CFG3
+    w = gen.IMAGE_EDITING
     inp = device_inputs(w, "cuda")
     run = Run(w, inp)
     qs = [inp["q_pre"](t) for t in range(2)]
@@ -311,7 +311,7 @@ def prefill_bench(args):
     del run, inp, qs, o
     torch.cuda.empty_cache()
     # text-to-image: widths from the first (dense) step, then requantise + attend
-    w = gen.CFG4
+    w = gen.TEXT_TO_IMAGE
     di = DenoiseInputs(w, "cuda")
     run = DenoiseRun(w, di.seg_k, di.seg_v)
     o = torch.empty(w.B, w.Hq, w.M, w.D, device="cuda")
@@ -358,7 +358,7 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    w = gen.CFG5
+    w = gen.LONG_CONTEXT_64K
     T = w.steps if args.decode_steps is None else args.decode_steps
     t0 = time.perf_counter()
     inp = device_inputs(w, "cuda", steps=T)

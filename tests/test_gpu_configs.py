@@ -102,22 +102,22 @@ def _decode_chain(w, heads, steps):
             check_attention(og, o_ref[:, 0], f"{w.name} b={b} h={h} t={t}")
 
 
-def test_cfg1_tiny_understanding():
-    _decode_chain(gen.CFG1, [(0, 0)], [0])
+def test_tiny_understanding():
+    _decode_chain(gen.TINY_UNDERSTANDING, [(0, 0)], [0])
 
 
-def test_cfg2_understanding_7b():
-    _decode_chain(gen.CFG2, [(0, 0), (3, 3)], [0, 1, 255])
+def test_understanding_7b():
+    _decode_chain(gen.UNDERSTANDING_7B, [(0, 0), (3, 3)], [0, 1, 255])
 
 
-def test_cfg5_long_context_64k():
-    _decode_chain(gen.CFG5, [(0, 0), (7, 2), (15, 3)], [0, 1, 200, 511])
+def test_long_context_64k():
+    _decode_chain(gen.LONG_CONTEXT_64K, [(0, 0), (7, 2), (15, 3)], [0, 1, 200, 511])
 
 
-def test_cfg3_image_editing_prefill():
+def test_image_editing_prefill():
     """Editing workload at full context sizes with a 512-query block (scoring
     window = the block, as at the first full-KV step)."""
-    w = gen.scaled(gen.CFG3, W=512, M=512, steps=2)
+    w = gen.scaled(gen.IMAGE_EDITING, W=512, M=512, steps=2)
     inp = device_inputs(w, "cuda")
     run = Run(w, inp)
     q0 = inp["q_pre"](0)
@@ -188,13 +188,13 @@ def _check_denoise_outputs(w, b, ref, outs, steps, rows=None):
             assert np.allclose(sg, rs, rtol=1e-5, atol=1e-4), (t, h)
 
 
-def test_cfg4_text_to_image_chain():
+def test_text_to_image_chain():
     """Text-to-image at its full context (768 text + 4096 latent rows per KV
     head, batch 8) with a 128-query block per query head, all 50 timesteps:
     drift of latent keys and queries, per-step requantisation, rescoring every
     10 steps with per-head int2/int4 widths under the 2.5x budget.  The oracle
     follows batch elements 0 and 5 through every decision."""
-    w = gen.scaled(gen.CFG4, M=128)
+    w = gen.scaled(gen.TEXT_TO_IMAGE, M=128)
     check = [0, 1, 10, 11, 49]
     run, bits, mass, outs = _denoise_gpu(w, check)
     Hkv = w.Hkv
@@ -222,13 +222,13 @@ def test_cfg4_text_to_image_chain():
             assert np.array_equal(cv[off[bh]:off[bh] + n], pk["codes_v"]), (b, h)
 
 
-def test_cfg4_text_to_image_full_sampled():
+def test_text_to_image_full_sampled():
     """Text-to-image at full size (4096-query blocks, batch 8, 50 timesteps).
     The oracle attends sampled query rows of batch element 0 with the widths
     the GPU chose; the per-row latent mass that drives the choice is checked
     on the same rows, and the widths follow from the GPU's masses by the
     budget rule."""
-    w = gen.CFG4
+    w = gen.TEXT_TO_IMAGE
     check = [0, 10, 49]
     run, bits, mass, outs = _denoise_gpu(w, check)
     b, Hkv, G = 0, w.Hkv, w.group_size

@@ -338,25 +338,25 @@ def gold():
 def test_accounting_closed_forms(ref, gold):
     acc = gold["accounting"]
     D = 64
-    c1 = acc["cfg1"]
+    c1 = acc["tiny_understanding"]
     assert int(math.floor(0.2 * 256)) == c1["k"]
     stored = ref.dense_bytes(64, D, "f16") + ref.evicted_bytes(51, D, "f32") + ref.packed_bytes(256, D, 32, 4, "f32")
     assert stored == c1["stored"] and ref.dense_bytes(576, D, "f32") == c1["original"]
     D = 128
-    c2 = acc["cfg2"]
+    c2 = acc["understanding_7b"]
     orig = ref.dense_bytes(512 + 4096, D, "bf16")
     k = ref.evict_rows(orig / 5.0, ref.dense_bytes(512, D, "bf16"), 4096, D, "bf16")
     assert (orig, k) == (c2["original"], c2["k"])
     assert ref.dense_bytes(512, D, "bf16") + ref.evicted_bytes(k, D, "bf16") == c2["stored"]
-    c3 = acc["cfg3"]
+    c3 = acc["image_editing"]
     stored = ref.dense_bytes(1024, D, "bf16") + ref.evicted_bytes(1024, D, "bf16") + ref.packed_bytes(4096, D, 64, 4, "bf16")
     assert stored == c3["stored"] and ref.dense_bytes(9216, D, "bf16") == c3["original"]
-    c5 = acc["cfg5"]
+    c5 = acc["long_context_64k"]
     orig = ref.dense_bytes(65536, D, "bf16")
     fixed = ref.packed_bytes(4096, D, 64, 4, "bf16")
     k = ref.evict_rows(orig / 5.0, fixed, 61440, D, "bf16")
     assert (orig, k, fixed + ref.evicted_bytes(k, D, "bf16")) == (c5["original"], c5["k"], c5["stored"])
-    c4 = acc["cfg4"]
+    c4 = acc["text_to_image"]
     orig = 4 * ref.dense_bytes(768 + 4096, D, "bf16")
     fixed = 4 * ref.dense_bytes(768, D, "bf16")
     bits = ref.assign_bits([0.3, 0.1, 0.4, 0.2], 4096, D, 64, "bf16", orig / 2.5, fixed)
@@ -397,7 +397,7 @@ def test_generator_pins(gen):
     big = gen.normal(77, 0, 400000)
     assert abs(big.mean()) < 0.01 and abs(big.std() - 1) < 0.01
     assert abs(np.mean(big ** 4) - 3) < 0.05  # Gaussian kurtosis
-    w = gen.CFG2
+    w = gen.UNDERSTANDING_7B
     whole = gen.segment_kv(w, 1, "k", bh0=0, nbh=2, row0=0, n=64)
     piece = gen.segment_kv(w, 1, "k", bh0=1, nbh=1, row0=16, n=8)
     assert np.array_equal(whole[1, 16:24], piece[0])
@@ -412,7 +412,7 @@ def test_generator_drift(gen):
     """Random-walk drift: a slice of a tensor drifts exactly as inside the
     whole, each step adds sigma * N(0,1) to the fp64 master, and the stored
     copy is the master rounded to the storage dtype."""
-    w = gen.scaled(gen.CFG4, M=8)
+    w = gen.scaled(gen.TEXT_TO_IMAGE, M=8)
     k, m = gen.segment_kv(w, 1, "k", bh0=0, nbh=3, row0=0, n=64, master=True)
     whole = gen.Drift(w, gen.T_DRIFT_K, m.copy(), "bf16")
     part = gen.Drift(w, gen.T_DRIFT_K, m[2].copy(), "bf16", start=2 * 64 * w.D)

@@ -126,7 +126,7 @@ class SegSpec:
 @dataclass(frozen=True)
 class Workload:
     name: str
-    cfg_id: int
+    recipe_id: int                      # first id of every input stream of the workload
     B: int
     Hq: int
     Hkv: int
@@ -155,24 +155,24 @@ class Workload:
         return sum(s.n for s in self.segments)
 
 
-CFG1 = Workload(
-    name="tiny_understanding", cfg_id=1, B=1, Hq=4, Hkv=1, D=64, q_dtype="f32",
+TINY_UNDERSTANDING = Workload(
+    name="tiny_understanding", recipe_id=1, B=1, Hq=4, Hkv=1, D=64, q_dtype="f32",
     segments=(SegSpec("text", 64, "keep", "f16"),
               SegSpec("vit", 256, "evict", "f32", keep_ratio=0.2),
               SegSpec("vae", 256, "quant", "f32", bits=4, group=32)),
     W=16, mode="decode", steps=1, M=1, n_outlier=4, outlier_scale=10.0,
     notes="1 layer, batch 1, 4 query heads on 1 KV head, head dim 64, fp32")
 
-CFG2 = Workload(
-    name="understanding_7b", cfg_id=2, B=4, Hq=28, Hkv=4, D=128, q_dtype="bf16",
+UNDERSTANDING_7B = Workload(
+    name="understanding_7b", recipe_id=2, B=4, Hq=28, Hkv=4, D=128, q_dtype="bf16",
     segments=(SegSpec("text", 512, "keep", "bf16"),
               SegSpec("vit", 4096, "evict", "bf16")),
     W=32, mode="decode", steps=256, M=1, budget_ratio=5.0,
     n_outlier=2, outlier_scale=8.0, tail_capacity=256,
     notes="512 text + 4096 ViT, 5x budget, 256 decode steps")
 
-CFG3 = Workload(
-    name="image_editing", cfg_id=3, B=2, Hq=28, Hkv=4, D=128, q_dtype="bf16",
+IMAGE_EDITING = Workload(
+    name="image_editing", recipe_id=3, B=2, Hq=28, Hkv=4, D=128, q_dtype="bf16",
     segments=(SegSpec("text", 1024, "keep", "bf16"),
               SegSpec("vit", 4096, "evict", "bf16", keep_ratio=0.25),
               SegSpec("vae", 4096, "quant", "bf16", bits=4, group=64)),
@@ -180,8 +180,8 @@ CFG3 = Workload(
     n_outlier=2, outlier_scale=8.0,
     notes="1024 text + 4096 ViT + 4096 VAE; 4096-query prefill x 25 timesteps")
 
-CFG4 = Workload(
-    name="text_to_image", cfg_id=4, B=8, Hq=28, Hkv=4, D=128, q_dtype="bf16",
+TEXT_TO_IMAGE = Workload(
+    name="text_to_image", recipe_id=4, B=8, Hq=28, Hkv=4, D=128, q_dtype="bf16",
     segments=(SegSpec("text", 768, "keep", "bf16"),
               SegSpec("latent", 4096, "quant", "bf16", bits=None, group=64)),
     W=4096, mode="prefill", steps=50, M=4096, budget_ratio=2.5,
@@ -189,8 +189,8 @@ CFG4 = Workload(
     notes="768 text + 4096 latent int2/int4 per head, 2.5x; 50 x 4096-query "
           "prefill, rescoring every 10 steps, random-walk drift sigma 0.05")
 
-CFG5 = Workload(
-    name="long_context_64k", cfg_id=5, B=16, Hq=28, Hkv=4, D=128, q_dtype="bf16",
+LONG_CONTEXT_64K = Workload(
+    name="long_context_64k", recipe_id=5, B=16, Hq=28, Hkv=4, D=128, q_dtype="bf16",
     segments=(SegSpec("text", 4096, "quant", "bf16", bits=4, group=64),
               SegSpec("vit", 15 * 4096, "evict", "bf16", heavy_tail=True)),
     W=32, mode="decode", steps=512, M=1, budget_ratio=5.0,
@@ -198,7 +198,8 @@ CFG5 = Workload(
     notes="65536-token context (4096 text + 15x4096 ViT), 5x budget, "
           "512 decode steps")
 
-CONFIGS = {1: CFG1, 2: CFG2, 3: CFG3, 4: CFG4, 5: CFG5}
+WORKLOADS = {w.name: w for w in (TINY_UNDERSTANDING, UNDERSTANDING_7B, IMAGE_EDITING,
+                                 TEXT_TO_IMAGE, LONG_CONTEXT_64K)}
 
 
 def scaled(w: Workload, **kw) -> Workload:
@@ -217,7 +218,7 @@ def outlier_channels(w: Workload, bh: int) -> np.ndarray:
     smallest seeded uniforms (a seeded random choice)."""
     if w.n_outlier == 0:
         return np.zeros(0, np.int64)
-    u = uniform(stream(w.seed, w.cfg_id, T_OUTLIER, bh), 0, w.D)
+    u = uniform(stream(w.seed, w.recipe_id, T_OUTLIER, bh), 0, w.D)
     return np.sort(np.argsort(u, kind="stable")[: w.n_outlier])
 
 
@@ -232,7 +233,7 @@ def heavy_dir(w: Workload, bh0: int, nbh: int) -> np.ndarray:
     """Unit direction u per KV row-block for heavy-tailed logits."""
     u = np.empty((nbh, w.D))
     for i in range(nbh):
-        z = normal(stream(w.seed, w.cfg_id, T_UDIR, bh0 + i), 0, w.D)
+        z = normal(stream(w.seed, w.recipe_id, T_UDIR, bh0 + i), 0, w.D)
         u[i] = z / np.sqrt(np.sum(z * z))
     return u
 
@@ -242,7 +243,7 @@ def heavy_coef(w: Workload, seg_index: int, bh0: int, nbh: int, row0: int,
     """(sqrt(D)/2) * tau_j with tau_j ~ Student-t(3) = z / sqrt(chi2_3 / 3)."""
     out = np.empty((nbh, n))
     for i in range(nbh):
-        z = normal(stream(w.seed, w.cfg_id, T_TAU, seg_index, bh0 + i), 4 * row0, 4 * n)
+        z = normal(stream(w.seed, w.recipe_id, T_TAU, seg_index, bh0 + i), 4 * row0, 4 * n)
         z = z.reshape(n, 4)
         chi2 = np.sum(z[:, 1:] ** 2, axis=1)
         out[i] = (math.sqrt(w.D) / 2.0) * z[:, 0] / np.sqrt(chi2 / 3.0)
@@ -272,7 +273,7 @@ def segment_kv(w: Workload, seg_index: int, which: str, bh0: int = 0,
     nbh = w.B * w.Hkv if nbh is None else nbh
     n = seg.n - row0 if n is None else n
     tensor = T_K if which == "k" else T_V
-    base = stream(w.seed, w.cfg_id, tensor, seg_index)
+    base = stream(w.seed, w.recipe_id, tensor, seg_index)
     if which == "v":
         return _rows(base, bh0, nbh, n, w.D, row0, seg.dtype, master=master)
     cs = key_channel_scale(w, bh0, nbh)
@@ -300,7 +301,7 @@ def queries(w: Workload, tensor: int, n: int, row0: int = 0, bh0: int = 0,
     T_QOBS observation window, T_QDEC decode steps (row = step),
     T_QPRE prefill block of timestep `step`."""
     nbh = w.B * w.Hq if nbh is None else nbh
-    base = stream(w.seed, w.cfg_id, tensor, step)
+    base = stream(w.seed, w.recipe_id, tensor, step)
     return _rows(base, bh0, nbh, n, w.D, row0, w.q_dtype,
                  add_dir=_query_dir(w, bh0, nbh), master=master)
 
@@ -311,7 +312,7 @@ def decode_kv(w: Workload, which: str, row0: int, n: int, bh0: int = 0,
     stored in the protected tail (bf16 for the 7B-shaped workloads)."""
     nbh = w.B * w.Hkv if nbh is None else nbh
     tensor = T_KDEC if which == "k" else T_VDEC
-    base = stream(w.seed, w.cfg_id, tensor)
+    base = stream(w.seed, w.recipe_id, tensor)
     dt = "bf16" if w.q_dtype == "bf16" else w.q_dtype
     cs = key_channel_scale(w, bh0, nbh) if which == "k" else None
     return _rows(base, bh0, nbh, n, w.D, row0, dt, cs)
@@ -331,7 +332,7 @@ class Drift:
     def step(self) -> np.ndarray:
         self.t += 1
         out = np.empty(self.master.shape, NP_STORAGE[self.dtype])
-        base = stream(self.w.seed, self.w.cfg_id, self.tensor)
+        base = stream(self.w.seed, self.w.recipe_id, self.tensor)
         lib().ucgen_drift(base, self.t, self.w.drift_sigma, self.start, self.master.size,
                           self.master.ctypes.data, DTYPE_CODE[self.dtype], out.ctypes.data)
         return out
