@@ -19,6 +19,7 @@ CPU oracle on a bounded sample of the same workload.
 from __future__ import annotations
 
 import argparse
+import glob
 import json
 import os
 import sys
@@ -111,6 +112,80 @@ class HipEvents:
         self.ev = []
 
 
+def _counters(path: str, kernel: str, per_dispatch: bool = False):
+    """Counter values of one kernel from a rocprofv3 counter_collection.csv:
+    the average per dispatch, or one dict per dispatch (with its grid size)."""
+    import csv
+    rows = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            name = r["Kernel_Name"].replace("(anonymous namespace)::", "")
+            if kernel not in name.split("(")[0]:
+                continue
+            e = rows.setdefault(r["Dispatch_Id"], {"_grid": int(r["Grid_Size"])})
+            e[r["Counter_Name"]] = float(r["Counter_Value"])
+    if per_dispatch:
+        return [rows[k] for k in sorted(rows, key=int)]
+    out = {"_dispatches": len(rows)}
+    for e in rows.values():
+        for k, v in e.items():
+            if not k.startswith("_"):
+                out[k] = out.get(k, 0.0) + v / len(rows)
+    return out
+
+
+def summarize_prefill(d: str, command: str):
+    """Kernel statistics of the prefill benchmark and matrix-core counters of
+    its attention kernel, written to profiles/prefill_attend_4096q.md.
+    SQ_VALU_MFMA_BUSY_CYCLES is summed over the chip's SIMDs and
+    GRBM_GUI_ACTIVE over its XCDs, so utilisation = busy / (SIMDs x
+    GRBM_GUI_ACTIVE / XCDs)."""
+    import workloads as gen
+    CUS, XCDS = 256, 8
+    stats = _csv(os.path.join(d, "ptrace", "**", "*kernel_stats.csv"))
+    lines = ["# Kernel statistics and matrix-core counters of the 4096-query prefill benchmark",
+             "", "Commands (rocprofv3 on one MI355X):", "", "```", command, "```", "",
+             "| kernel | calls | avg us | min us | max us | % |", "|---|---|---|---|---|---|"]
+    for r in sorted(stats, key=lambda r: -float(r["TotalDurationNs"]))[:10]:
+        name = r["Name"].replace("(anonymous namespace)::", "").split("(")[0]
+        name = name.replace("void ", "").replace("uc::", "")
+        lines.append(f"| {name[:80]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.2f} |")
+    grids = {}
+    for w in (gen.IMAGE_EDITING, gen.TEXT_TO_IMAGE):
+        qb = (w.group_size * w.M + 127) // 128
+        grids[((qb * w.B * w.Hkv + 7) // 8 * 8) * 256] = w
+    pm = glob.glob(os.path.join(d, "ppmc", "**", "*counter_collection.csv"), recursive=True)
+    if pm:
+        lines += ["", "Counters per dispatch of prefill_mfma_kernel (one counter pass; "
+                      "dispatches run serialised under counter collection):", "",
+                  "| workload | MFMA busy cycles | x 1024 flop | algorithmic flop | "
+                  "GRBM_GUI_ACTIVE / XCD | MFMA utilisation | VALU insts | LDS insts | "
+                  "LDS conflict cycles |", "|---|---|---|---|---|---|---|---|---|"]
+        for e in _counters(pm[0], "prefill_mfma_kernel", per_dispatch=True):
+            w = grids.get(e["_grid"])
+            busy = e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            act = e.get("GRBM_GUI_ACTIVE", 0.0) / XCDS
+            alg = float("nan")
+            if w is not None:  # attended rows: fixed-fraction evictions keep floor(ratio * n)
+                n_att = sum(int(sg.n * sg.keep_ratio) if sg.policy == "evict" else sg.n
+                            for sg in w.segments)
+                alg = 4.0 * w.M * n_att * w.D * w.Hq * w.B
+            util = busy / (4 * CUS * act) if act else float("nan")
+            lines.append(f"| {w.name if w else e['_grid']} | {busy:.4g} | {busy * 1024:.4g} | "
+                         f"{alg:.4g} | {act:.4g} | {util:.3f} | "
+                         f"{e.get('SQ_INSTS_VALU', 0):.4g} | {e.get('SQ_INSTS_LDS', 0):.4g} | "
+                         f"{e.get('SQ_LDS_BANK_CONFLICT', 0):.4g} |")
+        lines += ["", "The busy-cycle count times 1024 reproduces the algorithmic flop count "
+                      "4 M N D Hq B of each step (one 16x16x32 product = 16384 flop = 16 busy "
+                      "cycles), so the kernel issues no padded or repeated matrix products; "
+                      "utilisation is busy cycles over the SIMD-cycles of the dispatch."]
+    with open(os.path.join(ROOT, "profiles", "prefill_attend_4096q.md"), "w") as f:
+        f.write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def summarize_profiles(d: str, command: str):
     """Per-dispatch HBM bytes of the decode attention call from FETCH_SIZE /
     WRITE_SIZE (KiB per dispatch), each scaled by the factor that makes the
@@ -170,6 +245,20 @@ def summarize_profiles(d: str, command: str):
         lines.append(f"- {kn}: read {fb / 1e6:.2f} MB, written {wb / 1e6:.2f} MB "
                      f"({out[f'{kn}_dispatches']} dispatches)")
     lines.append(f"- per call (both kernels): {out['traffic_bytes_per_call'] / 1e6:.2f} MB")
+    dp = glob.glob(os.path.join(d, "dpmc", "**", "*counter_collection.csv"), recursive=True)
+    if dp:
+        c = _counters(dp[0], DECODE_KERNELS[0])
+        hit, miss = c.get("TCC_HIT_sum"), c.get("TCC_MISS_sum")
+        lines += ["", f"Counters of {DECODE_KERNELS[0]} (average per dispatch, "
+                      f"{c['_dispatches']} dispatches, one counter pass):", ""]
+        for k in sorted(x for x in c if not x.startswith("_")):
+            lines.append(f"- {k}: {c[k]:.4g}")
+        if hit is not None and miss is not None:
+            lines.append(f"- L2 hit fraction: {hit / (hit + miss):.3f} "
+                         f"(misses x 128 B = {miss * 128 / 1e6:.1f} MB)")
+        if c.get("SQ_INSTS_LDS"):
+            lines.append(f"- LDS bank-conflict cycles per LDS instruction: "
+                         f"{c.get('SQ_LDS_BANK_CONFLICT', 0.0) / c['SQ_INSTS_LDS']:.3f}")
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     with open(os.path.join(ROOT, "profiles", "decode_attend_64k_traffic.json"), "w") as f:
         json.dump(out, f, indent=1)
@@ -336,7 +425,10 @@ def prefill_bench(args):
 def main():
     args = parse()
     if args.summarize_profiles:
-        summarize_profiles(args.summarize_profiles, args.profile_command)
+        if args.prefill:
+            summarize_prefill(args.summarize_profiles, args.profile_command)
+        else:
+            summarize_profiles(args.summarize_profiles, args.profile_command)
         return
     if args.prefill:
         if args.gpus != 1:
