@@ -15,6 +15,7 @@ brute force or library routines; none is "parity unpinned".
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from typing import Dict, List, Optional, Sequence, Tuple
 
@@ -54,6 +55,7 @@ def lib():
             "ucref_evict_rows": (i64, [dbl, dbl, i64, i32, i32]),
             "ucref_assign_bits": (i32, [i32, vp, i64, i32, i32, i32, dbl, dbl, vp]),
             "ucref_type_budget": (i32, [i32, vp, vp, dbl, vp]),
+            "ucref_quant_config": (i32, [dbl, i64, i32, i32, i32, i32]),
             "ucref_retention_next": (dbl, [dbl, dbl, dbl, dbl, dbl]),
             "ucref_set_threads": (i32, [i32]),
         }
@@ -273,6 +275,21 @@ def type_budget(mass: Sequence[float], b_prev: Sequence[float], B_total: float) 
                                out.ctypes.data) != 0:
         raise ValueError("ucref_type_budget: invalid arguments")
     return out
+
+
+def quant_config(budget: float, N: int, D: int, dtype: str, n_heads: int,
+                 first: int = 0) -> Tuple[int, int, int]:
+    """(index, bits, group) of the most faithful quantization configuration at
+    or after `first` whose n_heads packed segments fit the budget (the last
+    one if none fits).  Configurations: widths 8, 4, 2; groups 32 ... D.
+
+    Pinned by: hand-computed byte counts at the boundaries of each
+    configuration, monotone in the budget, never before `first`."""
+    i = int(lib().ucref_quant_config(float(budget), N, D, DT[dtype], n_heads, first))
+    if i < 0:
+        raise ValueError("ucref_quant_config: invalid arguments")
+    ng = int(math.log2(D // 32)) + 1
+    return i, 8 >> (i // ng), 32 << (i % ng)
 
 
 def retention_next(rho, rho_init, rho_min, M_c, M_0) -> float:

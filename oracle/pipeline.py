@@ -17,8 +17,8 @@ import numpy as np
 
 import workloads as gen
 
-from . import (assign_bits, attend, dense_bytes, dequant, evict_rows, packed_bytes, quantize,
-               score64, select, widen)
+from . import (assign_bits, attend, dense_bytes, dequant, evict_rows, packed_bytes, quant_config,
+               quantize, retention_next, score64, select, type_budget, widen)
 
 
 def sm_scale(D: int) -> float:
@@ -217,4 +217,181 @@ def denoise_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None
             else:
                 bits = list(bits_given[t])
             out["bits"][t] = list(bits)
+    return out
+
+
+def stored(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Values that are exactly representable in dtype -> their stored form
+    (bf16 and fp16 as uint16 bits, fp32 as float32); checked by widening back."""
+    x32 = np.ascontiguousarray(x, np.float64).astype(np.float32)
+    if dtype == "bf16":
+        out = (x32.view(np.uint32) >> 16).astype(np.uint16)
+    elif dtype == "f16":
+        out = x32.astype(np.float16).view(np.uint16)
+    else:
+        out = x32
+    if not np.array_equal(widen(out, dtype), x):
+        raise ValueError("values are not exactly representable in " + dtype)
+    return out
+
+
+def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
+                 given: Optional[Dict[int, Dict]] = None) -> Dict:
+    """Oracle chain of the dynamic budget (Sec. 3.3 Eq. 1-3, Sec. 3.4) for one
+    request (batch element b, its Hkv KV heads and Hq query heads) of a
+    prefill workload with fresh queries per timestep.
+
+    Candidate types are the eviction- and quantization-managed segments
+    (kept segments are fixed).  Per request: S_a = Hkv x the dense bytes of
+    type a's rows.
+    t = 0, the full-KV step: attention over the uncompressed cache gives
+      m^(0)_a = Mean over (query head, query row) of the probability on type
+      a's rows (Eq. 1 with one step), M^(0) = sum over candidates; scores for
+      eviction = column sums of the softmax over the whole context of the
+      step's queries (all M rows of the G query heads of each KV head).
+      rho^(1) = rho_init, B^(1) = rho^(1) sum_a S_a, b^(1) = Eq. 2 with
+      b^(0) = S.
+    Chunk c >= 1 = timesteps (c-1)C+1 .. cC.  Each step attends the cache as
+      compressed so far and adds its Mean(h, q) type masses to the chunk
+      average m^(c) (Eq. 1); after the chunk's last step (if a step follows):
+      rho^(c+1) = Eq. 3, B^(c+1) = rho^(c+1) sum_a S_a, b^(c+1) = Eq. 2.
+    Translation (Sec. 3.4), applied from the next step on:
+      evicting type: k = min(k_prev, floor(b_a / Hkv / (2 D sizeof + 4)));
+        fewer rows are chosen among the rows still kept by scores from the
+        last obs_window query rows of each query head at the chunk's last
+        step, the softmax running over the whole current cache (kept rows,
+        dequantised rows); eviction is irreversible.
+      quantised type: the most faithful (bits, group) at or after the current
+        one whose Hkv segments fit b_a; a change re-quantises the current
+        dequantised values (irreversible).
+
+    steps: timesteps whose attention is returned.  rows: query rows to attend
+    at those steps (then no masses are computed and every boundary's
+    decisions must be given).  given[t]: decisions of boundary t to use
+    instead of the oracle's own: "k", "cfg" and optionally "keep" (kept
+    positions per head).
+    Returns {"decisions": {t: {...}}, "att": {t: (o, lse, seg_lse)},
+    "keep": {t: kept positions per head}, "packed": {t: packed storage},
+    "mass": {t: per-type Mean masses of step t}}."""
+    G, Hq, Hkv, D, M = w.group_size, w.Hq, w.Hkv, w.D, w.M
+    segs = w.segments
+    nseg = len(segs)
+    ev = next(i for i, s in enumerate(segs) if s.policy == "evict")
+    qt = next(i for i, s in enumerate(segs) if s.policy == "quant")
+    cand = [ev, qt]
+    dt = segs[ev].dtype
+    sm = sm_scale(D)
+    ng = int(math.log2(D // 32)) + 1
+    bh0 = b * Hkv
+    seg_k = [gen.segment_kv(w, i, "k", bh0=bh0, nbh=Hkv) for i in range(nseg)]
+    seg_v = [gen.segment_kv(w, i, "v", bh0=bh0, nbh=Hkv) for i in range(nseg)]
+    S = {a: Hkv * dense_bytes(segs[a].n, D, segs[a].dtype) for a in cand}
+    S_total = float(sum(S.values()))
+    seg_id = np.concatenate([np.full(s.n, i, np.int32) for i, s in enumerate(segs)])
+    ev0 = sum(s.n for s in segs[:ev])          # first logical row of the evicting type
+    n_ev, n_qt = segs[ev].n, segs[qt].n
+    state = {"keep": None, "cfg": None, "packed": None,
+             "qk": widen(seg_k[qt], dt), "qv": widen(seg_v[qt], dt)}
+    out = {"decisions": {}, "att": {}, "keep": {}, "packed": {}, "mass": {}}
+
+    def logical():
+        """K, V [Hkv, N, D] of the full logical sequence and the present mask."""
+        ks = [state["qk"] if i == qt else widen(seg_k[i], s.dtype) for i, s in enumerate(segs)]
+        vs = [state["qv"] if i == qt else widen(seg_v[i], s.dtype) for i, s in enumerate(segs)]
+        present = np.ones((Hkv, seg_id.shape[0]), np.uint8)
+        if state["keep"] is not None:
+            present[:, ev0:ev0 + n_ev] = 0
+            for h in range(Hkv):
+                present[h, ev0 + state["keep"][h]] = 1
+        return np.concatenate(ks, axis=1), np.concatenate(vs, axis=1), present
+
+    def rescore(q_obs):
+        """Scores of the evicting type's present rows, per head, from the
+        softmax of q_obs over the present rows of the whole cache."""
+        K, _, present = logical()
+        sc = []
+        for h in range(Hkv):
+            idx = np.nonzero(present[h])[0]
+            s64, _ = score64(widen(q_obs[h * G:(h + 1) * G], w.q_dtype)[None],
+                             K[h, idx][None, None], seg_id[idx], nseg, sm)
+            sc.append(s64[0, 0][seg_id[idx] == ev])
+        return sc
+
+    def decide(t, m, b_prev, rho, q_obs):
+        g = given.get(t) if given else None
+        k_prev = n_ev if state["keep"] is None else state["keep"][0].shape[0]
+        rec = {"rho": rho, "B": rho * S_total}
+        if g is None:
+            bud = type_budget([m[a] for a in cand], [b_prev[a] for a in cand], rec["B"])
+            bud = {a: float(x) for a, x in zip(cand, bud)}
+            k_new = min(k_prev, evict_rows(bud[ev] / Hkv, 0.0, n_ev, D, dt))
+            c_new = quant_config(bud[qt], n_qt, D, dt, Hkv,
+                                 0 if state["cfg"] is None else state["cfg"][0])
+            rec.update(m={a: m[a] for a in cand}, b=bud)
+        else:
+            bud = None
+            k_new = int(g["k"])
+            c_new = (int(g["cfg"]), 8 >> (int(g["cfg"]) // ng), 32 << (int(g["cfg"]) % ng))
+        if state["keep"] is None or k_new < k_prev:
+            rows_ev = ([np.arange(n_ev, dtype=np.int32)] * Hkv if state["keep"] is None
+                       else state["keep"])
+            if g is not None and "keep" in g:
+                state["keep"] = [np.asarray(x, np.int32) for x in g["keep"]]
+            else:
+                sc = rescore(q_obs)
+                rec["scores"] = sc
+                state["keep"] = [rows_ev[h][select(sc[h].astype(np.float32)[None], k_new)[0]]
+                                 for h in range(Hkv)]
+        if state["cfg"] is None or c_new[0] != state["cfg"][0]:
+            _, bits, group = c_new
+            pk = quantize(stored(state["qk"], dt), stored(state["qv"], dt), dt, group,
+                          [bits] * Hkv)
+            state["qk"], state["qv"] = dequant(pk, n_qt, D, group, dt)
+            state["packed"], state["cfg"] = pk, c_new
+        rec.update(k=k_new, cfg=state["cfg"][0], bits=state["cfg"][1], group=state["cfg"][2])
+        out["decisions"][t] = rec
+        out["keep"][t] = [x.copy() for x in state["keep"]]
+        out["packed"][t] = state["packed"]
+        return bud
+
+    C = w.chunk_steps
+    rho = w.rho_init
+    b_prev = dict(S)
+    acc = {a: 0.0 for a in range(nseg)}
+    n_acc = 0
+    M0 = None
+    full = rows is None
+    for t in range(w.steps):
+        boundary = t == 0 or (t % C == 0 and t < w.steps - 1)
+        if not (full or t in steps or boundary):
+            continue
+        q = gen.queries(w, gen.T_QPRE, M, bh0=b * Hq, nbh=Hq, step=t)  # [Hq, M, D]
+        m_t = None
+        if full or t in steps:
+            K, V, present = logical()
+            qa = q if full else q[:, rows]
+            o, lse, sl, smass = attend(widen(qa, w.q_dtype)[None], K[None], V[None],
+                                       present[None], seg_id, nseg, sm)
+            if full:  # Eq. 1 bracket, Mean over the query heads and rows of this step
+                m_t = {a: float(smass[0, :, :, a].sum()) / (Hq * M) for a in range(nseg)}
+                out["mass"][t] = m_t
+            if t in steps:
+                out["att"][t] = (o[0], lse[0], sl[0])
+        if t == 0:
+            M0 = sum(m_t[a] for a in cand) if full else None
+            b_prev = decide(0, m_t, b_prev, rho, q)
+            continue
+        if full:
+            for a in range(nseg):
+                acc[a] += m_t[a]
+            n_acc += 1
+        if boundary:
+            if full:
+                m_c = {a: acc[a] / n_acc for a in range(nseg)}
+                rho = retention_next(rho, w.rho_init, w.rho_min, sum(m_c[a] for a in cand), M0)
+            else:
+                m_c = None
+            b_prev = decide(t, m_c, b_prev, rho, q[:, M - w.obs_window:])
+            acc = {a: 0.0 for a in range(nseg)}
+            n_acc = 0
     return out

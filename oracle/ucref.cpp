@@ -394,6 +394,26 @@ int ucref_assign_bits(int n_heads, const double* mass, int64_t N, int D, int G,
   return 0;
 }
 
+/* Sec. 3.4: a quantization policy's budget fixes its precision and its
+ * grouping.  Configurations are numbered in decreasing fidelity: widths 8, 4,
+ * 2 bits and, for one width, groups 32, 64, ..., D (finer first), so
+ * configuration i has bits = 8 >> (i / ng) and group = 32 << (i % ng) with ng
+ * the number of groups.  Returns the first configuration at or after `first`
+ * (a type never regains fidelity it gave up) whose n_heads packed segments
+ * fit the budget, or the last one if none fits; -1 for invalid arguments. */
+int ucref_quant_config(double budget, int64_t N, int D, int dtype, int n_heads, int first) {
+  if (D < 32 || (D & (D - 1)) || N < 0 || n_heads <= 0) return -1;
+  int ng = 0;
+  for (int g = 32; g <= D; g *= 2) ++ng;
+  const int n_cfg = 3 * ng;
+  if (first < 0 || first >= n_cfg) return -1;
+  for (int i = first; i < n_cfg; ++i) {
+    const int bits = 8 >> (i / ng), group = 32 << (i % ng);
+    if ((double)n_heads * (double)ucref_packed_bytes(N, D, group, bits, dtype) <= budget) return i;
+  }
+  return n_cfg - 1;
+}
+
 /* Sec. 3.3 Eq. 2 with the redistribution stated under it: each type gets
  * its mass share of B_total, capped at its previous allocation; what capped
  * types cannot take is shared again, in proportion to mass, among the

@@ -73,6 +73,9 @@ int ucref_assign_bits(int n_heads, const double* mass, int64_t N, int D, int G,
                       int dtype, double budget, double fixed, int32_t* bits);
 
 /* Sec. 3.3 Eq. 2 (type budgets) and Eq. 3 (retention schedule). */
+/* Sec. 3.4: index of the most faithful (bits, group) configuration at or
+ * after `first` that fits the budget (see ucref.cpp). */
+int ucref_quant_config(double budget, int64_t N, int D, int dtype, int n_heads, int first);
 int ucref_type_budget(int n, const double* mass, const double* b_prev,
                       double B_total, double* b_next);
 double ucref_retention_next(double rho, double rho_init, double rho_min,

@@ -143,6 +143,13 @@ class Workload:
     drift_sigma: float = 0.0
     rescore_every: int = 0
     tail_capacity: int = 0       # protected decode tail rows (decode append)
+    # dynamic budget (Sec. 3.3 Eq. 1-3): timesteps per statistics chunk, the
+    # initial and minimum retention ratios, and the observation rows per query
+    # head that re-score an evicting type at a chunk boundary
+    chunk_steps: int = 0
+    rho_init: float = 0.0
+    rho_min: float = 0.0
+    obs_window: int = 0
     seed: int = 0
     notes: str = ""
 
@@ -198,8 +205,22 @@ LONG_CONTEXT_64K = Workload(
     notes="65536-token context (4096 text + 15x4096 ViT), 5x budget, "
           "512 decode steps")
 
+# The editing workload under the dynamic budget: the same inputs (same stream
+# ids), the ViT row count and VAE code width set by Eq. 2 at every chunk
+# boundary instead of the fixed 25 % / int4 policies.
+IMAGE_EDITING_DYNAMIC = Workload(
+    **{**IMAGE_EDITING.__dict__,
+       "name": "image_editing_dynamic",
+       "segments": (SegSpec("text", 1024, "keep", "bf16"),
+                    SegSpec("vit", 4096, "evict", "bf16"),
+                    SegSpec("vae", 4096, "quant", "bf16", bits=None, group=None)),
+       "budget_ratio": None, "chunk_steps": 5, "rho_init": 0.30, "rho_min": 0.15,
+       "obs_window": 32,
+       "notes": "editing with Eq. 1-3: chunks of 5 timesteps, rho from 0.30 down to "
+                "at least 0.15 with the candidate mass, Eq. 2 type budgets"})
+
 WORKLOADS = {w.name: w for w in (TINY_UNDERSTANDING, UNDERSTANDING_7B, IMAGE_EDITING,
-                                 TEXT_TO_IMAGE, LONG_CONTEXT_64K)}
+                                 TEXT_TO_IMAGE, LONG_CONTEXT_64K, IMAGE_EDITING_DYNAMIC)}
 
 
 def scaled(w: Workload, **kw) -> Workload:
