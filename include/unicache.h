@@ -309,6 +309,41 @@ double uc_retention_next(double rho, double rho_init, double rho_min,
 int uc_set_path(int path);
 
 /* ------------------------------------------------------------------------ */
+/* Dequantised rows of a packed segment (App. E storage; the stored-value
+ * definition x_hat = round_to_dtype(fmaf(code, scale, min)) that attention
+ * uses).  k_out and v_out [B, Hkv, seg->n_rows, D] in seg->dtype, device,
+ * 16-byte aligned, receive rows 0 .. n_full-1 decoded and the residual tail
+ * rows copied.  Used to re-quantise a segment at a lower width or coarser
+ * grouping when its budget shrinks (Sec. 3.4; the loss is irreversible).
+ * A head whose code offset or width lies outside the segment's capacities
+ * gets NaN rows. */
+uc_status uc_dequantize_segment(const uc_shape* shape, const uc_segment* seg,
+                                void* k_out, void* v_out, void* stream);
+
+/* Logical indices after a second eviction inside already compacted rows
+ * (App. E: retained entries keep their logical token indices; Sec. 3.3:
+ * eviction is irreversible, so a smaller budget selects among the rows still
+ * kept).  out[bh, j] = outer[bh, inner[bh, j]] for bh < BH and j < k, where
+ * outer [BH, n_outer] holds the logical indices of the compacted rows and
+ * inner [BH, k] the positions kept among them (as uc_select_keep returns
+ * them); an inner value outside [0, n_outer) gives -1.  All int32, device;
+ * out must not overlap outer or inner. */
+uc_status uc_compose_index(const int32_t* outer, int n_outer, const int32_t* inner,
+                           int BH, int k, int32_t* out, void* stream);
+
+/* Sec. 3.4: a quantisation policy's budget sets its precision and grouping.
+ * Configurations are numbered in decreasing fidelity: widths 8, 4, 2 bits
+ * and, within one width, groups 32, 64, ..., D (finer first); configuration
+ * i has bits = 8 >> (i / ng), group = 32 << (i % ng), ng = log2(D / 32) + 1.
+ * Returns the first configuration at or after `first` (a type never regains
+ * fidelity it gave up) whose n_heads packed segments of N rows fit
+ * budget_bytes, or the last one if none fits, and writes its bits and group;
+ * -1 for invalid arguments (D not a power of two >= 32, N < 0, n_heads < 1,
+ * first out of range). */
+int uc_quant_config(double budget_bytes, int64_t N, int D, uc_dtype dt, int n_heads,
+                    int first, int* bits, int* group);
+
+/* ------------------------------------------------------------------------ */
 /* Timing hook (instrumentation, for measuring the attention kernel on its
  * own).  The next uc_attend_mixed call made on the calling thread records
  * `start` on its stream immediately before the kernel that reads the

@@ -83,6 +83,9 @@ def _load():
         "uc_last_error": (ctypes.c_char_p, []),
         "uc_set_path": (i32, [i32]),
         "uc_set_kernel_events": (i32, [vp, vp]),
+        "uc_dequantize_segment": (i32, [shp, segp, vp, vp, vp]),
+        "uc_compose_index": (i32, [vp, i32, vp, i32, i32, vp, vp]),
+        "uc_quant_config": (i32, [dbl, i64, i32, i32, i32, i32, vp, vp]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -261,6 +264,34 @@ def uc_quantize_segment(shape: uc_shape, k: torch.Tensor, v: torch.Tensor, N: in
     _check(lib.uc_quantize_segment(ctypes.byref(shape), k.data_ptr(), v.data_ptr(),
                                    TORCH_DT[k.dtype], N, ctypes.byref(out.desc),
                                    _stream(stream)), "uc_quantize_segment")
+
+
+def uc_dequantize_segment(shape: uc_shape, seg: Segment, k_out: torch.Tensor,
+                          v_out: torch.Tensor, stream=None):
+    """Packed segment -> dense rows [B, Hkv, n_rows, D] in its dtype."""
+    _check(lib.uc_dequantize_segment(ctypes.byref(shape), ctypes.byref(seg.desc), k_out.data_ptr(),
+                                     v_out.data_ptr(), _stream(stream)), "uc_dequantize_segment")
+
+
+def uc_compose_index(outer: torch.Tensor, inner: torch.Tensor, out: torch.Tensor, stream=None):
+    """out[bh, j] = outer[bh, inner[bh, j]] (int32 tensors [BH, n_outer],
+    [BH, k], [BH, k])."""
+    BH, n_outer = outer.shape[0], outer.shape[-1]
+    k = inner.shape[-1]
+    _check(lib.uc_compose_index(outer.data_ptr(), n_outer, inner.data_ptr(), BH, k,
+                                out.data_ptr(), _stream(stream)), "uc_compose_index")
+    return out
+
+
+def uc_quant_config(budget: float, N: int, D: int, dt: int, n_heads: int, first: int = 0):
+    """(index, bits, group) of the most faithful configuration at or after
+    `first` that fits the budget (the last one if none does)."""
+    bits, group = ctypes.c_int(), ctypes.c_int()
+    i = int(lib.uc_quant_config(float(budget), N, D, dt, n_heads, first, ctypes.byref(bits),
+                                ctypes.byref(group)))
+    if i < 0:
+        raise UcError(UC_E_INVALID, "uc_quant_config", "invalid arguments")
+    return i, bits.value, group.value
 
 
 def uc_append_rows(shape: uc_shape, k_new: torch.Tensor, v_new: torch.Tensor, n_new: int,

@@ -434,6 +434,36 @@ uc_status uc_quantize_segment(const uc_shape* shape, const void* k, const void* 
   return launched(launch_quantize(*shape, k, v, dt, N, ks, (hipStream_t)stream));
 }
 
+uc_status uc_dequantize_segment(const uc_shape* shape, const uc_segment* seg, void* k_out,
+                                void* v_out, void* stream) {
+  uc_status st = check_shape(shape);
+  if (st) return st;
+  if (!seg || seg->kind != UC_SEG_PACKED) return fail(UC_E_INVALID, "seg must be a packed segment");
+  KSeg ks;
+  st = check_segment(*shape, *seg, 0, ks, false);
+  if (st) return st;
+  if (seg->n_rows == 0) return ok();
+  if (!k_out || !v_out) return fail(UC_E_INVALID, "k_out or v_out is NULL");
+  if (!aligned16(k_out) || !aligned16(v_out)) return fail(UC_E_INVALID, "k_out/v_out not 16-byte aligned");
+  return launched(launch_dequantize(*shape, ks, k_out, v_out, (hipStream_t)stream));
+}
+
+uc_status uc_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH, int k,
+                           int32_t* out, void* stream) {
+  if (BH < 0 || k < 0 || n_outer < 0) return fail(UC_E_INVALID, "BH, k and n_outer must be >= 0");
+  if ((int64_t)BH * k == 0) return ok();
+  if (!outer || !inner || !out) return fail(UC_E_INVALID, "NULL pointer");
+  const char* o0 = (const char*)out;
+  const char* o1 = o0 + (size_t)BH * k * sizeof(int32_t);
+  auto overlaps = [&](const int32_t* p, size_t n) {
+    const char* a = (const char*)p;
+    return a < o1 && o0 < a + n * sizeof(int32_t);
+  };
+  if (overlaps(outer, (size_t)BH * n_outer) || overlaps(inner, (size_t)BH * k))
+    return fail(UC_E_INVALID, "out overlaps outer or inner");
+  return launched(launch_compose_index(outer, n_outer, inner, BH, k, out, (hipStream_t)stream));
+}
+
 // ---------------------------------------------------------------- append
 uc_status uc_append_rows(const uc_shape* shape, const void* k_new, const void* v_new, int n_new,
                          const uc_segment* seg, int pos, void* stream) {
@@ -479,6 +509,26 @@ int64_t uc_evict_rows_for_budget(double budget_bytes, double fixed_bytes, int64_
   const double k = floor((budget_bytes - fixed_bytes) / per);
   if (!(k > 0.0)) return 0;
   return k >= (double)N ? N : (int64_t)k;
+}
+
+int uc_quant_config(double budget_bytes, int64_t N, int D, uc_dtype dt, int n_heads, int first,
+                    int* bits, int* group) {
+  if (D < 32 || !pow2(D) || N < 0 || n_heads < 1 || !dtype_ok(dt)) return -1;
+  int ng = 0;
+  for (int g = 32; g <= D; g *= 2) ++ng;
+  const int n_cfg = 3 * ng;
+  if (first < 0 || first >= n_cfg) return -1;
+  int pick = n_cfg - 1;
+  for (int i = first; i < n_cfg; ++i) {
+    const int64_t per_head = uc_packed_bytes(N, D, 32 << (i % ng), 8 >> (i / ng), dt);
+    if ((double)n_heads * (double)per_head <= budget_bytes) {
+      pick = i;
+      break;
+    }
+  }
+  if (bits) *bits = 8 >> (pick / ng);
+  if (group) *group = 32 << (pick % ng);
+  return pick;
 }
 
 uc_status uc_assign_bits(int n_heads, const float* mass, int64_t N, int D, int G, uc_dtype dt,

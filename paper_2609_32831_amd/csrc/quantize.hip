@@ -129,7 +129,61 @@ __global__ void copy_tail_kernel(KSeg seg, const void* __restrict__ k, const voi
       *reinterpret_cast<const uint4*>((const char*)v + src);
 }
 
+// Dequantisation of a whole packed segment into dense rows of its dtype:
+// one thread per (row, channel) element of one (b, h_kv) (blockIdx.y);
+// rows < n_full decode their code, tail rows are copied.
+__global__ void dequantize_kernel(KSeg s, void* __restrict__ kout, void* __restrict__ vout,
+                                  int D) {
+  const int bh = blockIdx.y;
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int N = s.n_rows;
+  if (e >= (int64_t)N * D) return;
+  const int r = (int)(e / D), c = (int)(e % D);
+  const int64_t o = (int64_t)bh * N * D + e;
+  float xk, xv;
+  if (r >= s.n_full) {
+    const int64_t t = ((int64_t)bh * s.tail_len + (r - s.n_full)) * D + c;
+    xk = load_elem(s.tail_k, s.dtype, t);
+    xv = load_elem(s.tail_v, s.dtype, t);
+  } else {
+    int b;
+    int64_t off;
+    if (!head_codes(s, bh, D, b, off)) {
+      xk = xv = __builtin_nanf("");
+    } else {
+      const int G = s.group, ngk = s.n_full / G, ngv = D / G;
+      const int64_t byte = off + (int64_t)r * (D * b / 8) + c * b / 8;
+      const int shift = (c % (8 / b)) * b, mask = (1 << b) - 1;
+      const int ck = (s.codes_k[byte] >> shift) & mask;
+      const int cv = (s.codes_v[byte] >> shift) & mask;
+      const int64_t ki = ((int64_t)bh * ngk + r / G) * D + c;
+      const int64_t vi = ((int64_t)bh * s.n_full + r) * ngv + c / G;
+      xk = round_to(__builtin_fmaf((float)ck, s.scale_k[ki], s.min_k[ki]), s.dtype);
+      xv = round_to(__builtin_fmaf((float)cv, s.scale_v[vi], s.min_v[vi]), s.dtype);
+    }
+  }
+  if (s.dtype == UC_F32) {
+    static_cast<float*>(kout)[o] = xk;
+    static_cast<float*>(vout)[o] = xv;
+  } else if (s.dtype == UC_BF16) {
+    static_cast<uint16_t*>(kout)[o] = f32_to_bf16_bits(xk);
+    static_cast<uint16_t*>(vout)[o] = f32_to_bf16_bits(xv);
+  } else {
+    static_cast<uint16_t*>(kout)[o] = f32_to_f16_bits(xk);
+    static_cast<uint16_t*>(vout)[o] = f32_to_f16_bits(xv);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_dequantize(const uc_shape& sh, const KSeg& seg, void* kout, void* vout,
+                             hipStream_t st) {
+  const int64_t n = (int64_t)seg.n_rows * sh.D;
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(dequantize_kernel, dim3((unsigned)((n + 255) / 256), sh.B * sh.Hkv),
+                     dim3(256), 0, st, seg, kout, vout, sh.D);
+  return hipGetLastError();
+}
 
 hipError_t launch_quantize(const uc_shape& sh, const void* k, const void* v, int dt, int N,
                            const KSeg& out, hipStream_t st) {

@@ -138,6 +138,17 @@ __global__ void gather_kernel(const int32_t* __restrict__ keep, int N, int k, co
   *reinterpret_cast<uint4*>(vdst + dof) = *reinterpret_cast<const uint4*>(vsrc + so);
 }
 
+// out[bh, j] = outer[bh, inner[bh, j]] (-1 for an inner value out of range).
+__global__ void compose_index_kernel(const int32_t* __restrict__ outer, int n_outer,
+                                     const int32_t* __restrict__ inner, int k,
+                                     int32_t* __restrict__ out) {
+  const int bh = blockIdx.y;
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= k) return;
+  const int i = inner[(int64_t)bh * k + j];
+  out[(int64_t)bh * k + j] = (i >= 0 && i < n_outer) ? outer[(int64_t)bh * n_outer + i] : -1;
+}
+
 // Decode append: rows pos..pos+n_new-1 of a dense segment.
 __global__ void append_kernel(const char* knew, const char* vnew, int n_new, char* kd, char* vd,
                               int row_stride, int pos, int row_bytes) {
@@ -169,6 +180,14 @@ hipError_t launch_gather(const int32_t* keep, int BH, int N, int k, const void* 
   hipLaunchKernelGGL(gather_kernel, dim3((unsigned)((lanes + 255) / 256), BH), dim3(256), 0, st,
                      keep, N, k, (const char*)ksrc, (const char*)vsrc, (char*)kdst, (char*)vdst,
                      row_bytes);
+  return hipGetLastError();
+}
+
+hipError_t launch_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH,
+                                int k, int32_t* out, hipStream_t st) {
+  if (k == 0 || BH == 0) return hipSuccess;
+  hipLaunchKernelGGL(compose_index_kernel, dim3((k + 255) / 256, BH), dim3(256), 0, st, outer,
+                     n_outer, inner, k, out);
   return hipGetLastError();
 }
 

@@ -133,6 +133,10 @@ hipError_t kernel_timer_end(hipStream_t st);
 
 hipError_t launch_quantize(const uc_shape& sh, const void* k, const void* v, int dt, int N,
                            const KSeg& out, hipStream_t st);
+hipError_t launch_dequantize(const uc_shape& sh, const KSeg& seg, void* kout, void* vout,
+                             hipStream_t st);
+hipError_t launch_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH,
+                                int k, int32_t* out, hipStream_t st);
 hipError_t launch_attend_generic(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
                                  const void* q, int q_dt, int M, float sm_scale, float* partial,
                                  bool want_o, hipStream_t st);

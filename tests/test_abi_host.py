@@ -116,6 +116,20 @@ def test_select_quantize_append_validation(uc):
     assert L.uc_segment_mass(ctypes.byref(sh), 0, 1, FAKE, FAKE, FAKE, None) == E
 
 
+def test_dynamic_budget_entry_validation(uc):
+    sh = uc.uc_shape(1, 4, 2, 128)
+    dense = _dense(uc, 64)
+    # dequantisation needs a packed segment; compose needs non-overlapping out
+    assert uc.lib.uc_dequantize_segment(ctypes.byref(sh), ctypes.byref(dense), 16, 16, None) == \
+        uc.UC_E_INVALID
+    assert uc.lib.uc_compose_index(4096, 8, 8192, -1, 4, 16384, None) == uc.UC_E_INVALID
+    assert uc.lib.uc_compose_index(4096, 8, 8192, 2, 4, 4096 + 16, None) == uc.UC_E_INVALID
+    assert uc.lib.uc_compose_index(4096, 8, 8192, 2, 0, 16384, None) == uc.UC_OK
+    with pytest.raises(uc.UcError):
+        uc.uc_quant_config(1e6, 4096, 96, uc.UC_BF16, 4)
+    assert uc.lib.uc_quant_config(1e6, 4096, 128, uc.UC_BF16, 4, 9, None, None) == -1
+
+
 def test_kernel_events_setting(uc):
     # null events are accepted and mean "record nothing"; the setting is
     # cleared by the next attention call even when that call fails validation
@@ -163,4 +177,9 @@ def test_host_helpers_agree_with_oracle(uc, ref):
         args = (float(rng.uniform(0.2, 1)), 0.6, 0.2, float(rng.uniform(0, 2)), 1.0)
         a = uc.uc_retention_next(*args)
         assert a == ref.retention_next(*args) or (math.isnan(a) and math.isnan(ref.retention_next(*args)))
+        Dq = int(rng.choice([32, 64, 128]))
+        first = int(rng.integers(0, 3 * (int(math.log2(Dq // 32)) + 1)))
+        qb = float(rng.uniform(0, 8 * Dq * rows // 2 + 1e5))
+        assert uc.uc_quant_config(qb, rows, Dq, dt, nh, first) == \
+            ref.quant_config(qb, rows, Dq, name, nh, first)
     assert uc.uc_packed_bytes(100, 128, 48, 4, 2) == -1
