@@ -267,9 +267,10 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
 
     steps: timesteps whose attention is returned.  rows: query rows to attend
     at those steps (then no masses are computed and every boundary's
-    decisions must be given).  given[t]: decisions of boundary t to use
+    decisions must be given).  given[t]: decisions of boundary t to apply
     instead of the oracle's own: "k", "cfg" and optionally "keep" (kept
-    positions per head).
+    positions per head); the oracle's own decision from the same state is
+    still recorded (decisions[t]["own"]) when the masses are known.
     Returns {"decisions": {t: {...}}, "att": {t: (o, lse, seg_lse)},
     "keep": {t: kept positions per head}, "packed": {t: packed storage},
     "mass": {t: per-type Mean masses of step t}}."""
@@ -318,37 +319,48 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
         return sc
 
     def decide(t, m, b_prev, rho, q_obs):
+        """Boundary t: the oracle's own decision (when masses are known) and
+        the decision applied (the given one, if any, else its own)."""
         g = given.get(t) if given else None
         k_prev = n_ev if state["keep"] is None else state["keep"][0].shape[0]
+        rows_ev = ([np.arange(n_ev, dtype=np.int32)] * Hkv if state["keep"] is None
+                   else state["keep"])
         rec = {"rho": rho, "B": rho * S_total}
-        if g is None:
+        own = None
+        bud = None
+        if m is not None:
             bud = type_budget([m[a] for a in cand], [b_prev[a] for a in cand], rec["B"])
             bud = {a: float(x) for a, x in zip(cand, bud)}
-            k_new = min(k_prev, evict_rows(bud[ev] / Hkv, 0.0, n_ev, D, dt))
-            c_new = quant_config(bud[qt], n_qt, D, dt, Hkv,
-                                 0 if state["cfg"] is None else state["cfg"][0])
+            own = {"k": min(k_prev, evict_rows(bud[ev] / Hkv, 0.0, n_ev, D, dt)),
+                   "cfg": quant_config(bud[qt], n_qt, D, dt, Hkv,
+                                       0 if state["cfg"] is None else state["cfg"][0])[0]}
             rec.update(m={a: m[a] for a in cand}, b=bud)
-        else:
-            bud = None
-            k_new = int(g["k"])
-            c_new = (int(g["cfg"]), 8 >> (int(g["cfg"]) // ng), 32 << (int(g["cfg"]) % ng))
-        if state["keep"] is None or k_new < k_prev:
-            rows_ev = ([np.arange(n_ev, dtype=np.int32)] * Hkv if state["keep"] is None
-                       else state["keep"])
+        k_new = int(g["k"]) if g is not None else own["k"]
+        cfg_new = int(g["cfg"]) if g is not None else own["cfg"]
+        reselect = state["keep"] is None or k_new < k_prev
+        if own is not None and (state["keep"] is None or own["k"] < k_prev):
+            sc = rescore(q_obs)
+            rec["scores"] = sc
+            own["keep"] = [rows_ev[h][select(sc[h].astype(np.float32)[None], own["k"])[0]]
+                           for h in range(Hkv)]
+        if reselect:
             if g is not None and "keep" in g:
                 state["keep"] = [np.asarray(x, np.int32) for x in g["keep"]]
+            elif own is not None and own["k"] == k_new and "keep" in own:
+                state["keep"] = own["keep"]
             else:
                 sc = rescore(q_obs)
                 rec["scores"] = sc
                 state["keep"] = [rows_ev[h][select(sc[h].astype(np.float32)[None], k_new)[0]]
                                  for h in range(Hkv)]
-        if state["cfg"] is None or c_new[0] != state["cfg"][0]:
-            _, bits, group = c_new
+        if state["cfg"] is None or cfg_new != state["cfg"][0]:
+            bits, group = 8 >> (cfg_new // ng), 32 << (cfg_new % ng)
             pk = quantize(stored(state["qk"], dt), stored(state["qv"], dt), dt, group,
                           [bits] * Hkv)
             state["qk"], state["qv"] = dequant(pk, n_qt, D, group, dt)
-            state["packed"], state["cfg"] = pk, c_new
-        rec.update(k=k_new, cfg=state["cfg"][0], bits=state["cfg"][1], group=state["cfg"][2])
+            state["packed"], state["cfg"] = pk, (cfg_new, bits, group)
+        rec.update(k=k_new, cfg=state["cfg"][0], bits=state["cfg"][1], group=state["cfg"][2],
+                   own=own)
         out["decisions"][t] = rec
         out["keep"][t] = [x.copy() for x in state["keep"]]
         out["packed"][t] = state["packed"]

@@ -18,8 +18,10 @@ import torch
 
 from . import (NAME_DT, TORCH_DT, dense_segment, make_shape, packed_layout, packed_segment,
                uc_append_rows, uc_assign_bits, uc_attend_mixed, uc_attend_workspace_size,
-               uc_dense_bytes, uc_evict_rows_for_budget, uc_packed_bytes, uc_quantize_segment,
-               uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep)
+               uc_compose_index, uc_dense_bytes, uc_dequantize_segment, uc_evict_rows_for_budget,
+               uc_packed_bytes, uc_quant_config, uc_quantize_segment, uc_retention_next,
+               uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep,
+               uc_type_budget)
 
 TORCH = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -293,3 +295,172 @@ class DenoiseRun:
         new = self.assign(m)
         self.set_bits(new)
         return new
+
+
+class DynamicRun:
+    """One request (batch element) of a prefill workload under the dynamic
+    budget of Sec. 3.3 (Eq. 1-3) with the Sec. 3.4 translation, on the
+    library's kernels; host-side control flow only.
+
+    Timestep 0 attends the uncompressed cache (the first full-KV step): its
+    per-segment log-sum-exps give m^(0), and scores over the whole context
+    from the step's query block select the kept rows of the evicting type.
+    Later timesteps attend the compressed cache and record their type masses;
+    after every chunk of chunk_steps timesteps (if a timestep follows) the
+    chunk's mean masses set rho (Eq. 3) and the type budgets (Eq. 2), which
+    become a row count for the evicting type (fewer rows are chosen among
+    those still kept, scored by the last obs_window query rows of each query
+    head over the current cache, and their logical indices composed) and a
+    (bits, group) configuration for the quantised type (a change re-quantises
+    its dequantised rows).  Eviction and re-quantisation are irreversible."""
+
+    def __init__(self, w, seg_k, seg_v, device="cuda"):
+        """seg_k / seg_v: per segment, the request's rows [1, Hkv, n, D]."""
+        self.w, self.device = w, device
+        Hq, Hkv, D, M = w.Hq, w.Hkv, w.D, w.M
+        self.shape = make_shape(1, Hq, Hkv, D)
+        self.sm = sm_scale(D)
+        segs = w.segments
+        self.nseg = len(segs)
+        self.ev = next(i for i, s in enumerate(segs) if s.policy == "evict")
+        self.qt = next(i for i, s in enumerate(segs) if s.policy == "quant")
+        self.cand = [self.ev, self.qt]
+        self.dt = NAME_DT[segs[self.ev].dtype]
+        self.tdt = TORCH[segs[self.ev].dtype]
+        self.n_ev, self.n_qt = segs[self.ev].n, segs[self.qt].n
+        self.dense = [dense_segment(seg_k[i], seg_v[i]) for i in range(self.nseg)]
+        self.S = {a: Hkv * uc_dense_bytes(segs[a].n, D, NAME_DT[segs[a].dtype]) for a in self.cand}
+        self.S_total = float(sum(self.S.values()))
+        self.ng = int(math.log2(D // 32)) + 1
+        q_dt = NAME_DT[w.q_dtype]
+        # workspaces sized for the largest configuration: every row present,
+        # the quantised type at the finest grouping
+        biggest = packed_segment(1, Hkv, self.n_qt, D, 32, self.tdt, bits=8, device=device)
+        full = list(self.dense)
+        mixed = [biggest if i == self.qt else d for i, d in enumerate(self.dense)]
+        ws_att = max(uc_attend_workspace_size(self.shape, full, q_dt, M),
+                     uc_attend_workspace_size(self.shape, mixed, q_dt, M))
+        ws_sc = max(uc_score_workspace_size(self.shape, full, M),
+                    uc_score_workspace_size(self.shape, mixed, max(1, w.obs_window)))
+        del biggest
+        self.ws_att = torch.empty(max(ws_att, 256), dtype=torch.uint8, device=device)
+        self.ws_sc = torch.empty(max(ws_sc, 256), dtype=torch.uint8, device=device)
+        self.lse = torch.empty(1, Hq, M, device=device)
+        self.seg_lse = torch.empty(1, Hq, M, self.nseg, device=device)
+        self.mass = torch.zeros(w.steps, 1, Hkv, self.nseg, device=device)
+        self.scores = torch.empty(1, Hkv, self.n_ev, device=device)
+        self.deq_k = torch.empty(1, Hkv, self.n_qt, D, dtype=self.tdt, device=device)
+        self.deq_v = torch.empty_like(self.deq_k)
+        # state
+        self.compact = None     # dense segment of the kept rows of the evicting type
+        self.idx = None         # [Hkv, k] int32 logical positions of those rows
+        self.packed = None      # packed segment of the quantised type
+        self.cfg = None         # (index, bits, group)
+        self.rho = w.rho_init
+        self.b_prev = dict(self.S)
+        self.M0 = None
+        self.chunk = []         # timesteps of the current chunk
+        self.decisions: Dict[int, Dict] = {}
+
+    # ---- helpers -----------------------------------------------------------
+    def segments(self):
+        if self.compact is None:
+            return list(self.dense)
+        out = list(self.dense)
+        out[self.ev] = self.compact
+        out[self.qt] = self.packed
+        return out
+
+    def type_mass(self, rows):
+        """Mean over (query head, query row) of each type's probability, per
+        timestep in rows (Eq. 1 bracket); one host read."""
+        m = self.mass[rows].sum(dim=(1, 2)).double().cpu().numpy() / (self.w.Hq * self.w.M)
+        return m  # [len(rows), nseg]
+
+    def _select(self, q_obs, W, k_new):
+        """Scores of the evicting type's current rows from q_obs [1, Hq, W, D]
+        over the current cache; keep the best k_new of them (compacted, with
+        composed logical indices)."""
+        w = self.w
+        Hkv, D = w.Hkv, w.D
+        segs = self.segments()
+        n_cur = segs[self.ev].n_rows
+        sc = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)  # contiguous [1, Hkv, n_cur]
+        outs = [None] * self.nseg
+        outs[self.ev] = sc
+        uc_score_importance(self.shape, segs, q_obs, W, self.sm, outs, None, ws=self.ws_sc)
+        local = torch.empty(Hkv, k_new, dtype=torch.int32, device=self.device)
+        src = segs[self.ev].t
+        kd = torch.empty(1, Hkv, k_new, D, dtype=self.tdt, device=self.device)
+        vd = torch.empty_like(kd)
+        uc_select_keep(sc.reshape(Hkv, n_cur), k_new, 0, local, src["k"].reshape(Hkv, -1, D),
+                       src["v"].reshape(Hkv, -1, D), kd.view(Hkv, k_new, D),
+                       vd.view(Hkv, k_new, D))
+        if self.idx is None:
+            idx = local
+        else:
+            idx = torch.empty(Hkv, k_new, dtype=torch.int32, device=self.device)
+            uc_compose_index(self.idx, local, idx)
+        self.compact = dense_segment(kd, vd, idx=idx)
+        self.idx = idx
+
+    def _quantize(self, cfg):
+        """(Re-)quantise the quantised type with configuration cfg, from its
+        original rows the first time, else from its dequantised rows."""
+        w = self.w
+        _, bits, group = cfg
+        pk = packed_segment(1, w.Hkv, self.n_qt, w.D, group, self.tdt, bits=bits,
+                            device=self.device)
+        if self.packed is None:
+            src_k, src_v = self.dense[self.qt].t["k"], self.dense[self.qt].t["v"]
+        else:
+            uc_dequantize_segment(self.shape, self.packed, self.deq_k, self.deq_v)
+            src_k, src_v = self.deq_k, self.deq_v
+        uc_quantize_segment(self.shape, src_k, src_v, self.n_qt, pk)
+        self.packed, self.cfg = pk, cfg
+
+    def _decide(self, t, m, q_obs, W):
+        """Eq. 2 budgets and their translation at boundary t (m: per-type
+        chunk mass); the new state applies from the next timestep."""
+        w = self.w
+        B_next = self.rho * self.S_total
+        bud = uc_type_budget([m[a] for a in self.cand], [self.b_prev[a] for a in self.cand],
+                             B_next)
+        bud = {a: float(x) for a, x in zip(self.cand, bud)}
+        k_prev = self.n_ev if self.compact is None else self.compact.n_rows
+        k_new = min(k_prev, uc_evict_rows_for_budget(bud[self.ev] / w.Hkv, 0.0, self.n_ev, w.D,
+                                                     self.dt))
+        cfg = uc_quant_config(bud[self.qt], self.n_qt, w.D, self.dt, w.Hkv,
+                              0 if self.cfg is None else self.cfg[0])
+        if self.compact is None or k_new < k_prev:
+            self._select(q_obs, W, k_new)
+        if self.cfg is None or cfg[0] != self.cfg[0]:
+            self._quantize(cfg)
+        self.b_prev = bud
+        rec = {"rho": self.rho, "B": B_next, "m": {a: float(m[a]) for a in self.cand},
+               "b": bud, "k": k_new, "cfg": self.cfg[0], "bits": self.cfg[1],
+               "group": self.cfg[2]}
+        self.decisions[t] = rec
+        return rec
+
+    # ---- one timestep --------------------------------------------------------
+    def step(self, t: int, q: torch.Tensor, o: torch.Tensor):
+        """Timestep t with query block q [1, Hq, M, D]; returns the boundary
+        decision taken after it, if any."""
+        w = self.w
+        uc_attend_mixed(self.shape, self.segments(), q, w.M, self.sm, o, self.lse, self.seg_lse,
+                        ws=self.ws_att)
+        uc_segment_mass(self.shape, w.M, self.nseg, self.lse, self.seg_lse, self.mass[t])
+        if t == 0:
+            m0 = self.type_mass([0])[0]
+            self.M0 = float(sum(m0[a] for a in self.cand))
+            return self._decide(0, m0, q, w.M)
+        self.chunk.append(t)
+        if t % w.chunk_steps == 0 and t < w.steps - 1:
+            m_c = self.type_mass(self.chunk).mean(axis=0)
+            self.rho = uc_retention_next(self.rho, w.rho_init, w.rho_min,
+                                         float(sum(m_c[a] for a in self.cand)), self.M0)
+            q_obs = q[:, :, w.M - w.obs_window:].contiguous()
+            self.chunk = []
+            return self._decide(t, m_c, q_obs, w.obs_window)
+        return None

@@ -1,0 +1,95 @@
+"""GPU parity of the dynamic budget (Sec. 3.3 Eq. 1-3 with the Sec. 3.4
+translation) on the editing workload: the library's kernels run every step
+(attention with per-segment statistics, type masses, scoring of the kept rows,
+top-k inside the compacted rows with composed indices, dequantisation and
+re-quantisation), the host only takes the budget decisions.  The oracle
+follows the same requests; at every boundary it re-derives the decision from
+the same state, and the kept sets, codes and attention outputs are compared
+to the usual bars (bit-exact storage, 2e-3 / 1e-3 attention)."""
+import numpy as np
+import pytest
+import torch
+
+pytestmark = pytest.mark.gpu
+
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+import oracle.pipeline as op  # noqa: E402
+import workloads as gen  # noqa: E402
+from gpu_util import check_attention  # noqa: E402
+from paper_2609_32831_amd.runner import DynamicRun  # noqa: E402
+from workloads.device import device_inputs  # noqa: E402
+
+
+def _case(name, **kw):
+    print("CASE", name, " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
+
+
+def _run_request(w, inp, b, check):
+    seg_k = [t[b:b + 1].contiguous() for t in inp["seg_k"]]
+    seg_v = [t[b:b + 1].contiguous() for t in inp["seg_v"]]
+    run = DynamicRun(w, seg_k, seg_v)
+    outs, keeps, codes = {}, {}, {}
+    for t in range(w.steps):
+        q = inp["q_pre"](t)[b:b + 1].contiguous()
+        o = torch.empty(1, w.Hq, w.M, w.D, device="cuda")
+        d = run.step(t, q, o)
+        if t in check:
+            outs[t] = o[0].cpu().numpy()
+        if d is not None:
+            keeps[t] = run.idx.cpu().numpy().copy()
+            codes[t] = {n: run.packed.t[n].cpu().numpy().copy()
+                        for n in ("codes_k", "codes_v", "scale_k", "min_k", "scale_v", "min_v")}
+    torch.cuda.synchronize()
+    masses = run.type_mass(list(range(w.steps)))
+    return run, outs, keeps, codes, masses
+
+
+@pytest.mark.parametrize("b", [0, 1])
+def test_image_editing_dynamic_budget(b):
+    w = gen.scaled(gen.IMAGE_EDITING_DYNAMIC, M=128, W=128)
+    check = [0, 1, 6, 11, 24]
+    _case(w.name, b=b, M=w.M, steps=w.steps)
+    inp = device_inputs(w, "cuda")
+    run, outs, keeps, codes, masses = _run_request(w, inp, b, check)
+    given = {t: {"k": d["k"], "cfg": d["cfg"], "keep": keeps[t]} for t, d in run.decisions.items()}
+    ref = op.budget_chain(w, b, check, given=given)
+    assert sorted(ref["decisions"]) == sorted(run.decisions) == [0, 5, 10, 15, 20]
+    # type masses of every timestep (Eq. 1 bracket)
+    for t, m in ref["mass"].items():
+        for a in range(len(w.segments)):
+            assert abs(masses[t][a] - m[a]) <= 2e-5 * m[a] + 1e-7, (t, a, masses[t][a], m[a])
+    for t, d in run.decisions.items():
+        r = ref["decisions"][t]
+        own = r["own"]
+        assert abs(d["rho"] - r["rho"]) <= 1e-5 * r["rho"], (t, d["rho"], r["rho"])
+        for a in d["b"]:
+            assert abs(d["b"][a] - r["b"][a]) <= 1e-4 * max(r["b"][a], 1.0), (t, a)
+        # the oracle's own decision from the same state
+        assert d["k"] == own["k"] and d["cfg"] == own["cfg"], (t, d, own)
+        if "keep" in own:
+            for h in range(w.Hkv):
+                g, o_ = keeps[t][h], own["keep"][h]
+                if not np.array_equal(g, o_):
+                    # only rows at the cut may differ (scores within 1e-6)
+                    sc = r["scores"][h]
+                    tau = np.sort(sc)[::-1][d["k"] - 1]
+                    prev = (np.arange(w.segments[1].n) if t == 0
+                            else given[max(x for x in given if x < t)]["keep"][h])
+                    pos = {int(v): i for i, v in enumerate(prev)}
+                    for x in np.setxor1d(g, o_):
+                        assert abs(sc[pos[int(x)]] - tau) <= 1e-6 * max(1.0, abs(tau)), (t, h, x)
+        # storage of the quantised type, bit for bit
+        pk = ref["packed"][t]
+        for n in ("codes_k", "codes_v"):
+            assert np.array_equal(codes[t][n][: pk[n].size], pk[n]), (t, n)
+        for n in ("scale_k", "min_k", "scale_v", "min_v"):
+            assert np.array_equal(codes[t][n].reshape(pk[n].shape).view(np.uint32),
+                                  pk[n].view(np.uint32)), (t, n)
+    G = w.group_size
+    for t in check:
+        o_ref = ref["att"][t][0]
+        for h in range(w.Hkv):
+            check_attention(outs[t][h * G:(h + 1) * G], o_ref[h * G:(h + 1) * G],
+                            f"{w.name} b={b} h={h} t={t}")

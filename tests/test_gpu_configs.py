@@ -153,6 +153,52 @@ def test_image_editing_prefill():
             check_attention(og, o_ref, f"{w.name} b={b} h={h} t={t}")
 
 
+def test_image_editing_full_sampled():
+    """Editing at full size, in the benchmark's launch configuration: scoring
+    on the first 4096-query latent block over the uncompressed cache, 25 % of
+    the ViT rows kept, int4 VAE, then 4096-query prefill steps.  The oracle
+    recomputes the compression of sampled KV heads in full and the attention
+    of sampled query rows."""
+    w = gen.IMAGE_EDITING
+    inp = device_inputs(w, "cuda")
+    run = Run(w, inp)
+    run.score(q_obs=inp["q_pre"](0), W=w.M)
+    run.select()
+    run.quantize()
+    steps = [0, w.steps - 1]
+    outs = {}
+    for t in steps:
+        o = torch.empty(w.B, w.Hq, w.M, w.D, device="cuda")
+        run.prefill_step(inp["q_pre"](t), o)
+        outs[t] = o.cpu().numpy()
+    torch.cuda.synchronize()
+    pols = op.plan(w)
+    G = w.group_size
+    rows = np.arange(5, w.M, 257)
+    vit = 1
+    n_text, n_vit = w.segments[0].n, w.segments[1].n
+    for (b, h) in [(0, 0), (1, 2)]:
+        _case(w.name, b=b, h=h, rows=len(rows))
+        bh = b * w.Hkv + h
+        hi = op.head_inputs(w, b, h)
+        hi["q_obs"] = gen.queries(w, gen.T_QPRE, w.M, bh0=b * w.Hq + h * G, nbh=G, step=0)
+        comp = op.compress_head(w, hi, pols)
+        gs = run.scores[vit].reshape(w.B * w.Hkv, -1)[bh].cpu().numpy().astype(np.float64)
+        s64 = comp["score64"][n_text:n_text + n_vit]
+        _check_scores(gs, s64, G * w.M)
+        gk = run.keep[vit][bh].cpu().numpy()[: pols[vit]["k"]]
+        if _check_keep(gk, comp["keep"][vit], s64, pols[vit]["k"]):
+            pres = np.zeros(n_vit, np.uint8)
+            pres[gk] = 1
+            comp["present"][vit] = pres
+        _packed_equal(run.mixed[2], comp["packed"][2], bh)
+        for t in steps:
+            q = gen.queries(w, gen.T_QPRE, w.M, bh0=b * w.Hq + h * G, nbh=G, step=t)[:, rows]
+            o_ref, _, _, _ = op.attend_head(w, comp, q, w.q_dtype)
+            og = outs[t][b, h * G:(h + 1) * G][:, rows]
+            check_attention(og, o_ref, f"{w.name} b={b} h={h} t={t}")
+
+
 def _denoise_gpu(w, check):
     """All timesteps of a drifting denoising workload on the GPU; returns the
     width decisions, the latent masses at rescoring steps, outputs and
