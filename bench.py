@@ -53,6 +53,9 @@ def parse():
                     help="instead of the decode job: time the multi-query attention of the "
                          "image-editing and text-to-image workloads and report "
                          "matrix-core utilisation (one JSON line each)")
+    ap.add_argument("--dynamic", action="store_true",
+                    help="instead of the decode job: the editing workload under the dynamic "
+                         "budget (Eq. 1-3), reporting the chunk-boundary overhead (one JSON line)")
     ap.add_argument("--profile-command", default="",
                     help="with --summarize-profiles: the commands that produced DIR (recorded)")
     return ap.parse_args()
@@ -422,6 +425,70 @@ def prefill_bench(args):
                       "steps": n}), flush=True)
 
 
+def dynamic_bench(args):
+    """The editing workload under the dynamic budget (Sec. 3.3 Eq. 1-3): per
+    request, timestep 0 on the full cache plus the initial compression, then
+    24 compressed timesteps with a budget decision after every 5.  Reports
+    the attention time, the time of the chunk-boundary work (type masses to
+    the host, Eq. 2/3, re-scoring and top-k inside the kept rows, index
+    composition, re-quantisation) and its fraction of the attention time."""
+    import torch
+
+    import workloads as gen
+    from paper_2609_32831_amd import uc_attend_mixed, uc_segment_mass
+    from paper_2609_32831_amd.runner import DynamicRun
+    from workloads.device import device_inputs
+
+    w = gen.IMAGE_EDITING_DYNAMIC
+    inp = device_inputs(w, "cuda")
+    qs = [inp["q_pre"](t) for t in range(w.steps)]
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    res = []
+    for b in range(w.B):
+        seg_k = [t[b:b + 1].contiguous() for t in inp["seg_k"]]
+        seg_v = [t[b:b + 1].contiguous() for t in inp["seg_v"]]
+        q_b = [q[b:b + 1].contiguous() for q in qs]
+        o = torch.empty(1, w.Hq, w.M, w.D, device="cuda")
+        for rep in range(max(1, args.warmup) + 1):  # the last repetition is timed
+            run = DynamicRun(w, seg_k, seg_v)
+            ev = HipEvents(3 * w.steps)
+            torch.cuda.synchronize()
+            for t in range(w.steps):
+                ev.record(3 * t, stream)
+                # the attention and the per-step type masses
+                uc_attend_mixed(run.shape, run.segments(), q_b[t], w.M, run.sm, o, run.lse,
+                                run.seg_lse, ws=run.ws_att)
+                uc_segment_mass(run.shape, w.M, run.nseg, run.lse, run.seg_lse, run.mass[t])
+                ev.record(3 * t + 1, stream)
+                run.after_step(t, q_b[t])
+                ev.record(3 * t + 2, stream)
+            torch.cuda.synchronize()
+        att = [ev.elapsed_ms(3 * t, 3 * t + 1) for t in range(w.steps)]
+        bnd = [ev.elapsed_ms(3 * t + 1, 3 * t + 2) for t in range(w.steps)]
+        ev.close()
+        d = run.decisions
+        res.append({"att": att, "bnd": bnd, "dec": d})
+    att0 = sum(r["att"][0] for r in res)
+    init = sum(r["bnd"][0] for r in res)
+    att = sum(sum(r["att"][1:]) for r in res)
+    bnd = sum(sum(r["bnd"][1:]) for r in res)
+    last = res[0]["dec"][max(res[0]["dec"])]
+    print(json.dumps({"metric": "dynamic budget overhead (Eq. 1-3 at chunk boundaries)",
+                      "workload": w.name, "requests": w.B, "timesteps": w.steps,
+                      "chunk_steps": w.chunk_steps,
+                      "full_kv_step_ms": round(att0 / w.B, 4),
+                      "initial_compression_ms": round(init / w.B, 4),
+                      "compressed_step_ms": round(att / w.B / (w.steps - 1), 4),
+                      "boundary_ms_total": round(bnd / w.B, 4),
+                      "boundary_frac_of_attention": round(bnd / att, 4),
+                      "decisions_request0": {str(t): {"rho": round(x["rho"], 5), "k": x["k"],
+                                                      "bits": x["bits"], "group": x["group"]}
+                                             for t, x in res[0]["dec"].items()},
+                      "final_k": last["k"], "final_bits": last["bits"],
+                      "final_group": last["group"]}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_profiles:
@@ -434,6 +501,11 @@ def main():
         if args.gpus != 1:
             sys.exit(2)
         prefill_bench(args)
+        return
+    if args.dynamic:
+        if args.gpus != 1:
+            sys.exit(2)
+        dynamic_bench(args)
         return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "

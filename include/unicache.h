@@ -243,7 +243,8 @@ size_t uc_attend_workspace_size(const uc_shape* shape, const uc_segment* segs,
  * lse [B, Hq, M] and seg_lse [B, Hq, M, n_segs] as written by uc_attend_mixed;
  * mass_out [B, Hkv, n_segs] float receives
  *   sum over (g, m) of exp(seg_lse[b, h_kv*G + g, m, a] - lse[b, h_kv*G + g, m])
- * accumulated in double.  Dividing by G*M gives the Mean over heads and
+ * with each term the binary32 exponential of the exact double difference
+ * (relative error below 1e-6), accumulated in double.  Dividing by G*M gives the Mean over heads and
  * queries of Eq. 1 for one layer and step. */
 uc_status uc_segment_mass(const uc_shape* shape, int M, int n_segs,
                           const float* lse, const float* seg_lse,

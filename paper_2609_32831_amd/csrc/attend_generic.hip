@@ -335,23 +335,26 @@ __global__ void mass_finalize_kernel(ChunkPlan plan, int nseg, const double* __r
 }
 
 // Eq. 1 bracket from attention statistics: sum over the query heads of a KV
-// head and the query rows of P mass per segment = exp(seg_lse - lse).
-__global__ __launch_bounds__(256) void segment_mass_kernel(int Hq, int Hkv, int M, int nseg,
-                                                           const float* __restrict__ lse,
-                                                           const float* __restrict__ seg_lse,
-                                                           float* mass) {
-  __shared__ double red[4][kMaxSeg];
+// head and the query rows of P mass per segment = exp(seg_lse - lse).  One
+// 1024-thread workgroup per (b, h_kv); each term is exp of the exact
+// double-precision difference evaluated in binary32 (relative error below
+// 1e-6), and the terms are summed in double.
+__global__ __launch_bounds__(1024) void segment_mass_kernel(int Hq, int Hkv, int M, int nseg,
+                                                            const float* __restrict__ lse,
+                                                            const float* __restrict__ seg_lse,
+                                                            float* mass) {
+  __shared__ double red[16][kMaxSeg];
   const int bh = blockIdx.x, b = bh / Hkv, hkv = bh % Hkv, G = Hq / Hkv;
   double acc[kMaxSeg];
   for (int a = 0; a < kMaxSeg; ++a) acc[a] = 0.0;
   const int n = G * M;
+  // the G*M rows of one KV head are contiguous in lse / seg_lse
+  const int64_t q0 = ((int64_t)b * Hq + hkv * G) * M;
   for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const int g = i / M, m = i % M;
-    const int64_t qi = ((int64_t)b * Hq + hkv * G + g) * M + m;
-    const double L = lse[qi];
+    const double L = lse[q0 + i];
     for (int a = 0; a < nseg; ++a) {
-      const float sl = seg_lse[qi * nseg + a];
-      if (sl != -INFINITY) acc[a] += exp((double)sl - L);
+      const float sl = seg_lse[(q0 + i) * nseg + a];
+      if (sl != -INFINITY) acc[a] += (double)expf((float)((double)sl - L));
     }
   }
   for (int a = 0; a < nseg; ++a) {
@@ -361,7 +364,9 @@ __global__ __launch_bounds__(256) void segment_mass_kernel(int Hq, int Hkv, int 
   __syncthreads();
   if (threadIdx.x < nseg) {
     const int a = threadIdx.x;
-    mass[(int64_t)bh * nseg + a] = (float)(red[0][a] + red[1][a] + red[2][a] + red[3][a]);
+    double t = 0.0;
+    for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += red[w][a];
+    mass[(int64_t)bh * nseg + a] = (float)t;
   }
 }
 
@@ -421,8 +426,8 @@ hipError_t launch_mass_finalize(const ChunkPlan& plan, int BH, int n_segs,
 
 hipError_t launch_segment_mass(const uc_shape& sh, int M, int n_segs, const float* lse,
                                const float* seg_lse, float* mass, hipStream_t st) {
-  hipLaunchKernelGGL(segment_mass_kernel, dim3(sh.B * sh.Hkv), dim3(256), 0, st, sh.Hq, sh.Hkv, M,
-                     n_segs, lse, seg_lse, mass);
+  hipLaunchKernelGGL(segment_mass_kernel, dim3(sh.B * sh.Hkv), dim3(1024), 0, st, sh.Hq, sh.Hkv,
+                     M, n_segs, lse, seg_lse, mass);
   return hipGetLastError();
 }
 

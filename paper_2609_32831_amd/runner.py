@@ -341,7 +341,7 @@ class DynamicRun:
         ws_att = max(uc_attend_workspace_size(self.shape, full, q_dt, M),
                      uc_attend_workspace_size(self.shape, mixed, q_dt, M))
         ws_sc = max(uc_score_workspace_size(self.shape, full, M),
-                    uc_score_workspace_size(self.shape, mixed, max(1, w.obs_window)))
+                    uc_score_workspace_size(self.shape, full, max(1, w.obs_window)))
         del biggest
         self.ws_att = torch.empty(max(ws_att, 256), dtype=torch.uint8, device=device)
         self.ws_sc = torch.empty(max(ws_sc, 256), dtype=torch.uint8, device=device)
@@ -349,8 +349,12 @@ class DynamicRun:
         self.seg_lse = torch.empty(1, Hq, M, self.nseg, device=device)
         self.mass = torch.zeros(w.steps, 1, Hkv, self.nseg, device=device)
         self.scores = torch.empty(1, Hkv, self.n_ev, device=device)
+        # the quantised type's current rows, dequantised: the source of a
+        # re-quantisation and, as a dense segment, what the re-scoring sees
+        # (the same values attention reads), so scoring runs on matrix cores
         self.deq_k = torch.empty(1, Hkv, self.n_qt, D, dtype=self.tdt, device=device)
         self.deq_v = torch.empty_like(self.deq_k)
+        self.deq = dense_segment(self.deq_k, self.deq_v)
         # state
         self.compact = None     # dense segment of the kept rows of the evicting type
         self.idx = None         # [Hkv, k] int32 logical positions of those rows
@@ -384,6 +388,8 @@ class DynamicRun:
         w = self.w
         Hkv, D = w.Hkv, w.D
         segs = self.segments()
+        if self.packed is not None:
+            segs[self.qt] = self.deq
         n_cur = segs[self.ev].n_rows
         sc = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)  # contiguous [1, Hkv, n_cur]
         outs = [None] * self.nseg
@@ -414,9 +420,9 @@ class DynamicRun:
         if self.packed is None:
             src_k, src_v = self.dense[self.qt].t["k"], self.dense[self.qt].t["v"]
         else:
-            uc_dequantize_segment(self.shape, self.packed, self.deq_k, self.deq_v)
-            src_k, src_v = self.deq_k, self.deq_v
+            src_k, src_v = self.deq_k, self.deq_v  # the current rows, dequantised
         uc_quantize_segment(self.shape, src_k, src_v, self.n_qt, pk)
+        uc_dequantize_segment(self.shape, pk, self.deq_k, self.deq_v)
         self.packed, self.cfg = pk, cfg
 
     def _decide(self, t, m, q_obs, W):
@@ -451,6 +457,12 @@ class DynamicRun:
         uc_attend_mixed(self.shape, self.segments(), q, w.M, self.sm, o, self.lse, self.seg_lse,
                         ws=self.ws_att)
         uc_segment_mass(self.shape, w.M, self.nseg, self.lse, self.seg_lse, self.mass[t])
+        return self.after_step(t, q)
+
+    def after_step(self, t: int, q: torch.Tensor):
+        """The budget bookkeeping after timestep t's attention and type masses
+        (a decision at a chunk boundary)."""
+        w = self.w
         if t == 0:
             m0 = self.type_mass([0])[0]
             self.M0 = float(sum(m0[a] for a in self.cand))

@@ -93,3 +93,60 @@ def test_image_editing_dynamic_budget(b):
         for h in range(w.Hkv):
             check_attention(outs[t][h * G:(h + 1) * G], o_ref[h * G:(h + 1) * G],
                             f"{w.name} b={b} h={h} t={t}")
+
+
+def test_image_editing_dynamic_full_sampled():
+    """Full size (4096-query blocks, 25 timesteps), request 0, in the
+    benchmark's launch configuration.  The decisions must follow from the
+    GPU's own type masses by the oracle's rules (Eq. 3, Eq. 2, Sec. 3.4
+    translation) and eviction must stay nested; with those decisions the
+    oracle re-derives the storage (bit for bit) and the attention of sampled
+    query rows."""
+    import oracle as ref
+    w = gen.IMAGE_EDITING_DYNAMIC
+    b = 0
+    check = [0, 6, 24]
+    _case(w.name, b=b, M=w.M, steps=w.steps)
+    inp = device_inputs(w, "cuda")
+    run, outs, keeps, codes, masses = _run_request(w, inp, b, check)
+    cand = [1, 2]
+    n_ev, n_qt, D, Hkv = w.segments[1].n, w.segments[2].n, w.D, w.Hkv
+    S = {a: Hkv * 2 * w.segments[a].n * D * 2 for a in cand}
+    rho, b_prev, k_prev, c_prev, M0 = w.rho_init, dict(S), n_ev, 0, None
+    bounds = sorted(run.decisions)
+    assert bounds == [0, 5, 10, 15, 20]
+    for i, t in enumerate(bounds):
+        d = run.decisions[t]
+        if t == 0:
+            m = masses[0]
+            M0 = m[1] + m[2]
+        else:
+            m = masses[bounds[i - 1] + 1:t + 1].mean(axis=0)
+            rho = ref.retention_next(rho, w.rho_init, w.rho_min, m[1] + m[2], M0)
+        assert abs(d["rho"] - rho) <= 1e-12 * rho, t
+        bud = ref.type_budget([m[a] for a in cand], [b_prev[a] for a in cand], rho * sum(S.values()))
+        assert np.allclose([d["b"][a] for a in cand], bud, rtol=1e-9), t
+        k = min(k_prev, ref.evict_rows(bud[0] / Hkv, 0.0, n_ev, D, "bf16"))
+        c = ref.quant_config(bud[1], n_qt, D, "bf16", Hkv, c_prev)[0]
+        assert (d["k"], d["cfg"]) == (k, c), (t, d, k, c)
+        assert keeps[t].shape == (Hkv, k)
+        if i > 0:
+            prev = keeps[bounds[i - 1]]
+            assert all(np.all(np.isin(keeps[t][h], prev[h])) for h in range(Hkv))
+        b_prev, k_prev, c_prev = dict(zip(cand, bud)), k, c
+    given = {t: {"k": d["k"], "cfg": d["cfg"], "keep": keeps[t]} for t, d in run.decisions.items()}
+    rows = np.arange(7, w.M, 509)
+    r = op.budget_chain(w, b, check, rows=rows, given=given)
+    for t in bounds:
+        pk = r["packed"][t]
+        for n in ("codes_k", "codes_v"):
+            assert np.array_equal(codes[t][n][: pk[n].size], pk[n]), (t, n)
+        for n in ("scale_k", "min_k", "scale_v", "min_v"):
+            assert np.array_equal(codes[t][n].reshape(pk[n].shape).view(np.uint32),
+                                  pk[n].view(np.uint32)), (t, n)
+    G = w.group_size
+    for t in check:
+        o_ref = r["att"][t][0]
+        for h in range(Hkv):
+            check_attention(outs[t][h * G:(h + 1) * G][:, rows], o_ref[h * G:(h + 1) * G],
+                            f"{w.name} b={b} h={h} t={t}")
