@@ -98,7 +98,10 @@ typedef struct {
  *             read by attention (softmax is invariant to row order).
  *
  * Packed segment (kind = UC_SEG_PACKED), N = n_rows, G = group,
- * n_full = G * floor(N / G), tail_len = N - n_full:
+ * n_full = G * floor(N / G), tail_len = N - n_full, and the per-head strides
+ * C_full = n_full, T = tail_len when row_stride = 0; with a row capacity
+ * R = row_stride >= N (a segment that grows, see uc_stream_append)
+ * C_full = G * floor(R / G) and T = G, so rows never move as N grows:
  *   bits      code width in {2, 4, 8}: the uniform width when head_bits is
  *             NULL, else an upper bound on the per-head widths (the library
  *             picks kernels from it).
@@ -107,17 +110,20 @@ typedef struct {
  *             whose entry breaks this get NaN attention outputs.
  *   code_off  device int64 [B*Hkv]: byte offset of each (b, h_kv)'s codes in
  *             codes_k / codes_v, a multiple of 16.  NULL (with head_bits NULL)
- *             means (b*Hkv + h) * n_full * D * bits / 8.
+ *             means (b*Hkv + h) * C_full * D * bits / 8.
  *   codes_bytes  capacity in bytes of each of codes_k and codes_v.
  *   codes_k, codes_v  row r of a head occupies D*bits/8 bytes at
  *             offset + r*D*bits/8; channel c sits in byte c*bits/8 at bit
  *             (c % (8/bits)) * bits (least significant bits first).
- *   scale_k, min_k  float [B, Hkv, n_full/G, D]: keys are quantised per
- *             channel over groups of G consecutive rows.
- *   scale_v, min_v  float [B, Hkv, n_full, D/G]: values are quantised per
- *             row over groups of G consecutive channels.
- *   tail_k, tail_v  [B, Hkv, tail_len, D] of `dtype`: the last N - n_full rows,
- *             unquantised.  May be NULL when tail_len == 0.
+ *   scale_k, min_k  float [B, Hkv, C_full/G, D] (the first n_full/G groups
+ *             of each head live): keys are quantised per channel over groups
+ *             of G consecutive rows.
+ *   scale_v, min_v  float [B, Hkv, C_full, D/G] (the first n_full rows of
+ *             each head live): values are quantised per row over groups of G
+ *             consecutive channels.
+ *   tail_k, tail_v  [B, Hkv, T, D] of `dtype`: rows 0..tail_len-1 of each
+ *             head hold the last N - n_full rows, unquantised.  May be NULL
+ *             when tail_len == 0 and row_stride == 0.
  *   A code q of a group with scale s and minimum m stands for the value
  *   round_to(dtype, fmaf((float)q, s, m)).
  *
@@ -128,7 +134,7 @@ typedef struct {
   int32_t kind;       /* uc_seg_kind */
   int32_t dtype;      /* uc_dtype */
   int32_t n_rows;     /* logical rows per (b, h_kv); may be 0 */
-  int32_t row_stride; /* dense only: allocated rows per (b, h_kv); 0 = n_rows */
+  int32_t row_stride; /* allocated rows per (b, h_kv) (capacity); 0 = n_rows */
   void* k;
   void* v;
   const int32_t* idx;
@@ -320,6 +326,22 @@ int uc_set_path(int path);
  * gets NaN rows. */
 uc_status uc_dequantize_segment(const uc_shape* shape, const uc_segment* seg,
                                 void* k_out, void* v_out, void* stream);
+
+/* Streaming residual tail (App. E storage: the N mod G most recent rows of a
+ * quantised segment stay unquantised in its tail).  Appends n_new rows
+ * k_new / v_new [B, Hkv, n_new, D] (seg->dtype, device, 16-byte aligned) to a
+ * packed segment with a row capacity (row_stride > 0) and the uniform code
+ * layout (head_bits and code_off NULL): the rows enter the tail, and every
+ * time the tail holds G rows they are quantised as the segment's next row
+ * group exactly as uc_quantize_segment quantises a group (key scale/min per
+ * channel over the G rows, value scale/min per row and channel group), so the
+ * segment always equals the quantisation of all its rows.  seg->n_rows is the
+ * row count before the call; the caller adds n_new to it afterwards.
+ * Requires n_rows + n_new <= row_stride; UC_E_UNSUPPORTED for per-head
+ * widths.  Calls on one segment are ordered by the stream. */
+uc_status uc_stream_append(const uc_shape* shape, const uc_segment* seg,
+                           const void* k_new, const void* v_new, int n_new,
+                           void* stream);
 
 /* Logical indices after a second eviction inside already compacted rows
  * (App. E: retained entries keep their logical token indices; Sec. 3.3:

@@ -84,6 +84,7 @@ def _load():
         "uc_set_path": (i32, [i32]),
         "uc_set_kernel_events": (i32, [vp, vp]),
         "uc_dequantize_segment": (i32, [shp, segp, vp, vp, vp]),
+        "uc_stream_append": (i32, [shp, segp, vp, vp, i32, vp]),
         "uc_compose_index": (i32, [vp, i32, vp, i32, i32, vp, vp]),
         "uc_quant_config": (i32, [dbl, i64, i32, i32, i32, i32, vp, vp]),
     }
@@ -158,36 +159,40 @@ def packed_layout(BH: int, N: int, D: int, G: int, head_bits: Sequence[int]):
 
 def packed_segment(B: int, Hkv: int, N: int, D: int, G: int, dtype: torch.dtype,
                    bits: int = 4, head_bits: Optional[Sequence[int]] = None,
-                   device="cuda") -> Segment:
-    """Allocate the buffers of a packed segment (to be filled by
-    uc_quantize_segment).  head_bits: optional per-(b, h_kv) code widths."""
+                   device="cuda", capacity: int = 0) -> Segment:
+    """Allocate the buffers of a packed segment of N rows (to be filled by
+    uc_quantize_segment).  head_bits: optional per-(b, h_kv) code widths.
+    capacity > 0: room for that many rows per head (a segment that grows by
+    uc_stream_append; strides follow the capacity)."""
     BH = B * Hkv
     n_full = G * (N // G)
     tail = N - n_full
+    cap_full = G * (capacity // G) if capacity else n_full
+    tail_rows = G if capacity else tail
     t = {}
     if head_bits is not None:
-        off, total = packed_layout(BH, N, D, G, head_bits)
+        off, total = packed_layout(BH, cap_full, D, G, head_bits)
         t["head_bits"] = torch.tensor(list(head_bits), dtype=torch.uint8, device=device)
         t["code_off"] = torch.tensor(off, dtype=torch.int64, device=device)
     else:
-        total = BH * n_full * D * bits // 8
+        total = BH * cap_full * D * bits // 8
     t["codes_k"] = torch.zeros(max(total, 16), dtype=torch.uint8, device=device)
     t["codes_v"] = torch.zeros(max(total, 16), dtype=torch.uint8, device=device)
-    t["scale_k"] = torch.zeros(B, Hkv, n_full // G, D, dtype=torch.float32, device=device)
+    t["scale_k"] = torch.zeros(B, Hkv, cap_full // G, D, dtype=torch.float32, device=device)
     t["min_k"] = torch.zeros_like(t["scale_k"])
-    t["scale_v"] = torch.zeros(B, Hkv, n_full, D // G, dtype=torch.float32, device=device)
+    t["scale_v"] = torch.zeros(B, Hkv, cap_full, D // G, dtype=torch.float32, device=device)
     t["min_v"] = torch.zeros_like(t["scale_v"])
-    t["tail_k"] = torch.zeros(B, Hkv, tail, D, dtype=dtype, device=device)
+    t["tail_k"] = torch.zeros(B, Hkv, tail_rows, D, dtype=dtype, device=device)
     t["tail_v"] = torch.zeros_like(t["tail_k"])
-    d = uc_segment(kind=UC_SEG_PACKED, dtype=TORCH_DT[dtype], n_rows=N, row_stride=0,
+    d = uc_segment(kind=UC_SEG_PACKED, dtype=TORCH_DT[dtype], n_rows=N, row_stride=capacity,
                    group=G, bits=bits if head_bits is None else int(max(head_bits)),
                    head_bits=_ptr(t.get("head_bits")), code_off=_ptr(t.get("code_off")),
                    codes_bytes=total, codes_k=t["codes_k"].data_ptr(),
                    codes_v=t["codes_v"].data_ptr(), scale_k=t["scale_k"].data_ptr(),
                    min_k=t["min_k"].data_ptr(), scale_v=t["scale_v"].data_ptr(),
                    min_v=t["min_v"].data_ptr(),
-                   tail_k=t["tail_k"].data_ptr() if tail else None,
-                   tail_v=t["tail_v"].data_ptr() if tail else None)
+                   tail_k=t["tail_k"].data_ptr() if tail_rows else None,
+                   tail_v=t["tail_v"].data_ptr() if tail_rows else None)
     return Segment(d, t)
 
 
@@ -271,6 +276,16 @@ def uc_dequantize_segment(shape: uc_shape, seg: Segment, k_out: torch.Tensor,
     """Packed segment -> dense rows [B, Hkv, n_rows, D] in its dtype."""
     _check(lib.uc_dequantize_segment(ctypes.byref(shape), ctypes.byref(seg.desc), k_out.data_ptr(),
                                      v_out.data_ptr(), _stream(stream)), "uc_dequantize_segment")
+
+
+def uc_stream_append(shape: uc_shape, seg: Segment, k_new: torch.Tensor, v_new: torch.Tensor,
+                     n_new: int, stream=None):
+    """Append n_new rows [B, Hkv, n_new, D] to a packed segment with a row
+    capacity; full row groups of the tail are quantised.  Advances
+    seg.n_rows."""
+    _check(lib.uc_stream_append(ctypes.byref(shape), ctypes.byref(seg.desc), k_new.data_ptr(),
+                                v_new.data_ptr(), n_new, _stream(stream)), "uc_stream_append")
+    seg.n_rows = seg.n_rows + n_new
 
 
 def uc_compose_index(outer: torch.Tensor, inner: torch.Tensor, out: torch.Tensor, stream=None):

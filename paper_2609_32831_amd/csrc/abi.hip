@@ -117,11 +117,17 @@ uc_status check_segment(const uc_shape& sh, const uc_segment& s, int idx, KSeg& 
   ks.bits = s.bits;
   ks.n_full = (int)n_full_of(s.n_rows, G);
   ks.tail_len = s.n_rows - ks.n_full;
+  if (s.row_stride < 0 || (s.row_stride > 0 && s.row_stride < s.n_rows))
+    return fail(UC_E_INVALID, "segment %d: row_stride %d < n_rows %d", idx, s.row_stride, s.n_rows);
+  ks.row_stride = s.row_stride;
+  ks.cap_full = s.row_stride ? (int)n_full_of(s.row_stride, G) : ks.n_full;
+  ks.kgroups = ks.cap_full / G;
+  ks.tail_stride = s.row_stride ? G : ks.tail_len;
   ks.head_bits = s.head_bits;
   ks.code_off = s.code_off;
   ks.codes_bytes = s.codes_bytes;
   if (!s.head_bits && !s.code_off) {
-    const uint64_t need = (uint64_t)BH * ks.n_full * sh.D * s.bits / 8;
+    const uint64_t need = (uint64_t)BH * ks.cap_full * sh.D * s.bits / 8;
     if (s.codes_bytes < need)
       return fail(UC_E_INVALID, "segment %d: codes_bytes %llu < %llu needed", idx,
                   (unsigned long long)s.codes_bytes, (unsigned long long)need);
@@ -130,7 +136,7 @@ uc_status check_segment(const uc_shape& sh, const uc_segment& s, int idx, KSeg& 
     if (!s.codes_k || !s.codes_v || !s.scale_k || !s.min_k || !s.scale_v || !s.min_v)
       return fail(UC_E_INVALID, "segment %d: packed buffer NULL", idx);
   }
-  if (ks.tail_len > 0 && (!s.tail_k || !s.tail_v))
+  if ((ks.tail_len > 0 || s.row_stride > 0) && (!s.tail_k || !s.tail_v))
     return fail(UC_E_INVALID, "segment %d: tail of %d rows but tail_k/tail_v NULL", idx, ks.tail_len);
   const void* ptrs[] = {s.codes_k, s.codes_v, s.scale_k, s.min_k, s.scale_v, s.min_v, s.tail_k, s.tail_v};
   for (const void* p : ptrs)
@@ -446,6 +452,27 @@ uc_status uc_dequantize_segment(const uc_shape* shape, const uc_segment* seg, vo
   if (!k_out || !v_out) return fail(UC_E_INVALID, "k_out or v_out is NULL");
   if (!aligned16(k_out) || !aligned16(v_out)) return fail(UC_E_INVALID, "k_out/v_out not 16-byte aligned");
   return launched(launch_dequantize(*shape, ks, k_out, v_out, (hipStream_t)stream));
+}
+
+uc_status uc_stream_append(const uc_shape* shape, const uc_segment* seg, const void* k_new,
+                           const void* v_new, int n_new, void* stream) {
+  uc_status st = check_shape(shape);
+  if (st) return st;
+  if (!seg || seg->kind != UC_SEG_PACKED) return fail(UC_E_INVALID, "seg must be a packed segment");
+  if (seg->row_stride <= 0) return fail(UC_E_INVALID, "seg needs a row capacity (row_stride > 0)");
+  if (seg->head_bits || seg->code_off)
+    return fail(UC_E_UNSUPPORTED, "streaming needs the uniform code layout (no head_bits/code_off)");
+  KSeg ks;
+  st = check_segment(*shape, *seg, 0, ks, true);
+  if (st) return st;
+  if (n_new < 0) return fail(UC_E_INVALID, "n_new < 0");
+  if ((int64_t)seg->n_rows + n_new > seg->row_stride)
+    return fail(UC_E_INVALID, "n_rows + n_new = %lld > row_stride %d",
+                (long long)seg->n_rows + n_new, seg->row_stride);
+  if (n_new == 0) return ok();
+  if (!k_new || !v_new) return fail(UC_E_INVALID, "k_new or v_new is NULL");
+  if (!aligned16(k_new) || !aligned16(v_new)) return fail(UC_E_INVALID, "k_new/v_new not 16-byte aligned");
+  return launched(launch_stream_append(*shape, ks, k_new, v_new, n_new, (hipStream_t)stream));
 }
 
 uc_status uc_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH, int k,

@@ -452,12 +452,12 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
   const int p1 = min(r1, ks.n_full);
   if (p1 > r0) {
     const int lgG = __builtin_ctz((unsigned)ks.group);
-    const int ngk = ks.n_full >> lgG, ngv = D >> lgG;
+    const int ngk = ks.n_full >> lgG, ngv = D >> lgG;  // live key groups, value groups per row
     const uint32_t cbytes = (uint32_t)ks.n_full * (D * bits / 8);
     PackedSeg P;
     P.ck = rsrc(ks.codes_k + off, cbytes);
     P.cv = rsrc(ks.codes_v + off, cbytes);
-    const int64_t sko = (int64_t)bh * ngk * D, svo = (int64_t)bh * ks.n_full * ngv;
+    const int64_t sko = (int64_t)bh * ks.kgroups * D, svo = (int64_t)bh * ks.cap_full * ngv;
     P.sk = rsrc(ks.scale_k + sko, (uint32_t)ngk * D * 4);
     P.mk = rsrc(ks.min_k + sko, (uint32_t)ngk * D * 4);
     P.sv = rsrc(ks.scale_v + svo, (uint32_t)ks.n_full * ngv * 4);
@@ -471,7 +471,7 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
   }
   const int t0 = max(r0, ks.n_full);
   if (r1 > t0) {
-    const int64_t base = (int64_t)bh * ks.tail_len * D;
+    const int64_t base = (int64_t)bh * ks.tail_stride * D;
     dense_loop(st, (const uint16_t*)ks.tail_k + base, (const uint16_t*)ks.tail_v + base,
                t0 - ks.n_full, r1 - ks.n_full, (wave - rot) & (WAVES - 1), lane, lq, scale_log2,
                lv);

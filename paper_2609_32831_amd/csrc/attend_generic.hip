@@ -35,7 +35,7 @@ struct RowLoader {
         vv[i] = load_elem(s.v, s.dtype, base + 64 * i);
       }
     } else if (r < s.n_full) {
-      const int rb = D * bits / 8, G = s.group, ngk = s.n_full / G;
+      const int rb = D * bits / 8, G = s.group;
       const uint8_t* ck = s.codes_k + off + (int64_t)r * rb;
       const uint8_t* cv = s.codes_v + off + (int64_t)r * rb;
       const int mask = (1 << bits) - 1, per_byte = 8 / bits;
@@ -44,13 +44,13 @@ struct RowLoader {
         const int d = lane + 64 * i;
         const int sh = (d % per_byte) * bits, by = d / per_byte;
         const int qk = (ck[by] >> sh) & mask, qv = (cv[by] >> sh) & mask;
-        const int64_t ik = ((int64_t)bh * ngk + r / G) * D + d;
-        const int64_t iv = ((int64_t)bh * s.n_full + r) * (D / G) + d / G;
+        const int64_t ik = ((int64_t)bh * s.kgroups + r / G) * D + d;
+        const int64_t iv = ((int64_t)bh * s.cap_full + r) * (D / G) + d / G;
         kv[i] = round_to(fmaf((float)qk, s.scale_k[ik], s.min_k[ik]), s.dtype);
         vv[i] = round_to(fmaf((float)qv, s.scale_v[iv], s.min_v[iv]), s.dtype);
       }
     } else {
-      const int64_t base = ((int64_t)bh * s.tail_len + (r - s.n_full)) * D + lane;
+      const int64_t base = ((int64_t)bh * s.tail_stride + (r - s.n_full)) * D + lane;
 #pragma unroll
       for (int i = 0; i < PER; ++i) {
         kv[i] = load_elem(s.tail_k, s.dtype, base + 64 * i);
@@ -261,17 +261,17 @@ __global__ __launch_bounds__(256) void score_colsum_kernel(KSegs segs, ChunkPlan
 #pragma unroll
       for (int d = 0; d < D; ++d) kr[d] = load_elem(s.k, s.dtype, base + d);
     } else if (r < s.n_full) {
-      const int rb = D * bits / 8, Gq = s.group, ngk = s.n_full / Gq;
+      const int rb = D * bits / 8, Gq = s.group;
       const uint8_t* ck = s.codes_k + off + (int64_t)r * rb;
       const int mask = (1 << bits) - 1, per_byte = 8 / bits;
 #pragma unroll
       for (int d = 0; d < D; ++d) {
         const int qk = (ck[d / per_byte] >> ((d % per_byte) * bits)) & mask;
-        const int64_t ik = ((int64_t)bh * ngk + r / Gq) * D + d;
+        const int64_t ik = ((int64_t)bh * s.kgroups + r / Gq) * D + d;
         kr[d] = round_to(fmaf((float)qk, s.scale_k[ik], s.min_k[ik]), s.dtype);
       }
     } else {
-      const int64_t base = ((int64_t)bh * s.tail_len + (r - s.n_full)) * D;
+      const int64_t base = ((int64_t)bh * s.tail_stride + (r - s.n_full)) * D;
 #pragma unroll
       for (int d = 0; d < D; ++d) kr[d] = load_elem(s.tail_k, s.dtype, base + d);
     }

@@ -329,7 +329,7 @@ __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
     ko = u4{nan2, nan2, nan2, nan2};
     vo = ko;
   } else {
-    const int rb = D * bits / 8, G = s.group, ngk = s.n_full / G;
+    const int rb = D * bits / 8, G = s.group;
     const uint8_t* ck = s.codes_k + off + (int64_t)r * rb + c8 * bits;  // 8 channels = bits bytes
     const uint8_t* cv = s.codes_v + off + (int64_t)r * rb + c8 * bits;
     uint64_t wk = 0, wv = 0;
@@ -338,10 +338,10 @@ __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
       wv |= (uint64_t)cv[i] << (8 * i);
     }
     const int mask = (1 << bits) - 1;
-    const float* sk = s.scale_k + ((int64_t)bh * ngk + r / G) * D + c8 * 8;
-    const float* mk = s.min_k + ((int64_t)bh * ngk + r / G) * D + c8 * 8;
+    const float* sk = s.scale_k + ((int64_t)bh * s.kgroups + r / G) * D + c8 * 8;
+    const float* mk = s.min_k + ((int64_t)bh * s.kgroups + r / G) * D + c8 * 8;
     // value groups: G consecutive channels of the row (G may be below 8)
-    const int64_t vrow = ((int64_t)bh * s.n_full + r) * (D / G);
+    const int64_t vrow = ((int64_t)bh * s.cap_full + r) * (D / G);
     uint32_t kw[4], vw[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -425,7 +425,7 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
     }
     if (s.tail_len > 0)
       vs.v[vs.n++] = View{(const uint16_t*)s.tail_k, (const uint16_t*)s.tail_v,
-                          (int64_t)s.tail_len * D, s.tail_len, i};
+                          (int64_t)s.tail_stride * D, s.tail_len, i};
   }
   // drop empty views (their tiles would be empty); keep the order
   int n = 0;

@@ -41,11 +41,10 @@ __device__ inline uint32_t pack_word(int code, int c, int b) {
 __global__ void quantize_k_kernel(KSeg seg, const void* __restrict__ k, int dt, int N, int D) {
   const int g = blockIdx.x, bh = blockIdx.y, c = threadIdx.x;
   const int G = seg.group;
-  const int ngk = seg.n_full / G;
   int b;
   int64_t off;
-  float* scale = const_cast<float*>(seg.scale_k) + ((int64_t)bh * ngk + g) * D + c;
-  float* mnp = const_cast<float*>(seg.min_k) + ((int64_t)bh * ngk + g) * D + c;
+  float* scale = const_cast<float*>(seg.scale_k) + ((int64_t)bh * seg.kgroups + g) * D + c;
+  float* mnp = const_cast<float*>(seg.min_k) + ((int64_t)bh * seg.kgroups + g) * D + c;
   if (!head_codes(seg, bh, D, b, off) || (off & 15)) {
     *scale = __builtin_nanf("");
     return;
@@ -97,7 +96,7 @@ __global__ void quantize_v_kernel(KSeg seg, const void* __restrict__ v, int dt, 
     const float s = ok ? __fdiv_rn(mx - mn, (float)((1 << b) - 1)) : __builtin_nanf("");
     ss[threadIdx.x] = s;
     ms[threadIdx.x] = mn;
-    const int64_t mi = ((int64_t)bh * seg.n_full + r) * ngv + c / G;
+    const int64_t mi = ((int64_t)bh * seg.cap_full + r) * ngv + c / G;
     const_cast<float*>(seg.scale_v)[mi] = s;
     const_cast<float*>(seg.min_v)[mi] = mn;
   }
@@ -122,7 +121,7 @@ __global__ void copy_tail_kernel(KSeg seg, const void* __restrict__ k, const voi
   const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 16;
   if (i >= tail_bytes) return;
   const int64_t src = ((int64_t)bh * N + seg.n_full) * row_bytes + i;
-  const int64_t dst = (int64_t)bh * tail_bytes + i;
+  const int64_t dst = (int64_t)bh * seg.tail_stride * row_bytes + i;
   *reinterpret_cast<uint4*>((char*)seg.tail_k + dst) =
       *reinterpret_cast<const uint4*>((const char*)k + src);
   *reinterpret_cast<uint4*>((char*)seg.tail_v + dst) =
@@ -142,7 +141,7 @@ __global__ void dequantize_kernel(KSeg s, void* __restrict__ kout, void* __restr
   const int64_t o = (int64_t)bh * N * D + e;
   float xk, xv;
   if (r >= s.n_full) {
-    const int64_t t = ((int64_t)bh * s.tail_len + (r - s.n_full)) * D + c;
+    const int64_t t = ((int64_t)bh * s.tail_stride + (r - s.n_full)) * D + c;
     xk = load_elem(s.tail_k, s.dtype, t);
     xv = load_elem(s.tail_v, s.dtype, t);
   } else {
@@ -151,13 +150,13 @@ __global__ void dequantize_kernel(KSeg s, void* __restrict__ kout, void* __restr
     if (!head_codes(s, bh, D, b, off)) {
       xk = xv = __builtin_nanf("");
     } else {
-      const int G = s.group, ngk = s.n_full / G, ngv = D / G;
+      const int G = s.group, ngv = D / G;
       const int64_t byte = off + (int64_t)r * (D * b / 8) + c * b / 8;
       const int shift = (c % (8 / b)) * b, mask = (1 << b) - 1;
       const int ck = (s.codes_k[byte] >> shift) & mask;
       const int cv = (s.codes_v[byte] >> shift) & mask;
-      const int64_t ki = ((int64_t)bh * ngk + r / G) * D + c;
-      const int64_t vi = ((int64_t)bh * s.n_full + r) * ngv + c / G;
+      const int64_t ki = ((int64_t)bh * s.kgroups + r / G) * D + c;
+      const int64_t vi = ((int64_t)bh * s.cap_full + r) * ngv + c / G;
       xk = round_to(__builtin_fmaf((float)ck, s.scale_k[ki], s.min_k[ki]), s.dtype);
       xv = round_to(__builtin_fmaf((float)cv, s.scale_v[vi], s.min_v[vi]), s.dtype);
     }
@@ -174,7 +173,58 @@ __global__ void dequantize_kernel(KSeg s, void* __restrict__ kout, void* __restr
   }
 }
 
+// Streaming append: rows j0 .. j0+n-1 of each head's new rows (n_new per
+// head) go to tail rows pos .. pos+n-1 (16 bytes per lane).
+__global__ void stream_copy_kernel(const char* __restrict__ knew, const char* __restrict__ vnew,
+                                   int n_new, int j0, int n, char* tk, char* tv, int tail_stride,
+                                   int pos, int row_bytes) {
+  const int bh = blockIdx.y;
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 16;
+  if (i >= (int64_t)n * row_bytes) return;
+  const int64_t src = ((int64_t)bh * n_new + j0) * row_bytes + i;
+  const int64_t dst = ((int64_t)bh * tail_stride + pos) * row_bytes + i;
+  *reinterpret_cast<uint4*>(tk + dst) = *reinterpret_cast<const uint4*>(knew + src);
+  *reinterpret_cast<uint4*>(tv + dst) = *reinterpret_cast<const uint4*>(vnew + src);
+}
+
 }  // namespace
+
+// Rows enter the tail; whenever it holds G rows they are quantised in place
+// as the next row group of the codes and scales (a view of the segment whose
+// storage starts at that group; the strides stay the segment's) and the tail
+// empties.
+hipError_t launch_stream_append(const uc_shape& sh, const KSeg& seg, const void* knew,
+                                const void* vnew, int n_new, hipStream_t st) {
+  const int G = seg.group, D = sh.D, BH = sh.B * sh.Hkv;
+  const int row_bytes = D * dtype_bytes(seg.dtype), code_row = D * seg.bits / 8;
+  int n_full = seg.n_full, tail = seg.tail_len;
+  for (int j = 0; j < n_new;) {
+    const int take = min(G - tail, n_new - j);
+    const int64_t lanes = (int64_t)take * row_bytes / 16;
+    hipLaunchKernelGGL(stream_copy_kernel, dim3((unsigned)((lanes + 255) / 256), BH), dim3(256), 0,
+                       st, (const char*)knew, (const char*)vnew, n_new, j, take,
+                       (char*)seg.tail_k, (char*)seg.tail_v, seg.tail_stride, tail, row_bytes);
+    j += take;
+    tail += take;
+    if (tail == G) {
+      KSeg v = seg;
+      v.n_rows = v.n_full = G;
+      v.tail_len = 0;
+      v.codes_k = seg.codes_k + (int64_t)n_full * code_row;
+      v.codes_v = seg.codes_v + (int64_t)n_full * code_row;
+      v.codes_bytes = seg.codes_bytes - (uint64_t)n_full * code_row;
+      v.scale_k = seg.scale_k + (int64_t)(n_full / G) * D;
+      v.min_k = seg.min_k + (int64_t)(n_full / G) * D;
+      v.scale_v = seg.scale_v + (int64_t)n_full * (D / G);
+      v.min_v = seg.min_v + (int64_t)n_full * (D / G);
+      hipError_t e = launch_quantize(sh, seg.tail_k, seg.tail_v, seg.dtype, G, v, st);
+      if (e != hipSuccess) return e;
+      n_full += G;
+      tail = 0;
+    }
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_dequantize(const uc_shape& sh, const KSeg& seg, void* kout, void* vout,
                              hipStream_t st) {

@@ -17,6 +17,9 @@ constexpr int kMaxSeg = UC_MAX_SEGMENTS;
 struct KSeg {
   int kind, dtype, n_rows, row_stride;
   int group, bits, n_full, tail_len;
+  // packed strides per (b, h_kv): rows of code / value-scale storage, key
+  // scale groups, tail rows (n_full, n_full/G, tail_len without a capacity)
+  int cap_full, kgroups, tail_stride;
   const void* k;
   const void* v;
   const uint8_t* head_bits;
@@ -92,7 +95,7 @@ __device__ inline bool head_codes(const KSeg& s, int bh, int D, int& bits, int64
     off = s.code_off[bh];
   } else {
     bits = s.bits;
-    off = s.code_off ? s.code_off[bh] : (int64_t)bh * s.n_full * D * s.bits / 8;
+    off = s.code_off ? s.code_off[bh] : (int64_t)bh * s.cap_full * D * s.bits / 8;
   }
   // per-head widths are bounded by the segment's bits (kernels are chosen by it)
   if (bits != 2 && bits != 4 && bits != 8) return false;
@@ -135,6 +138,8 @@ hipError_t launch_quantize(const uc_shape& sh, const void* k, const void* v, int
                            const KSeg& out, hipStream_t st);
 hipError_t launch_dequantize(const uc_shape& sh, const KSeg& seg, void* kout, void* vout,
                              hipStream_t st);
+hipError_t launch_stream_append(const uc_shape& sh, const KSeg& seg, const void* knew,
+                                const void* vnew, int n_new, hipStream_t st);
 hipError_t launch_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH,
                                 int k, int32_t* out, hipStream_t st);
 hipError_t launch_attend_generic(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
