@@ -21,7 +21,7 @@ from . import (NAME_DT, TORCH_DT, dense_segment, make_shape, packed_layout, pack
                uc_compose_index, uc_dense_bytes, uc_dequantize_segment, uc_evict_rows_for_budget,
                uc_packed_bytes, uc_quant_config, uc_quantize_segment, uc_retention_next,
                uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep,
-               uc_type_budget)
+               uc_stream_append, uc_type_budget)
 
 TORCH = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -87,6 +87,10 @@ class Run:
         self.scores: Dict[int, torch.Tensor] = {}
         self.keep: Dict[int, torch.Tensor] = {}
         self.mixed = []
+        # streaming tail: decode rows join the first quantised segment
+        self.stream = None
+        if w.mode == "decode" and w.stream_tail:
+            self.stream = next(i for i, p in enumerate(self.pol) if p.kind == "quant")
         for i, (s, p) in enumerate(zip(w.segments, self.pol)):
             dt = TORCH[s.dtype]
             if p.kind == "keep":
@@ -102,8 +106,10 @@ class Run:
                 hb = head_bits if p.bits is None else None
                 if p.bits is None and hb is None:
                     hb = [4] * BH
+                cap = s.n + w.steps if i == self.stream else 0
                 self.mixed.append(packed_segment(B, Hkv, s.n, D, s.group, dt,
-                                                 bits=p.bits or 4, head_bits=hb, device=device))
+                                                 bits=p.bits or 4, head_bits=hb, device=device,
+                                                 capacity=cap))
         self.tail = None
         if w.mode == "decode" and w.tail_capacity:
             tk = torch.zeros(B, Hkv, w.tail_capacity, D, dtype=TORCH["bf16"] if w.q_dtype == "bf16"
@@ -114,14 +120,19 @@ class Run:
         self.mass = torch.empty(B, Hkv, self.n_score, device=device)
         self.ws_score = torch.empty(max(uc_score_workspace_size(self.shape, self.full, w.W), 256),
                                     dtype=torch.uint8, device=device)
+        # workspaces are sized with the growing segments at full length
         if self.tail is not None:
             self.tail.n_rows = w.tail_capacity
+        if self.stream is not None:
+            self.mixed[self.stream].n_rows = w.segments[self.stream].n + w.steps
         M = w.M
         q_dt = NAME_DT[w.q_dtype]
         self.ws_attend = torch.empty(max(uc_attend_workspace_size(self.shape, self.mixed, q_dt, M), 256),
                                      dtype=torch.uint8, device=device)
         if self.tail is not None:
             self.tail.n_rows = 0
+        if self.stream is not None:
+            self.mixed[self.stream].n_rows = w.segments[self.stream].n
 
     # -- compression (once per prefill / per chunk) --------------------------
     def score(self, q_obs=None, W=None):
@@ -146,6 +157,7 @@ class Run:
     def quantize(self, k_src=None, v_src=None):
         for i, p in enumerate(self.pol):
             if p.kind == "quant":
+                self.mixed[i].n_rows = self.w.segments[i].n  # a streamed segment restarts
                 k = self.inp["seg_k"][i] if k_src is None else k_src
                 v = self.inp["seg_v"][i] if v_src is None else v_src
                 uc_quantize_segment(self.shape, k, v, self.w.segments[i].n, self.mixed[i])
@@ -164,6 +176,8 @@ class Run:
         if self.tail is not None:
             uc_append_rows(self.shape, inp["k_dec"][t], inp["v_dec"][t], 1, self.tail, t)
             self.tail.n_rows = t + 1
+        if self.stream is not None:  # the row joins the quantised segment's tail
+            uc_stream_append(self.shape, self.mixed[self.stream], inp["k_dec"][t], inp["v_dec"][t], 1)
         uc_attend_mixed(self.shape, self.mixed, inp["q_dec"][t], 1, self.sm, o, lse, seg_lse,
                         ws=self.ws_attend)
 
@@ -191,15 +205,17 @@ class Run:
         w = self.w
         BH = w.B * w.Hkv
         per = 0
-        for s, p, seg in zip(w.segments, self.pol, self.mixed):
+        for i, (s, p) in enumerate(zip(w.segments, self.pol)):
             eb = 4 if s.dtype == "f32" else (2)
             if p.kind == "keep":
                 per += s.n * 2 * w.D * eb
             elif p.kind == "evict":
                 per += p.k * 2 * w.D * eb
             else:
-                per += uc_packed_bytes(s.n, w.D, s.group, p.bits or 4, NAME_DT[s.dtype])
-        per += tail_rows * 2 * w.D * 2
+                n = s.n + (tail_rows if i == self.stream else 0)  # streamed rows join it
+                per += uc_packed_bytes(n, w.D, s.group, p.bits or 4, NAME_DT[s.dtype])
+        if self.stream is None:
+            per += tail_rows * 2 * w.D * 2
         qb = 4 if w.q_dtype == "f32" else 2
         M = w.M if w.mode == "prefill" else 1
         return BH * per + w.B * w.Hq * M * w.D * (qb + 4)

@@ -45,17 +45,38 @@ def _check_scores(gpu, ref64, total):
 
 
 def _packed_equal(seg, pk, bh):
-    """Codes/scales/minima of one head of a GPU packed segment vs the oracle's."""
+    """Codes/scales/minima of one head of a GPU packed segment vs the oracle's
+    quantisation of that head (the GPU segment may have room for more rows:
+    its per-head strides then follow its capacity)."""
     t = seg.t
-    n = pk["codes_k"].shape[0]
-    codes_per_head = n  # oracle quantised one head
-    off = bh * codes_per_head
+    n = pk["codes_k"].shape[0]                 # code bytes of the oracle's head
+    rows = pk["scale_v"].shape[1]              # its quantised rows
+    cap_rows = t["scale_v"].shape[2]           # the GPU segment's rows per head
+    off = bh * (n // rows) * cap_rows if rows else 0
     assert np.array_equal(t["codes_k"][off:off + n].cpu().numpy(), pk["codes_k"])
     assert np.array_equal(t["codes_v"][off:off + n].cpu().numpy(), pk["codes_v"])
     B, Hkv = t["scale_k"].shape[:2]
     for name in ("scale_k", "min_k", "scale_v", "min_v"):
-        g = t[name].reshape(B * Hkv, *t[name].shape[2:])[bh].cpu().numpy()
+        g = t[name].reshape(B * Hkv, *t[name].shape[2:])[bh][: pk[name].shape[1]].cpu().numpy()
         assert np.array_equal(g.view(np.uint32), pk[name][0].view(np.uint32)), name
+
+
+def _streamed_head(w, comp, hi, t, pols):
+    """The oracle's view of a streamed segment after decode step t: the
+    quantisation of its rows followed by the decode rows 0..t (a streaming
+    tail equals the batch quantisation of all its rows)."""
+    import oracle as ref
+    i = next(j for j, p in enumerate(pols) if p["kind"] == "quant")
+    s, p = w.segments[i], pols[i]
+    kk = np.concatenate([hi["seg_k"][i], hi["k_dec"][: t + 1]])
+    vv = np.concatenate([hi["seg_v"][i], hi["v_dec"][: t + 1]])
+    pk = ref.quantize(kk[None], vv[None], s.dtype, p["group"], [p["bits"]])
+    kh, vh = ref.dequant(pk, kk.shape[0], w.D, p["group"], s.dtype)
+    c = dict(comp)
+    c["khat"], c["vhat"], c["present"] = list(comp["khat"]), list(comp["vhat"]), list(comp["present"])
+    c["khat"][i], c["vhat"][i] = kh[0], vh[0]
+    c["present"][i] = np.ones(kk.shape[0], np.uint8)
+    return c, pk, i
 
 
 def _decode_chain(w, heads, steps):
@@ -95,11 +116,28 @@ def _decode_chain(w, heads, steps):
         gm = run.mass.reshape(w.B * w.Hkv, -1)[bh].cpu().numpy()
         assert np.allclose(gm, comp["mass"], rtol=2e-5, atol=1e-6 * tot)
         for t in steps:
-            o_ref, _, _, _ = op.attend_head(w, comp, hi["q_dec"][:, t:t + 1], w.q_dtype,
+            c = comp
+            if run.stream is not None:
+                c, _, _ = _streamed_head(w, comp, hi, t, pols)
+            o_ref, _, _, _ = op.attend_head(w, c, hi["q_dec"][:, t:t + 1], w.q_dtype,
                                             hi["k_dec"][: t + 1] if run.tail is not None else None,
                                             hi["v_dec"][: t + 1] if run.tail is not None else None)
             og = o[t, b, h * G:(h + 1) * G, 0].cpu().numpy()
             check_attention(og, o_ref[:, 0], f"{w.name} b={b} h={h} t={t}")
+        if run.stream is not None:  # the grown segment, bit for bit, after the last step
+            _, pk, i = _streamed_head(w, comp, hi, T - 1, pols)
+            seg = run.mixed[i]
+            G_, bits = pols[i]["group"], pols[i]["bits"]
+            n = w.segments[i].n + T
+            n_full = G_ * (n // G_)
+            rb = w.D * bits // 8
+            cap_full = seg.t["scale_v"].shape[2]
+            ck = seg.t["codes_k"][bh * cap_full * rb: bh * cap_full * rb + n_full * rb].cpu().numpy()
+            assert np.array_equal(ck, pk["codes_k"][: n_full * rb])
+            sv = seg.t["scale_v"].reshape(w.B * w.Hkv, cap_full, -1)[bh, :n_full].cpu().numpy()
+            assert np.array_equal(sv.view(np.uint32), pk["scale_v"][0].view(np.uint32))
+            tl = host_bytes(seg.t["tail_k"]).reshape(w.B * w.Hkv, G_, w.D)[bh, : n - n_full]
+            assert np.array_equal(tl, pk["tail_k"][0])
 
 
 def test_tiny_understanding():
@@ -112,6 +150,12 @@ def test_understanding_7b():
 
 def test_long_context_64k():
     _decode_chain(gen.LONG_CONTEXT_64K, [(0, 0), (7, 2), (15, 3)], [0, 1, 200, 511])
+
+
+def test_long_context_64k_streaming():
+    """The 64k decode workload with the decode rows streamed into the int4
+    text segment (a new quantised group every 64 steps)."""
+    _decode_chain(gen.LONG_CONTEXT_64K_STREAMING, [(0, 0), (9, 1)], [0, 62, 63, 64, 300, 511])
 
 
 def test_image_editing_prefill():

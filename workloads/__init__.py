@@ -143,6 +143,7 @@ class Workload:
     drift_sigma: float = 0.0
     rescore_every: int = 0
     tail_capacity: int = 0       # protected decode tail rows (decode append)
+    stream_tail: bool = False    # decode rows join the quantised segment's residual tail
     # dynamic budget (Sec. 3.3 Eq. 1-3): timesteps per statistics chunk, the
     # initial and minimum retention ratios, and the observation rows per query
     # head that re-score an evicting type at a chunk boundary
@@ -219,8 +220,17 @@ IMAGE_EDITING_DYNAMIC = Workload(
        "notes": "editing with Eq. 1-3: chunks of 5 timesteps, rho from 0.30 down to "
                 "at least 0.15 with the candidate mass, Eq. 2 type budgets"})
 
+# The 64k decode workload with a streaming residual tail: each decode step's
+# K/V row enters the int4 text segment's bf16 tail, and every 64 rows form a
+# new quantised group (no separate protected dense tail).
+LONG_CONTEXT_64K_STREAMING = Workload(
+    **{**LONG_CONTEXT_64K.__dict__, "name": "long_context_64k_streaming", "tail_capacity": 0,
+       "stream_tail": True,
+       "notes": "long_context_64k with decode rows streamed into the int4 g64 text segment"})
+
 WORKLOADS = {w.name: w for w in (TINY_UNDERSTANDING, UNDERSTANDING_7B, IMAGE_EDITING,
-                                 TEXT_TO_IMAGE, LONG_CONTEXT_64K, IMAGE_EDITING_DYNAMIC)}
+                                 TEXT_TO_IMAGE, LONG_CONTEXT_64K, IMAGE_EDITING_DYNAMIC,
+                                 LONG_CONTEXT_64K_STREAMING)}
 
 
 def scaled(w: Workload, **kw) -> Workload:
