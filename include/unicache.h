@@ -343,6 +343,18 @@ uc_status uc_stream_append(const uc_shape* shape, const uc_segment* seg,
                            const void* k_new, const void* v_new, int n_new,
                            void* stream);
 
+/* Attention concentration for calibration-based policy assignment (Sec. 3.2;
+ * App. B, "Calibration Setting": the fraction of a type's attention mass that
+ * its top 10 % of tokens capture; a type at 0.5 or above is assigned
+ * eviction, otherwise quantisation).  For every row r < BH of scores [BH, N]
+ * (non-negative, e.g. one segment's uc_score_importance output per
+ * (b, h_kv)): frac_out[r] = (sum of the k largest scores) / (sum of all N
+ * scores), summed in double; 0 when the sum is 0.  0 <= k <= N.  ws must hold
+ * uc_topk_mass_workspace_size(BH, k) bytes. */
+uc_status uc_topk_mass(const float* scores, int BH, int N, int k, float* frac_out,
+                       void* ws, size_t ws_bytes, void* stream);
+size_t uc_topk_mass_workspace_size(int BH, int k);
+
 /* Logical indices after a second eviction inside already compacted rows
  * (App. E: retained entries keep their logical token indices; Sec. 3.3:
  * eviction is irreversible, so a smaller budget selects among the rows still

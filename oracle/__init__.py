@@ -56,6 +56,7 @@ def lib():
             "ucref_assign_bits": (i32, [i32, vp, i64, i32, i32, i32, dbl, dbl, vp]),
             "ucref_type_budget": (i32, [i32, vp, vp, dbl, vp]),
             "ucref_quant_config": (i32, [dbl, i64, i32, i32, i32, i32]),
+            "ucref_topk_mass": (i32, [i32, i32, vp, i32, vp]),
             "ucref_retention_next": (dbl, [dbl, dbl, dbl, dbl, dbl]),
             "ucref_set_threads": (i32, [i32]),
         }
@@ -274,6 +275,20 @@ def type_budget(mass: Sequence[float], b_prev: Sequence[float], B_total: float) 
     if lib().ucref_type_budget(m.shape[0], m.ctypes.data, bp.ctypes.data, B_total,
                                out.ctypes.data) != 0:
         raise ValueError("ucref_type_budget: invalid arguments")
+    return out
+
+
+def topk_mass(scores: np.ndarray, k: int) -> np.ndarray:
+    """scores [BH, N] f32 -> fraction of each row's sum on its k largest
+    entries (float64).
+
+    Pinned by: uniform rows give k/N, one dominant entry gives ~1, k = N gives
+    1, k = 0 gives 0, brute force against numpy's sort."""
+    s = _c(scores, np.float32)
+    BH, N = s.shape
+    out = np.empty(BH)
+    if lib().ucref_topk_mass(BH, N, s.ctypes.data, k, out.ctypes.data) != 0:
+        raise ValueError("ucref_topk_mass: invalid arguments")
     return out
 
 

@@ -285,6 +285,26 @@ int ucref_select(int BH, int N, const float* scores, int k, int n_recent,
   return 0;
 }
 
+/* ---- calibration statistic -------------------------------------------------
+ * Sec. 3.2 and App. B ("Calibration Setting"): attention concentration of a
+ * type = the fraction of its attention mass captured by its top 10 % of
+ * tokens.  For every row: the k largest scores (sorted copy) summed in
+ * double, divided by the double sum of all scores (0 if that sum is 0). */
+int ucref_topk_mass(int BH, int N, const float* scores, int k, double* frac) {
+  if (k < 0 || k > N) return -1;
+  for (int r = 0; r < BH; ++r) {
+    std::vector<float> s(scores + (int64_t)r * N, scores + (int64_t)(r + 1) * N);
+    std::sort(s.begin(), s.end(), [](float a, float b) { return a > b; });
+    double top = 0.0, all = 0.0;
+    for (int i = 0; i < N; ++i) {
+      all += s[i];
+      if (i < k) top += s[i];
+    }
+    frac[r] = all > 0.0 ? top / all : 0.0;
+  }
+  return 0;
+}
+
 /* ---- attention --------------------------------------------------------------
  * App. E ("Attention over heterogeneous cache segments": one softmax shared by
  * all segments; the reference implementation evaluates compression with

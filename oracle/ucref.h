@@ -73,6 +73,10 @@ int ucref_assign_bits(int n_heads, const double* mass, int64_t N, int D, int G,
                       int dtype, double budget, double fixed, int32_t* bits);
 
 /* Sec. 3.3 Eq. 2 (type budgets) and Eq. 3 (retention schedule). */
+/* Sec. 3.2 / App. B: fraction of each row's score mass on its k largest
+ * scores. */
+int ucref_topk_mass(int BH, int N, const float* scores, int k, double* frac);
+
 /* Sec. 3.4: index of the most faithful (bits, group) configuration at or
  * after `first` that fits the budget (see ucref.cpp). */
 int ucref_quant_config(double budget, int64_t N, int D, int dtype, int n_heads, int first);

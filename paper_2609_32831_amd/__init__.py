@@ -86,6 +86,8 @@ def _load():
         "uc_dequantize_segment": (i32, [shp, segp, vp, vp, vp]),
         "uc_stream_append": (i32, [shp, segp, vp, vp, i32, vp]),
         "uc_compose_index": (i32, [vp, i32, vp, i32, i32, vp, vp]),
+        "uc_topk_mass": (i32, [vp, i32, i32, i32, vp, vp, sz, vp]),
+        "uc_topk_mass_workspace_size": (sz, [i32, i32]),
         "uc_quant_config": (i32, [dbl, i64, i32, i32, i32, i32, vp, vp]),
     }
     for name, (res, args) in sigs.items():
@@ -286,6 +288,16 @@ def uc_stream_append(shape: uc_shape, seg: Segment, k_new: torch.Tensor, v_new: 
     _check(lib.uc_stream_append(ctypes.byref(shape), ctypes.byref(seg.desc), k_new.data_ptr(),
                                 v_new.data_ptr(), n_new, _stream(stream)), "uc_stream_append")
     seg.n_rows = seg.n_rows + n_new
+
+
+def uc_topk_mass(scores: torch.Tensor, k: int, frac_out: torch.Tensor, stream=None):
+    """scores [BH, N] -> frac_out [BH]: share of each row's sum on its k
+    largest entries."""
+    BH, N = scores.shape[0], scores.shape[-1]
+    ws = _ws(lib.uc_topk_mass_workspace_size(BH, k), scores.device)
+    _check(lib.uc_topk_mass(scores.data_ptr(), BH, N, k, frac_out.data_ptr(), ws.data_ptr(),
+                            ws.numel(), _stream(stream)), "uc_topk_mass")
+    return frac_out
 
 
 def uc_compose_index(outer: torch.Tensor, inner: torch.Tensor, out: torch.Tensor, stream=None):

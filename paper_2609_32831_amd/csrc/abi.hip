@@ -475,6 +475,21 @@ uc_status uc_stream_append(const uc_shape* shape, const uc_segment* seg, const v
   return launched(launch_stream_append(*shape, ks, k_new, v_new, n_new, (hipStream_t)stream));
 }
 
+size_t uc_topk_mass_workspace_size(int BH, int k) {
+  if (BH < 1 || k < 0) return 0;
+  return (((size_t)BH * k * sizeof(int32_t)) + 255) & ~(size_t)255;
+}
+
+uc_status uc_topk_mass(const float* scores, int BH, int N, int k, float* frac_out, void* ws,
+                       size_t ws_bytes, void* stream) {
+  if (BH < 1 || N < 0) return fail(UC_E_INVALID, "BH must be >= 1 and N >= 0");
+  if (k < 0 || k > N) return fail(UC_E_INVALID, "k = %d outside [0, N = %d]", k, N);
+  if (!frac_out || (N > 0 && !scores)) return fail(UC_E_INVALID, "NULL pointer");
+  const size_t need = uc_topk_mass_workspace_size(BH, k);
+  if (k > 0 && (ws_bytes < need || !ws)) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  return launched(launch_topk_mass(scores, BH, N, k, frac_out, (int32_t*)ws, (hipStream_t)stream));
+}
+
 uc_status uc_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH, int k,
                            int32_t* out, void* stream) {
   if (BH < 0 || k < 0 || n_outer < 0) return fail(UC_E_INVALID, "BH, k and n_outer must be >= 0");

@@ -138,6 +138,30 @@ __global__ void gather_kernel(const int32_t* __restrict__ keep, int N, int k, co
   *reinterpret_cast<uint4*>(vdst + dof) = *reinterpret_cast<const uint4*>(vsrc + so);
 }
 
+// Fraction of a row's score mass on its k selected positions (double sums).
+__global__ void topk_fraction_kernel(const float* __restrict__ scores,
+                                     const int32_t* __restrict__ keep, int N, int k,
+                                     float* __restrict__ frac) {
+  __shared__ double red[2][4];
+  const int r = blockIdx.x;
+  const float* s = scores + (int64_t)r * N;
+  double top = 0.0, all = 0.0;
+  for (int j = threadIdx.x; j < k; j += blockDim.x) top += s[keep[(int64_t)r * k + j]];
+  for (int i = threadIdx.x; i < N; i += blockDim.x) all += s[i];
+  top = wave_sum_d(top);
+  all = wave_sum_d(all);
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = top;
+    red[1][threadIdx.x >> 6] = all;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const double t = red[0][0] + red[0][1] + red[0][2] + red[0][3];
+    const double a = red[1][0] + red[1][1] + red[1][2] + red[1][3];
+    frac[r] = a > 0.0 ? (float)(t / a) : 0.0f;
+  }
+}
+
 // out[bh, j] = outer[bh, inner[bh, j]] (-1 for an inner value out of range).
 __global__ void compose_index_kernel(const int32_t* __restrict__ outer, int n_outer,
                                      const int32_t* __restrict__ inner, int k,
@@ -180,6 +204,16 @@ hipError_t launch_gather(const int32_t* keep, int BH, int N, int k, const void* 
   hipLaunchKernelGGL(gather_kernel, dim3((unsigned)((lanes + 255) / 256), BH), dim3(256), 0, st,
                      keep, N, k, (const char*)ksrc, (const char*)vsrc, (char*)kdst, (char*)vdst,
                      row_bytes);
+  return hipGetLastError();
+}
+
+hipError_t launch_topk_mass(const float* scores, int BH, int N, int k, float* frac,
+                            int32_t* keep, hipStream_t st) {
+  if (k > 0) {
+    hipError_t e = launch_select(scores, BH, N, k, 0, keep, st);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL(topk_fraction_kernel, dim3(BH), dim3(256), 0, st, scores, keep, N, k, frac);
   return hipGetLastError();
 }
 

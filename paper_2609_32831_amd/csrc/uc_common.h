@@ -140,6 +140,8 @@ hipError_t launch_dequantize(const uc_shape& sh, const KSeg& seg, void* kout, vo
                              hipStream_t st);
 hipError_t launch_stream_append(const uc_shape& sh, const KSeg& seg, const void* knew,
                                 const void* vnew, int n_new, hipStream_t st);
+hipError_t launch_topk_mass(const float* scores, int BH, int N, int k, float* frac,
+                            int32_t* keep, hipStream_t st);
 hipError_t launch_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH,
                                 int k, int32_t* out, hipStream_t st);
 hipError_t launch_attend_generic(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,

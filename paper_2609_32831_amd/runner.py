@@ -21,7 +21,7 @@ from . import (NAME_DT, TORCH_DT, dense_segment, make_shape, packed_layout, pack
                uc_compose_index, uc_dense_bytes, uc_dequantize_segment, uc_evict_rows_for_budget,
                uc_packed_bytes, uc_quant_config, uc_quantize_segment, uc_retention_next,
                uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep,
-               uc_stream_append, uc_type_budget)
+               uc_stream_append, uc_topk_mass, uc_type_budget)
 
 TORCH = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -492,3 +492,36 @@ class DynamicRun:
             self.chunk = []
             return self._decide(t, m_c, q_obs, w.obs_window)
         return None
+
+
+def calibrate_policies(w, inp: Dict, examples: int, q_obs: Optional[torch.Tensor] = None,
+                       W: Optional[int] = None, top: float = 0.1, threshold: float = 0.5,
+                       device="cuda"):
+    """Calibration-based policy assignment (Sec. 3.2; App. B, "Calibration
+    Setting"): for every segment type, the fraction of its attention mass
+    that its top `top` share of tokens captures, per (example, KV head), from
+    the importance scores of the observation queries over the whole context;
+    averaged over the first `examples` batch elements (the calibration
+    examples) and their KV heads.  A type at `threshold` or above is assigned
+    eviction, otherwise quantisation.  Returns {segment name: (concentration,
+    policy)} and the per-(b, h_kv) fractions [examples * Hkv, n_segments]."""
+    B, Hkv, D = w.B, w.Hkv, w.D
+    assert 0 < examples <= B
+    shape = make_shape(B, w.Hq, Hkv, D)
+    full = [dense_segment(inp["seg_k"][i], inp["seg_v"][i]) for i in range(len(w.segments))]
+    q_obs = inp["q_obs"] if q_obs is None else q_obs
+    W = w.W if W is None else W
+    scores = [torch.empty(B, Hkv, s.n, device=device) for s in w.segments]
+    uc_score_importance(shape, full, q_obs, W, sm_scale(D), scores)
+    frac = torch.empty(B * Hkv, len(w.segments), device=device)
+    for i, s in enumerate(w.segments):
+        k = int(math.ceil(top * s.n))
+        col = torch.empty(B * Hkv, device=device)
+        uc_topk_mass(scores[i].view(B * Hkv, s.n), k, col)
+        frac[:, i] = col
+    f = frac[: examples * Hkv].double().cpu().numpy()
+    out = {}
+    for i, s in enumerate(w.segments):
+        c = float(f[:, i].mean())
+        out[s.name] = (c, "evict" if c >= threshold else "quant")
+    return out, f

@@ -197,3 +197,23 @@ def test_chain_forced_requantisation(ref, gen, chain):
         V = np.concatenate([vs[0][h], vs[1][h][kept], vh[h]])
         P = _softmax_rows(q[hq], K, op.sm_scale(D))
         assert np.allclose(r["att"][6][0][hq], P @ V, rtol=1e-12, atol=1e-13), hq
+
+
+def test_topk_mass_closed_forms_and_brute_force(ref):
+    """Sec. 3.2 / App. B concentration statistic."""
+    assert np.allclose(ref.topk_mass(np.ones((3, 50), np.float32), 5), 0.1, rtol=0, atol=1e-15)
+    s = np.full((1, 100), 1e-3, np.float32)
+    s[0, 37] = 10.0
+    exp = (10.0 + 9 * np.float64(np.float32(1e-3))) / (10.0 + 99 * np.float64(np.float32(1e-3)))
+    assert abs(ref.topk_mass(s, 10)[0] - exp) < 1e-12
+    rng = np.random.default_rng(3)
+    x = rng.integers(0, 5, (4, 333)).astype(np.float32)  # ties on purpose
+    for k in (0, 1, 34, 333):
+        got = ref.topk_mass(x, k)
+        for r in range(4):
+            srt = np.sort(x[r].astype(np.float64))[::-1]
+            want = srt[:k].sum() / srt.sum() if srt.sum() > 0 else 0.0
+            assert abs(got[r] - want) < 1e-12, (k, r)
+    assert np.all(ref.topk_mass(np.zeros((2, 10), np.float32), 3) == 0.0)
+    with pytest.raises(ValueError):
+        ref.topk_mass(x, 334)
