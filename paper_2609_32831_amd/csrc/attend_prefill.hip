@@ -44,8 +44,9 @@ constexpr int kMaxViews = 2 * kMaxSeg;
 struct View {
   const uint16_t* k;
   const uint16_t* v;
-  int64_t bh_stride;  // elements between consecutive (b, h_kv)
-  int n;              // rows
+  const uint16_t* vh;  // the V rows converted to fp16 once per call, [BH, n, D]
+  int64_t bh_stride;   // elements between consecutive (b, h_kv) of k and v
+  int n;               // rows
   int seg;
 };
 
@@ -76,11 +77,15 @@ struct Stage {
   u4 k[2], v[2];
 };
 
+// F16: V comes from the view's fp16 copy
+template <bool F16>
 __device__ inline void stage_load(const Views& vs, int t, int bh, Stage& S) {
   int row0;
   const View& w = vs.v[tile_view(vs, t, row0)];
   const __amdgpu_buffer_rsrc_t rk = rsrc(w.k + bh * w.bh_stride, (uint32_t)w.n * ROWB);
-  const __amdgpu_buffer_rsrc_t rv = rsrc(w.v + bh * w.bh_stride, (uint32_t)w.n * ROWB);
+  const __amdgpu_buffer_rsrc_t rv =
+      F16 ? rsrc(w.vh + (int64_t)bh * w.n * D, (uint32_t)w.n * ROWB)
+          : rsrc(w.v + bh * w.bh_stride, (uint32_t)w.n * ROWB);
   const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
   const int off = (row0 + r) * ROWB + c * 16;
   S.k[0] = bload(rk, off, 0);
@@ -89,22 +94,12 @@ __device__ inline void stage_load(const Views& vs, int t, int bh, Stage& S) {
   S.v[1] = bload(rv, off, 16 * ROWB);
 }
 
-// F16: V is staged as fp16 (the range check found every value in range)
-template <bool F16>
 __device__ inline void stage_store(char* buf, const Stage& S) {
   const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
   *reinterpret_cast<u4*>(buf + toff(r, c)) = S.k[0];
   *reinterpret_cast<u4*>(buf + toff(r + 16, c)) = S.k[1];
-  u4 v0 = S.v[0], v1 = S.v[1];
-  if (F16) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      v0[e] = bf2_to_h2(v0[e]);
-      v1[e] = bf2_to_h2(v1[e]);
-    }
-  }
-  *reinterpret_cast<u4*>(buf + TILEB + toff(r, c)) = v0;
-  *reinterpret_cast<u4*>(buf + TILEB + toff(r + 16, c)) = v1;
+  *reinterpret_cast<u4*>(buf + TILEB + toff(r, c)) = S.v[0];
+  *reinterpret_cast<u4*>(buf + TILEB + toff(r + 16, c)) = S.v[1];
 }
 
 // softmax of one query tile's 8 logits per lane; returns the probability
@@ -173,18 +168,18 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
   const int T = vs.tiles;
   {
     Stage S;
-    stage_load(vs, 0, bh, S);
-    stage_store<F16>(lds, S);
+    stage_load<F16>(vs, 0, bh, S);
+    stage_store(lds, S);
     if (T > 1) {
-      stage_load(vs, 1, bh, S);
-      stage_store<F16>(lds + STAGEB, S);
+      stage_load<F16>(vs, 1, bh, S);
+      stage_store(lds + STAGEB, S);
     }
   }
   __syncthreads();
   for (int t = 0; t < T; ++t) {
     Stage S;
     const bool pre = t + 2 < T;
-    if (pre) stage_load(vs, t + 2, bh, S);
+    if (pre) stage_load<F16>(vs, t + 2, bh, S);
     const char* lk = lds + (t % STAGES) * STAGEB;
     const char* lv = lk + TILEB;
     int row0;
@@ -234,7 +229,7 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
         }
       }
     }
-    if (pre) stage_store<F16>(lds + ((t + 2) % STAGES) * STAGEB, S);
+    if (pre) stage_store(lds + ((t + 2) % STAGES) * STAGEB, S);
     __syncthreads();
   }
   return cur_view;
@@ -315,7 +310,8 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const ui
 // out[b, h, r, c] = round_to_bf16(fmaf(code, scale, min)); one thread per
 // 8 channels of one row, K and V
 __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
-                               uint16_t* __restrict__ vout, int* __restrict__ v_unsafe) {
+                               uint16_t* __restrict__ vout, uint16_t* __restrict__ vhout,
+                               int* __restrict__ v_unsafe) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // (bh, row, c8)
   const int c8 = (int)(e % (D / 8));
   const int64_t rr = e / (D / 8);
@@ -360,16 +356,22 @@ __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
   const int64_t oi = ((int64_t)bh * s.n_full + r) * D + c8 * 8;
   *reinterpret_cast<u4*>(kout + oi) = ko;
   *reinterpret_cast<u4*>(vout + oi) = vo;
+  *reinterpret_cast<u4*>(vhout + oi) =
+      u4{bf2_to_h2(vo[0]), bf2_to_h2(vo[1]), bf2_to_h2(vo[2]), bf2_to_h2(vo[3])};
   if (bf2_over_f16(vo[0]) || bf2_over_f16(vo[1]) || bf2_over_f16(vo[2]) || bf2_over_f16(vo[3]))
     atomicOr(v_unsafe, 1);
 }
 
 // V rows of a dense view: flag values that fp16 cannot hold
-__global__ void vrange_kernel(const uint16_t* __restrict__ v, int64_t bh_stride, int n_rows,
-                              int* __restrict__ v_unsafe) {
+// fp16 copy of a view's bf16 V rows ([BH, n, D], round to nearest even) and
+// the range check: a value with no fp16 counterpart sets the flag
+__global__ void vconvert_kernel(const uint16_t* __restrict__ v, int64_t bh_stride, int n_rows,
+                                uint16_t* __restrict__ vh, int* __restrict__ v_unsafe) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;  // 8 elements each
   if (e >= (int64_t)n_rows * (D / 8)) return;
   const u4 x = *reinterpret_cast<const u4*>(v + blockIdx.y * bh_stride + e * 8);
+  *reinterpret_cast<u4*>(vh + (int64_t)blockIdx.y * n_rows * D + e * 8) =
+      u4{bf2_to_h2(x[0]), bf2_to_h2(x[1]), bf2_to_h2(x[2]), bf2_to_h2(x[3])};
   if (bf2_over_f16(x[0]) || bf2_over_f16(x[1]) || bf2_over_f16(x[2]) || bf2_over_f16(x[3]))
     atomicOr(v_unsafe, 1);
 }
@@ -387,12 +389,21 @@ bool prefill_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int 
 }
 
 // Workspace: a flag word (some V value outside fp16's range), then bf16 K
-// and V of every packed segment's whole row groups.
+// and V plus fp16 V of every packed segment's whole row groups, and the fp16
+// V copy of every dense view (dense segments, residual tails).
 size_t prefill_mfma_workspace(const uc_shape& sh, const KSegs& segs) {
+  const size_t BH = (size_t)sh.B * sh.Hkv;
+  auto round = [](size_t x) { return (x + 255) & ~(size_t)255; };
   size_t bytes = 256;
-  for (int i = 0; i < segs.n; ++i)
-    if (segs.s[i].kind == UC_SEG_PACKED)
-      bytes += (((size_t)sh.B * sh.Hkv * segs.s[i].n_full * D * 2 * 2) + 255) & ~(size_t)255;
+  for (int i = 0; i < segs.n; ++i) {
+    const KSeg& s = segs.s[i];
+    if (s.kind == UC_SEG_PACKED) {
+      bytes += round(BH * s.n_full * D * 2 * 3);
+      bytes += round(BH * s.tail_len * D * 2);
+    } else {
+      bytes += round(BH * s.n_rows * D * 2);
+    }
+  }
   return bytes;
 }
 
@@ -409,22 +420,28 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   hipLaunchKernelGGL(flag_clear_kernel, dim3(1), dim3(1), 0, st, v_unsafe);
   for (int i = 0; i < segs.n; ++i) {
     const KSeg& s = segs.s[i];
+    auto take = [&](size_t bytes) {
+      char* p = wp;
+      wp += (bytes + 255) & ~(size_t)255;
+      return (uint16_t*)p;
+    };
     if (s.kind == UC_SEG_DENSE) {
-      vs.v[vs.n++] = View{(const uint16_t*)s.k, (const uint16_t*)s.v, (int64_t)s.row_stride * D,
-                          s.n_rows, i};
+      vs.v[vs.n++] = View{(const uint16_t*)s.k, (const uint16_t*)s.v,
+                          take((size_t)BH * s.n_rows * D * 2), (int64_t)s.row_stride * D, s.n_rows, i};
       continue;
     }
     if (s.n_full > 0) {
-      uint16_t* kd = (uint16_t*)wp;
+      uint16_t* kd = take((size_t)BH * s.n_full * D * 2 * 3);
       uint16_t* vd = kd + (size_t)BH * s.n_full * D;
-      wp += (((size_t)BH * s.n_full * D * 2 * 2) + 255) & ~(size_t)255;
+      uint16_t* vh = vd + (size_t)BH * s.n_full * D;
       const int64_t n_thr = (int64_t)BH * s.n_full * (D / 8);
       hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)((n_thr + 255) / 256)), dim3(256), 0, st,
-                         s, BH, kd, vd, v_unsafe);
-      vs.v[vs.n++] = View{kd, vd, (int64_t)s.n_full * D, s.n_full, i};
+                         s, BH, kd, vd, vh, v_unsafe);
+      vs.v[vs.n++] = View{kd, vd, vh, (int64_t)s.n_full * D, s.n_full, i};
     }
+    uint16_t* th = take((size_t)BH * s.tail_len * D * 2);
     if (s.tail_len > 0)
-      vs.v[vs.n++] = View{(const uint16_t*)s.tail_k, (const uint16_t*)s.tail_v,
+      vs.v[vs.n++] = View{(const uint16_t*)s.tail_k, (const uint16_t*)s.tail_v, th,
                           (int64_t)s.tail_stride * D, s.tail_len, i};
   }
   // drop empty views (their tiles would be empty); keep the order
@@ -435,10 +452,10 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   for (int i = 0; i < n; ++i) {
     tiles += (vs.v[i].n + TILE - 1) / TILE;
     if (segs.s[vs.v[i].seg].kind == UC_SEG_PACKED && vs.v[i].v != (const uint16_t*)segs.s[vs.v[i].seg].tail_v)
-      continue;  // dequantised rows were checked by the dequant kernel
+      continue;  // dequantised rows were converted and checked by the dequant kernel
     const int64_t per = (int64_t)vs.v[i].n * (D / 8);
-    hipLaunchKernelGGL(vrange_kernel, dim3((unsigned)((per + 255) / 256), BH), dim3(256), 0, st,
-                       vs.v[i].v, vs.v[i].bh_stride, vs.v[i].n, v_unsafe);
+    hipLaunchKernelGGL(vconvert_kernel, dim3((unsigned)((per + 255) / 256), BH), dim3(256), 0, st,
+                       vs.v[i].v, vs.v[i].bh_stride, vs.v[i].n, (uint16_t*)vs.v[i].vh, v_unsafe);
   }
   vs.tiles = tiles;
   hipError_t e = hipGetLastError();
