@@ -157,8 +157,35 @@ __device__ inline float col_sum(float x) {
   return x;
 }
 
-// the key-tile loop of one workgroup (see the file comment); returns the
-// view of the last tile
+// K rows of tile buffer lk as A operands (shared by the query tiles)
+__device__ inline void load_ka(const char* lk, int i16, int g4, u4 (&ka)[8]) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    ka[k] = *reinterpret_cast<const u4*>(lk + toff(i16, k * 4 + g4));
+    ka[4 + k] = *reinterpret_cast<const u4*>(lk + toff(16 + i16, k * 4 + g4));
+  }
+}
+
+// S^T = K Q^T of one tile for every query tile of the wave
+__device__ inline void tile_scores(const u4 (&ka)[8], const u4 (&qop)[QTW][4], f4 (&s)[QTW][2]) {
+#pragma unroll
+  for (int qt = 0; qt < QTW; ++qt) {
+    f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      s0 = mfma(ka[k], qop[qt][k], s0);
+      s1 = mfma(ka[4 + k], qop[qt][k], s1);
+    }
+    s[qt][0] = s0;
+    s[qt][1] = s1;
+  }
+}
+
+// the key-tile loop of one workgroup (see the file comment), software
+// pipelined: while tile t's softmax runs on the vector ALUs, the scores of
+// tile t+1 run on the matrix cores (their K rows are in LDS one iteration
+// early: the three-deep ring holds tiles t, t+1 and the one being staged).
+// Returns the view of the last tile.
 template <bool F16>
 __device__ __attribute__((always_inline)) inline int tile_loop(
     const Views& vs, int bh, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW],
@@ -176,12 +203,17 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     }
   }
   __syncthreads();
+  f4 sc[QTW][2];
+  {
+    u4 ka[8];
+    load_ka(lds, i16, g4, ka);
+    tile_scores(ka, qop, sc);
+  }
   for (int t = 0; t < T; ++t) {
     Stage S;
     const bool pre = t + 2 < T;
     if (pre) stage_load<F16>(vs, t + 2, bh, S);
-    const char* lk = lds + (t % STAGES) * STAGEB;
-    const char* lv = lk + TILEB;
+    const char* lv = lds + (t % STAGES) * STAGEB + TILEB;
     int row0;
     const int vi = tile_view(vs, t, row0);
     const int n_valid = min(TILE, vs.v[vi].n - row0);
@@ -198,23 +230,15 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
       }
     }
     cur_view = vi;
-    // K rows of the tile as A operands, shared by the query tiles
-    u4 ka[8];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      ka[k] = *reinterpret_cast<const u4*>(lk + toff(i16, k * 4 + g4));
-      ka[4 + k] = *reinterpret_cast<const u4*>(lk + toff(16 + i16, k * 4 + g4));
-    }
     u4 phi[QTW], plo[QTW];
 #pragma unroll
-    for (int qt = 0; qt < QTW; ++qt) {
-      f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        s0 = mfma(ka[k], qop[qt][k], s0);
-        s1 = mfma(ka[4 + k], qop[qt][k], s1);
-      }
-      tile_softmax<F16>(st[qt], s0, s1, scale_log2, n_valid, g4, phi[qt], plo[qt]);
+    for (int qt = 0; qt < QTW; ++qt)
+      tile_softmax<F16>(st[qt], sc[qt][0], sc[qt][1], scale_log2, n_valid, g4, phi[qt], plo[qt]);
+    // scores of the next tile (past the last tile: a stale buffer, unused)
+    {
+      u4 ka[8];
+      load_ka(lds + ((t + 1) % STAGES) * STAGEB, i16, g4, ka);
+      tile_scores(ka, qop, sc);
     }
 #pragma unroll
     for (int d = 0; d < 8; ++d) {
