@@ -316,6 +316,30 @@ double uc_retention_next(double rho, double rho_init, double rho_min,
 int uc_set_path(int path);
 
 /* ------------------------------------------------------------------------ */
+/* Batched attention over requests of different segment layouts (App. E,
+ * "Batched attention and CFG execution": compatible attention calls are
+ * combined into one variable-length launch).  shape->B is the number of
+ * requests; request r has its own segments segs[r][0 .. n_segs[r]-1], each
+ * described with the layout of a single batch element (B = 1: k/v
+ * [1, Hkv, row_stride, D], codes and scales of Hkv heads, ...), so row counts,
+ * segment kinds and policies may differ between requests.  q [B, Hq, M, D]
+ * and o [B, Hq, M, D], lse [B, Hq, M] (optional) are laid out as for B batch
+ * elements.  Each request's o and lse equal those of uc_attend_mixed on its
+ * own segments (up to the order of floating-point sums).  When every request
+ * fits the matrix-core decode kernel (bf16, D = 128, G*M <= 16, packed groups
+ * >= 32 and widths <= 4) all of them run in one launch (plus the merge of
+ * partial results); otherwise the requests run one call each.  segs and
+ * n_segs are host arrays; ws must hold uc_attend_batch_workspace_size(...)
+ * bytes (descriptors and partial records).  No per-segment lse. */
+uc_status uc_attend_batch(const uc_shape* shape, const uc_segment* const* segs,
+                          const int* n_segs, const void* q, uc_dtype q_dt, int M,
+                          float sm_scale, float* o, float* lse, void* ws,
+                          size_t ws_bytes, void* stream);
+size_t uc_attend_batch_workspace_size(const uc_shape* shape,
+                                      const uc_segment* const* segs,
+                                      const int* n_segs, uc_dtype q_dt, int M);
+
+/* ------------------------------------------------------------------------ */
 /* Dequantised rows of a packed segment (App. E storage; the stored-value
  * definition x_hat = round_to_dtype(fmaf(code, scale, min)) that attention
  * uses).  k_out and v_out [B, Hkv, seg->n_rows, D] in seg->dtype, device,

@@ -84,6 +84,8 @@ def _load():
         "uc_set_path": (i32, [i32]),
         "uc_set_kernel_events": (i32, [vp, vp]),
         "uc_dequantize_segment": (i32, [shp, segp, vp, vp, vp]),
+        "uc_attend_batch": (i32, [shp, vp, vp, vp, i32, i32, ctypes.c_float, vp, vp, vp, sz, vp]),
+        "uc_attend_batch_workspace_size": (sz, [shp, vp, vp, i32, i32]),
         "uc_stream_append": (i32, [shp, segp, vp, vp, i32, vp]),
         "uc_compose_index": (i32, [vp, i32, vp, i32, i32, vp, vp]),
         "uc_topk_mass": (i32, [vp, i32, i32, i32, vp, vp, sz, vp]),
@@ -271,6 +273,34 @@ def uc_quantize_segment(shape: uc_shape, k: torch.Tensor, v: torch.Tensor, N: in
     _check(lib.uc_quantize_segment(ctypes.byref(shape), k.data_ptr(), v.data_ptr(),
                                    TORCH_DT[k.dtype], N, ctypes.byref(out.desc),
                                    _stream(stream)), "uc_quantize_segment")
+
+
+def _batch_arrays(reqs: Sequence[Sequence[Segment]]):
+    arrs = [_seg_array(r) for r in reqs]
+    ptrs = (ctypes.c_void_p * len(reqs))(*[ctypes.cast(a, ctypes.c_void_p) for a in arrs])
+    counts = (ctypes.c_int * len(reqs))(*[len(r) for r in reqs])
+    return arrs, ptrs, counts
+
+
+def uc_attend_batch_workspace_size(shape: uc_shape, reqs: Sequence[Sequence[Segment]], q_dt: int,
+                                   M: int) -> int:
+    arrs, ptrs, counts = _batch_arrays(reqs)
+    return int(lib.uc_attend_batch_workspace_size(ctypes.byref(shape), ptrs, counts, q_dt, M))
+
+
+def uc_attend_batch(shape: uc_shape, reqs: Sequence[Sequence[Segment]], q: torch.Tensor, M: int,
+                    sm_scale: float, o: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                    ws: Optional[torch.Tensor] = None, stream=None):
+    """Requests of different segment layouts (each a list of one-request
+    segments) attended in one call; q / o / lse as for len(reqs) batch
+    elements."""
+    arrs, ptrs, counts = _batch_arrays(reqs)
+    if ws is None:
+        ws = _ws(lib.uc_attend_batch_workspace_size(ctypes.byref(shape), ptrs, counts,
+                                                    TORCH_DT[q.dtype], M), q.device)
+    _check(lib.uc_attend_batch(ctypes.byref(shape), ptrs, counts, q.data_ptr(), TORCH_DT[q.dtype],
+                               M, ctypes.c_float(sm_scale), o.data_ptr(), _ptr(lse),
+                               ws.data_ptr(), ws.numel(), _stream(stream)), "uc_attend_batch")
 
 
 def uc_dequantize_segment(shape: uc_shape, seg: Segment, k_out: torch.Tensor,

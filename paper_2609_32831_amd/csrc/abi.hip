@@ -34,6 +34,12 @@ size_t decode_mfma_workspace(const uc_shape& sh, const KSegs& segs, int M);
 hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
                               hipStream_t st);
+int decode_batch_wgs(const uc_shape& sh);
+size_t decode_batch_desc_bytes(int n_req, int n_segs_total);
+size_t decode_batch_workspace(const uc_shape& sh, int M, int n_segs_total);
+hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, int n_wgs,
+                               const void* q, int M, float sm_scale, float* o, float* lse,
+                               void* ws, hipStream_t st);
 }  // namespace uc
 
 namespace {
@@ -295,6 +301,112 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
   if (e == hipSuccess) e = kernel_timer_end(s);
   if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, M, partial, o, lse, seg_lse, s);
   return launched(e);
+}
+
+// ---------------------------------------------------------------- batched requests
+// Validates every request against a one-request shape; true if all of them
+// can run in the batched decode kernel.
+static uc_status batch_check(const uc_shape* shape, const uc_segment* const* segs,
+                             const int* n_segs, uc_dtype q_dt, int M, std::vector<KSegs>& ks,
+                             bool& batched) {
+  uc_status st = check_shape(shape);
+  if (st) return st;
+  if (!segs || !n_segs) return fail(UC_E_INVALID, "segs or n_segs is NULL");
+  if (!dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad q dtype %d", q_dt);
+  if (M < 1) return fail(UC_E_INVALID, "M must be >= 1 (got %d)", M);
+  const uc_shape one{1, shape->Hq, shape->Hkv, shape->D};
+  ks.resize(shape->B);
+  batched = g_path.load() == UC_PATH_AUTO;
+  for (int r = 0; r < shape->B; ++r) {
+    st = check_segments(&one, segs[r], n_segs[r], ks[r]);
+    if (st) {
+      char why[sizeof g_err];
+      snprintf(why, sizeof why, "%s", g_err);
+      return fail(st, "request %d: %s", r, why);
+    }
+    batched = batched && decode_mfma_eligible(one, ks[r], q_dt, M);
+  }
+  return UC_OK;
+}
+
+size_t uc_attend_batch_workspace_size(const uc_shape* shape, const uc_segment* const* segs,
+                                      const int* n_segs, uc_dtype q_dt, int M) {
+  std::vector<KSegs> ks;
+  bool batched = false;
+  if (batch_check(shape, segs, n_segs, q_dt, M, ks, batched)) return 0;
+  int total = 0;
+  for (int r = 0; r < shape->B; ++r) total += n_segs[r];
+  if (batched) return decode_batch_workspace(*shape, M, total);
+  const uc_shape one{1, shape->Hq, shape->Hkv, shape->D};
+  size_t need = 0;
+  for (int r = 0; r < shape->B; ++r)
+    need = std::max(need, uc_attend_workspace_size(&one, segs[r], n_segs[r], q_dt, M));
+  return need;
+}
+
+uc_status uc_attend_batch(const uc_shape* shape, const uc_segment* const* segs, const int* n_segs,
+                          const void* q, uc_dtype q_dt, int M, float sm_scale, float* o,
+                          float* lse, void* ws, size_t ws_bytes, void* stream) {
+  TimerScope timer;
+  std::vector<KSegs> ks;
+  bool batched = false;
+  uc_status st = batch_check(shape, segs, n_segs, q_dt, M, ks, batched);
+  if (st) return st;
+  if (!q || !o) return fail(UC_E_INVALID, "q or o is NULL");
+  if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
+  if ((int64_t)shape->B * shape->Hq * M > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
+  hipStream_t s = (hipStream_t)stream;
+  if (batched) {
+    int total = 0;
+    for (int r = 0; r < shape->B; ++r) total += n_segs[r];
+    const size_t need = decode_batch_workspace(*shape, M, total);
+    if (ws_bytes < need || !ws) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+    // request table and flat descriptors, in the workspace's layout, sent to
+    // the GPU inside small kernels' arguments (no staging, no host wait)
+    const size_t tbytes = (((size_t)shape->B * sizeof(BatchDesc)) + 255) & ~(size_t)255;
+    std::vector<char> desc(decode_batch_desc_bytes(shape->B, total), 0);
+    BatchDesc* table = (BatchDesc*)desc.data();
+    KSeg* flat = (KSeg*)(desc.data() + tbytes);
+    // workgroups per KV head in proportion to each request's rows
+    const int budget = decode_batch_wgs(*shape);
+    double all_rows = 0.0;
+    std::vector<double> rows(shape->B, 0.0);
+    for (int r = 0; r < shape->B; ++r) {
+      for (int i = 0; i < n_segs[r]; ++i) rows[r] += ks[r].s[i].n_rows;
+      all_rows += rows[r];
+    }
+    // (the minimum of one per request is taken out of the budget first, so
+    // the grid stays within one round of resident workgroups)
+    const int spare = std::max(0, budget - shape->B);
+    int pos = 0, W_max = 1, n_wgs = 0;
+    for (int r = 0; r < shape->B; ++r) {
+      const int Wr = std::min(budget, 1 + (int)(spare * rows[r] / all_rows));
+      W_max = std::max(W_max, Wr);
+      table[r] = BatchDesc{pos, n_segs[r], Wr, n_wgs};
+      n_wgs += Wr * shape->Hkv;
+      for (int i = 0; i < n_segs[r]; ++i) flat[pos++] = ks[r].s[i];
+    }
+    hipError_t e = launch_blob_upload(desc.data(), desc.size(), ws, s);
+    if (e == hipSuccess)
+      e = launch_decode_batch(*shape, total, W_max, n_wgs, q, M, sm_scale, o, lse, ws, s);
+    return launched(e);
+  }
+  // one call per request (the timing hook is not applied here)
+  g_ev_active[0] = g_ev_active[1] = nullptr;
+  const uc_shape one{1, shape->Hq, shape->Hkv, shape->D};
+  const size_t qrow = (size_t)shape->Hq * M * shape->D * (q_dt == UC_F32 ? 4 : 2);
+  for (int r = 0; r < shape->B; ++r) {
+    st = uc_attend_mixed(&one, segs[r], n_segs[r], (const char*)q + r * qrow, q_dt, M, sm_scale,
+                         o + (size_t)r * shape->Hq * M * shape->D,
+                         lse ? lse + (size_t)r * shape->Hq * M : nullptr, nullptr, ws, ws_bytes,
+                         stream);
+    if (st) {
+      char why[sizeof g_err];
+      snprintf(why, sizeof why, "%s", g_err);
+      return fail(st, "request %d: %s", r, why);
+    }
+  }
+  return ok();
 }
 
 // ---------------------------------------------------------------- scoring

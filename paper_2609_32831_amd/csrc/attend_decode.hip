@@ -480,13 +480,18 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
   return true;
 }
 
-__global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodePlan pl,
-                                                             const uint16_t* __restrict__ q,
-                                                             int Hq, int Hkv, int M,
-                                                             float scale_log2,
-                                                             float* __restrict__ partial) {
+// BATCH: requests of different segment layouts in one launch; blockIdx.y is
+// (request, h_kv), each request's segments (a one-request layout) come from
+// the static descriptors reqs[request] completed with this call's row counts,
+// and its query rows follow those of the requests before it (as batch
+// elements do)
+template <bool BATCH>
+__device__ __attribute__((always_inline)) inline void decode_body(
+    const KSegs& segs, const BatchDesc* __restrict__ table, const KSeg* __restrict__ flat,
+    const DecodePlan& pl, int w, int bh,
+    const uint16_t* __restrict__ q, int Hq, int Hkv, int M, float scale_log2,
+    float* __restrict__ partial) {
   __shared__ __attribute__((aligned(16))) char lds[WAVES * 2 * TILEB + QOPB];
-  const int w = blockIdx.x, bh = blockIdx.y;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i16 = lane & 15, g4 = lane >> 4;
   const int G = Hq / Hkv, nq = G * M, b = bh / Hkv, hkv = bh % Hkv;
@@ -518,11 +523,21 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
   // a packed segment's codes into its tail), so no wave collects every
   // segment's remainder tile
   int rot = 0;
-  for (int si = 0; si < pl.n_seg; ++si) {
-    const KSeg& ks = segs.s[si];
-    const int r0 = share_row(ks.n_rows, w, W);
-    const int r1 = share_row(ks.n_rows, w + 1, W);
-    ok &= segment_share(st, ks, bh, r0, r1, wave, rot, lane, lq, scale_log2, lk, lv);
+  const int first = BATCH ? table[b].first : 0;
+  // a batched request splits its rows among its own W_r workgroups; its
+  // first workgroup marks the record slots W_r .. W-1 of its rows empty
+  const int Wr = BATCH ? table[b].W : W;
+  const int n_seg = BATCH ? table[b].n : pl.n_seg;
+  if (BATCH && w == 0) {
+    for (int e = threadIdx.x; e < nq * (W - Wr); e += blockDim.x)
+      c.partial[(qrow_of(c, e / (W - Wr)) * c.C + Wr + e % (W - Wr)) * (D + 2)] = -INFINITY;
+  }
+  const int sbh = BATCH ? hkv : bh;  // (b, h_kv) within the segments' own layout
+  for (int si = 0; si < n_seg; ++si) {
+    const KSeg& ks = BATCH ? flat[first + si] : segs.s[si];
+    const int r0 = share_row(ks.n_rows, w, Wr);
+    const int r1 = share_row(ks.n_rows, w + 1, Wr);
+    ok &= segment_share(st, ks, sbh, r0, r1, wave, rot, lane, lq, scale_log2, lk, lv);
     if (pl.per_seg) {
       flush(st, lds, c, si * W + w, ok, lane, wave);
       state_init(st);
@@ -530,6 +545,38 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
     }
   }
   if (!pl.per_seg) flush(st, lds, c, w, ok, lane, wave);
+}
+
+__global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodePlan pl,
+                                                             const uint16_t* __restrict__ q,
+                                                             int Hq, int Hkv, int M,
+                                                             float scale_log2,
+                                                             float* __restrict__ partial) {
+  decode_body<false>(segs, nullptr, nullptr, pl, blockIdx.x, blockIdx.y, q, Hq, Hkv, M, scale_log2,
+                     partial);
+}
+
+__global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* __restrict__ table,
+                                                              const KSeg* __restrict__ flat,
+                                                              DecodePlan pl,
+                                                              const uint16_t* __restrict__ q,
+                                                              int Hq, int Hkv, int M,
+                                                              float scale_log2,
+                                                              float* __restrict__ partial) {
+  // the request of this workgroup: the last table entry starting at or
+  // before it (starts ascend); then its KV head and share
+  const int g = blockIdx.x;
+  int lo = 0, hi = pl.n_seg - 1;  // n_seg holds the number of requests here
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (table[mid].start <= g) lo = mid;
+    else hi = mid - 1;
+  }
+  const int local = g - table[lo].start, Wr = table[lo].W;
+  KSegs none;
+  none.n = 0;
+  decode_body<true>(none, table, flat, pl, local % Wr, lo * Hkv + local / Wr, q, Hq, Hkv, M,
+                    scale_log2, partial);
 }
 
 int device_cus() {
@@ -597,6 +644,52 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   for (int i = 0; i <= kMaxSeg; ++i)
     cp.first[i] = p.per_seg ? min(i, segs.n) * p.W : (i == 0 ? 0 : p.W);
   return launch_attend_combine(sh, segs, cp, M, partial, o, lse, seg_lse, st);
+}
+
+// Requests of different layouts: sh.B = number of requests; the workspace
+// holds the request table and the flat segment descriptors (written by the
+// caller through launch_blob_upload), then the partial records; q / o / lse
+// are laid out as for sh.B batch elements.  Each request gets workgroups per
+// KV head in proportion to its rows (at least one), all of them in one
+// one-dimensional grid; the record stride per query row is the largest share
+// and the workspace is sized for the budget decode_batch_wgs (so it does not
+// depend on row counts).
+int decode_batch_wgs(const uc_shape& sh) { return max(1, (2 * device_cus()) / sh.Hkv); }
+
+size_t decode_batch_desc_bytes(int n_req, int n_segs_total) {
+  const size_t t = (((size_t)n_req * sizeof(BatchDesc)) + 255) & ~(size_t)255;
+  return t + ((((size_t)n_segs_total * sizeof(KSeg)) + 255) & ~(size_t)255);
+}
+
+size_t decode_batch_workspace(const uc_shape& sh, int M, int n_segs_total) {
+  const size_t rec = (size_t)sh.B * sh.Hq * M * decode_batch_wgs(sh) * (D + 2) * sizeof(float);
+  return decode_batch_desc_bytes(sh.B, n_segs_total) + ((rec + 255) & ~(size_t)255);
+}
+
+hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, int n_wgs,
+                               const void* q, int M, float sm_scale, float* o, float* lse,
+                               void* ws, hipStream_t st) {
+  DecodePlan p{};
+  p.W = W_max;
+  p.n_seg = sh.B;  // the batched kernel reads the number of requests from here
+  p.per_seg = 0;
+  const BatchDesc* table = (const BatchDesc*)ws;
+  const KSeg* flat =
+      (const KSeg*)((char*)ws + ((((size_t)sh.B * sizeof(BatchDesc)) + 255) & ~(size_t)255));
+  float* partial = (float*)((char*)ws + decode_batch_desc_bytes(sh.B, n_segs_total));
+  hipError_t e = kernel_timer_begin(st);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(decode_batch_kernel, dim3(n_wgs), dim3(256), 0, st, table, flat, p,
+                     (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
+  e = hipGetLastError();
+  if (e == hipSuccess) e = kernel_timer_end(st);
+  if (e != hipSuccess) return e;
+  KSegs none{};
+  none.n = 1;
+  ChunkPlan cp{};
+  cp.n_chunks = p.W;
+  for (int i = 0; i <= kMaxSeg; ++i) cp.first[i] = i == 0 ? 0 : p.W;
+  return launch_attend_combine(sh, none, cp, M, partial, o, lse, nullptr, st);
 }
 
 }  // namespace uc

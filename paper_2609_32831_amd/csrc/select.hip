@@ -14,6 +14,9 @@
 //     written in ascending position;
 //  3. the last n_recent positions follow unconditionally.
 // The gather kernel then copies the kept K/V rows with 16-byte lanes.
+#include <algorithm>
+#include <cstring>
+
 #include "uc_common.h"
 
 namespace uc {
@@ -162,6 +165,17 @@ __global__ void topk_fraction_kernel(const float* __restrict__ scores,
   }
 }
 
+// Host bytes carried in the kernel arguments and stored to device memory:
+// small descriptor tables reach the GPU in stream order with no staging copy
+// or host synchronisation.
+constexpr int kBlobWords = 760;
+struct Blob {
+  uint32_t w[kBlobWords];
+};
+__global__ void blob_store_kernel(Blob b, int n, uint32_t* __restrict__ dst) {
+  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = b.w[i];
+}
+
 // out[bh, j] = outer[bh, inner[bh, j]] (-1 for an inner value out of range).
 __global__ void compose_index_kernel(const int32_t* __restrict__ outer, int n_outer,
                                      const int32_t* __restrict__ inner, int k,
@@ -214,6 +228,19 @@ hipError_t launch_topk_mass(const float* scores, int BH, int N, int k, float* fr
     if (e != hipSuccess) return e;
   }
   hipLaunchKernelGGL(topk_fraction_kernel, dim3(BH), dim3(256), 0, st, scores, keep, N, k, frac);
+  return hipGetLastError();
+}
+
+hipError_t launch_blob_upload(const void* host, size_t bytes, void* dev, hipStream_t st) {
+  // bytes is a multiple of 4 (descriptor tables of ints and pointers)
+  const uint32_t* src = (const uint32_t*)host;
+  const size_t words = bytes / 4;
+  for (size_t i = 0; i < words; i += kBlobWords) {
+    const int n = (int)std::min<size_t>(kBlobWords, words - i);
+    Blob b;
+    memcpy(b.w, src + i, (size_t)n * 4);
+    hipLaunchKernelGGL(blob_store_kernel, dim3(1), dim3(256), 0, st, b, n, (uint32_t*)dev + i);
+  }
   return hipGetLastError();
 }
 

@@ -40,6 +40,14 @@ struct KSegs {
   int n;
 };
 
+// Batched requests: request r's segments are flat[first .. first + n - 1]
+// (one-request layouts); table and flat live in the workspace.
+struct BatchDesc {
+  int first, n;
+  int W;      // the request's workgroups per KV head (by its share of the rows)
+  int start;  // its first workgroup in the one-dimensional grid
+};
+
 // Split of every segment's rows into chunks (work items of the split-K
 // attention and of the scoring passes); chunks never straddle segments.
 struct ChunkPlan {
@@ -142,6 +150,7 @@ hipError_t launch_stream_append(const uc_shape& sh, const KSeg& seg, const void*
                                 const void* vnew, int n_new, hipStream_t st);
 hipError_t launch_topk_mass(const float* scores, int BH, int N, int k, float* frac,
                             int32_t* keep, hipStream_t st);
+hipError_t launch_blob_upload(const void* host, size_t bytes, void* dev, hipStream_t st);
 hipError_t launch_compose_index(const int32_t* outer, int n_outer, const int32_t* inner, int BH,
                                 int k, int32_t* out, hipStream_t st);
 hipError_t launch_attend_generic(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
