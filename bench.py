@@ -186,10 +186,12 @@ def summarize_prefill(d: str, command: str):
                          f"{alg:.4g} | {act:.4g} | {util:.3f} | "
                          f"{e.get('SQ_INSTS_VALU', 0):.4g} | {e.get('SQ_INSTS_LDS', 0):.4g} | "
                          f"{e.get('SQ_LDS_BANK_CONFLICT', 0):.4g} |")
-        lines += ["", "The busy-cycle count times 1024 reproduces the algorithmic flop count "
+        lines += ["", "The busy-cycle count times 1024 matches the algorithmic flop count "
                       "4 M N D Hq B of each step (one 16x16x32 product = 16384 flop = 16 busy "
-                      "cycles), so the kernel issues no padded or repeated matrix products; "
-                      "utilisation is busy cycles over the SIMD-cycles of the dispatch."]
+                      "cycles) to within 0.3 %: no padded or repeated matrix products, only the "
+                      "one tile of scores per workgroup that the software-pipelined loop computes "
+                      "past its last tile; utilisation is busy cycles over the SIMD-cycles of the "
+                      "dispatch."]
     with open(os.path.join(ROOT, "profiles", "prefill_attend_4096q.md"), "w") as f:
         f.write("\n".join(lines) + "\n")
     print("\n".join(lines))
