@@ -29,7 +29,9 @@ hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const Ch
                                  hipStream_t st);
 hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
                                  const void* q, int W, float sm_scale, const float* lse,
-                                 float* const* scores, double* mass_partial, hipStream_t st);
+                                 float* const* scores, double* mass_partial, double* colpart,
+                                 hipStream_t st);
+int score_mfma_qblocks(int nq);
 size_t decode_mfma_workspace(const uc_shape& sh, const KSegs& segs, int M);
 hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
@@ -420,15 +422,25 @@ static ChunkPlan score_mfma_plan(const KSegs& ks) {
   return make_plan(ks, score_mfma_chunk_rows(), 1 << 30);
 }
 
-// workspace parts: pass-1 records, row log-sum-exps, chunk masses (fp64);
+// workspace parts: pass-1 records, row log-sum-exps, chunk masses (fp64),
+// and (matrix-core path) the column pass's per-group column sums (fp64);
 // every part grows monotonically with the row counts
 static void score_ws_parts(const uc_shape& sh, const KSegs& ks, int W, bool fast, size_t& part1,
-                           size_t& lse_b, size_t& mass_b) {
+                           size_t& lse_b, size_t& mass_b, size_t& col_b) {
   lse_b = align256((size_t)sh.B * sh.Hq * W * sizeof(float));
+  col_b = 0;
   if (fast) {
-    const int C = score_mfma_plan(ks).n_chunks;
+    const ChunkPlan p = score_mfma_plan(ks);
+    const int C = p.n_chunks;
     part1 = align256((size_t)sh.B * sh.Hq * W * C * 2 * sizeof(float));
     mass_b = align256((size_t)sh.B * sh.Hkv * C * sizeof(double));
+    // groups x chunks x heads is at most min(query blocks, 512 / (chunks x
+    // heads) + 1) x chunks x heads: sized by that bound, which (unlike the
+    // group count itself) never shrinks as rows are added
+    const size_t base = (size_t)sh.B * sh.Hkv * C;
+    const size_t qb = (size_t)score_mfma_qblocks((sh.Hq / sh.Hkv) * W);
+    if (qb > 1)
+      col_b = align256(std::min(qb * base, 512 + base) * score_mfma_chunk_rows() * sizeof(double));
     return;
   }
   part1 = generic_ws(sh, ks, kLseRows, kLseMaxChunks, W, false);
@@ -440,10 +452,10 @@ size_t uc_score_workspace_size(const uc_shape* shape, const uc_segment* segs, in
   if (check_segments(shape, segs, n_segs, ks) || W < 1) return 0;
   // the larger of the two paths' needs, so the size does not depend on the
   // query dtype or the selected path
-  size_t a, b, c, a2, b2, c2;
-  score_ws_parts(*shape, ks, W, false, a, b, c);
-  score_ws_parts(*shape, ks, W, true, a2, b2, c2);
-  return std::max(a + b + c, a2 + b2 + c2);
+  size_t a, b, c, d, a2, b2, c2, d2;
+  score_ws_parts(*shape, ks, W, false, a, b, c, d);
+  score_ws_parts(*shape, ks, W, true, a2, b2, c2, d2);
+  return std::max(a + b + c + d, a2 + b2 + c2 + d2);
 }
 
 uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int n_segs,
@@ -459,13 +471,15 @@ uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int
   if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
   if ((int64_t)shape->B * shape->Hq * W > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
   const bool fast = score_fast(*shape, ks, q_dt);
-  size_t a, b, c;
-  score_ws_parts(*shape, ks, W, fast, a, b, c);
-  if (!ws || ws_bytes < a + b + c) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, a + b + c);
+  size_t a, b, c, d;
+  score_ws_parts(*shape, ks, W, fast, a, b, c, d);
+  if (!ws || ws_bytes < a + b + c + d)
+    return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, a + b + c + d);
   hipStream_t s = (hipStream_t)stream;
   float* partial = (float*)ws;
   float* lse = (float*)((char*)ws + a);
   double* mpart = (double*)((char*)ws + a + b);
+  double* colpart = d ? (double*)((char*)ws + a + b + c) : nullptr;
   float* sp[kMaxSeg] = {};
   if (scores_out)
     for (int i = 0; i < n_segs; ++i) sp[i] = scores_out[i];
@@ -475,7 +489,8 @@ uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int
     const ChunkPlan p = score_mfma_plan(ks);
     e = launch_score_lse_mfma(*shape, ks, p, q_obs, W, sm_scale, partial, s);
     if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, W, partial, nullptr, lse, nullptr, s);
-    if (e == hipSuccess) e = launch_score_col_mfma(*shape, ks, p, q_obs, W, sm_scale, lse, sp, mpart, s);
+    if (e == hipSuccess)
+      e = launch_score_col_mfma(*shape, ks, p, q_obs, W, sm_scale, lse, sp, mpart, colpart, s);
     p2 = p;
   } else {
     const ChunkPlan p1 = score_lse_plan(ks);

@@ -23,6 +23,8 @@
 // Column sums: a lane sums its key's probabilities over the query tiles in
 // fp32, the 16 query columns of a tile are added by a butterfly, and the
 // query blocks are accumulated in fp64 in LDS; chunk masses are fp64.
+#include <algorithm>
+
 #include "mfma_util.h"
 #include "uc_common.h"
 
@@ -204,18 +206,22 @@ struct ScoreOut {
   float* p[kMaxSeg];
 };
 
-// grid (chunks, b*h_kv); every query block of the head
+// grid (chunks, query-block groups, b*h_kv): the query blocks
+// [s*qbs, (s+1)*qbs) of the head.  With one group the scores and chunk mass
+// are written directly; with several, each group's column sums (double) go
+// to colpart and score_col_reduce_kernel adds them in group order.
 __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan plan,
                                                            const uint16_t* __restrict__ q, int Hq,
                                                            int Hkv, int W, float scale_log2,
                                                            const float* __restrict__ lse,
                                                            ScoreOut out,
-                                                           double* __restrict__ mass_partial) {
+                                                           double* __restrict__ mass_partial,
+                                                           int qbs, double* __restrict__ colpart) {
   __shared__ __attribute__((aligned(16))) char qs[QB * QROW];
   __shared__ float ls[QB];
   __shared__ double colsum[CHUNK];
   __shared__ double red[WAVES];
-  const int c = blockIdx.x, bh = blockIdx.y;
+  const int c = blockIdx.x, sg = blockIdx.y, bh = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i16 = lane & 15, g4 = lane >> 4;
   const int G = Hq / Hkv, nq = G * W, b = bh / Hkv, hkv = bh % Hkv;
@@ -228,7 +234,8 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
 
   const int64_t base = (int64_t)bh * ks.row_stride * D;
   const __amdgpu_buffer_rsrc_t rk = rsrc((const uint16_t*)ks.k + base, (uint32_t)r1 * ROWB);
-  for (int q0 = 0; q0 < nq; q0 += QB) {
+  const int q_end = min(nq, (sg + 1) * qbs * QB);
+  for (int q0 = sg * qbs * QB; q0 < q_end; q0 += QB) {
     const int nqt = min(QT, (nq - q0 + 15) / 16);
     __syncthreads();  // the previous block's readers are done
     stage_q(qs, qh, q0, nq);
@@ -283,6 +290,11 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
     }
   }
   __syncthreads();
+  if (colpart) {  // one group of several: its column sums, reduced later
+    double* cp = colpart + (((int64_t)sg * gridDim.z + bh) * plan.n_chunks + c) * CHUNK;
+    for (int e = threadIdx.x; e < CHUNK; e += blockDim.x) cp[e] = colsum[e];
+    return;
+  }
   // scores (rows past r1 were masked by never being written) and the
   // chunk's mass (fixed-order reduction: deterministic)
   float* sp = out.p[si];
@@ -292,6 +304,36 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
       if (sp) sp[(int64_t)bh * ks.n_rows + r0 + e] = (float)colsum[e];
       part += colsum[e];
     }
+  }
+  part = wave_sum_d(part);
+  if (lane == 0) red[wave] = part;
+  __syncthreads();
+  if (threadIdx.x == 0 && mass_partial)
+    mass_partial[(int64_t)bh * plan.n_chunks + c] = red[0] + red[1] + red[2] + red[3];
+}
+
+// grid (chunks, b*h_kv): the groups' column sums added in group order, then
+// the scores and the chunk's mass as the single-group kernel writes them
+__global__ __launch_bounds__(256) void score_col_reduce_kernel(KSegs segs, ChunkPlan plan,
+                                                               int n_groups,
+                                                               const double* __restrict__ colpart,
+                                                               ScoreOut out,
+                                                               double* __restrict__ mass_partial) {
+  __shared__ double red[4];
+  const int c = blockIdx.x, bh = blockIdx.y, BH = gridDim.y;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int r0, r1;
+  const int si = chunk_rows(plan, segs, c, r0, r1);
+  const KSeg& ks = segs.s[si];
+  float* sp = out.p[si];
+  double part = 0.0;
+  for (int e = threadIdx.x; e < CHUNK; e += blockDim.x) {
+    if (r0 + e >= r1) continue;
+    double v = 0.0;
+    for (int g = 0; g < n_groups; ++g)
+      v += colpart[(((int64_t)g * BH + bh) * plan.n_chunks + c) * CHUNK + e];
+    if (sp) sp[(int64_t)bh * ks.n_rows + r0 + e] = (float)v;
+    part += v;
   }
   part = wave_sum_d(part);
   if (lane == 0) red[wave] = part;
@@ -313,6 +355,15 @@ int score_mfma_chunk_rows() { return CHUNK; }
 
 int score_mfma_qblocks(int nq) { return (nq + QB - 1) / QB; }
 
+// query-block groups of the column pass: enough workgroups to fill the chip
+// (about 512) when chunks x heads alone do not
+static int score_col_groups(const uc_shape& sh, const ChunkPlan& plan, int W) {
+  const int qblocks = score_mfma_qblocks((sh.Hq / sh.Hkv) * W);
+  const int base = plan.n_chunks * sh.B * sh.Hkv;
+  const int want = (512 + base - 1) / base;
+  return std::max(1, std::min(qblocks, want));
+}
+
 hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
                                  const void* q, int W, float sm_scale, float* partial,
                                  hipStream_t st) {
@@ -325,12 +376,21 @@ hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const Ch
 
 hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
                                  const void* q, int W, float sm_scale, const float* lse,
-                                 float* const* scores, double* mass_partial, hipStream_t st) {
+                                 float* const* scores, double* mass_partial, double* colpart,
+                                 hipStream_t st) {
   ScoreOut so{};
   for (int i = 0; i < segs.n; ++i) so.p[i] = scores ? scores[i] : nullptr;
-  dim3 grid(plan.n_chunks, sh.B * sh.Hkv);
+  const int groups = score_col_groups(sh, plan, W);
+  const int qblocks = score_mfma_qblocks((sh.Hq / sh.Hkv) * W);
+  const int qbs = (qblocks + groups - 1) / groups;
+  const int n_groups = (qblocks + qbs - 1) / qbs;
+  dim3 grid(plan.n_chunks, n_groups, sh.B * sh.Hkv);
   hipLaunchKernelGGL(score_col_kernel, grid, dim3(256), 0, st, segs, plan, (const uint16_t*)q,
-                     sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so, mass_partial);
+                     sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so, mass_partial, qbs,
+                     n_groups > 1 ? colpart : nullptr);
+  if (n_groups > 1)
+    hipLaunchKernelGGL(score_col_reduce_kernel, dim3(plan.n_chunks, sh.B * sh.Hkv), dim3(256), 0,
+                       st, segs, plan, n_groups, (const double*)colpart, so, mass_partial);
   return hipGetLastError();
 }
 
