@@ -40,6 +40,10 @@ def parse():
     ap.add_argument("--decode-steps", type=int, default=None,
                     help="decode steps per job (default: the workload's 512)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--event-every", type=int, default=8,
+                    help="decode steps between timed ones: every event record on the stream "
+                         "costs the GPU about 3 us, so the kernel and call events bracket "
+                         "steps 0, n, 2n, ... of each job and the rest run unobserved")
     ap.add_argument("--cpu-sample-heads", type=int, default=16)
     ap.add_argument("--cpu-sample-steps", type=int, default=8)
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -650,9 +654,14 @@ def main():
 
     stream = torch.cuda.current_stream()
     o = torch.empty(T, w.B, w.Hq, 1, w.D, device="cuda")
-    # per step: events 4t, 4t+1 around the uc_attend_mixed call, and 4t+2,
-    # 4t+3, which the library records around its attention kernel alone (the
-    # merge of partial results falls outside them)
+    # sampled steps: 4t+2, 4t+3, which the library records around its
+    # attention kernel alone (the merge of partial results falls outside
+    # them), on steps t % every == 0; 4t, 4t+1 around the whole attention call
+    # on steps t % every == every // 2 (so that no call bracket holds the
+    # kernel pair's records, unless every == 1)
+    every = max(1, args.event_every)
+    sampled = [t for t in range(T) if t % every == 0]
+    sampled_call = [t for t in range(T) if t % every == every // 2]
     ev = HipEvents(4 * T)
     ev_c = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
 
@@ -663,18 +672,23 @@ def main():
         if record:
             ev_c[1].record(stream)
         for t in range(T):
-            if run.tail is not None:
-                uc.uc_append_rows(run.shape, inp["k_dec"][t], inp["v_dec"][t], 1, run.tail, t)
-                run.tail.n_rows = t + 1
-            else:  # the row joins the quantised text segment's residual tail
+            if run.tail is None:  # the row joins the quantised text segment's residual tail
                 uc.uc_stream_append(run.shape, run.mixed[run.stream], inp["k_dec"][t],
                                     inp["v_dec"][t], 1)
-            if record:
+            kern_t = record and t % every == 0
+            call_t = record and t % every == every // 2
+            if call_t:
                 ev.record(4 * t, stream)
+            if kern_t:
                 uc.uc_set_kernel_events(ev.handle(4 * t + 2), ev.handle(4 * t + 3))
-            uc.uc_attend_mixed(run.shape, run.mixed, inp["q_dec"][t], 1, run.sm, o[t],
-                               ws=run.ws_attend)
-            if record:
+            if run.tail is not None:  # row t joins the protected tail inside the attention launch
+                uc.uc_attend_append(run.shape, run.mixed, len(run.mixed) - 1, inp["k_dec"][t],
+                                    inp["v_dec"][t], 1, inp["q_dec"][t], 1, run.sm, o[t],
+                                    ws=run.ws_attend)
+            else:
+                uc.uc_attend_mixed(run.shape, run.mixed, inp["q_dec"][t], 1, run.sm, o[t],
+                                   ws=run.ws_attend)
+            if call_t:
                 ev.record(4 * t + 1, stream)
 
     for _ in range(args.warmup):
@@ -690,8 +704,8 @@ def main():
     for k in range(args.steps):
         job(True)
         torch.cuda.synchronize()
-        attend_ms += sum(ev.elapsed_ms(4 * t, 4 * t + 1) for t in range(T))
-        kernel_ms += sum(ev.elapsed_ms(4 * t + 2, 4 * t + 3) for t in range(T))
+        attend_ms += sum(ev.elapsed_ms(4 * t, 4 * t + 1) for t in sampled_call)
+        kernel_ms += sum(ev.elapsed_ms(4 * t + 2, 4 * t + 3) for t in sampled)
         compress_ms += ev_c[0].elapsed_time(ev_c[1])
         print(f"# job {k + 1}/{args.steps} done", file=sys.stderr, flush=True)
     end.record(stream)
@@ -700,11 +714,15 @@ def main():
     ms_per_step = total_ms / args.steps
     tokens = w.B * T
     value = tokens / (ms_per_step / 1e3)
-    att_us = attend_ms / (args.steps * T) * 1e3
-    kern_us = kernel_ms / (args.steps * T) * 1e3
-    # algorithmic bytes per attend call, averaged over the tail lengths 1..T
-    avg_bytes = sum(run.attended_bytes(t + 1) for t in range(T)) / T
+    att_us = attend_ms / (args.steps * len(sampled_call)) * 1e3
+    kern_us = kernel_ms / (args.steps * len(sampled)) * 1e3
+    # algorithmic bytes per attend call, averaged over the sampled steps'
+    # tail lengths
+    avg_bytes = sum(run.attended_bytes(t + 1) for t in sampled) / len(sampled)
+    call_bytes = sum(run.attended_bytes(t + 1) for t in sampled_call) / len(sampled_call)
     achieved = avg_bytes / (kern_us * 1e-6) / 1e9
+    # the decode steps alone: the timed jobs less their compression
+    decode_ms = ms_per_step - compress_ms / args.steps
     traffic = None
     tp = os.path.join(ROOT, "profiles", "decode_attend_64k_traffic.json")
     if os.path.exists(tp) and not args.streaming:
@@ -743,8 +761,9 @@ def main():
                      "avg_launch_us": round(kern_us, 2),
                      "algorithmic_bytes_per_launch": int(avg_bytes)},
         "attend_call_us": round(att_us, 2),
-        "attend_call_frac": round(avg_bytes / (att_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
-        "decode_only_tokens_per_s": round(w.B / (att_us * 1e-6), 1),
+        "attend_call_frac": round(call_bytes / (att_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
+        "decode_step_us": round(decode_ms / T * 1e3, 2),
+        "decode_only_tokens_per_s": round(tokens / (decode_ms / 1e3), 1),
         "compress_ms": round(compress_ms / args.steps, 3),
     }
     if args.calibrate_copy:

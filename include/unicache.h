@@ -20,6 +20,8 @@
  *                        (App. E "Attention over heterogeneous cache segments")
  *   uc_append_rows       decode-time write of new K/V rows into a protected
  *                        dense segment (Sec. 3.1, protected objects)
+ *   uc_attend_append     one decode step: the append and the attention in
+ *                        one launch (Sec. 3.1 and App. E)
  *   host helpers         byte accounting and budget -> policy configuration
  *                        (Sec. 3.3 Eq. 2 and Eq. 3, Sec. 3.4)
  *
@@ -266,6 +268,30 @@ uc_status uc_append_rows(const uc_shape* shape, const void* k_new,
                          const void* v_new, int n_new, const uc_segment* seg,
                          int pos, void* stream);
 
+/* One decode step with the append fused in (Sec. 3.1 protected segment and
+ * Sec. 3.4 attention over the reassembled sequence).  The result is that of
+ *   uc_append_rows(shape, k_new, v_new, n_new, &segs[tail], segs[tail].n_rows)
+ * followed by uc_attend_mixed over segs with segs[tail].n_rows raised by
+ * n_new, up to the order of floating-point summation.
+ *   segs[tail]   a dense segment with row_stride >= n_rows + n_new; its n_rows
+ *                is the row count BEFORE this call, and the caller raises it
+ *                by n_new afterwards (segs is read, never written).
+ *   k_new, v_new [B, Hkv, n_new, D] device, dtype of segs[tail], 16-byte
+ *                aligned; n_new = 0 is a plain uc_attend_mixed.
+ *   q .. stream  as for uc_attend_mixed; ws needs uc_attend_workspace_size of
+ *                the segments as they stand after the append.
+ * With the decode matrix-core kernel (bf16, D = 128, (Hq/Hkv)*M <= 16, no
+ * seg_lse, fewer than UC_MAX_SEGMENTS segments) one launch attends the new
+ * rows straight from k_new / v_new and also stores them into segs[tail];
+ * otherwise the library runs the two calls above (every check, the workspace
+ * size included, comes before either launch, so an error stores nothing). */
+uc_status uc_attend_append(const uc_shape* shape, const uc_segment* segs,
+                           int n_segs, int tail, const void* k_new,
+                           const void* v_new, int n_new, const void* q,
+                           uc_dtype q_dt, int M, float sm_scale, float* o,
+                           float* lse, float* seg_lse, void* ws,
+                           size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Host helpers: storage accounting and budget -> policy configuration
  * (Sec. 3.3 "S_a, the original storage cost"; Sec. 3.4: an eviction policy is
@@ -404,13 +430,14 @@ int uc_quant_config(double budget_bytes, int64_t N, int D, uc_dtype dt, int n_he
 
 /* ------------------------------------------------------------------------ */
 /* Timing hook (instrumentation, for measuring the attention kernel on its
- * own).  The next uc_attend_mixed call made on the calling thread records
+ * own).  The next attention call (uc_attend_mixed, uc_attend_append or
+ * uc_attend_batch) made on the calling thread records
  * `start` on its stream immediately before the kernel that reads the
  * segments and `stop` immediately after it, so the pair brackets that kernel
  * alone: the merge of partial results and the prefill path's dequantisation
  * pass fall outside it.  Both are hipEvent_t handles passed as void*,
  * created and owned by the caller; either may be NULL.  The setting is per
- * thread and applies to exactly one uc_attend_mixed call, which clears it
+ * thread and applies to exactly one such call, which clears it
  * (also when that call fails validation, in which case nothing is recorded).
  * An event-record failure makes that call return UC_E_DEVICE. */
 uc_status uc_set_kernel_events(void* start, void* stop);

@@ -72,6 +72,8 @@ def _load():
         "uc_attend_workspace_size": (sz, [shp, segp, i32, i32, i32]),
         "uc_segment_mass": (i32, [shp, i32, i32, vp, vp, vp, vp]),
         "uc_append_rows": (i32, [shp, vp, vp, i32, segp, i32, vp]),
+        "uc_attend_append": (i32, [shp, segp, i32, i32, vp, vp, i32, vp, i32, i32,
+                                   ctypes.c_float, vp, vp, vp, vp, sz, vp]),
         "uc_dense_bytes": (i64, [i64, i32, i32]),
         "uc_evicted_bytes": (i64, [i64, i32, i32]),
         "uc_packed_bytes": (i64, [i64, i32, i32, i32, i32]),
@@ -357,6 +359,28 @@ def uc_append_rows(shape: uc_shape, k_new: torch.Tensor, v_new: torch.Tensor, n_
                               ctypes.byref(seg.desc), pos, _stream(stream)), "uc_append_rows")
 
 
+def uc_attend_append(shape: uc_shape, segs: Sequence[Segment], tail: int, k_new: torch.Tensor,
+                     v_new: torch.Tensor, n_new: int, q: torch.Tensor, M: int, sm_scale: float,
+                     o: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                     seg_lse: Optional[torch.Tensor] = None, ws: Optional[torch.Tensor] = None,
+                     stream=None):
+    """One decode step: k_new / v_new join segs[tail] and the queries attend
+    over every segment; segs[tail].n_rows is raised by n_new on success."""
+    arr = _seg_array(segs)
+    q_dt = TORCH_DT[q.dtype]
+    if ws is None:  # sized for the segments as they stand after the append
+        arr[tail].n_rows += n_new
+        ws = _ws(lib.uc_attend_workspace_size(ctypes.byref(shape), arr, len(segs), q_dt, M),
+                 q.device)
+        arr[tail].n_rows -= n_new
+    _check(lib.uc_attend_append(ctypes.byref(shape), arr, len(segs), tail, _ptr(k_new),
+                                _ptr(v_new), n_new, q.data_ptr(), q_dt, M,
+                                ctypes.c_float(sm_scale), o.data_ptr(), _ptr(lse), _ptr(seg_lse),
+                                ws.data_ptr(), ws.numel(), _stream(stream)), "uc_attend_append")
+    segs[tail].n_rows += n_new
+    return o
+
+
 def uc_segment_mass(shape: uc_shape, M: int, n_segs: int, lse: torch.Tensor,
                     seg_lse: torch.Tensor, mass_out: torch.Tensor, stream=None):
     _check(lib.uc_segment_mass(ctypes.byref(shape), M, n_segs, lse.data_ptr(),
@@ -414,8 +438,8 @@ def uc_last_error() -> str:
 
 
 def uc_set_kernel_events(start, stop) -> None:
-    """Bracket the attention kernel of the next uc_attend_mixed call on this
-    thread with two events (torch.cuda.Event objects that have been recorded
+    """Bracket the attention kernel of the next attention call (uc_attend_mixed,
+    uc_attend_append, uc_attend_batch) on this thread with two events (torch.cuda.Event objects that have been recorded
     once, so that their handles exist; or raw hipEvent_t values; or None)."""
     def handle(ev):
         if ev is None:

@@ -35,7 +35,7 @@ int score_mfma_qblocks(int nq);
 size_t decode_mfma_workspace(const uc_shape& sh, const KSegs& segs, int M);
 hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
-                              hipStream_t st);
+                              hipStream_t st, const AppendOp* ap = nullptr);
 int decode_batch_wgs(const uc_shape& sh);
 size_t decode_batch_desc_bytes(int n_req, int n_segs_total);
 size_t decode_batch_workspace(const uc_shape& sh, int M, int n_segs_total);
@@ -50,17 +50,23 @@ thread_local char g_err[512] = "";
 std::atomic<int> g_path{UC_PATH_AUTO};
 
 // timing events: pending (set by uc_set_kernel_events) and active (taken by
-// one uc_attend_mixed call for its duration)
+// one attention call for its duration; an entry point that calls another
+// keeps them for the inner call's attention kernel)
 thread_local hipEvent_t g_ev_pending[2] = {nullptr, nullptr};
 thread_local hipEvent_t g_ev_active[2] = {nullptr, nullptr};
+thread_local int g_ev_depth = 0;
 
 struct TimerScope {
   TimerScope() {
-    g_ev_active[0] = g_ev_pending[0];
-    g_ev_active[1] = g_ev_pending[1];
-    g_ev_pending[0] = g_ev_pending[1] = nullptr;
+    if (g_ev_depth++ == 0) {
+      g_ev_active[0] = g_ev_pending[0];
+      g_ev_active[1] = g_ev_pending[1];
+      g_ev_pending[0] = g_ev_pending[1] = nullptr;
+    }
   }
-  ~TimerScope() { g_ev_active[0] = g_ev_active[1] = nullptr; }
+  ~TimerScope() {
+    if (--g_ev_depth == 0) g_ev_active[0] = g_ev_active[1] = nullptr;
+  }
 };
 
 uc_status fail(uc_status s, const char* fmt, ...) {
@@ -303,6 +309,73 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
   if (e == hipSuccess) e = kernel_timer_end(s);
   if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, M, partial, o, lse, seg_lse, s);
   return launched(e);
+}
+
+// ---------------------------------------------------------------- decode step, append fused
+uc_status uc_attend_append(const uc_shape* shape, const uc_segment* segs, int n_segs, int tail,
+                           const void* k_new, const void* v_new, int n_new, const void* q,
+                           uc_dtype q_dt, int M, float sm_scale, float* o, float* lse,
+                           float* seg_lse, void* ws, size_t ws_bytes, void* stream) {
+  TimerScope timer;
+  if (!segs) return fail(UC_E_INVALID, "segs is NULL");
+  if (n_segs < 1 || n_segs > kMaxSeg) return fail(UC_E_INVALID, "n_segs %d not in [1,%d]", n_segs, kMaxSeg);
+  if (tail < 0 || tail >= n_segs) return fail(UC_E_INVALID, "tail %d not in [0,%d)", tail, n_segs);
+  if (segs[tail].kind != UC_SEG_DENSE) return fail(UC_E_INVALID, "segment %d (tail) is not dense", tail);
+  if (n_new < 0) return fail(UC_E_INVALID, "n_new must be >= 0 (got %d)", n_new);
+  // the segments as they stand after the append: validates capacity and rows
+  uc_segment after[kMaxSeg];
+  memcpy(after, segs, (size_t)n_segs * sizeof(uc_segment));
+  const int pos = segs[tail].n_rows;
+  if (pos < 0) return fail(UC_E_INVALID, "segment %d: n_rows < 0", tail);
+  if (n_new > 0) {
+    if (!segs[tail].row_stride || (int64_t)pos + n_new > segs[tail].row_stride)
+      return fail(UC_E_INVALID, "tail rows %lld after the append exceed row_stride %d",
+                  (long long)pos + n_new, segs[tail].row_stride);
+    if (!k_new || !v_new) return fail(UC_E_INVALID, "k_new or v_new is NULL");
+    if (!aligned16(k_new) || !aligned16(v_new))
+      return fail(UC_E_INVALID, "k_new/v_new not 16-byte aligned");
+  }
+  after[tail].n_rows = pos + n_new;
+  KSegs ks;
+  uc_status st = check_segments(shape, after, n_segs, ks);
+  if (st) return st;
+  if (!q || !o) return fail(UC_E_INVALID, "q or o is NULL");
+  if (!dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad q dtype %d", q_dt);
+  if (M < 1) return fail(UC_E_INVALID, "M must be >= 1 (got %d)", M);
+  if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
+  if ((int64_t)shape->B * shape->Hq * M > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
+  hipStream_t s = (hipStream_t)stream;
+  const bool fused = n_new > 0 && !seg_lse && n_segs < kMaxSeg && g_path.load() == UC_PATH_AUTO &&
+                     decode_mfma_eligible(*shape, ks, q_dt, M);
+  if (!fused) {
+    // the two calls this one stands for, checked before either is enqueued
+    const size_t need = uc_attend_workspace_size(shape, after, n_segs, q_dt, M);
+    if (ws_bytes < need || (need && !ws)) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+    if (n_new > 0) {
+      KSeg t = ks.s[tail];
+      hipError_t e = launch_append(*shape, k_new, v_new, n_new, t, pos, s);
+      if (e != hipSuccess) return launched(e);
+    }
+    return uc_attend_mixed(shape, after, n_segs, q, q_dt, M, sm_scale, o, lse, seg_lse, ws,
+                           ws_bytes, stream);
+  }
+  // the tail as it stood, plus the new rows as a dense segment of their own
+  // read from k_new / v_new (softmax does not depend on the rows' order);
+  // without per-segment outputs every record belongs to one softmax
+  const size_t need = decode_mfma_workspace(*shape, ks, M);
+  if (ws_bytes < need || (need && !ws)) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+  ks.s[tail].n_rows = pos;
+  KSeg& nk = ks.s[ks.n++];
+  memset(&nk, 0, sizeof nk);
+  nk.kind = UC_SEG_DENSE;
+  nk.dtype = ks.s[tail].dtype;
+  nk.n_rows = n_new;
+  nk.row_stride = n_new;
+  nk.k = k_new;
+  nk.v = v_new;
+  AppendOp ap{(const char*)k_new, (const char*)v_new, (char*)ks.s[tail].k, (char*)ks.s[tail].v,
+              n_new, ks.s[tail].row_stride, pos, shape->D * dtype_bytes(nk.dtype)};
+  return launched(launch_decode_mfma(*shape, ks, q, M, sm_scale, o, lse, nullptr, ws, s, &ap));
 }
 
 // ---------------------------------------------------------------- batched requests

@@ -488,7 +488,7 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
 template <bool BATCH>
 __device__ __attribute__((always_inline)) inline void decode_body(
     const KSegs& segs, const BatchDesc* __restrict__ table, const KSeg* __restrict__ flat,
-    const DecodePlan& pl, int w, int bh,
+    const DecodePlan& pl, const AppendOp& ap, int w, int bh,
     const uint16_t* __restrict__ q, int Hq, int Hkv, int M, float scale_log2,
     float* __restrict__ partial) {
   __shared__ __attribute__((aligned(16))) char lds[WAVES * 2 * TILEB + QOPB];
@@ -497,14 +497,32 @@ __device__ __attribute__((always_inline)) inline void decode_body(
   const int G = Hq / Hkv, nq = G * M, b = bh / Hkv, hkv = bh % Hkv;
   const int W = pl.W;
 
+
   // query block: slot i16 = g * M + m  (query head hkv*G + g, row m)
+  // (the group's query rows are consecutive; slots past nq read as zeros
+  // through the range check, so all four loads issue without branches)
   u4 qop[4];
   {
-    const bool live = i16 < nq;
-    const int64_t qrow = live ? (((int64_t)b * Hq + hkv * G + i16 / M) * M + i16 % M) : 0;
+    const __amdgpu_buffer_rsrc_t rq = rsrc(q + ((int64_t)b * Hq + hkv * G) * M * D,
+                                           (uint32_t)nq * D * 2);
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
-      qop[t] = live ? *reinterpret_cast<const u4*>(q + qrow * D + t * 32 + g4 * 8) : u4{0, 0, 0, 0};
+    for (int t = 0; t < 4; ++t) qop[t] = bload(rq, (i16 * D + t * 32 + g4 * 8) * 2, 0);
+  }
+  // fused append: this call attends the new rows from k_new / v_new (a
+  // segment of their own) and stores them into the protected segment for the
+  // calls after it; no workgroup of this launch reads the rows written here
+  // (every range ends at the segment's row count before the append).  Issued
+  // after the query loads so that both wait out one memory latency together.
+  if (!BATCH && ap.n_new > 0 && w == 0) {
+    const int per = ap.n_new * ap.row_bytes / 16;
+    for (int e = threadIdx.x; e < per; e += blockDim.x) {
+      const int64_t src = (int64_t)bh * ap.n_new * ap.row_bytes + (int64_t)e * 16;
+      const int64_t dst = ((int64_t)bh * ap.row_stride + ap.pos) * ap.row_bytes + (int64_t)e * 16;
+      const u4 kr = *reinterpret_cast<const u4*>(ap.kn + src);  // both loads before
+      const u4 vr = *reinterpret_cast<const u4*>(ap.vn + src);  // either store
+      *reinterpret_cast<u4*>(ap.kd + dst) = kr;
+      *reinterpret_cast<u4*>(ap.vd + dst) = vr;
+    }
   }
   char* lk = lds + wave * 2 * TILEB;
   char* lv = lk + TILEB;
@@ -535,8 +553,12 @@ __device__ __attribute__((always_inline)) inline void decode_body(
   const int sbh = BATCH ? hkv : bh;  // (b, h_kv) within the segments' own layout
   for (int si = 0; si < n_seg; ++si) {
     const KSeg& ks = BATCH ? flat[first + si] : segs.s[si];
-    const int r0 = share_row(ks.n_rows, w, Wr);
-    const int r1 = share_row(ks.n_rows, w + 1, Wr);
+    // the appended rows (the last segment) go to the last workgroup, whose
+    // shares of the other segments are the remainders; workgroup 0 already
+    // holds the start of the protected segment
+    const int ws = (!BATCH && ap.n_new > 0 && si == n_seg - 1) ? Wr - 1 - w : w;
+    const int r0 = share_row(ks.n_rows, ws, Wr);
+    const int r1 = share_row(ks.n_rows, ws + 1, Wr);
     ok &= segment_share(st, ks, sbh, r0, r1, wave, rot, lane, lq, scale_log2, lk, lv);
     if (pl.per_seg) {
       flush(st, lds, c, si * W + w, ok, lane, wave);
@@ -548,12 +570,13 @@ __device__ __attribute__((always_inline)) inline void decode_body(
 }
 
 __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodePlan pl,
+                                                             AppendOp ap,
                                                              const uint16_t* __restrict__ q,
                                                              int Hq, int Hkv, int M,
                                                              float scale_log2,
                                                              float* __restrict__ partial) {
-  decode_body<false>(segs, nullptr, nullptr, pl, blockIdx.x, blockIdx.y, q, Hq, Hkv, M, scale_log2,
-                     partial);
+  decode_body<false>(segs, nullptr, nullptr, pl, ap, blockIdx.x, blockIdx.y, q, Hq, Hkv, M,
+                     scale_log2, partial);
 }
 
 __global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* __restrict__ table,
@@ -575,8 +598,9 @@ __global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* _
   const int local = g - table[lo].start, Wr = table[lo].W;
   KSegs none;
   none.n = 0;
-  decode_body<true>(none, table, flat, pl, local % Wr, lo * Hkv + local / Wr, q, Hq, Hkv, M,
-                    scale_log2, partial);
+  const AppendOp no_append{};
+  decode_body<true>(none, table, flat, pl, no_append, local % Wr, lo * Hkv + local / Wr, q, Hq,
+                    Hkv, M, scale_log2, partial);
 }
 
 int device_cus() {
@@ -624,8 +648,9 @@ size_t decode_mfma_workspace(const uc_shape& sh, const KSegs& segs, int M) {
 
 hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
-                              hipStream_t st) {
+                              hipStream_t st, const AppendOp* ap) {
   DecodePlan p{};
+  const AppendOp none{};
   p.W = decode_w(sh);
   p.n_seg = segs.n;
   p.per_seg = seg_lse != nullptr;
@@ -633,7 +658,8 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   hipError_t e = kernel_timer_begin(st);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(decode_mfma_kernel, dim3(p.W, sh.B * sh.Hkv), dim3(256), 0, st, segs, p,
-                     (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
+                     ap ? *ap : none, (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e,
+                     partial);
   e = hipGetLastError();
   if (e == hipSuccess) e = kernel_timer_end(st);
   if (e != hipSuccess) return e;

@@ -40,6 +40,17 @@ struct KSegs {
   int n;
 };
 
+// Decode append fused into the decode kernel: rows pos .. pos+n_new-1 of
+// every (b, h_kv) of a dense segment receive k_new / v_new [BH, n_new, row]
+// (the first workgroup of each (b, h_kv) copies them); n_new = 0: none.
+struct AppendOp {
+  const char* kn;
+  const char* vn;
+  char* kd;
+  char* vd;
+  int n_new, row_stride, pos, row_bytes;
+};
+
 // Batched requests: request r's segments are flat[first .. first + n - 1]
 // (one-request layouts); table and flat live in the workspace.
 struct BatchDesc {

@@ -17,7 +17,7 @@ import numpy as np
 import torch
 
 from . import (NAME_DT, TORCH_DT, dense_segment, make_shape, packed_layout, packed_segment,
-               uc_append_rows, uc_assign_bits, uc_attend_mixed, uc_attend_workspace_size,
+               uc_assign_bits, uc_attend_append, uc_attend_mixed, uc_attend_workspace_size,
                uc_compose_index, uc_dense_bytes, uc_dequantize_segment, uc_evict_rows_for_budget,
                uc_packed_bytes, uc_quant_config, uc_quantize_segment, uc_retention_next,
                uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep,
@@ -173,9 +173,12 @@ class Run:
     # -- hot loop --------------------------------------------------------------
     def decode_step(self, t: int, o: torch.Tensor, lse=None, seg_lse=None):
         inp = self.inp
-        if self.tail is not None:
-            uc_append_rows(self.shape, inp["k_dec"][t], inp["v_dec"][t], 1, self.tail, t)
-            self.tail.n_rows = t + 1
+        if self.tail is not None:  # row t joins the protected tail in the same launch
+            assert self.tail.n_rows == t
+            uc_attend_append(self.shape, self.mixed, len(self.mixed) - 1, inp["k_dec"][t],
+                             inp["v_dec"][t], 1, inp["q_dec"][t], 1, self.sm, o, lse, seg_lse,
+                             ws=self.ws_attend)
+            return
         if self.stream is not None:  # the row joins the quantised segment's tail
             uc_stream_append(self.shape, self.mixed[self.stream], inp["k_dec"][t], inp["v_dec"][t], 1)
         uc_attend_mixed(self.shape, self.mixed, inp["q_dec"][t], 1, self.sm, o, lse, seg_lse,
@@ -199,9 +202,10 @@ class Run:
         return tot
 
     def attended_bytes(self, tail_rows: int = 0) -> int:
-        """Algorithmic HBM bytes one attention call reads: every stored row it
-        attends (dense rows, codes, float scales/minima, tails; not the index
-        arrays) for all (b, h_kv), plus queries and fp32 outputs."""
+        """Algorithmic HBM bytes of one decode step's attention launch: every
+        stored row it attends (dense rows, codes, float scales/minima, tails;
+        not the index arrays) for all (b, h_kv), queries and fp32 outputs, and
+        with a protected tail the new row it also stores there."""
         w = self.w
         BH = w.B * w.Hkv
         per = 0
@@ -215,7 +219,7 @@ class Run:
                 n = s.n + (tail_rows if i == self.stream else 0)  # streamed rows join it
                 per += uc_packed_bytes(n, w.D, s.group, p.bits or 4, NAME_DT[s.dtype])
         if self.stream is None:
-            per += tail_rows * 2 * w.D * 2
+            per += (tail_rows + (1 if tail_rows else 0)) * 2 * w.D * 2
         qb = 4 if w.q_dtype == "f32" else 2
         M = w.M if w.mode == "prefill" else 1
         return BH * per + w.B * w.Hq * M * w.D * (qb + 4)

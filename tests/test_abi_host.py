@@ -116,6 +116,35 @@ def test_select_quantize_append_validation(uc):
     assert L.uc_segment_mass(ctypes.byref(sh), 0, 1, FAKE, FAKE, FAKE, None) == E
 
 
+def _attend_append(uc, shape, segs, tail, n_new, kn=FAKE, vn=FAKE, q=FAKE, M=1, ws_bytes=1 << 40):
+    arr = (uc.uc_segment * len(segs))(*segs)
+    return uc.lib.uc_attend_append(ctypes.byref(shape), arr, len(segs), tail, kn, vn, n_new, q,
+                                   uc.UC_BF16, M, ctypes.c_float(0.1), FAKE, None, None, FAKE,
+                                   ws_bytes, None)
+
+
+def test_attend_append_validation(uc):
+    sh = uc.uc_shape(1, 4, 1, 128)
+    E = uc.UC_E_INVALID
+    tail = _dense(uc, 7, stride=8)
+    segs = [_dense(uc, 64), tail]
+    assert _attend_append(uc, sh, segs, 2, 1) == E  # tail index out of range
+    assert _attend_append(uc, sh, segs, -1, 1) == E
+    assert _attend_append(uc, sh, [_dense(uc, 64), _packed(uc, 128)], 1, 1) == E  # not dense
+    assert "not dense" in uc.uc_last_error()
+    assert _attend_append(uc, sh, segs, 1, -1) == E
+    assert _attend_append(uc, sh, segs, 1, 2) == E  # 7 + 2 rows > capacity 8
+    assert "exceed row_stride" in uc.uc_last_error()
+    assert _attend_append(uc, sh, [_dense(uc, 64), _dense(uc, 3)], 1, 1) == E  # no capacity
+    assert _attend_append(uc, sh, segs, 1, 1, kn=None) == E
+    assert _attend_append(uc, sh, segs, 1, 1, vn=FAKE + 4) == E  # misaligned
+    assert _attend_append(uc, sh, segs, 1, 1, q=None) == E
+    assert _attend_append(uc, sh, segs, 1, 1, M=0) == E
+    assert _attend_append(uc, sh, segs, 1, 1, ws_bytes=16) == uc.UC_E_WORKSPACE
+    # an empty tail with nothing else to attend is an error only without new rows
+    assert _attend_append(uc, sh, [_dense(uc, 0, stride=4)], 0, 0) == E
+
+
 def test_dynamic_budget_entry_validation(uc):
     sh = uc.uc_shape(1, 4, 2, 128)
     dense = _dense(uc, 64)
