@@ -148,8 +148,8 @@ __global__ __launch_bounds__(256) void attend_generic_kernel(KSegs segs, ChunkPl
 // (lane % 16) * D/16 ...): each record group merges every fourth record
 // online (independent loads, running maximum), then the four groups are
 // merged with cross-lane exchanges.  Records with m = -inf hold no rows
-// (nothing of them is read but m).  Per-segment log-sum-exps take one more
-// pass over m and l only.
+// (their other fields are loaded but never used).  Per-segment log-sum-exps
+// take one more pass over m and l only.
 template <int D>
 __global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int nseg, int ps,
                                                             const float* __restrict__ partial,
@@ -163,25 +163,35 @@ __global__ __launch_bounds__(64) void attend_combine_kernel(ChunkPlan plan, int 
   float m = -INFINITY, l = 0.0f, acc[PD];
 #pragma unroll
   for (int i = 0; i < PD; ++i) acc[i] = 0.0f;
-#pragma unroll 2
-  for (int c = rg; c < C; c += 4) {
-    const float* pc = P + (int64_t)c * ps;
-    const float mc = pc[0];
-    if (mc == -INFINITY) continue;
-    const float lc = pc[1];
-    float oc[PD];
-    if (o) {
+  // two records per pass, every load issued before any value is used (one
+  // memory latency per pass, not one per field); an empty record's other
+  // fields are not defined, so it is dropped by selects after loading
+  for (int c0 = rg; c0 < C; c0 += 8) {
+    const bool two = c0 + 4 < C;
+    const float* pr[2] = {P + (int64_t)c0 * ps, P + (int64_t)(two ? c0 + 4 : c0) * ps};
+    float mc[2], lc[2], oc[2][PD];
 #pragma unroll
-      for (int i = 0; i < PD; ++i) oc[i] = pc[2 + d0 + i];
-    }
-    const float mn = fmaxf(m, mc);
-    const float a = exp2f(m - mn), b = exp2f(mc - mn);
-    l = fmaf(l, a, lc * b);
-    if (o) {
+    for (int r = 0; r < 2; ++r) {
+      mc[r] = pr[r][0];
+      lc[r] = pr[r][1];
+      if (o) {
 #pragma unroll
-      for (int i = 0; i < PD; ++i) acc[i] = fmaf(acc[i], a, oc[i] * b);
+        for (int i = 0; i < PD; ++i) oc[r][i] = pr[r][2 + d0 + i];
+      }
     }
-    m = mn;
+    if (!two) mc[1] = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const bool live = mc[r] != -INFINITY;
+      const float mn = fmaxf(m, mc[r]);
+      const float a = exp2f(m - mn), b = exp2f(mc[r] - mn);
+      l = live ? fmaf(l, a, lc[r] * b) : l;
+      if (o) {
+#pragma unroll
+        for (int i = 0; i < PD; ++i) acc[i] = live ? fmaf(acc[i], a, oc[r][i] * b) : acc[i];
+      }
+      m = live ? mn : m;
+    }
   }
   float M = fmaxf(m, __shfl_xor(m, 16, 64));
   M = fmaxf(M, __shfl_xor(M, 32, 64));
