@@ -44,8 +44,8 @@ def parse():
                     help="decode steps between timed ones: every event record on the stream "
                          "costs the GPU about 3 us, so the kernel and call events bracket "
                          "steps 0, n, 2n, ... of each job and the rest run unobserved")
-    ap.add_argument("--cpu-sample-heads", type=int, default=16)
-    ap.add_argument("--cpu-sample-steps", type=int, default=8)
+    ap.add_argument("--cpu-sample-heads", type=int, default=32)
+    ap.add_argument("--cpu-sample-steps", type=int, default=64)
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="after the run, copy a 1 GiB device buffer 3 times (a plain copy "
                          "kernel of known size, for scaling HBM byte counters)")
@@ -63,6 +63,10 @@ def parse():
     ap.add_argument("--batch", action="store_true",
                     help="instead of the decode job: 16 decode requests of different lengths, "
                          "one batched call against one call per request (one JSON line)")
+    ap.add_argument("--mall-check", action="store_true",
+                    help="decode kernel time on one copy of the compressed 64k cache vs "
+                         "alternating between two copies (reuse distance above the 256 MB "
+                         "last-level cache)")
     ap.add_argument("--dynamic", action="store_true",
                     help="instead of the decode job: the editing workload under the dynamic "
                          "budget (Eq. 1-3), reporting the chunk-boundary overhead (one JSON line)")
@@ -437,6 +441,76 @@ def prefill_bench(args):
                       "steps": n}), flush=True)
 
 
+def _clone_segment(seg):
+    """A copy of a segment (descriptor and every buffer it points into)."""
+    import ctypes
+
+    import torch
+
+    import paper_2609_32831_amd as uc
+    t2 = {k: (v.clone() if isinstance(v, torch.Tensor) else v) for k, v in seg.t.items()}
+    d = uc.uc_segment()
+    ctypes.memmove(ctypes.byref(d), ctypes.byref(seg.desc), ctypes.sizeof(d))
+    for f in ("k", "v", "idx", "head_bits", "code_off", "codes_k", "codes_v", "scale_k", "min_k",
+              "scale_v", "min_v", "tail_k", "tail_v"):
+        if getattr(seg.desc, f) and t2.get(f) is not None:
+            setattr(d, f, t2[f].data_ptr())
+    return uc.Segment(d, t2)
+
+
+def mall_check(args):
+    """The decode kernel on the 64k cache (tail of 256 rows) timed on one copy
+    of the compressed cache, and alternating between two identical copies:
+    each call reads 435 MB, more than the 256 MB last-level cache, and with
+    two copies a row is read again only after 870 MB of other rows.  Equal
+    times mean that the single-copy figure is not helped by cache reuse."""
+    import torch
+
+    import paper_2609_32831_amd as uc
+    import workloads as gen
+    from paper_2609_32831_amd.runner import Run
+    from workloads.device import device_inputs
+
+    w = gen.LONG_CONTEXT_64K
+    inp = device_inputs(w, "cuda", steps=w.steps)
+    run = Run(w, inp)
+    run.compress()
+    o = torch.empty(w.B, w.Hq, 1, w.D, device="cuda")
+    for t in range(256):
+        uc.uc_attend_append(run.shape, run.mixed, len(run.mixed) - 1, inp["k_dec"][t],
+                            inp["v_dec"][t], 1, inp["q_dec"][t], 1, run.sm, o, ws=run.ws_attend)
+    copies = [run.mixed, [_clone_segment(sg) for sg in run.mixed]]
+    torch.cuda.synchronize()
+    q = inp["q_dec"][300]
+    n = 64
+    evs = HipEvents(2 * n)
+
+    def timed(order):
+        for i in range(8):
+            uc.uc_attend_mixed(run.shape, copies[order[i % len(order)]], q, 1, run.sm, o,
+                               ws=run.ws_attend)
+        for i in range(n):
+            uc.uc_set_kernel_events(evs.handle(2 * i), evs.handle(2 * i + 1))
+            uc.uc_attend_mixed(run.shape, copies[order[i % len(order)]], q, 1, run.sm, o,
+                               ws=run.ws_attend)
+        torch.cuda.synchronize()
+        return sum(evs.elapsed_ms(2 * i, 2 * i + 1) for i in range(n)) / n * 1e3
+
+    res = {"one": [], "two": []}
+    for _ in range(3):
+        res["one"].append(timed([0]))
+        res["two"].append(timed([0, 1]))
+    nbytes = run.attended_bytes(256)
+    one, two = min(res["one"]), min(res["two"])
+    print(json.dumps({"metric": "decode kernel, one cache copy vs two alternating copies",
+                      "workload": w.name, "bytes_per_call": int(nbytes),
+                      "one_copy_us": round(one, 2), "two_copies_us": round(two, 2),
+                      "one_copy_frac": round(nbytes / one / 1e3 / HBM_PEAK_GBPS, 4),
+                      "two_copies_frac": round(nbytes / two / 1e3 / HBM_PEAK_GBPS, 4),
+                      "ratio": round(two / one, 4)}), flush=True)
+    evs.close()
+
+
 def dynamic_bench(args):
     """The editing workload under the dynamic budget (Sec. 3.3 Eq. 1-3): per
     request, timestep 0 on the full cache plus the initial compression, then
@@ -623,6 +697,11 @@ def main():
         if args.gpus != 1:
             sys.exit(2)
         dynamic_bench(args)
+        return
+    if args.mall_check:
+        if args.gpus != 1:
+            sys.exit(2)
+        mall_check(args)
         return
     if args.batch:
         if args.gpus != 1:

@@ -360,10 +360,19 @@ __device__ __attribute__((always_inline)) inline void packed_loop(State& st, con
 // (m, l, o) per segment for its query rows (slot s*W + w; m = -inf for an
 // empty share); otherwise one running state spans all segments and one record
 // per workgroup (slot w) is written.  The combine kernel merges the records.
+// Packed tiles cost several times the vector-ALU work of dense tiles per
+// byte; if every workgroup took its packed share first, the whole chip would
+// be ALU-bound for that phase and HBM underused.  With a split segment (the
+// largest dense one, chosen on the host when packed rows are present), each
+// workgroup instead takes the first part of its share of that segment, then
+// the other segments, then the rest; the part before is a fraction
+// ((w + bh) mod W) / W of its tiles, so the packed phases of the workgroups
+// are staggered over the launch.
 struct DecodePlan {
   int W;        // workgroups per (b, h_kv)
   int n_seg;
   int per_seg;  // 1: one record per segment and workgroup
+  int split;    // segment taken around the others (see above), or -1
 };
 
 // tile-aligned share w of n rows among W workgroups
@@ -551,14 +560,28 @@ __device__ __attribute__((always_inline)) inline void decode_body(
       c.partial[(qrow_of(c, e / (W - Wr)) * c.C + Wr + e % (W - Wr)) * (D + 2)] = -INFINITY;
   }
   const int sbh = BATCH ? hkv : bh;  // (b, h_kv) within the segments' own layout
-  for (int si = 0; si < n_seg; ++si) {
+  // items: the segments in order, or with a split segment (never with
+  // per-segment records or batched requests) its first part, the others in
+  // order, then its second part
+  const int split = BATCH ? -1 : pl.split;
+  const int n_items = split >= 0 ? n_seg + 1 : n_seg;
+  for (int it = 0; it < n_items; ++it) {
+    int si = it;
+    if (split >= 0) si = it == 0 || it == n_items - 1 ? split : (it - 1 < split ? it - 1 : it);
     const KSeg& ks = BATCH ? flat[first + si] : segs.s[si];
     // the appended rows (the last segment) go to the last workgroup, whose
     // shares of the other segments are the remainders; workgroup 0 already
     // holds the start of the protected segment
     const int ws = (!BATCH && ap.n_new > 0 && si == n_seg - 1) ? Wr - 1 - w : w;
-    const int r0 = share_row(ks.n_rows, ws, Wr);
-    const int r1 = share_row(ks.n_rows, ws + 1, Wr);
+    int r0 = share_row(ks.n_rows, ws, Wr);
+    int r1 = share_row(ks.n_rows, ws + 1, Wr);
+    if (split >= 0 && si == split) {
+      // r0 is tile-aligned, so both parts start on a tile boundary and only
+      // the second can end in a partial tile
+      const int rm = r0 + ((r1 - r0) / TILE * ((w + bh) % Wr) / Wr) * TILE;
+      if (it == 0) r1 = rm;
+      else r0 = rm;
+    }
     ok &= segment_share(st, ks, sbh, r0, r1, wave, rot, lane, lq, scale_log2, lk, lv);
     if (pl.per_seg) {
       flush(st, lds, c, si * W + w, ok, lane, wave);
@@ -654,6 +677,19 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   p.W = decode_w(sh);
   p.n_seg = segs.n;
   p.per_seg = seg_lse != nullptr;
+  // split the largest dense segment around the others when packed rows are
+  // present (staggered packed phases, see DecodePlan)
+  p.split = -1;
+  if (!p.per_seg && segs.n > 1) {
+    bool packed = false;
+    int best = -1;
+    for (int i = 0; i < segs.n; ++i) {
+      const KSeg& s = segs.s[i];
+      if (s.kind == UC_SEG_PACKED && s.n_full > 0) packed = true;
+      if (s.kind == UC_SEG_DENSE && (best < 0 || s.n_rows > segs.s[best].n_rows)) best = i;
+    }
+    if (packed && best >= 0 && segs.s[best].n_rows > 0) p.split = best;
+  }
   float* partial = (float*)ws;
   hipError_t e = kernel_timer_begin(st);
   if (e != hipSuccess) return e;
@@ -699,6 +735,7 @@ hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, 
   p.W = W_max;
   p.n_seg = sh.B;  // the batched kernel reads the number of requests from here
   p.per_seg = 0;
+  p.split = -1;
   const BatchDesc* table = (const BatchDesc*)ws;
   const KSeg* flat =
       (const KSeg*)((char*)ws + ((((size_t)sh.B * sizeof(BatchDesc)) + 255) & ~(size_t)255));
