@@ -297,6 +297,12 @@ DCASES = [
     (1, 28, 4, 2, 128, 4, False, (0, 100, 3, 130, 0, 4)),
     (2, 28, 4, 1, 64, 4, True, (128, 1000, 257, 2048 + 40, 5, 8)),   # int2/int4 per head
     (1, 28, 4, 1, 32, 4, False, (0, 0, 0, 31, 1, 1)),                # tail-only packed rows
+    # 64 KV heads, so that a head's shares are several tiles long: the largest
+    # dense segment is split around the others at every phase (compacted
+    # rows here, the first segment in the next case), its last share ending
+    # in a partial tile
+    (8, 56, 8, 1, 64, 4, False, (200, 3000, 1500, 2048 + 10, 37, 64)),
+    (8, 56, 8, 1, 32, 4, False, (2000, 300, 100, 1024, 3, 4)),
 ]
 
 
