@@ -113,6 +113,182 @@ __global__ void quantize_v_kernel(KSeg seg, const void* __restrict__ v, int dt, 
   }
 }
 
+// ---- vectorised forms for 2-byte dtypes and head dims 64 / 128: a lane
+// holds 8 consecutive channels of a row (one 16-byte load) and writes their
+// 8 codes as one 16-, 32- or 64-bit store.  Min and max are exact and the
+// scale, division and rounding are those of quant_code, so the results are
+// the same bits as the per-element forms above.
+
+// 8 channels starting at element e (16-byte aligned) as floats
+__device__ inline void load8(const void* p, int dt, int64_t e, float (&x)[8]) {
+  const uint4 w = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(p) + e);
+  const uint32_t u[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint16_t lo = (uint16_t)(u[j] & 0xFFFFu), hi = (uint16_t)(u[j] >> 16);
+    x[2 * j] = dt == UC_BF16 ? bf16_to_f32(lo) : f16_to_f32(lo);
+    x[2 * j + 1] = dt == UC_BF16 ? bf16_to_f32(hi) : f16_to_f32(hi);
+  }
+}
+
+// the b-bit codes of 8 consecutive channels (channel e at bit b*e) stored at p
+__device__ inline void store_codes8(uint8_t* p, const int (&code)[8], int b) {
+  uint64_t w = 0;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) w |= (uint64_t)code[e] << (b * e);
+  if (b == 2) *reinterpret_cast<uint16_t*>(p) = (uint16_t)w;
+  else if (b == 4) *reinterpret_cast<uint32_t*>(p) = (uint32_t)w;
+  else *reinterpret_cast<uint64_t*>(p) = w;
+}
+
+// Values, group G >= 8: a group is G/8 neighbouring lanes of one row; its
+// min and max combine by shuffles.  Block = 256 lanes = 256/(D/8) rows.
+__global__ __launch_bounds__(256) void quantize_v_vec_kernel(KSeg seg, const void* __restrict__ v,
+                                                             int dt, int N, int D) {
+  const int cpr = D / 8;  // lanes per row
+  const int c8 = threadIdx.x % cpr;
+  const int r = blockIdx.x * (256 / cpr) + threadIdx.x / cpr, bh = blockIdx.y;
+  const int G = seg.group, lpg = G / 8;
+  int b;
+  int64_t off;
+  const bool ok = head_codes(seg, bh, D, b, off) && !(off & 15);
+  const bool live = r < seg.n_full;
+  float x[8];
+  if (live) {
+    load8(v, dt, ((int64_t)bh * N + r) * D + c8 * 8, x);
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) x[e] = 0.0f;
+  }
+  float mn = x[0], mx = x[0];
+#pragma unroll
+  for (int e = 1; e < 8; ++e) {
+    mn = fminf(mn, x[e]);
+    mx = fmaxf(mx, x[e]);
+  }
+  // the lanes of a group are aligned and lie in one row, so rows past n_full
+  // only combine among themselves
+  for (int o = 1; o < lpg; o <<= 1) {
+    mn = fminf(mn, __shfl_xor(mn, o, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  }
+  const int qmax = ok ? (1 << b) - 1 : 1;
+  const float s = ok ? __fdiv_rn(mx - mn, (float)qmax) : __builtin_nanf("");
+  if (!live) return;
+  if (c8 % lpg == 0) {
+    const int64_t mi = ((int64_t)bh * seg.cap_full + r) * (D / G) + c8 / lpg;
+    const_cast<float*>(seg.scale_v)[mi] = s;
+    const_cast<float*>(seg.min_v)[mi] = mn;
+  }
+  if (!ok) return;
+  int code[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) code[e] = quant_code(x[e], mn, s, qmax);
+  store_codes8(const_cast<uint8_t*>(seg.codes_v) + off + (int64_t)r * (D * b / 8) + c8 * b, code,
+               b);
+}
+
+// Keys: one block of 256 lanes per (row group, bh); a lane holds 8 channels
+// of rows rr, rr + RB, ... of the group (RB = 256/(D/8) rows per pass, at
+// most 8 rows per lane since G <= D); per-channel min and max combine over
+// the lanes of a wave by shuffles, then over the four waves through LDS.
+__global__ __launch_bounds__(256) void quantize_k_vec_kernel(KSeg seg, const void* __restrict__ k,
+                                                             int dt, int N, int D) {
+  __shared__ float red[2][4][128];
+  const int cpr = D / 8, RB = 256 / cpr;
+  const int c8 = threadIdx.x % cpr, rr = threadIdx.x / cpr;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int g = blockIdx.x, bh = blockIdx.y, G = seg.group;
+  int b;
+  int64_t off;
+  float* scale = const_cast<float*>(seg.scale_k) + ((int64_t)bh * seg.kgroups + g) * D + c8 * 8;
+  float* mnp = const_cast<float*>(seg.min_k) + ((int64_t)bh * seg.kgroups + g) * D + c8 * 8;
+  if (!head_codes(seg, bh, D, b, off) || (off & 15)) {  // uniform over the block
+    if (rr == 0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) scale[e] = __builtin_nanf("");
+    }
+    return;
+  }
+  const int qmax = (1 << b) - 1;
+  const int64_t base = ((int64_t)bh * N + (int64_t)g * G) * D + c8 * 8;
+  uint4 raw[8];
+  float mn[8], mx[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    mn[e] = INFINITY;
+    mx[e] = -INFINITY;
+  }
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = rr + i * RB;
+    if (r < G) {
+      raw[i] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(k) + base +
+                                               (int64_t)r * D);
+      float x[8];
+      load8(k, dt, base + (int64_t)r * D, x);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        mn[e] = fminf(mn[e], x[e]);
+        mx[e] = fmaxf(mx[e], x[e]);
+      }
+    }
+  }
+  for (int o = cpr; o < 64; o <<= 1) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      mn[e] = fminf(mn[e], __shfl_xor(mn[e], o, 64));
+      mx[e] = fmaxf(mx[e], __shfl_xor(mx[e], o, 64));
+    }
+  }
+  if (lane < cpr) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      red[0][wave][c8 * 8 + e] = mn[e];
+      red[1][wave][c8 * 8 + e] = mx[e];
+    }
+  }
+  __syncthreads();
+  float s[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    float a = red[0][0][c8 * 8 + e], z = red[1][0][c8 * 8 + e];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      a = fminf(a, red[0][w][c8 * 8 + e]);
+      z = fmaxf(z, red[1][w][c8 * 8 + e]);
+    }
+    mn[e] = a;
+    s[e] = __fdiv_rn(z - a, (float)qmax);
+  }
+  if (rr == 0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      scale[e] = s[e];
+      mnp[e] = mn[e];
+    }
+  }
+  const int row_bytes = D * b / 8;
+  uint8_t* codes = const_cast<uint8_t*>(seg.codes_k) + off + (int64_t)g * G * row_bytes + c8 * b;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    const int r = rr + i * RB;
+    if (r < G) {
+      const uint32_t u[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+      int code[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint16_t lo = (uint16_t)(u[j] & 0xFFFFu), hi = (uint16_t)(u[j] >> 16);
+        const float x0 = dt == UC_BF16 ? bf16_to_f32(lo) : f16_to_f32(lo);
+        const float x1 = dt == UC_BF16 ? bf16_to_f32(hi) : f16_to_f32(hi);
+        code[2 * j] = quant_code(x0, mn[2 * j], s[2 * j], qmax);
+        code[2 * j + 1] = quant_code(x1, mn[2 * j + 1], s[2 * j + 1], qmax);
+      }
+      store_codes8(codes + (int64_t)r * row_bytes, code, b);
+    }
+  }
+}
+
 // Residual tail: rows n_full..N-1 copied unchanged (16 bytes per lane).
 __global__ void copy_tail_kernel(KSeg seg, const void* __restrict__ k, const void* __restrict__ v,
                                  int N, int row_bytes) {
@@ -239,11 +415,25 @@ hipError_t launch_quantize(const uc_shape& sh, const void* k, const void* v, int
                            const KSeg& out, hipStream_t st) {
   const int BH = sh.B * sh.Hkv, D = sh.D;
   if (out.n_full > 0) {
-    hipLaunchKernelGGL(quantize_k_kernel, dim3(out.n_full / out.group, BH), dim3(D), 0, st, out,
-                       k, dt, N, D);
-    const int rpb = 256 / D;
-    hipLaunchKernelGGL(quantize_v_kernel, dim3((out.n_full + rpb - 1) / rpb, BH), dim3(256), 0,
-                       st, out, v, dt, N, D);
+    // vectorised forms: 2-byte dtypes, head dim 64 or 128, 16-byte aligned
+    // rows (values also need groups of at least 8 channels)
+    const bool vec = dt != UC_F32 && (D == 64 || D == 128) && !((uintptr_t)k & 15) &&
+                     !((uintptr_t)v & 15);
+    if (vec)
+      hipLaunchKernelGGL(quantize_k_vec_kernel, dim3(out.n_full / out.group, BH), dim3(256), 0, st,
+                         out, k, dt, N, D);
+    else
+      hipLaunchKernelGGL(quantize_k_kernel, dim3(out.n_full / out.group, BH), dim3(D), 0, st, out,
+                         k, dt, N, D);
+    if (vec && out.group >= 8) {
+      const int rpb = 256 / (D / 8);
+      hipLaunchKernelGGL(quantize_v_vec_kernel, dim3((out.n_full + rpb - 1) / rpb, BH), dim3(256),
+                         0, st, out, v, dt, N, D);
+    } else {
+      const int rpb = 256 / D;
+      hipLaunchKernelGGL(quantize_v_kernel, dim3((out.n_full + rpb - 1) / rpb, BH), dim3(256), 0,
+                         st, out, v, dt, N, D);
+    }
   }
   if (out.tail_len > 0) {
     const int row_bytes = D * dtype_bytes(dt);

@@ -32,6 +32,12 @@ QCASES = [
     ("bf16", 1, 3, 77, 64, 8, 8),
     ("bf16", 1, 2, 100, 128, 128, 4),   # shorter than one group: all tail
     ("bf16", 1, 1, 64, 128, 64, 2),     # exactly one group, no tail
+    # shapes of the vectorised kernels: key groups shorter than a pass (8 rows),
+    # head dim 64 with 8-bit codes, per-head widths with whole-row groups
+    ("bf16", 1, 2, 300, 128, 8, 4),
+    ("f16", 2, 2, 640 + 63, 64, 64, 8),
+    ("bf16", 1, 4, 1024 + 5, 128, 128, [8, 2, 4, 8]),
+    ("bf16", 1, 1, 48, 128, 16, 2),
 ]
 
 
