@@ -30,40 +30,38 @@ __device__ inline uint32_t order_key(float f) {
   return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-// exclusive scan of one uint32 per thread over the block (16 waves)
-__device__ inline uint32_t block_exclusive_scan(uint32_t x, uint32_t* wave_tot) {
+constexpr int kSelWaves = kSelThreads / 64;
+
+// Exclusive prefix over the block's waves of one value per wave (lane 0's
+// x); returns it in every lane of the wave.  wave_tot holds kSelWaves words.
+__device__ inline uint32_t wave_exclusive(uint32_t x, uint32_t* wave_tot) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t inc = x;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    uint32_t y = __shfl_up(inc, o, 64);
-    if (lane >= o) inc += y;
-  }
-  if (lane == 63) wave_tot[wave] = inc;
+  if (lane == 0) wave_tot[wave] = x;
   __syncthreads();
-  if (wave == 0) {
-    uint32_t t = lane < kSelThreads / 64 ? wave_tot[lane] : 0u;
-    uint32_t ti = t;
-#pragma unroll
-    for (int o = 1; o < 16; o <<= 1) {
-      uint32_t y = __shfl_up(ti, o, 64);
-      if (lane >= o) ti += y;
-    }
-    if (lane < kSelThreads / 64) wave_tot[lane] = ti - t;
-  }
-  __syncthreads();
-  uint32_t r = wave_tot[wave] + inc - x;
+  uint32_t r = 0;
+  for (int w = 0; w < wave; ++w) r += wave_tot[w];
   __syncthreads();
   return r;
 }
 
+// Radix select finds tau (the k'-th largest order key) 8 bits at a time:
+// each wave counts the keys that match the prefix found so far in a
+// histogram of its own (so hot bins, where scores share an exponent, are
+// contended by 64 lanes only), the 16 histograms are summed, and one wave
+// locates the digit with a scan over the bins from the top.  Compaction:
+// wave w takes the w-th contiguous run of positions, reading 64 consecutive
+// keys at a time; a kept key's output slot is the number of kept keys before
+// it: (keys above tau before it) + min(keys equal to tau before it, need),
+// from ballots within the wave and exclusive sums over the waves.
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores, int N,
                                                              int k, int n_recent,
                                                              int32_t* __restrict__ keep) {
+  __shared__ uint32_t whist[kSelWaves][256];
   __shared__ uint32_t hist[256];
-  __shared__ uint32_t wave_tot[kSelThreads / 64];
+  __shared__ uint32_t wave_tot[kSelWaves];
   __shared__ uint32_t sh_digit, sh_need;
   const int bh = blockIdx.x, tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
   const float* s = scores + (int64_t)bh * N;
   int32_t* out = keep + (int64_t)bh * k;
   const int Nc = N - n_recent, kc = k - n_recent;
@@ -73,22 +71,42 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     for (int pass = 0; pass < 4; ++pass) {
       const int shift = 24 - 8 * pass;
       const uint32_t hi_mask = pass == 0 ? 0u : (0xFFFFFFFFu << (32 - 8 * pass));
-      for (int t = tid; t < 256; t += kSelThreads) hist[t] = 0u;
+      for (int t = lane; t < 256; t += 64) whist[wave][t] = 0u;
       __syncthreads();
       for (int i = tid; i < Nc; i += kSelThreads) {
         const uint32_t key = order_key(s[i]);
-        if ((key & hi_mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+        if ((key & hi_mask) == prefix) atomicAdd(&whist[wave][(key >> shift) & 255u], 1u);
       }
       __syncthreads();
-      if (tid == 0) {
-        uint32_t cum = 0;
-        for (int d = 255; d >= 0; --d) {
-          if (cum + hist[d] >= need) {
-            sh_digit = (uint32_t)d;
-            sh_need = need - cum;
-            break;
+      if (tid < 256) {
+        uint32_t h = 0;
+#pragma unroll
+        for (int w = 0; w < kSelWaves; ++w) h += whist[w][tid];
+        hist[tid] = h;
+      }
+      __syncthreads();
+      if (wave == 0) {
+        // lane l owns bins 255-4l .. 252-4l, taken from the top
+        uint32_t c[4], tot = 0;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          c[j] = hist[255 - 4 * lane - j];
+          tot += c[j];
+        }
+        uint32_t inc = tot;
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+          const uint32_t y = __shfl_up(inc, o, 64);
+          if (lane >= o) inc += y;
+        }
+        uint32_t before = inc - tot;  // keys in higher bins than this lane's
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          if (before < need && before + c[j] >= need) {
+            sh_digit = (uint32_t)(255 - 4 * lane - j);
+            sh_need = need - before;
           }
-          cum += hist[d];
+          before += c[j];
         }
       }
       __syncthreads();
@@ -98,28 +116,32 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
     }
   }
   // prefix is the k'-th largest key; `need` rows equal to it are kept
-  const int per = (Nc + kSelThreads - 1) / kSelThreads;
-  const int i0 = min(tid * per, Nc), i1 = min(i0 + per, Nc);
-  uint32_t cgt = 0, ceq = 0;
   if (kc > 0) {
-    for (int i = i0; i < i1; ++i) {
-      const uint32_t key = order_key(s[i]);
-      cgt += key > prefix;
-      ceq += key == prefix;
+    const int per = (Nc + kSelWaves - 1) / kSelWaves;
+    const int i0 = min(wave * per, Nc), i1 = min(i0 + per, Nc);
+    uint32_t cgt = 0, ceq = 0;
+    for (int b0 = i0; b0 < i1; b0 += 64) {
+      const int i = b0 + lane;
+      const uint32_t key = i < i1 ? order_key(s[i]) : 0u;
+      cgt += (uint32_t)__popcll(__ballot(i < i1 && key > prefix));
+      ceq += (uint32_t)__popcll(__ballot(i < i1 && key == prefix));
     }
-  }
-  const uint32_t gt_ex = block_exclusive_scan(cgt, wave_tot);
-  const uint32_t eq_ex = block_exclusive_scan(ceq, wave_tot);
-  if (kc > 0) {
-    uint32_t pos = gt_ex + min(eq_ex, need), eq_seen = eq_ex;
-    for (int i = i0; i < i1; ++i) {
-      const uint32_t key = order_key(s[i]);
-      if (key > prefix) {
-        out[pos++] = i;
-      } else if (key == prefix) {
-        if (eq_seen < need) out[pos++] = i;
-        ++eq_seen;
+    uint32_t gt = wave_exclusive(cgt, wave_tot);
+    uint32_t eq = wave_exclusive(ceq, wave_tot);
+    const uint64_t below = (1ull << lane) - 1ull;  // lanes before this one
+    for (int b0 = i0; b0 < i1; b0 += 64) {
+      const int i = b0 + lane;
+      const uint32_t key = i < i1 ? order_key(s[i]) : 0u;
+      const uint64_t bg = __ballot(i < i1 && key > prefix);
+      const uint64_t be = __ballot(i < i1 && key == prefix);
+      const uint32_t g_rank = gt + (uint32_t)__popcll(bg & below);
+      const uint32_t e_rank = eq + (uint32_t)__popcll(be & below);
+      if (i < i1) {
+        if (key > prefix) out[g_rank + min(e_rank, need)] = i;
+        else if (key == prefix && e_rank < need) out[g_rank + e_rank] = i;
       }
+      gt += (uint32_t)__popcll(bg);
+      eq += (uint32_t)__popcll(be);
     }
   }
   for (int j = tid; j < n_recent; j += kSelThreads) out[kc + j] = Nc + j;
