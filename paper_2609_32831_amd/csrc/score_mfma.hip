@@ -59,18 +59,23 @@ __device__ inline void k_issue(__amdgpu_buffer_rsrc_t rk, int row0, int lane, u4
   }
 }
 
-// S^T of a key tile against query tile qt: s0 = keys 0..15, s1 = keys 16..31;
-// lane (i16, g4) holds keys g4*4 + j (+16) of query column i16
-__device__ inline void s_tile(const u4 (&k)[8], const char* qs, int qt, int lane, f4& s0, f4& s1) {
+// B operands (Q^T) of query tile qt, four 32-dim steps, from the staged block
+__device__ inline void q_tile(const char* qs, int qt, int lane, u4 (&qb)[4]) {
   const int i16 = lane & 15, g4 = lane >> 4;
   const char* qrow = qs + (qt * 16 + i16) * QROW + g4 * 16;
+#pragma unroll
+  for (int t = 0; t < 4; ++t) qb[t] = *reinterpret_cast<const u4*>(qrow + t * 64);
+}
+
+// S^T of a key tile against one query tile: s0 = keys 0..15, s1 = keys
+// 16..31; lane (i16, g4) holds keys g4*4 + j (+16) of query column i16
+__device__ inline void s_tile(const u4 (&k)[8], const u4 (&qb)[4], f4& s0, f4& s1) {
   s0 = f4{0.f, 0.f, 0.f, 0.f};
   s1 = s0;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const u4 b = *reinterpret_cast<const u4*>(qrow + t * 64);
-    s0 = mfma(k[t], b, s0);
-    s1 = mfma(k[4 + t], b, s1);
+    s0 = mfma(k[t], qb[t], s0);
+    s1 = mfma(k[4 + t], qb[t], s1);
   }
 }
 
@@ -149,24 +154,31 @@ __global__ __launch_bounds__(256, 2) void score_lse_kernel(KSegs segs, ChunkPlan
       // the wave's state so far enters through one of the four key-row lanes
       float m = g4 == 0 ? red_m[wave][t * 16 + i16] : -INFINITY;
       float l = g4 == 0 ? red_l[wave][t * 16 + i16] : 0.0f;
+      u4 qb[4];
+      q_tile(qs, t, lane, qb);
 #pragma unroll
       for (int i = 0; i < TPW; ++i) {
         const int row0 = sc + (wave + i * WAVES) * TILE;
         if (row0 < r1) {
           f4 s0, s1;
-          s_tile(K.k[i], qs, t, lane, s0, s1);
+          s_tile(K.k[i], qb, s0, s1);
           float x[8];
-          logits(s0, s1, scale_log2, row0, r1, g4, x);
+          logits(s0, s1, 1.0f, row0, r1, g4, x);  // raw logits (masked)
+          // the scale is positive: the maximum of the raw logits gives it
           const float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
-                                 fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
+                                 fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7]))) * scale_log2;
           if (mx > m + kLazy) {  // per-lane state: raise the reference maximum
-            l *= exp2f(m - mx);
+            l *= __builtin_amdgcn_exp2f(m - mx);
             m = mx;
           }
+          // arguments are at most kLazy, so v_exp_f32 needs no range
+          // reduction; probabilities below 2^-126 of the reference flush
           float e = 0.0f;
 #pragma unroll
-          for (int j = 0; j < 8; ++j) e += exp2f(x[j] - m);
-          l += e;
+          for (int j = 0; j < 8; ++j) e += __builtin_amdgcn_exp2f(fmaf(x[j], scale_log2, -m));
+          // a lane whose keys are all past the range before any valid key
+          // keeps m = -inf and no sum
+          if (m != -INFINITY) l += e;
         }
       }
       // merge the four key-row lanes (g4) of each query column
@@ -253,15 +265,18 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
         for (int j = 0; j < 8; ++j) cs[i][j] = 0.0f;
       for (int t = 0; t < nqt; ++t) {
         const float lq = ls[t * 16 + i16];
+        u4 qb[4];
+        q_tile(qs, t, lane, qb);
 #pragma unroll
         for (int i = 0; i < TPW; ++i) {
           if (sc + (wave + i * WAVES) * TILE < r1) {
             f4 s0, s1;
-            s_tile(K.k[i], qs, t, lane, s0, s1);
+            s_tile(K.k[i], qb, s0, s1);
+            // p <= 1 (s <= lse); probabilities below 2^-126 flush to zero
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
-              cs[i][j] += exp2f(fmaf(s0[j], scale_log2, -lq));
-              cs[i][4 + j] += exp2f(fmaf(s1[j], scale_log2, -lq));
+              cs[i][j] += __builtin_amdgcn_exp2f(fmaf(s0[j], scale_log2, -lq));
+              cs[i][4 + j] += __builtin_amdgcn_exp2f(fmaf(s1[j], scale_log2, -lq));
             }
           }
         }
