@@ -72,6 +72,36 @@ __device__ inline int tile_view(const Views& vs, int t, int& row0) {
   return i;
 }
 
+// A walk over the logical sequence one 32-row tile at a time.  The current
+// view's row count, segment and this (b, h_kv)'s K and V rows stay in
+// scalars, so a step reads the view table (kernel arguments) only when it
+// crosses into the next view.
+template <bool F16>
+struct Cursor {
+  int vi, row0, n, seg;
+  const uint16_t* k;
+  const uint16_t* v;
+  __device__ inline void load(const Views& vs, int bh) {
+    const View& w = vs.v[vi];
+    n = w.n;
+    seg = w.seg;
+    k = w.k + bh * w.bh_stride;
+    v = F16 ? w.vh + (int64_t)bh * w.n * D : w.v + bh * w.bh_stride;
+  }
+  __device__ inline void start(const Views& vs, int bh, int t) {
+    vi = tile_view(vs, t, row0);
+    load(vs, bh);
+  }
+  __device__ inline void next(const Views& vs, int bh) {
+    row0 += TILE;
+    if (row0 >= n && vi + 1 < vs.n) {
+      ++vi;
+      row0 = 0;
+      load(vs, bh);
+    }
+  }
+};
+
 // one thread's share of staging a tile: rows tid/16 and tid/16 + 16, chunk tid%16
 struct Stage {
   u4 k[2], v[2];
@@ -79,15 +109,11 @@ struct Stage {
 
 // F16: V comes from the view's fp16 copy
 template <bool F16>
-__device__ inline void stage_load(const Views& vs, int t, int bh, Stage& S) {
-  int row0;
-  const View& w = vs.v[tile_view(vs, t, row0)];
-  const __amdgpu_buffer_rsrc_t rk = rsrc(w.k + bh * w.bh_stride, (uint32_t)w.n * ROWB);
-  const __amdgpu_buffer_rsrc_t rv =
-      F16 ? rsrc(w.vh + (int64_t)bh * w.n * D, (uint32_t)w.n * ROWB)
-          : rsrc(w.v + bh * w.bh_stride, (uint32_t)w.n * ROWB);
+__device__ inline void stage_load(const Cursor<F16>& cu, Stage& S) {
+  const __amdgpu_buffer_rsrc_t rk = rsrc(cu.k, (uint32_t)cu.n * ROWB);
+  const __amdgpu_buffer_rsrc_t rv = rsrc(cu.v, (uint32_t)cu.n * ROWB);
   const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
-  const int off = (row0 + r) * ROWB + c * 16;
+  const int off = (cu.row0 + r) * ROWB + c * 16;
   S.k[0] = bload(rk, off, 0);
   S.k[1] = bload(rk, off, 16 * ROWB);
   S.v[0] = bload(rv, off, 0);
@@ -191,15 +217,19 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     const Views& vs, int bh, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW],
     float scale_log2, int r_wave, int nq, int64_t qbase, int nseg, float* seg_lse, int i16,
     int g4) {
-  int cur_view = -1;
+  int cur_view = -1, cur_seg = -1;
   const int T = vs.tiles;
+  Cursor<F16> ct, cs;  // tile t (computed) and tile t + 2 (staged)
   {
     Stage S;
-    stage_load<F16>(vs, 0, bh, S);
+    ct.start(vs, bh, 0);
+    stage_load<F16>(ct, S);
     stage_store(lds, S);
     if (T > 1) {
-      stage_load<F16>(vs, 1, bh, S);
+      cs.start(vs, bh, 1);
+      stage_load<F16>(cs, S);
       stage_store(lds + STAGEB, S);
+      cs.next(vs, bh);
     }
   }
   __syncthreads();
@@ -212,24 +242,28 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
   for (int t = 0; t < T; ++t) {
     Stage S;
     const bool pre = t + 2 < T;
-    if (pre) stage_load<F16>(vs, t + 2, bh, S);
+    if (pre) {
+      stage_load<F16>(cs, S);
+      cs.next(vs, bh);
+    }
     const char* lv = lds + (t % STAGES) * STAGEB + TILEB;
-    int row0;
-    const int vi = tile_view(vs, t, row0);
-    const int n_valid = min(TILE, vs.v[vi].n - row0);
-    if (seg_lse && vi != cur_view && cur_view >= 0 && vs.v[vi].seg != vs.v[cur_view].seg) {
+    const int vi = ct.vi;
+    const int n_valid = min(TILE, ct.n - ct.row0);
+    if (seg_lse && vi != cur_view && cur_view >= 0 && ct.seg != cur_seg) {
       // the previous logical segment ended: its log-sum-exp per query row
 #pragma unroll
       for (int qt = 0; qt < QTW; ++qt) {
         const float ls = col_sum(st[qt].ls);
         const int r = r_wave + qt * 16 + i16;
         if (g4 == 0 && r < nq)
-          seg_lse[(qbase + r) * nseg + vs.v[cur_view].seg] =
+          seg_lse[(qbase + r) * nseg + cur_seg] =
               ls > 0.0f ? (st[qt].m + __log2f(ls)) * kLn2 : -INFINITY;
         st[qt].ls = 0.0f;
       }
     }
     cur_view = vi;
+    cur_seg = ct.seg;
+    ct.next(vs, bh);
     u4 phi[QTW], plo[QTW];
 #pragma unroll
     for (int qt = 0; qt < QTW; ++qt)
