@@ -38,6 +38,7 @@ constexpr int QROWS = WAVES * QTW * 16;    // query rows per workgroup
 constexpr int STAGES = 3;                  // key/value tiles staged in LDS
 constexpr int STAGEB = 2 * TILEB;          // K tile + V tile
 constexpr float kLazy = 8.0f;
+constexpr float kLazyExp = 256.0f;  // 2^kLazy
 constexpr int kMaxViews = 2 * kMaxSeg;
 
 // dense row views of the logical sequence, in order; seg = logical segment
@@ -147,9 +148,21 @@ __device__ inline void tile_softmax(QState& st, const f4& s0, const f4& s1, floa
       if (16 + g4 * 4 + j >= n_valid) p[4 + j] = -INFINITY;
     }
   }
-  float mx = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])),
-                   fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7]))) * scale_log2;
-  if (__builtin_amdgcn_ballot_w64(mx > st.m + kLazy)) {  // rare: raise the reference max
+  // probabilities against the current reference first; a lane sum above
+  // 2^kLazy (every logit more than kLazy above the reference makes one, and
+  // a first tile's -inf reference makes inf or NaN) sends the wave through
+  // the rare path that raises the reference to the column maximum and
+  // recomputes them, so in the common path no maximum is taken
+  float e[8], psum = 0.0f;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
+    psum += e[j];
+  }
+  if (__builtin_amdgcn_ballot_w64(!(psum <= kLazyExp))) {  // rare: raise the reference max
+    // the scale is positive, so the maximum of the raw logits gives the maximum
+    float mx = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])),
+                     fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7]))) * scale_log2;
     mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
     const float m_new = fmaxf(st.m, mx);
@@ -159,12 +172,12 @@ __device__ inline void tile_softmax(QState& st, const f4& s0, const f4& s1, floa
 #pragma unroll
     for (int d = 0; d < 8; ++d) st.acc[d] *= alpha;
     st.m = m_new;
-  }
-  float e[8], psum = 0.0f;
+    psum = 0.0f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
-    psum += e[j];
+    for (int j = 0; j < 8; ++j) {
+      e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
+      psum += e[j];
+    }
   }
   st.l += psum;
   st.ls += psum;
