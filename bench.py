@@ -349,6 +349,7 @@ def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
         "unit": "tokens/s",
         "cores": int(cores),
         "kind": "oracle",
+        "cpu": cpu_model(),
         "sample": (f"{BHs} of {w.B * w.Hkv} KV heads at full 65536-token context: "
                    f"scoring + selection + quantization ({t_compress:.2f} s) and "
                    f"{n_steps} of {T} decode steps ({t_att:.2f} s), extrapolated "
@@ -357,6 +358,63 @@ def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
 
 
 BF16_PEAK_TFLOPS = 2500.0
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_prefill_baseline(w, stride: int = 16):
+    """The CPU oracle's attention for one prefill step of workload w, timed on
+    KV head (0, 0) over every stride-th query row of its block and
+    extrapolated linearly to all query rows and KV heads.  The logical
+    sequence is built as the oracle defines it (kept rows masked in place,
+    packed rows quantised and dequantised, 4-bit where the widths are chosen
+    per head); which rows are kept does not change the oracle's work."""
+    import numpy as np
+
+    import oracle as ref
+    import oracle.pipeline as op
+    import workloads as gen
+
+    cores = ref.set_threads(0)
+    pols = op.plan(w)
+    hi = op.head_inputs(w, 0, 0)
+    comp = {"khat": [], "vhat": [], "present": []}
+    for i, (sg, p) in enumerate(zip(w.segments, pols)):
+        k_i, v_i = hi["seg_k"][i], hi["seg_v"][i]
+        pres = np.ones(sg.n, np.uint8)
+        if p["kind"] == "quant":
+            pk = ref.quantize(k_i[None], v_i[None], sg.dtype, p["group"], [p["bits"] or 4])
+            kh, vh = ref.dequant(pk, sg.n, w.D, p["group"], sg.dtype)
+            kh, vh = kh[0], vh[0]
+        else:
+            kh, vh = ref.widen(k_i, sg.dtype), ref.widen(v_i, sg.dtype)
+            if p["kind"] == "evict":
+                pres[:] = 0
+                pres[np.linspace(0, sg.n - 1, p["k"]).astype(np.int64)] = 1
+        comp["khat"].append(kh)
+        comp["vhat"].append(vh)
+        comp["present"].append(pres)
+    q = gen.queries(w, gen.T_QPRE, w.M, bh0=0, nbh=w.group_size, step=1)[:, ::stride]
+    t0 = time.perf_counter()
+    op.attend_head(w, comp, q, w.q_dtype)
+    t = time.perf_counter() - t0
+    rows = q.shape[1]
+    ms = t * (w.M / rows) * (w.B * w.Hkv) * 1e3
+    return {"value": round(ms, 1), "unit": "ms per step", "cores": int(cores), "kind": "oracle",
+            "cpu": cpu_model(),
+            "sample": (f"KV head (0, 0): {rows} of {w.M} query rows of each of its "
+                       f"{w.group_size} query heads over all {w.n_context} context rows "
+                       f"({t:.2f} s), extrapolated linearly to all rows and "
+                       f"{w.B * w.Hkv} KV heads")}
 
 
 def prefill_bench(args):
@@ -415,7 +473,9 @@ def prefill_bench(args):
                       "kernel_ms": round(t_k, 4),
                       "kernel_frac_of_bf16_peak": round(fl / t_k / 1e9 / BF16_PEAK_TFLOPS, 4),
                       "gflop_per_step": round(fl / 1e9, 1), "attended_rows": n_att,
-                      "compress_ms": round(t_c, 3), "steps": n}), flush=True)
+                      "compress_ms": round(t_c, 3), "steps": n,
+                      "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)}),
+          flush=True)
     del run, inp, qs, o
     torch.cuda.empty_cache()
     # text-to-image: widths from the first (dense) step, then requantise + attend
@@ -438,7 +498,9 @@ def prefill_bench(args):
                       "kernel_frac_of_bf16_peak": round(fl / t_k / 1e9 / BF16_PEAK_TFLOPS, 4),
                       "gflop_per_step": round(fl / 1e9, 1), "attended_rows": w.n_context,
                       "step_with_requantise_ms": round(t_s, 4), "bits": run.bits[:8],
-                      "steps": n}), flush=True)
+                      "steps": n,
+                      "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)}),
+          flush=True)
 
 
 def _clone_segment(seg):
