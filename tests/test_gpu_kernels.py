@@ -69,6 +69,50 @@ def test_quantize_bit_exact(case):
         assert np.array_equal(host_bytes(seg.t["tail_v"]).reshape(pk["tail_v"].shape), pk["tail_v"])
 
 
+def test_quantize_constant_and_ramp_groups():
+    """Groups whose values are constant (scale 0: codes 0, minimum = the
+    value) and exact ramps 0..15 (scale 1, minimum 0: code = value), through
+    the vectorised kernels (bf16, head dim 128, group 64, 4 bits), plus a
+    residual tail; bit-exact against the oracle and against the closed forms."""
+    _print_case(test="quantize_constant_ramp")
+    B, Hkv, D, G, N = 1, 2, 128, 64, 128 + 5
+    BH = B * Hkv
+    r = np.arange(N, dtype=np.float64)[None, :, None]
+    c = np.arange(D, dtype=np.float64)[None, None, :]
+    k = np.where(r < G, np.broadcast_to(c / 8.0, (BH, N, D)), np.broadcast_to(r % 16, (BH, N, D)))
+    v = np.where(c < G, np.broadcast_to(r / 4.0, (BH, N, D)), np.broadcast_to(c % 16, (BH, N, D)))
+    k = gen.round_to(np.ascontiguousarray(k), "bf16")
+    v = gen.round_to(np.ascontiguousarray(v), "bf16")
+    pk = ref.quantize(k, v, "bf16", G, [4] * BH)
+    seg = uc.packed_segment(B, Hkv, N, D, G, torch.bfloat16, bits=4)
+    shape = uc.make_shape(B, Hkv, Hkv, D)
+    uc.uc_quantize_segment(shape, dev(k, "bf16").reshape(B, Hkv, N, D),
+                           dev(v, "bf16").reshape(B, Hkv, N, D), N, seg)
+    torch.cuda.synchronize()
+    n = pk["codes_k"].shape[0]
+    ck = seg.t["codes_k"].cpu().numpy()[:n]
+    cv = seg.t["codes_v"].cpu().numpy()[:n]
+    assert np.array_equal(ck, pk["codes_k"]) and np.array_equal(cv, pk["codes_v"])
+    for name in ("scale_k", "min_k", "scale_v", "min_v"):
+        got = seg.t[name].cpu().numpy().reshape(pk[name].shape)
+        assert np.array_equal(got.view(np.uint32), pk[name].view(np.uint32)), name
+    sk = seg.t["scale_k"].cpu().numpy().reshape(BH, N // G, D)
+    mk = seg.t["min_k"].cpu().numpy().reshape(BH, N // G, D)
+    assert np.all(sk[:, 0] == 0.0) and np.array_equal(mk[:, 0], np.broadcast_to(np.arange(D) / 8.0, (BH, D)))
+    assert np.all(sk[:, 1] == 1.0) and np.all(mk[:, 1] == 0.0)
+    sv = seg.t["scale_v"].cpu().numpy().reshape(BH, N // G * G, D // G)
+    assert np.all(sv[:, :, 0] == 0.0) and np.all(sv[:, :, 1] == 1.0)
+    codes = ck.reshape(BH, N // G * G, D // 2)    # 4-bit codes, two channels per byte
+    lo, hi = codes & 15, codes >> 4
+    assert np.all(lo[:, :G] == 0) and np.all(hi[:, :G] == 0)          # constant key groups
+    rows = np.arange(G, 2 * G) % 16
+    assert np.all(lo[:, G:2 * G] == rows[None, :, None]) and np.all(hi[:, G:2 * G] == rows[None, :, None])
+    vcodes = cv.reshape(BH, N // G * G, D // 2)
+    want_v = np.arange(D)[G:] % 16
+    assert np.all((vcodes[:, :, G // 2:] & 15) == want_v[0::2]) and np.all((vcodes[:, :, G // 2:] >> 4) == want_v[1::2])
+    assert np.all(vcodes[:, :, : G // 2] == 0)
+
+
 # ------------------------------------------------------------------ select
 
 @pytest.mark.parametrize("N,k,nr", [(1, 1, 0), (100, 37, 0), (100, 37, 5), (4099, 1024, 0),
@@ -81,6 +125,8 @@ def test_select_bit_exact(N, k, nr):
     s = rng.integers(0, 50, (BH, N)).astype(np.float32) / 13.0  # many exact ties
     s[0] = rng.random(N).astype(np.float32)
     s[1, : N // 2] = 0.0
+    s[2] = 1.0                                                    # all equal: lowest indices
+    s[3] = rng.choice(np.array([-1.5, -0.0, 0.0, 2.0], np.float32), N)  # signs, -0 ties +0
     want = ref.select(s, k, nr)
     sd = torch.from_numpy(s).cuda()
     keep = torch.full((BH, max(k, 1)), -7, dtype=torch.int32, device="cuda")
