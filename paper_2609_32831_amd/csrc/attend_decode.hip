@@ -626,6 +626,8 @@ __global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* _
                     Hkv, M, scale_log2, partial);
 }
 
+}  // namespace
+
 int device_cus() {
   static int cus = 0;
   if (!cus) {
@@ -638,6 +640,8 @@ int device_cus() {
   }
   return cus;
 }
+
+namespace {
 
 // workgroups per (b, h_kv): two resident workgroups per CU in one round
 int decode_w(const uc_shape& sh) {

@@ -32,11 +32,14 @@ namespace {
 
 using namespace mf;
 
-constexpr int WAVES = 4;
 constexpr int QTW = 2;                     // query tiles per wave
-constexpr int QROWS = WAVES * QTW * 16;    // query rows per workgroup
-constexpr int STAGES = 3;                  // key/value tiles staged in LDS
-constexpr int STAGEB = 2 * TILEB;          // K tile + V tile
+constexpr int STAGES = 3;                  // stages of 32-row tiles in LDS
+constexpr int SUBB = 2 * TILEB;            // one tile: K rows + V rows
+// Two layouts: W waves per workgroup and TPS tiles per stage (one barrier per
+// stage).  <4, 1>: 128 query rows, two workgroups per CU; <8, 2>: 256 query
+// rows, one workgroup per CU, half the barriers and staging per query row.
+template <int W>
+constexpr int qrows() { return W * QTW * 16; }
 constexpr float kLazy = 8.0f;
 constexpr float kLazyExp = 256.0f;  // 2^kLazy
 constexpr int kMaxViews = 2 * kMaxSeg;
@@ -103,30 +106,38 @@ struct Cursor {
   }
 };
 
-// one thread's share of staging a tile: rows tid/16 and tid/16 + 16, chunk tid%16
+// one thread's share of staging the two tiles of a stage: row tid/16,
+// chunk tid%16 of each tile's K and V rows
 struct Stage {
   u4 k[2], v[2];
 };
 
-// F16: V comes from the view's fp16 copy
-template <bool F16>
-__device__ inline void stage_load(const Cursor<F16>& cu, Stage& S) {
+// A thread stages two 16-byte chunks of K and of V per stage: chunk i is
+// global chunk g = tid + i * NT, tile g / 512 of the stage, row (g % 512) / 16,
+// column chunk g % 16 (two rows of one tile with 256 threads, one row of each
+// of two tiles with 512).  F16: V comes from the view's fp16 copy.
+template <bool F16, int NT>
+__device__ inline void stage_load(const Cursor<F16>& cu, Stage& S, int i) {
   const __amdgpu_buffer_rsrc_t rk = rsrc(cu.k, (uint32_t)cu.n * ROWB);
   const __amdgpu_buffer_rsrc_t rv = rsrc(cu.v, (uint32_t)cu.n * ROWB);
-  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+  const int g = (threadIdx.x + i * NT) & 511, r = g >> 4, c = g & 15;
   const int off = (cu.row0 + r) * ROWB + c * 16;
-  S.k[0] = bload(rk, off, 0);
-  S.k[1] = bload(rk, off, 16 * ROWB);
-  S.v[0] = bload(rv, off, 0);
-  S.v[1] = bload(rv, off, 16 * ROWB);
+  S.k[i] = bload(rk, off, 0);
+  S.v[i] = bload(rv, off, 0);
 }
 
-__device__ inline void stage_store(char* buf, const Stage& S) {
-  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
-  *reinterpret_cast<u4*>(buf + toff(r, c)) = S.k[0];
-  *reinterpret_cast<u4*>(buf + toff(r + 16, c)) = S.k[1];
-  *reinterpret_cast<u4*>(buf + TILEB + toff(r, c)) = S.v[0];
-  *reinterpret_cast<u4*>(buf + TILEB + toff(r + 16, c)) = S.v[1];
+// chunk i into the LDS tile at buf (K rows, V rows at + TILEB)
+template <int NT>
+__device__ inline void stage_store(char* buf, const Stage& S, int i) {
+  const int g = (threadIdx.x + i * NT) & 511, r = g >> 4, c = g & 15;
+  *reinterpret_cast<u4*>(buf + toff(r, c)) = S.k[i];
+  *reinterpret_cast<u4*>(buf + TILEB + toff(r, c)) = S.v[i];
+}
+
+// LDS tile of tile t of the sequence
+template <int TPS>
+__device__ inline char* tile_buf(char* lds, int t) {
+  return lds + ((t / TPS) % STAGES) * (TPS * SUBB) + (t % TPS) * SUBB;
 }
 
 // softmax of one query tile's 8 logits per lane; returns the probability
@@ -225,23 +236,30 @@ __device__ inline void tile_scores(const u4 (&ka)[8], const u4 (&qop)[QTW][4], f
 // tile t+1 run on the matrix cores (their K rows are in LDS one iteration
 // early: the three-deep ring holds tiles t, t+1 and the one being staged).
 // Returns the view of the last tile.
-template <bool F16>
+template <bool F16, int W, int TPS>
 __device__ __attribute__((always_inline)) inline int tile_loop(
     const Views& vs, int bh, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW],
     float scale_log2, int r_wave, int nq, int64_t qbase, int nseg, float* seg_lse, int i16,
     int g4) {
   int cur_view = -1, cur_seg = -1;
   const int T = vs.tiles;
-  Cursor<F16> ct, cs;  // tile t (computed) and tile t + 2 (staged)
+  // tiles go through LDS in stages of TPS: stage j holds tiles TPS*j ..
+  // TPS*j + TPS - 1; during stage j the tiles of stage j + 2 are loaded and,
+  // after its last tile, stored, and one barrier per stage publishes them
+  constexpr int NT = W * 64;
+  Cursor<F16> ct, cs;  // tile t (computed) and the next tile to stage
   {
     Stage S;
     ct.start(vs, bh, 0);
-    stage_load<F16>(ct, S);
-    stage_store(lds, S);
-    if (T > 1) {
-      cs.start(vs, bh, 1);
-      stage_load<F16>(cs, S);
-      stage_store(lds + STAGEB, S);
+    cs.start(vs, bh, 0);
+    for (int u = 0; u < 2 * TPS && u < T; ++u) {
+      // the chunks of tile u (both with one tile per stage)
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        if (TPS == 1 || i == 0) stage_load<F16, NT>(cs, S, i);
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+        if (TPS == 1 || i == 0) stage_store<NT>(tile_buf<TPS>(lds, u), S, i);
       cs.next(vs, bh);
     }
   }
@@ -249,17 +267,30 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
   f4 sc[QTW][2];
   {
     u4 ka[8];
-    load_ka(lds, i16, g4, ka);
+    load_ka(tile_buf<TPS>(lds, 0), i16, g4, ka);
     tile_scores(ka, qop, sc);
   }
+  Stage S;
+  int n_pre = 0;  // tiles of the stage in flight
   for (int t = 0; t < T; ++t) {
-    Stage S;
-    const bool pre = t + 2 < T;
-    if (pre) {
-      stage_load<F16>(cs, S);
-      cs.next(vs, bh);
+    if (t % TPS == 0 && t + 2 * TPS < T) {  // the tiles of stage t/TPS + 2
+      if (TPS == 1) {
+        stage_load<F16, NT>(cs, S, 0);
+        stage_load<F16, NT>(cs, S, 1);
+        cs.next(vs, bh);
+        n_pre = 1;
+      } else {
+        stage_load<F16, NT>(cs, S, 0);
+        cs.next(vs, bh);
+        n_pre = 1;
+        if (t + 2 * TPS + 1 < T) {
+          stage_load<F16, NT>(cs, S, 1);
+          cs.next(vs, bh);
+          n_pre = 2;
+        }
+      }
     }
-    const char* lv = lds + (t % STAGES) * STAGEB + TILEB;
+    const char* lv = tile_buf<TPS>(lds, t) + TILEB;
     const int vi = ct.vi;
     const int n_valid = min(TILE, ct.n - ct.row0);
     if (seg_lse && vi != cur_view && cur_view >= 0 && ct.seg != cur_seg) {
@@ -281,10 +312,11 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
 #pragma unroll
     for (int qt = 0; qt < QTW; ++qt)
       tile_softmax<F16>(st[qt], sc[qt][0], sc[qt][1], scale_log2, n_valid, g4, phi[qt], plo[qt]);
-    // scores of the next tile (past the last tile: a stale buffer, unused)
+    // scores of the next tile (its stage is published; past the last tile:
+    // a stale buffer, unused)
     {
       u4 ka[8];
-      load_ka(lds + ((t + 1) % STAGES) * STAGEB, i16, g4, ka);
+      load_ka(tile_buf<TPS>(lds, t + 1), i16, g4, ka);
       tile_scores(ka, qop, sc);
     }
 #pragma unroll
@@ -300,20 +332,33 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
         }
       }
     }
-    if (pre) stage_store(lds + ((t + 2) % STAGES) * STAGEB, S);
-    __syncthreads();
+    if (t % TPS == TPS - 1 || t == T - 1) {  // the stage's last tile
+      const int t0 = t - t % TPS + 2 * TPS;  // first tile of the staged stage
+      if (TPS == 1) {
+        if (n_pre) {
+          stage_store<NT>(tile_buf<TPS>(lds, t0), S, 0);
+          stage_store<NT>(tile_buf<TPS>(lds, t0), S, 1);
+        }
+      } else {
+        if (n_pre >= 1) stage_store<NT>(tile_buf<TPS>(lds, t0), S, 0);
+        if (n_pre >= 2) stage_store<NT>(tile_buf<TPS>(lds, t0 + 1), S, 1);
+      }
+      n_pre = 0;
+      __syncthreads();
+    }
   }
   return cur_view;
 }
 
-__global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const uint16_t* __restrict__ q,
+template <int W, int TPS>
+__global__ __launch_bounds__(W * 64, W == 4 ? 2 : 1) void prefill_mfma_kernel(Views vs, const uint16_t* __restrict__ q,
                                                               int Hq, int Hkv, int M, int nseg,
                                                               int n_qblocks, int n_work,
                                                               float scale_log2, float* __restrict__ o,
                                                               float* __restrict__ lse,
                                                               float* __restrict__ seg_lse,
                                                               const int* __restrict__ v_unsafe) {
-  __shared__ __attribute__((aligned(16))) char lds[STAGES * STAGEB];
+  __shared__ __attribute__((aligned(16))) char lds[STAGES * TPS * SUBB];
   // XCD-aware work mapping: consecutive work items (the query blocks of one
   // head, which share its K/V rows) go to the same XCD
   const int per_xcd = (n_work + 7) / 8;
@@ -324,7 +369,7 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const ui
   const int i16 = lane & 15, g4 = lane >> 4;
   const int G = Hq / Hkv, nq = G * M, b = bh / Hkv, hkv = bh % Hkv;
   const int64_t qbase = ((int64_t)b * Hq + hkv * G) * M;  // first query row of the head
-  const int r_wave = qb * QROWS + wave * QTW * 16;        // first row of the wave
+  const int r_wave = qb * qrows<W>() + wave * QTW * 16;   // first row of the wave
 
   u4 qop[QTW][4];
   QState st[QTW];
@@ -352,9 +397,9 @@ __global__ __launch_bounds__(256, 2) void prefill_mfma_kernel(Views vs, const ui
     }
   }
   const bool f16 = *v_unsafe == 0;
-  const int cur_view = f16 ? tile_loop<true>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
+  const int cur_view = f16 ? tile_loop<true, W, TPS>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
                                              nseg, seg_lse, i16, g4)
-                           : tile_loop<false>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
+                           : tile_loop<false, W, TPS>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
                                               nseg, seg_lse, i16, g4);
   // outputs
 #pragma unroll
@@ -532,13 +577,25 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const int nq = (sh.Hq / sh.Hkv) * M;
-  const int n_qblocks = (nq + QROWS - 1) / QROWS;
+  // the 8-wave layout (one workgroup per CU) when its grid fills every round
+  // or runs many rounds; otherwise the 4-wave one (two per CU), whose last
+  // round leaves fewer CUs idle
+  const int cus = device_cus();
+  const int n8 = (nq + qrows<8>() - 1) / qrows<8>() * BH;
+  const bool wide = n8 % cus == 0 || n8 >= 8 * cus;
+  const int W = wide ? 8 : 4, qr = wide ? qrows<8>() : qrows<4>();
+  const int n_qblocks = (nq + qr - 1) / qr;
   const int n_work = n_qblocks * BH;
   const int grid = (n_work + 7) / 8 * 8;
   if ((e = kernel_timer_begin(st)) != hipSuccess) return e;
-  hipLaunchKernelGGL(prefill_mfma_kernel, dim3(grid), dim3(256), 0, st, vs, (const uint16_t*)q,
-                     sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sm_scale * kLog2e, o, lse,
-                     seg_lse, v_unsafe);
+  if (wide)
+    hipLaunchKernelGGL((prefill_mfma_kernel<8, 2>), dim3(grid), dim3(W * 64), 0, st, vs,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work,
+                       sm_scale * kLog2e, o, lse, seg_lse, v_unsafe);
+  else
+    hipLaunchKernelGGL((prefill_mfma_kernel<4, 1>), dim3(grid), dim3(W * 64), 0, st, vs,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work,
+                       sm_scale * kLog2e, o, lse, seg_lse, v_unsafe);
   e = hipGetLastError();
   return e == hipSuccess ? kernel_timer_end(st) : e;
 }

@@ -11,6 +11,9 @@ namespace uc {
 
 constexpr int kMaxSeg = UC_MAX_SEGMENTS;
 
+// compute units of the current device (cached after the first call)
+int device_cus();
+
 // Kernel-side copy of one segment descriptor, passed by value in kernel
 // arguments.  Derived fields (n_full, tail_len, row_stride) are resolved on
 // the host.

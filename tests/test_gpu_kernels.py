@@ -409,6 +409,10 @@ PCASES = [
     (1, 28, 4, 3, 128, 8, False, (0, 100, 3, 130, 0, 4)),             # 21 rows, 8-bit, empty text
     (1, 16, 1, 2, 32, 4, False, (1, 64, 33, 520, 1, 1)),              # 32 rows, 16 heads per KV
     (1, 28, 4, 40, 64, 4, False, (0, 0, 0, 31, 0, 1)),                # tail-only packed rows
+    # 256 KV heads of one 252-row block: a grid of one workgroup per CU, so the
+    # eight-wave layout with two tiles per stage runs; 15 tiles (the last
+    # stage holds one), partial tiles in every view
+    (64, 28, 4, 36, 64, 4, False, (70, 300, 111, 200 + 17, 3, 8)),
 ]
 
 
