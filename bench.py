@@ -67,6 +67,10 @@ def parse():
                     help="decode kernel time on one copy of the compressed 64k cache vs "
                          "alternating between two copies (reuse distance above the 256 MB "
                          "last-level cache)")
+    ap.add_argument("--understanding", action="store_true",
+                    help="the 7B-shaped understanding workload (4 requests, 4608-row context, "
+                         "256 decode steps): whole job, and the decode steps issued one by one "
+                         "and replayed as one HIP graph (one JSON line)")
     ap.add_argument("--dynamic", action="store_true",
                     help="instead of the decode job: the editing workload under the dynamic "
                          "budget (Eq. 1-3), reporting the chunk-boundary overhead (one JSON line)")
@@ -573,6 +577,90 @@ def mall_check(args):
     evs.close()
 
 
+def understanding_bench(args):
+    """The 7B-shaped understanding workload: compression (scores of a 32-row
+    observation window over all 4608 context rows, the top 406 ViT rows per
+    KV head kept and gathered) and 256 decode steps, each appending its K/V to
+    the protected tail inside one fused attention launch plus the combine.
+    Each step reads about 8.65 MB, which stays in the 256 MB last-level cache,
+    so the steps are bound by launches and latency: they are timed issued one
+    by one (the whole job, as the 64k benchmark times it) and captured once as
+    a HIP graph of all 256 steps and replayed; every replay's outputs are
+    compared with the steps issued one by one."""
+    import torch
+
+    import paper_2609_32831_amd as uc
+    import workloads as gen
+    from paper_2609_32831_amd.runner import Run
+    from workloads.device import device_inputs
+
+    w = gen.UNDERSTANDING_7B
+    T = w.steps
+    inp = device_inputs(w, "cuda", steps=T)
+    run = Run(w, inp)
+    o = torch.empty(T, w.B, w.Hq, 1, w.D, device="cuda")
+
+    def steps():
+        for t in range(T):
+            uc.uc_attend_append(run.shape, run.mixed, len(run.mixed) - 1, inp["k_dec"][t],
+                                inp["v_dec"][t], 1, inp["q_dec"][t], 1, run.sm, o[t],
+                                ws=run.ws_attend)
+
+    def job():
+        run.compress()
+        steps()
+
+    stream = torch.cuda.current_stream()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+    for _ in range(max(1, args.warmup)):
+        job()
+    torch.cuda.synchronize()
+    n = max(1, args.steps)
+    job_ms, step_ms = 0.0, 0.0
+    for _ in range(n):
+        ev[0].record(stream)
+        run.compress()
+        ev[1].record(stream)
+        steps()
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        job_ms += ev[0].elapsed_time(ev[2])
+        step_ms += ev[1].elapsed_time(ev[2])
+    job_ms /= n
+    step_ms /= n
+    o_eager = o.clone()
+    # the same 256 steps as one graph: the tail restarts at row 0, and each
+    # replay appends and attends exactly as the steps above did
+    run.tail.n_rows = 0
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.graph(g, stream=side):
+        steps()
+    torch.cuda.synchronize()
+    graph_ms, ok = 0.0, True
+    for _ in range(n):
+        o.zero_()
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        g.replay()
+        ev[3].record(stream)
+        torch.cuda.synchronize()
+        graph_ms += ev[0].elapsed_time(ev[3])
+        ok = ok and bool(torch.equal(o, o_eager))
+    graph_ms /= n
+    nbytes = sum(run.attended_bytes(t + 1) for t in range(T)) / T
+    tokens = w.B * T
+    print(json.dumps({"metric": "understanding decode", "workload": w.name,
+                      "tokens_per_s": round(tokens / (job_ms / 1e3), 1), "ms_per_job": round(job_ms, 3),
+                      "compress_ms": round(job_ms - step_ms, 3),
+                      "decode_step_us": round(step_ms / T * 1e3, 2),
+                      "decode_step_us_graph": round(graph_ms / T * 1e3, 2),
+                      "decode_tokens_per_s_graph": round(tokens / (graph_ms / 1e3), 1),
+                      "bytes_per_step": int(nbytes), "graph_matches_steps": ok, "jobs": n}),
+          flush=True)
+
+
 def dynamic_bench(args):
     """The editing workload under the dynamic budget (Sec. 3.3 Eq. 1-3): per
     request, timestep 0 on the full cache plus the initial compression, then
@@ -764,6 +852,11 @@ def main():
         if args.gpus != 1:
             sys.exit(2)
         mall_check(args)
+        return
+    if args.understanding:
+        if args.gpus != 1:
+            sys.exit(2)
+        understanding_bench(args)
         return
     if args.batch:
         if args.gpus != 1:
