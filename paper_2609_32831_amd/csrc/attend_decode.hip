@@ -679,6 +679,13 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   DecodePlan p{};
   const AppendOp none{};
   p.W = decode_w(sh);
+  {
+    // at least one 32-row tile per wave (four per workgroup): a short
+    // context gets fewer workgroups, and the merge fewer records per row
+    int tiles = ap && ap->n_new > 0 ? 1 : 0;
+    for (int i = 0; i < segs.n; ++i) tiles += (segs.s[i].n_rows + TILE - 1) / TILE;
+    p.W = max(1, min(p.W, (tiles + WAVES - 1) / WAVES));
+  }
   p.n_seg = segs.n;
   p.per_seg = seg_lse != nullptr;
   // split the largest dense segment around the others when packed rows are
