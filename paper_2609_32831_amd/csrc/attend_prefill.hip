@@ -424,7 +424,9 @@ __global__ __launch_bounds__(W * 64, W == 4 ? 2 : 1) void prefill_mfma_kernel(Vi
 
 // codes -> bf16 values of one packed segment's whole row groups:
 // out[b, h, r, c] = round_to_bf16(fmaf(code, scale, min)); one thread per
-// 8 channels of one row, K and V
+// 8 channels of one row, K and V: the 8 codes in one 16-, 32- or 64-bit load,
+// the key scales and minima in 16-byte loads, one value group (groups are at
+// least 8 channels)
 __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
                                uint16_t* __restrict__ vout, uint16_t* __restrict__ vhout,
                                int* __restrict__ v_unsafe) {
@@ -436,33 +438,42 @@ __global__ void dequant_kernel(KSeg s, int BH, uint16_t* __restrict__ kout,
   int bits;
   int64_t off;
   u4 ko, vo;
-  if (!head_codes(s, bh, D, bits, off)) {
+  if (!head_codes(s, bh, D, bits, off) || (off & 15)) {
     const uint32_t nan2 = 0x7FC07FC0u;
     ko = u4{nan2, nan2, nan2, nan2};
     vo = ko;
   } else {
     const int rb = D * bits / 8, G = s.group;
-    const uint8_t* ck = s.codes_k + off + (int64_t)r * rb + c8 * bits;  // 8 channels = bits bytes
-    const uint8_t* cv = s.codes_v + off + (int64_t)r * rb + c8 * bits;
-    uint64_t wk = 0, wv = 0;
-    for (int i = 0; i < bits; ++i) {
-      wk |= (uint64_t)ck[i] << (8 * i);
-      wv |= (uint64_t)cv[i] << (8 * i);
+    const int64_t cb = off + (int64_t)r * rb + c8 * bits;  // 8 channels = bits bytes
+    uint64_t wk, wv;
+    if (bits == 4) {
+      wk = *reinterpret_cast<const uint32_t*>(s.codes_k + cb);
+      wv = *reinterpret_cast<const uint32_t*>(s.codes_v + cb);
+    } else if (bits == 2) {
+      wk = *reinterpret_cast<const uint16_t*>(s.codes_k + cb);
+      wv = *reinterpret_cast<const uint16_t*>(s.codes_v + cb);
+    } else {
+      wk = *reinterpret_cast<const uint64_t*>(s.codes_k + cb);
+      wv = *reinterpret_cast<const uint64_t*>(s.codes_v + cb);
     }
     const int mask = (1 << bits) - 1;
-    const float* sk = s.scale_k + ((int64_t)bh * s.kgroups + r / G) * D + c8 * 8;
-    const float* mk = s.min_k + ((int64_t)bh * s.kgroups + r / G) * D + c8 * 8;
-    // value groups: G consecutive channels of the row (G may be below 8)
-    const int64_t vrow = ((int64_t)bh * s.cap_full + r) * (D / G);
+    const int64_t kg = ((int64_t)bh * s.kgroups + r / G) * D + c8 * 8;
+    const f4 sk0 = *reinterpret_cast<const f4*>(s.scale_k + kg);
+    const f4 sk1 = *reinterpret_cast<const f4*>(s.scale_k + kg + 4);
+    const f4 mk0 = *reinterpret_cast<const f4*>(s.min_k + kg);
+    const f4 mk1 = *reinterpret_cast<const f4*>(s.min_k + kg + 4);
+    const float sk[8] = {sk0[0], sk0[1], sk0[2], sk0[3], sk1[0], sk1[1], sk1[2], sk1[3]};
+    const float mk[8] = {mk0[0], mk0[1], mk0[2], mk0[3], mk1[0], mk1[1], mk1[2], mk1[3]};
+    const int64_t vi = ((int64_t)bh * s.cap_full + r) * (D / G) + (c8 * 8) / G;
+    const float sv = s.scale_v[vi], mv = s.min_v[vi];
     uint32_t kw[4], vw[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int c0 = 2 * j, c1 = 2 * j + 1;
-      const int64_t v0i = vrow + (c8 * 8 + c0) / G, v1i = vrow + (c8 * 8 + c1) / G;
       const float k0 = fmaf((float)((wk >> (c0 * bits)) & mask), sk[c0], mk[c0]);
       const float k1 = fmaf((float)((wk >> (c1 * bits)) & mask), sk[c1], mk[c1]);
-      const float v0 = fmaf((float)((wv >> (c0 * bits)) & mask), s.scale_v[v0i], s.min_v[v0i]);
-      const float v1 = fmaf((float)((wv >> (c1 * bits)) & mask), s.scale_v[v1i], s.min_v[v1i]);
+      const float v0 = fmaf((float)((wv >> (c0 * bits)) & mask), sv, mv);
+      const float v1 = fmaf((float)((wv >> (c1 * bits)) & mask), sv, mv);
       kw[j] = bf2(k0, k1);
       vw[j] = bf2(v0, v1);
     }
