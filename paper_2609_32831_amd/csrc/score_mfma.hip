@@ -99,22 +99,120 @@ __device__ inline int chunk_rows(const ChunkPlan& p, const KSegs& segs, int c, i
   return si;
 }
 
-// base-2 logits of one lane: 8 keys (tile rows g4*4 + j and 16 + g4*4 + j),
-// keys at or past r1 masked out
-__device__ inline void logits(const f4& s0, const f4& s1, float scale_log2, int row0, int r1,
-                              int g4, float (&x)[8]) {
-  if (row0 + TILE <= r1) {
+// raw logits of one lane for one key tile: 8 keys (tile rows g4*4 + j and
+// 16 + g4*4 + j); with MASK, keys at or past r1 are -inf
+template <bool MASK>
+__device__ inline void logits(const f4& s0, const f4& s1, int row0, int r1, int g4, float* x) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      x[j] = s0[j] * scale_log2;
-      x[4 + j] = s1[j] * scale_log2;
-    }
-  } else {
+  for (int j = 0; j < 4; ++j) {
+    x[j] = !MASK || row0 + g4 * 4 + j < r1 ? s0[j] : -INFINITY;
+    x[4 + j] = !MASK || row0 + 16 + g4 * 4 + j < r1 ? s1[j] : -INFINITY;
+  }
+}
+
+// Pass 1 on two key tiles (16 keys of the lane's query column): the lane's
+// running (m, l) over base-2 logits, re-referenced to the maximum so far, so
+// every v_exp_f32 argument is <= 0 (probabilities below 2^-126 of the
+// reference flush to zero).  A lane with no valid key yet keeps m = -inf and
+// l = 0.
+template <bool MASK>
+__device__ inline void lse_half(const f4 (&s)[2][2], int row0a, int row0b, int r1, int g4,
+                                float scale_log2, float& m, float& l) {
+  float x[16];
+  logits<MASK>(s[0][0], s[0][1], row0a, r1, g4, x);
+  logits<MASK>(s[1][0], s[1][1], row0b, r1, g4, x + 8);
+  float mx[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      x[j] = row0 + g4 * 4 + j < r1 ? s0[j] * scale_log2 : -INFINITY;
-      x[4 + j] = row0 + 16 + g4 * 4 + j < r1 ? s1[j] * scale_log2 : -INFINITY;
+  for (int j = 0; j < 4; ++j) mx[j] = fmaxf(fmaxf(x[j], x[4 + j]), fmaxf(x[8 + j], x[12 + j]));
+  // the scale is positive: the maximum of the raw logits gives it
+  const float mn = fmaxf(m, fmaxf(fmaxf(mx[0], mx[1]), fmaxf(mx[2], mx[3])) * scale_log2);
+  const float ref = mn == -INFINITY ? 0.0f : mn;
+  float e[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int j = 0; j < 16; ++j) e[j & 3] += __builtin_amdgcn_exp2f(fmaf(x[j], scale_log2, -ref));
+  l = fmaf(l, __builtin_amdgcn_exp2f(m - ref), (e[0] + e[1]) + (e[2] + e[3]));
+  m = mn;
+}
+
+// Pass 2 on two key tiles: p = exp2(s - lse) added to the lanes' column sums
+// (p <= 1 since s <= lse; probabilities below 2^-126 flush to zero)
+__device__ inline void col_half(const f4 (&s)[2][2], float lq, float scale_log2, float (&c0)[8],
+                                float (&c1)[8]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    c0[j] += __builtin_amdgcn_exp2f(fmaf(s[0][0][j], scale_log2, -lq));
+    c0[4 + j] += __builtin_amdgcn_exp2f(fmaf(s[0][1][j], scale_log2, -lq));
+    c1[j] += __builtin_amdgcn_exp2f(fmaf(s[1][0][j], scale_log2, -lq));
+    c1[4 + j] += __builtin_amdgcn_exp2f(fmaf(s[1][1][j], scale_log2, -lq));
+  }
+}
+
+static_assert(TPW == 4, "the sub-chunk loops take a wave's key tiles in two pairs");
+
+// One sub-chunk of pass 1 for one wave.  The loop over query tiles keeps the
+// matrix cores and the vector ALUs busy together: while the exponentials of
+// one pair of key tiles run, the scores of the next pair are computed (the
+// pair (2, 3) of query tile t, then the pair (0, 1) of tile t + 1).  The
+// loop body has no branch, so the compiler can interleave the two.  rm / rl
+// hold the wave's (m, l) per query row; the four key-row lanes of a query
+// column agree after the merge and all store it.
+template <bool MASK>
+__device__ inline void lse_sub(const KTiles& K, const char* qs, float* rm, float* rl, int nqt,
+                               int sc, int r1, int wave, int lane, float scale_log2) {
+  const int i16 = lane & 15, g4 = lane >> 4;
+  int row[TPW];
+#pragma unroll
+  for (int i = 0; i < TPW; ++i) row[i] = sc + (wave + i * WAVES) * TILE;
+  u4 qb[4];
+  f4 sa[2][2], sb[2][2];
+  q_tile(qs, 0, lane, qb);
+  s_tile(K.k[0], qb, sa[0][0], sa[0][1]);
+  s_tile(K.k[1], qb, sa[1][0], sa[1][1]);
+  for (int t = 0; t < nqt; ++t) {
+    // the wave's state so far enters through one of the four key-row lanes
+    float m = rm[t * 16 + i16], l = rl[t * 16 + i16];
+    m = g4 == 0 ? m : -INFINITY;
+    l = g4 == 0 ? l : 0.0f;
+    s_tile(K.k[2], qb, sb[0][0], sb[0][1]);
+    s_tile(K.k[3], qb, sb[1][0], sb[1][1]);
+    lse_half<MASK>(sa, row[0], row[1], r1, g4, scale_log2, m, l);
+    q_tile(qs, t + 1 < nqt ? t + 1 : t, lane, qb);  // the last round's pair is unused
+    s_tile(K.k[0], qb, sa[0][0], sa[0][1]);
+    s_tile(K.k[1], qb, sa[1][0], sa[1][1]);
+    lse_half<MASK>(sb, row[2], row[3], r1, g4, scale_log2, m, l);
+    // merge the four key-row lanes (g4) of each query column
+#pragma unroll
+    for (int o = 16; o <= 32; o <<= 1) {
+      const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(l, o, 64);
+      const float mn = fmaxf(m, m2);
+      const float ref = mn == -INFINITY ? 0.0f : mn;
+      l = fmaf(l, __builtin_amdgcn_exp2f(m - ref), l2 * __builtin_amdgcn_exp2f(m2 - ref));
+      m = mn;
     }
+    rm[t * 16 + i16] = m;
+    rl[t * 16 + i16] = l;
+  }
+}
+
+// One sub-chunk of pass 2 for one wave, pipelined like pass 1.  Tiles past
+// r1 read zero rows; their sums land in column slots nobody reads.
+__device__ inline void col_sub(const KTiles& K, const char* qs, const float* ls, int nqt,
+                               int lane, float scale_log2, float (&cs)[TPW][8]) {
+  const int i16 = lane & 15;
+  u4 qb[4];
+  f4 sa[2][2], sb[2][2];
+  q_tile(qs, 0, lane, qb);
+  s_tile(K.k[0], qb, sa[0][0], sa[0][1]);
+  s_tile(K.k[1], qb, sa[1][0], sa[1][1]);
+  for (int t = 0; t < nqt; ++t) {
+    const float lq = ls[t * 16 + i16];
+    s_tile(K.k[2], qb, sb[0][0], sb[0][1]);
+    s_tile(K.k[3], qb, sb[1][0], sb[1][1]);
+    col_half(sa, lq, scale_log2, cs[0], cs[1]);
+    q_tile(qs, t + 1 < nqt ? t + 1 : t, lane, qb);  // the last round's pair is unused
+    s_tile(K.k[0], qb, sa[0][0], sa[0][1]);
+    s_tile(K.k[1], qb, sa[1][0], sa[1][1]);
+    col_half(sb, lq, scale_log2, cs[2], cs[3]);
   }
 }
 
@@ -128,7 +226,6 @@ __global__ __launch_bounds__(256, 2) void score_lse_kernel(KSegs segs, ChunkPlan
   __shared__ float red_m[WAVES][QB], red_l[WAVES][QB];
   const int c = blockIdx.x, qb = blockIdx.y, bh = blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i16 = lane & 15, g4 = lane >> 4;
   const int G = Hq / Hkv, nq = G * W, b = bh / Hkv, hkv = bh % Hkv;
   int r0, r1;
   const int si = chunk_rows(plan, segs, c, r0, r1);
@@ -150,51 +247,10 @@ __global__ __launch_bounds__(256, 2) void score_lse_kernel(KSegs segs, ChunkPlan
     KTiles K;
 #pragma unroll
     for (int i = 0; i < TPW; ++i) k_issue(rk, sc + (wave + i * WAVES) * TILE, lane, K.k[i]);
-    for (int t = 0; t < nqt; ++t) {
-      // the wave's state so far enters through one of the four key-row lanes
-      float m = g4 == 0 ? red_m[wave][t * 16 + i16] : -INFINITY;
-      float l = g4 == 0 ? red_l[wave][t * 16 + i16] : 0.0f;
-      u4 qb[4];
-      q_tile(qs, t, lane, qb);
-#pragma unroll
-      for (int i = 0; i < TPW; ++i) {
-        const int row0 = sc + (wave + i * WAVES) * TILE;
-        if (row0 < r1) {
-          f4 s0, s1;
-          s_tile(K.k[i], qb, s0, s1);
-          float x[8];
-          logits(s0, s1, 1.0f, row0, r1, g4, x);  // raw logits (masked)
-          // the scale is positive: the maximum of the raw logits gives it
-          const float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
-                                 fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7]))) * scale_log2;
-          if (mx > m + kLazy) {  // per-lane state: raise the reference maximum
-            l *= __builtin_amdgcn_exp2f(m - mx);
-            m = mx;
-          }
-          // arguments are at most kLazy, so v_exp_f32 needs no range
-          // reduction; probabilities below 2^-126 of the reference flush
-          float e = 0.0f;
-#pragma unroll
-          for (int j = 0; j < 8; ++j) e += __builtin_amdgcn_exp2f(fmaf(x[j], scale_log2, -m));
-          // a lane whose keys are all past the range before any valid key
-          // keeps m = -inf and no sum
-          if (m != -INFINITY) l += e;
-        }
-      }
-      // merge the four key-row lanes (g4) of each query column
-#pragma unroll
-      for (int o = 16; o <= 32; o <<= 1) {
-        const float m2 = __shfl_xor(m, o, 64), l2 = __shfl_xor(l, o, 64);
-        const float mn = fmaxf(m, m2);
-        l = (m == -INFINITY ? 0.0f : l * exp2f(m - mn)) +
-            (m2 == -INFINITY ? 0.0f : l2 * exp2f(m2 - mn));
-        m = mn;
-      }
-      if (g4 == 0) {  // the four lanes now agree; one keeps the wave's state
-        red_m[wave][t * 16 + i16] = m;
-        red_l[wave][t * 16 + i16] = l;
-      }
-    }
+    if (sc + SUB <= r1)
+      lse_sub<false>(K, qs, red_m[wave], red_l[wave], nqt, sc, r1, wave, lane, scale_log2);
+    else
+      lse_sub<true>(K, qs, red_m[wave], red_l[wave], nqt, sc, r1, wave, lane, scale_log2);
   }
   __syncthreads();
   const int C = plan.n_chunks;
@@ -263,24 +319,7 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
       for (int i = 0; i < TPW; ++i)
 #pragma unroll
         for (int j = 0; j < 8; ++j) cs[i][j] = 0.0f;
-      for (int t = 0; t < nqt; ++t) {
-        const float lq = ls[t * 16 + i16];
-        u4 qb[4];
-        q_tile(qs, t, lane, qb);
-#pragma unroll
-        for (int i = 0; i < TPW; ++i) {
-          if (sc + (wave + i * WAVES) * TILE < r1) {
-            f4 s0, s1;
-            s_tile(K.k[i], qb, s0, s1);
-            // p <= 1 (s <= lse); probabilities below 2^-126 flush to zero
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              cs[i][j] += __builtin_amdgcn_exp2f(fmaf(s0[j], scale_log2, -lq));
-              cs[i][4 + j] += __builtin_amdgcn_exp2f(fmaf(s1[j], scale_log2, -lq));
-            }
-          }
-        }
-      }
+      col_sub(K, qs, ls, nqt, lane, scale_log2, cs);
       // sum the 16 query columns (lanes i16), then add to the chunk's sums
 #pragma unroll
       for (int i = 0; i < TPW; ++i) {
