@@ -446,6 +446,12 @@ uc_status uc_set_kernel_events(void* start, void* stop);
 const char* uc_status_string(uc_status s);
 /* Thread-local description of the calling thread's last error ("" if none). */
 const char* uc_last_error(void);
+/* Name of the main kernel the calling thread's last successful launch of
+ * uc_attend_mixed, uc_attend_append, uc_attend_batch or uc_score_importance
+ * ran ("decode_mfma", "decode_mfma_append", "prefill_mfma", "attend_valu",
+ * "decode_batch", "score_mfma", "score_valu"; "" before any).  Lets tests
+ * assert the path a case reaches; static storage, never freed. */
+const char* uc_last_kernel(void);
 
 #ifdef __cplusplus
 }

@@ -140,9 +140,10 @@ def denoise_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None
     mass order within the batch element's storage budget.
 
     steps: timesteps whose attention is returned (rows: optional query rows
-    of every query head, default all).  bits_given[t]: widths decided at step
-    t to use instead of the oracle's own decision (for runs where only sampled
-    rows can be attended and the full masses are not computed).
+    of every query head, default all).  The masses of a rescoring step always
+    cover all M query rows.  bits_given[t]: widths decided at step t to use
+    instead of the oracle's own decision (then that step's masses are not
+    computed).
     Returns {"bits": {t: widths}, "mass": {t: [Hkv] latent masses},
     "att": {t: (o, lse, seg_lse) per KV head}, "packed": {t: quantised latent
     per KV head (steps with widths in force)}}."""
@@ -180,7 +181,7 @@ def denoise_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None
                 bits = list(bits_given[t])
             continue
         need_mass = rescore and (bits_given is None or t not in bits_given)
-        att, mass = [], []
+        att, heads = [], []
         for h in range(Hkv):
             ks, vs = [], []
             for i, s in enumerate(w.segments):
@@ -197,21 +198,25 @@ def denoise_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None
                     kh, vh = dequant(pk, N, D, Gq, s.dtype)
                     ks.append(kh[0])
                     vs.append(vh[0])
-            K = np.concatenate(ks)[None, None]
-            V = np.concatenate(vs)[None, None]
+            heads.append((np.concatenate(ks), np.concatenate(vs)))
+            if t not in steps:
+                continue
+            K, V = heads[h][0][None, None], heads[h][1][None, None]
             qh = widen(q[h * G:(h + 1) * G], w.q_dtype)          # [G, M, D]
-            if need_mass or rows is None:
-                o, lse, sl, smass = attend(qh[None], K, V, None, seg_id, nseg, sm)
-                mass.append(float(smass[0, :, :, lat].sum()))  # over the G heads and M rows
-                if rows is not None:
-                    o, lse, sl = o[:, :, rows], lse[:, :, rows], sl[:, :, rows]
-            else:
-                o, lse, sl, _ = attend(qh[:, rows][None], K, V, None, seg_id, nseg, sm)
+            if rows is not None:
+                qh = qh[:, rows]
+            o, lse, sl, _ = attend(qh[None], K, V, None, seg_id, nseg, sm)
             att.append((o[0], lse[0], sl[0]))
         if t in steps:
             out["att"][t] = att
         if rescore:
             if need_mass:
+                # Eq. 1 bracket per KV head: probability on the latent rows,
+                # summed over the head's G query heads and all M query rows
+                # (one scorer call over every head of the batch element)
+                Kall = np.stack([k for k, _ in heads])[None]    # [1, Hkv, N, D]
+                _, ms = score64(widen(q, w.q_dtype)[None], Kall, seg_id, nseg, sm)
+                mass = ms[0, :, lat]
                 out["mass"][t] = np.asarray(mass, np.float64)
                 bits = [int(x) for x in assign_bits(mass, N, D, Gq, ls.dtype, budget_b, fixed_b)]
             else:
@@ -236,7 +241,7 @@ def stored(x: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
-                 given: Optional[Dict[int, Dict]] = None) -> Dict:
+                 given: Optional[Dict[int, Dict]] = None, first_masses: bool = False) -> Dict:
     """Oracle chain of the dynamic budget (Sec. 3.3 Eq. 1-3, Sec. 3.4) for one
     request (batch element b, its Hkv KV heads and Hq query heads) of a
     prefill workload with fresh queries per timestep.
@@ -267,7 +272,9 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
 
     steps: timesteps whose attention is returned.  rows: query rows to attend
     at those steps (then no masses are computed and every boundary's
-    decisions must be given).  given[t]: decisions of boundary t to apply
+    decisions must be given; with first_masses the full-KV step's masses and
+    scores are still computed over all query rows, so boundary 0 records the
+    oracle's own decision).  given[t]: decisions of boundary t to apply
     instead of the oracle's own: "k", "cfg" and optionally "keep" (kept
     positions per head); the oracle's own decision from the same state is
     still recorded (decisions[t]["own"]) when the masses are known.
@@ -310,6 +317,9 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
         """Scores of the evicting type's present rows, per head, from the
         softmax of q_obs over the present rows of the whole cache."""
         K, _, present = logical()
+        if state["keep"] is None:  # every row present: one scorer call for all heads
+            s64, _ = score64(widen(q_obs, w.q_dtype)[None], K[None], seg_id, nseg, sm)
+            return [s64[0, h][seg_id == ev] for h in range(Hkv)]
         sc = []
         for h in range(Hkv):
             idx = np.nonzero(present[h])[0]
@@ -318,7 +328,7 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
             sc.append(s64[0, 0][seg_id[idx] == ev])
         return sc
 
-    def decide(t, m, b_prev, rho, q_obs):
+    def decide(t, m, b_prev, rho, q_obs, pre=None):
         """Boundary t: the oracle's own decision (when masses are known) and
         the decision applied (the given one, if any, else its own)."""
         g = given.get(t) if given else None
@@ -339,7 +349,7 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
         cfg_new = int(g["cfg"]) if g is not None else own["cfg"]
         reselect = state["keep"] is None or k_new < k_prev
         if own is not None and (state["keep"] is None or own["k"] < k_prev):
-            sc = rescore(q_obs)
+            sc = pre if (pre is not None and state["keep"] is None) else rescore(q_obs)
             rec["scores"] = sc
             own["keep"] = [rows_ev[h][select(sc[h].astype(np.float32)[None], own["k"])[0]]
                            for h in range(Hkv)]
@@ -379,6 +389,15 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
             continue
         q = gen.queries(w, gen.T_QPRE, M, bh0=b * Hq, nbh=Hq, step=t)  # [Hq, M, D]
         m_t = None
+        pre = None
+        if t == 0 and not full and first_masses:
+            # the full-KV step over all M query rows: Eq. 1 masses and the
+            # eviction scores from one scorer call over every head
+            K, _, _ = logical()
+            s64, ms = score64(widen(q, w.q_dtype)[None], K[None], seg_id, nseg, sm)
+            m_t = {a: float(ms[0, :, a].sum()) / (Hq * M) for a in range(nseg)}
+            out["mass"][0] = m_t
+            pre = [s64[0, h][seg_id == ev] for h in range(Hkv)]
         if full or t in steps:
             K, V, present = logical()
             qa = q if full else q[:, rows]
@@ -390,8 +409,8 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
             if t in steps:
                 out["att"][t] = (o[0], lse[0], sl[0])
         if t == 0:
-            M0 = sum(m_t[a] for a in cand) if full else None
-            b_prev = decide(0, m_t, b_prev, rho, q)
+            M0 = sum(m_t[a] for a in cand) if m_t is not None else None
+            b_prev = decide(0, m_t, b_prev, rho, q, pre)
             continue
         if full:
             for a in range(nseg):

@@ -83,6 +83,7 @@ def _load():
         "uc_retention_next": (dbl, [dbl, dbl, dbl, dbl, dbl]),
         "uc_status_string": (ctypes.c_char_p, [i32]),
         "uc_last_error": (ctypes.c_char_p, []),
+        "uc_last_kernel": (ctypes.c_char_p, []),
         "uc_set_path": (i32, [i32]),
         "uc_set_kernel_events": (i32, [vp, vp]),
         "uc_dequantize_segment": (i32, [shp, segp, vp, vp, vp]),
@@ -435,6 +436,11 @@ def uc_status_string(s: int) -> str:
 
 def uc_last_error() -> str:
     return lib.uc_last_error().decode()
+
+
+def uc_last_kernel() -> str:
+    """Main kernel of this thread's last attention or scoring launch."""
+    return lib.uc_last_kernel().decode()
 
 
 def uc_set_kernel_events(start, stop) -> None:

@@ -47,6 +47,7 @@ hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, 
 namespace {
 
 thread_local char g_err[512] = "";
+thread_local const char* g_last_kernel = "";
 std::atomic<int> g_path{UC_PATH_AUTO};
 
 // timing events: pending (set by uc_set_kernel_events) and active (taken by
@@ -258,6 +259,8 @@ const char* uc_status_string(uc_status s) {
 
 const char* uc_last_error(void) { return g_err; }
 
+const char* uc_last_kernel(void) { return g_last_kernel; }
+
 int uc_set_path(int path) {
   if (path != UC_PATH_AUTO && path != UC_PATH_VALU) return -1;
   return g_path.exchange(path);
@@ -292,18 +295,21 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
     const size_t need = decode_mfma_workspace(*shape, ks, M);
     if (ws_bytes < need || (need && !ws))
       return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+    g_last_kernel = "decode_mfma";
     return launched(launch_decode_mfma(*shape, ks, q, M, sm_scale, o, lse, seg_lse, ws, s));
   }
   if (g_path.load() == UC_PATH_AUTO && prefill_mfma_eligible(*shape, ks, q_dt, M)) {
     const size_t need = prefill_mfma_workspace(*shape, ks);
     if (ws_bytes < need || (need && !ws))
       return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
+    g_last_kernel = "prefill_mfma";
     return launched(launch_prefill_mfma(*shape, ks, q, M, sm_scale, o, lse, seg_lse, ws, s));
   }
   const ChunkPlan p = attend_plan(ks);
   const size_t need = generic_ws(*shape, ks, kAttRows, kAttMaxChunks, M, true);
   if (ws_bytes < need || !ws) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   float* partial = (float*)ws;
+  g_last_kernel = "attend_valu";
   hipError_t e = kernel_timer_begin(s);
   if (e == hipSuccess) e = launch_attend_generic(*shape, ks, p, q, q_dt, M, sm_scale, partial, true, s);
   if (e == hipSuccess) e = kernel_timer_end(s);
@@ -375,6 +381,7 @@ uc_status uc_attend_append(const uc_shape* shape, const uc_segment* segs, int n_
   nk.v = v_new;
   AppendOp ap{(const char*)k_new, (const char*)v_new, (char*)ks.s[tail].k, (char*)ks.s[tail].v,
               n_new, ks.s[tail].row_stride, pos, shape->D * dtype_bytes(nk.dtype)};
+  g_last_kernel = "decode_mfma_append";
   return launched(launch_decode_mfma(*shape, ks, q, M, sm_scale, o, lse, nullptr, ws, s, &ap));
 }
 
@@ -461,6 +468,7 @@ uc_status uc_attend_batch(const uc_shape* shape, const uc_segment* const* segs, 
       n_wgs += Wr * shape->Hkv;
       for (int i = 0; i < n_segs[r]; ++i) flat[pos++] = ks[r].s[i];
     }
+    g_last_kernel = "decode_batch";
     hipError_t e = launch_blob_upload(desc.data(), desc.size(), ws, s);
     if (e == hipSuccess)
       e = launch_decode_batch(*shape, total, W_max, n_wgs, q, M, sm_scale, o, lse, ws, s);
@@ -558,6 +566,7 @@ uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int
     for (int i = 0; i < n_segs; ++i) sp[i] = scores_out[i];
   hipError_t e;
   ChunkPlan p2;
+  g_last_kernel = fast ? "score_mfma" : "score_valu";
   if (fast) {
     const ChunkPlan p = score_mfma_plan(ks);
     e = launch_score_lse_mfma(*shape, ks, p, q_obs, W, sm_scale, partial, s);

@@ -217,3 +217,21 @@ def test_topk_mass_closed_forms_and_brute_force(ref):
     assert np.all(ref.topk_mass(np.zeros((2, 10), np.float32), 3) == 0.0)
     with pytest.raises(ValueError):
         ref.topk_mass(x, 334)
+
+
+def test_chain_first_masses_with_sampled_rows(ref, gen, chain):
+    """The sampled-row mode with first_masses (used at full size): the
+    full-KV step's masses, the oracle's own first decision and its kept rows
+    equal those of the chain that attends every row."""
+    import oracle.pipeline as op
+    w, r = chain
+    given = {t: {"k": d["k"], "cfg": d["cfg"], "keep": r["keep"][t]}
+             for t, d in r["decisions"].items()}
+    rs = op.budget_chain(w, 0, [3], rows=np.array([0, 5, 9]), given=given, first_masses=True)
+    for a in range(3):
+        assert abs(rs["mass"][0][a] - r["mass"][0][a]) < 1e-14, a
+    own, d0 = rs["decisions"][0]["own"], r["decisions"][0]
+    assert (own["k"], own["cfg"]) == (d0["k"], d0["cfg"])
+    for h in range(w.Hkv):
+        assert np.array_equal(own["keep"][h], r["keep"][0][h]), h
+    assert rs["decisions"][5]["own"] is None  # later boundaries: given only

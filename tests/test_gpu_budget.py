@@ -79,7 +79,7 @@ def test_image_editing_dynamic_budget(b):
                             else given[max(x for x in given if x < t)]["keep"][h])
                     pos = {int(v): i for i, v in enumerate(prev)}
                     for x in np.setxor1d(g, o_):
-                        assert abs(sc[pos[int(x)]] - tau) <= 1e-6 * max(1.0, abs(tau)), (t, h, x)
+                        assert abs(sc[pos[int(x)]] - tau) <= 1e-6, (t, h, x)  # absolute band
         # storage of the quantised type, bit for bit
         pk = ref["packed"][t]
         for n in ("codes_k", "codes_v"):
@@ -97,11 +97,12 @@ def test_image_editing_dynamic_budget(b):
 
 def test_image_editing_dynamic_full_sampled():
     """Full size (4096-query blocks, 25 timesteps), request 0, in the
-    benchmark's launch configuration.  The decisions must follow from the
-    GPU's own type masses by the oracle's rules (Eq. 3, Eq. 2, Sec. 3.4
-    translation) and eviction must stay nested; with those decisions the
-    oracle re-derives the storage (bit for bit) and the attention of sampled
-    query rows."""
+    benchmark's launch configuration.  The first decision (full-KV step)
+    must equal the oracle's own, from its own type masses and scores over
+    all query rows; every later decision must follow from the GPU's type
+    masses by the oracle's rules (Eq. 3, Eq. 2, Sec. 3.4 translation) and
+    eviction must stay nested; with those decisions the oracle re-derives the
+    storage (bit for bit) and the attention of sampled query rows."""
     import oracle as ref
     w = gen.IMAGE_EDITING_DYNAMIC
     b = 0
@@ -136,7 +137,20 @@ def test_image_editing_dynamic_full_sampled():
         b_prev, k_prev, c_prev = dict(zip(cand, bud)), k, c
     given = {t: {"k": d["k"], "cfg": d["cfg"], "keep": keeps[t]} for t, d in run.decisions.items()}
     rows = np.arange(7, w.M, 509)
-    r = op.budget_chain(w, b, check, rows=rows, given=given)
+    _case(w.name, b=b, own_decision="t=0")
+    r = op.budget_chain(w, b, check, rows=rows, given=given, first_masses=True)
+    # the oracle's own first decision at full size: type masses of the
+    # full-KV step over all 4096 query rows, and its kept rows
+    for a in range(len(w.segments)):
+        assert abs(masses[0][a] - r["mass"][0][a]) <= 2e-5 * r["mass"][0][a] + 1e-7, a
+    own = r["decisions"][0]["own"]
+    assert (run.decisions[0]["k"], run.decisions[0]["cfg"]) == (own["k"], own["cfg"])
+    for h in range(Hkv):
+        g, o_ = keeps[0][h], own["keep"][h]
+        sc = np.asarray(r["decisions"][0]["scores"][h], np.float64)
+        tau = np.sort(sc)[::-1][own["k"] - 1]
+        for x in np.setxor1d(g, o_):  # only rows at the cut may differ
+            assert abs(sc[int(x)] - tau) <= 1e-6, (h, x, sc[int(x)] - tau)
     for t in bounds:
         pk = r["packed"][t]
         for n in ("codes_k", "codes_v"):

@@ -331,3 +331,16 @@ def test_text_to_image_budget_admits_three_upgrades(ref, gen):
                                                 orig / w.budget_ratio, fixed)]
         assert bits.count(4) == g["n_int4"] and bits.count(2) == g["n_int2"]
         assert bits[int(np.argmin(mass))] == 2
+
+
+def test_denoise_masses_without_attention(dchain):
+    """Rescoring steps that return no attention still compute their masses
+    over all query rows (the path the full-size runs take): the widths and
+    masses equal those of the chain that also attends those steps."""
+    import oracle.pipeline as op
+    w, r = dchain
+    rs = op.denoise_chain(w, 0, [11], rows=np.array([1, 6]))
+    assert rs["bits"] == r["bits"]
+    for t in r["mass"]:
+        assert np.array_equal(rs["mass"][t], r["mass"][t]), t
+    assert sorted(rs["att"]) == [11]
