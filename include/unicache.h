@@ -240,6 +240,25 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs,
                           float sm_scale, float* o, float* lse, float* seg_lse,
                           void* ws, size_t ws_bytes, void* stream);
 
+/* uc_attend_mixed for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same computation, kernels and results, with the workspace taken from
+ * a static device array of UC_SCRATCH_BYTES bytes that the library holds on
+ * every GPU it runs on until the process ends.  The call allocates nothing
+ * (no hipMalloc, no allocating library routine); the caller still passes q,
+ * o and the optional lse / seg_lse.  A call whose uc_attend_workspace_size
+ * exceeds UC_SCRATCH_BYTES (large prefill blocks over packed segments) fails
+ * with UC_E_UNSUPPORTED before any launch.  Every call on one GPU shares
+ * that GPU's array: calls that may overlap on one GPU (different streams
+ * without ordering between them) race and must not be issued; calls ordered
+ * on one stream are safe.  The array's contents are not preserved between
+ * calls and need no initialisation. */
+#define UC_SCRATCH_BYTES (16u << 20)
+uc_status uc_attend_mixed_noalloc(const uc_shape* shape, const uc_segment* segs,
+                                  int n_segs, const void* q, uc_dtype q_dt, int M,
+                                  float sm_scale, float* o, float* lse, float* seg_lse,
+                                  void* stream);
+
 /* Workspace bytes for uc_attend_mixed.  The value never decreases when a
  * segment gains rows, so a workspace sized for the largest row counts (say a
  * decode tail at full capacity) serves every call with fewer rows. */

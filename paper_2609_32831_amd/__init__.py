@@ -70,6 +70,8 @@ def _load():
         "uc_attend_mixed": (i32, [shp, segp, i32, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp,
                                   sz, vp]),
         "uc_attend_workspace_size": (sz, [shp, segp, i32, i32, i32]),
+        "uc_attend_mixed_noalloc": (i32, [shp, segp, i32, vp, i32, i32, ctypes.c_float, vp, vp,
+                                          vp, vp]),
         "uc_segment_mass": (i32, [shp, i32, i32, vp, vp, vp, vp]),
         "uc_append_rows": (i32, [shp, vp, vp, i32, segp, i32, vp]),
         "uc_attend_append": (i32, [shp, segp, i32, i32, vp, vp, i32, vp, i32, i32,
@@ -233,6 +235,22 @@ def uc_attend_mixed(shape: uc_shape, segs: Sequence[Segment], q: torch.Tensor, M
     _check(lib.uc_attend_mixed(ctypes.byref(shape), arr, len(segs), q.data_ptr(), q_dt, M,
                                ctypes.c_float(sm_scale), o.data_ptr(), _ptr(lse), _ptr(seg_lse),
                                ws.data_ptr(), ws.numel(), _stream(stream)), "uc_attend_mixed")
+    return o
+
+
+UC_SCRATCH_BYTES = 16 << 20
+
+
+def uc_attend_mixed_noalloc(shape: uc_shape, segs: Sequence[Segment], q: torch.Tensor, M: int,
+                            sm_scale: float, o: torch.Tensor, lse: Optional[torch.Tensor] = None,
+                            seg_lse: Optional[torch.Tensor] = None, stream=None):
+    """uc_attend_mixed with the library's static scratch array as workspace
+    (no device allocation by the library or here)."""
+    arr = _seg_array(segs)
+    _check(lib.uc_attend_mixed_noalloc(ctypes.byref(shape), arr, len(segs), q.data_ptr(),
+                                       TORCH_DT[q.dtype], M, ctypes.c_float(sm_scale),
+                                       o.data_ptr(), _ptr(lse), _ptr(seg_lse), _stream(stream)),
+           "uc_attend_mixed_noalloc")
     return o
 
 

@@ -9,6 +9,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 #include <vector>
 
 #include "uc_common.h"
@@ -315,6 +316,56 @@ uc_status uc_attend_mixed(const uc_shape* shape, const uc_segment* segs, int n_s
   if (e == hipSuccess) e = kernel_timer_end(s);
   if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, M, partial, o, lse, seg_lse, s);
   return launched(e);
+}
+
+// ---------------------------------------------------------------- allocation-free attention
+// One file-scope scratch array per GPU, in place of the caller's workspace.
+// The host takes its device address once per device with that device current
+// and uses only that address afterwards (the array's name is a host-side
+// stand-in in host code).
+static __device__ __align__(256) unsigned char scratch[UC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+uc_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(UC_E_DEVICE, "hipGetDevice: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(UC_E_UNSUPPORTED, "device %d >= %d", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p)
+      return fail(UC_E_DEVICE, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return UC_OK;
+}
+}  // namespace
+
+extern "C" uc_status uc_attend_mixed_noalloc(const uc_shape* shape, const uc_segment* segs,
+                                             int n_segs, const void* q, uc_dtype q_dt, int M,
+                                             float sm_scale, float* o, float* lse,
+                                             float* seg_lse, void* stream) {
+  KSegs ks;
+  uc_status st = check_segments(shape, segs, n_segs, ks);
+  if (st) return st;
+  if (M < 1 || !dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad M (%d) or q dtype (%d)", M, q_dt);
+  const size_t need = uc_attend_workspace_size(shape, segs, n_segs, q_dt, M);
+  if (need > UC_SCRATCH_BYTES)
+    return fail(UC_E_UNSUPPORTED,
+                "this call needs %zu bytes of scratch, above the %u-byte static array; use "
+                "uc_attend_mixed with a workspace", need, (unsigned)UC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  st = scratch_address(&ws);
+  if (st) return st;
+  return uc_attend_mixed(shape, segs, n_segs, q, q_dt, M, sm_scale, o, lse, seg_lse, ws,
+                         UC_SCRATCH_BYTES, stream);
 }
 
 // ---------------------------------------------------------------- decode step, append fused
