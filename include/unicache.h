@@ -351,6 +351,68 @@ double uc_retention_next(double rho, double rho_init, double rho_min,
                          double M_c, double M_0);
 
 /* ------------------------------------------------------------------------ */
+/* Dynamic storage budget of one request, decided on the device from the type
+ * masses the attention passes produced (Sec. 3.3 Eq. 1-3; Sec. 3.4, a budget
+ * becomes the rows an eviction-managed type keeps and the precision and
+ * grouping of a quantisation-managed type; App. E "Efficient
+ * attention-guided allocation": a small kernel determines the allocation for
+ * the next chunk).  Two candidate types take part: segment `ev`
+ * (eviction-managed) and segment `qt` (quantisation-managed); other segments
+ * are kept and stay outside the budget. */
+typedef struct {
+  int32_t Hq, Hkv, D, M;   /* query heads, KV heads, head dim, query rows per timestep */
+  int32_t n_segs;          /* segments per row of the mass array */
+  int32_t ev, qt;          /* segment indices of the two candidate types */
+  int32_t n_ev, n_qt;      /* their rows per KV head before any compression */
+  int32_t dtype;           /* their element type (uc_dtype) */
+  double rho_init, rho_min;
+} uc_budget_params;
+
+/* Device-resident state, 8-byte aligned; the caller zero-fills it before the
+ * first boundary (n_boundaries = 0).  After each uc_budget_step:
+ *   rho, B      retention ratio and total budget B = rho * (S_ev + S_qt),
+ *               S_a = Hkv * dense bytes of type a's original rows
+ *   M0          candidate mass of the first (full-KV) boundary
+ *   m[0], m[1]  Eq. 1 chunk masses of ev and qt
+ *   b[0], b[1]  Eq. 2 budgets of ev and qt in bytes (the b^(c-1) of the next)
+ *   k           rows per KV head ev keeps: min(previous k, the rows whose
+ *               bytes (2*D*elem + 4 per row) fit b[0] / Hkv)
+ *   cfg, bits, group  qt's configuration (as uc_quant_config numbers them):
+ *               the first at or after the previous one whose Hkv packed
+ *               segments fit b[1]
+ *   k_prev, cfg_prev  the values before this boundary (n_ev and -1 at the
+ *               first): k < k_prev means re-selection, cfg != cfg_prev
+ *               re-quantisation */
+typedef struct {
+  double rho, B, M0;
+  double m[2];
+  double b[2];
+  int32_t k, cfg, bits, group;
+  int32_t k_prev, cfg_prev;
+  int32_t n_boundaries, reserved;
+} uc_budget_state;
+
+/* One chunk boundary.  mass: device float [n_steps, Hkv, n_segs], the raw
+ * per-segment sums of the chunk's timesteps as uc_segment_mass writes them
+ * (one request, B = 1).  Eq. 1: m_a = (1 / n_steps) sum over the steps of
+ * (sum over KV heads of mass) / (Hq * M), summed in double.  At the first
+ * boundary (the full-KV step, n_boundaries = 0): M0 = m_ev + m_qt,
+ * rho = rho_init, b^(0) = S.  Later: rho = Eq. 3 with M_c = m_ev + m_qt.
+ * Then B, Eq. 2 over (ev, qt) and the Sec. 3.4 translation; one workgroup,
+ * enqueued on `stream`, no host synchronisation. */
+uc_status uc_budget_step(const uc_budget_params* params, const float* mass, int n_steps,
+                         uc_budget_state* state, void* stream);
+
+/* Calibration-based policy assignment (Sec. 3.2; App. B "Calibration
+ * Setting").  frac: device float [rows, n_types], one concentration per
+ * (calibration example, KV head) and type, as uc_topk_mass writes them.
+ * conc_out[a] (device double) = the mean over the rows of frac[., a], summed
+ * in double in row order; evict_out[a] (device int32) = 1 if conc_out[a] >=
+ * threshold (eviction), else 0 (quantisation).  n_types <= UC_MAX_SEGMENTS. */
+uc_status uc_calibrate_policy(const float* frac, int rows, int n_types, double threshold,
+                              double* conc_out, int32_t* evict_out, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Kernel path selection for uc_attend_mixed (process-wide; for cross-checks):
  * UC_PATH_AUTO (default) uses the matrix-core kernels where the inputs allow
  * (bf16 rows and queries, D = 128, at most 16 query rows per KV head for

@@ -51,6 +51,23 @@ class uc_segment(ctypes.Structure):
                 ("tail_v", ctypes.c_void_p)]
 
 
+class uc_budget_params(ctypes.Structure):
+    _fields_ = [("Hq", ctypes.c_int32), ("Hkv", ctypes.c_int32), ("D", ctypes.c_int32),
+                ("M", ctypes.c_int32), ("n_segs", ctypes.c_int32), ("ev", ctypes.c_int32),
+                ("qt", ctypes.c_int32), ("n_ev", ctypes.c_int32), ("n_qt", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("rho_init", ctypes.c_double),
+                ("rho_min", ctypes.c_double)]
+
+
+class uc_budget_state(ctypes.Structure):
+    _fields_ = [("rho", ctypes.c_double), ("B", ctypes.c_double), ("M0", ctypes.c_double),
+                ("m", ctypes.c_double * 2), ("b", ctypes.c_double * 2),
+                ("k", ctypes.c_int32), ("cfg", ctypes.c_int32), ("bits", ctypes.c_int32),
+                ("group", ctypes.c_int32), ("k_prev", ctypes.c_int32),
+                ("cfg_prev", ctypes.c_int32), ("n_boundaries", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run paper_2609_32831_amd/build.py "
@@ -96,6 +113,8 @@ def _load():
         "uc_topk_mass": (i32, [vp, i32, i32, i32, vp, vp, sz, vp]),
         "uc_topk_mass_workspace_size": (sz, [i32, i32]),
         "uc_quant_config": (i32, [dbl, i64, i32, i32, i32, i32, vp, vp]),
+        "uc_budget_step": (i32, [ctypes.POINTER(uc_budget_params), vp, i32, vp, vp]),
+        "uc_calibrate_policy": (i32, [vp, i32, i32, dbl, vp, vp, vp]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -446,6 +465,39 @@ def uc_type_budget(mass: Sequence[float], b_prev: Sequence[float], B_total: floa
 def uc_retention_next(rho: float, rho_init: float, rho_min: float, M_c: float,
                       M_0: float) -> float:
     return float(lib.uc_retention_next(rho, rho_init, rho_min, M_c, M_0))
+
+
+def budget_state_tensor(device="cuda") -> torch.Tensor:
+    """Zero-filled device storage for one uc_budget_state (before the first
+    boundary)."""
+    return torch.zeros(ctypes.sizeof(uc_budget_state), dtype=torch.uint8, device=device)
+
+
+def budget_state_read(state: torch.Tensor) -> uc_budget_state:
+    """Copy a device uc_budget_state to the host (waits for the stream)."""
+    return uc_budget_state.from_buffer_copy(bytes(state.cpu().numpy()))
+
+
+def uc_budget_step(params: uc_budget_params, mass: torch.Tensor, n_steps: int,
+                   state: torch.Tensor, stream=None) -> None:
+    """mass: device float [n_steps, Hkv, n_segs] (contiguous)."""
+    assert mass.dtype == torch.float32 and mass.is_contiguous()
+    assert mass.numel() == n_steps * params.Hkv * params.n_segs
+    assert state.numel() == ctypes.sizeof(uc_budget_state)
+    _check(lib.uc_budget_step(ctypes.byref(params), mass.data_ptr(), n_steps, state.data_ptr(),
+                              _stream(stream)), "uc_budget_step")
+
+
+def uc_calibrate_policy(frac: torch.Tensor, threshold: float, conc_out: torch.Tensor,
+                        evict_out: torch.Tensor, stream=None) -> None:
+    """frac: device float [rows, n_types]; conc_out double [n_types], evict_out
+    int32 [n_types]."""
+    rows, n_types = frac.shape
+    assert frac.dtype == torch.float32 and frac.is_contiguous()
+    assert conc_out.dtype == torch.float64 and evict_out.dtype == torch.int32
+    assert conc_out.numel() == evict_out.numel() == n_types
+    _check(lib.uc_calibrate_policy(frac.data_ptr(), rows, n_types, threshold, conc_out.data_ptr(),
+                                   evict_out.data_ptr(), _stream(stream)), "uc_calibrate_policy")
 
 
 def uc_status_string(s: int) -> str:

@@ -12,6 +12,7 @@
 #include <mutex>
 #include <vector>
 
+#include "budget_rules.h"
 #include "uc_common.h"
 
 using namespace uc;
@@ -792,45 +793,24 @@ int64_t uc_dense_bytes(int64_t rows, int D, uc_dtype dt) {
 }
 
 int64_t uc_evicted_bytes(int64_t rows, int D, uc_dtype dt) {
-  return rows * (2 * (int64_t)D * dtype_bytes(dt) + (int64_t)sizeof(int32_t));
+  return rules::evicted_bytes(rows, D, dtype_bytes(dt));
 }
 
 int64_t uc_packed_bytes(int64_t N, int D, int G, int bits, uc_dtype dt) {
-  if (N < 0 || D < 1 || G < 1 || D % G || !(bits == 2 || bits == 4 || bits == 8) || !dtype_ok(dt))
-    return -1;
-  const int64_t nf = (int64_t)G * (N / G);
-  const int64_t codes = 2 * nf * D * bits / 8;
-  const int64_t kmeta = (nf / G) * D * 2 * (int64_t)sizeof(float);
-  const int64_t vmeta = nf * (D / G) * 2 * (int64_t)sizeof(float);
-  return codes + kmeta + vmeta + uc_dense_bytes(N - nf, D, dt);
+  if (!dtype_ok(dt)) return -1;
+  return rules::packed_bytes(N, D, G, bits, dtype_bytes(dt));
 }
 
 int64_t uc_evict_rows_for_budget(double budget_bytes, double fixed_bytes, int64_t N, int D,
                                  uc_dtype dt) {
-  const double per = (double)uc_evicted_bytes(1, D, dt);
-  const double k = floor((budget_bytes - fixed_bytes) / per);
-  if (!(k > 0.0)) return 0;
-  return k >= (double)N ? N : (int64_t)k;
+  return rules::evict_rows(budget_bytes, fixed_bytes, N, D, dtype_bytes(dt));
 }
 
 int uc_quant_config(double budget_bytes, int64_t N, int D, uc_dtype dt, int n_heads, int first,
                     int* bits, int* group) {
   if (D < 32 || !pow2(D) || N < 0 || n_heads < 1 || !dtype_ok(dt)) return -1;
-  int ng = 0;
-  for (int g = 32; g <= D; g *= 2) ++ng;
-  const int n_cfg = 3 * ng;
-  if (first < 0 || first >= n_cfg) return -1;
-  int pick = n_cfg - 1;
-  for (int i = first; i < n_cfg; ++i) {
-    const int64_t per_head = uc_packed_bytes(N, D, 32 << (i % ng), 8 >> (i / ng), dt);
-    if ((double)n_heads * (double)per_head <= budget_bytes) {
-      pick = i;
-      break;
-    }
-  }
-  if (bits) *bits = 8 >> (pick / ng);
-  if (group) *group = 32 << (pick % ng);
-  return pick;
+  if (first < 0 || first >= 3 * rules::quant_groups(D)) return -1;
+  return rules::quant_config(budget_bytes, N, D, dtype_bytes(dt), n_heads, first, bits, group);
 }
 
 uc_status uc_assign_bits(int n_heads, const float* mass, int64_t N, int D, int G, uc_dtype dt,
@@ -855,44 +835,38 @@ uc_status uc_type_budget(int n_types, const double* mass, const double* b_prev, 
                          double* b_next) {
   if (n_types < 1 || n_types > 64 || !mass || !b_prev || !b_next)
     return fail(UC_E_INVALID, "bad arguments");
-  bool active[64], done = false;
-  for (int a = 0; a < n_types; ++a) {
-    b_next[a] = 0.0;
-    active[a] = mass[a] > 0.0;
-  }
-  double remaining = B_total;
-  while (!done) {
-    double msum = 0.0;
-    int n_active = 0;
-    for (int a = 0; a < n_types; ++a)
-      if (active[a]) {
-        msum += mass[a];
-        ++n_active;
-      }
-    if (n_active == 0) break;
-    bool capped_any = false;
-    bool capped[64] = {};
-    for (int a = 0; a < n_types; ++a)
-      if (active[a] && mass[a] / msum * remaining >= b_prev[a]) capped[a] = capped_any = true;
-    if (!capped_any) {
-      for (int a = 0; a < n_types; ++a)
-        if (active[a]) b_next[a] = mass[a] / msum * remaining;
-      done = true;
-    } else {
-      for (int a = 0; a < n_types; ++a)
-        if (capped[a]) {
-          b_next[a] = b_prev[a];
-          remaining -= b_prev[a];
-          active[a] = false;
-        }
-    }
-  }
+  rules::type_budget(n_types, mass, b_prev, B_total, b_next);
   return ok();
 }
 
 double uc_retention_next(double rho, double rho_init, double rho_min, double M_c, double M_0) {
-  if (!(rho_min > 0.0 && rho_min <= rho_init && rho_init <= 1.0 && M_0 > 0.0)) return NAN;
-  return std::min(rho, std::max(rho_min, rho_init * M_c / M_0));
+  return rules::retention_next(rho, rho_init, rho_min, M_c, M_0);
+}
+
+// ---------------------------------------------------------------- budget decisions on the device
+uc_status uc_budget_step(const uc_budget_params* p, const float* mass, int n_steps,
+                         uc_budget_state* state, void* stream) {
+  if (!p || !mass || !state) return fail(UC_E_INVALID, "NULL pointer");
+  if (p->Hq < 1 || p->Hkv < 1 || p->Hq % p->Hkv || p->M < 1 || p->D < 32 || !pow2(p->D))
+    return fail(UC_E_INVALID, "bad Hq / Hkv / M / D (%d, %d, %d, %d)", p->Hq, p->Hkv, p->M, p->D);
+  if (p->n_segs < 1 || p->n_segs > kMaxSeg) return fail(UC_E_INVALID, "n_segs %d", p->n_segs);
+  if (p->ev < 0 || p->ev >= p->n_segs || p->qt < 0 || p->qt >= p->n_segs || p->ev == p->qt)
+    return fail(UC_E_INVALID, "ev (%d) and qt (%d) must be distinct segments", p->ev, p->qt);
+  if (p->n_ev < 0 || p->n_qt < 0 || !dtype_ok(p->dtype)) return fail(UC_E_INVALID, "bad rows or dtype");
+  if (!(p->rho_min > 0.0 && p->rho_min <= p->rho_init && p->rho_init <= 1.0))
+    return fail(UC_E_INVALID, "need 0 < rho_min <= rho_init <= 1");
+  if (n_steps < 1) return fail(UC_E_INVALID, "n_steps must be >= 1");
+  if (((uintptr_t)state & 7u) || ((uintptr_t)mass & 3u)) return fail(UC_E_INVALID, "misaligned pointer");
+  return launched(launch_budget_step(*p, mass, n_steps, state, (hipStream_t)stream));
+}
+
+uc_status uc_calibrate_policy(const float* frac, int rows, int n_types, double threshold,
+                              double* conc_out, int32_t* evict_out, void* stream) {
+  if (rows < 1 || n_types < 1 || n_types > kMaxSeg) return fail(UC_E_INVALID, "bad rows or n_types");
+  if (!frac || !conc_out || !evict_out) return fail(UC_E_INVALID, "NULL pointer");
+  if (!isfinite(threshold)) return fail(UC_E_INVALID, "threshold must be finite");
+  return launched(launch_calibrate_policy(frac, rows, n_types, threshold, conc_out, evict_out,
+                                          (hipStream_t)stream));
 }
 
 }  // extern "C"

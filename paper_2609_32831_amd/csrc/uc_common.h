@@ -185,6 +185,10 @@ hipError_t launch_gather(const int32_t* keep, int BH, int N, int k, const void* 
                          hipStream_t st);
 hipError_t launch_append(const uc_shape& sh, const void* knew, const void* vnew, int n_new,
                          const KSeg& seg, int pos, hipStream_t st);
+hipError_t launch_budget_step(const uc_budget_params& p, const float* mass, int n_steps,
+                              uc_budget_state* state, hipStream_t st);
+hipError_t launch_calibrate_policy(const float* frac, int rows, int n_types, double threshold,
+                                   double* conc, int32_t* evict, hipStream_t st);
 hipError_t launch_segment_mass(const uc_shape& sh, int M, int n_segs, const float* lse,
                                const float* seg_lse, float* mass, hipStream_t st);
 }  // namespace uc

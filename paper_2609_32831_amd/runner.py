@@ -16,12 +16,13 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (NAME_DT, TORCH_DT, dense_segment, make_shape, packed_layout, packed_segment,
-               uc_assign_bits, uc_attend_append, uc_attend_mixed, uc_attend_workspace_size,
-               uc_compose_index, uc_dense_bytes, uc_dequantize_segment, uc_evict_rows_for_budget,
-               uc_packed_bytes, uc_quant_config, uc_quantize_segment, uc_retention_next,
+from . import (NAME_DT, TORCH_DT, budget_state_read, budget_state_tensor, dense_segment,
+               make_shape, packed_layout, packed_segment, uc_assign_bits, uc_attend_append,
+               uc_attend_mixed, uc_attend_workspace_size, uc_budget_params, uc_budget_step,
+               uc_calibrate_policy, uc_compose_index, uc_dense_bytes, uc_dequantize_segment,
+               uc_evict_rows_for_budget, uc_evicted_bytes, uc_packed_bytes, uc_quantize_segment,
                uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep,
-               uc_stream_append, uc_topk_mass, uc_type_budget)
+               uc_stream_append, uc_topk_mass)
 
 TORCH = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -196,7 +197,7 @@ class Run:
             if p.kind == "keep":
                 tot += uc_dense_bytes(s.n, w.D, NAME_DT[s.dtype])
             elif p.kind == "evict":
-                tot += p.k * (2 * w.D * (4 if s.dtype == "f32" else 2) + 4)
+                tot += uc_evicted_bytes(p.k, w.D, NAME_DT[s.dtype])
             else:
                 tot += uc_packed_bytes(s.n, w.D, s.group, p.bits or 4, NAME_DT[s.dtype])
         return tot
@@ -323,16 +324,19 @@ class DynamicRun:
     library's kernels; host-side control flow only.
 
     Timestep 0 attends the uncompressed cache (the first full-KV step): its
-    per-segment log-sum-exps give m^(0), and scores over the whole context
-    from the step's query block select the kept rows of the evicting type.
-    Later timesteps attend the compressed cache and record their type masses;
-    after every chunk of chunk_steps timesteps (if a timestep follows) the
-    chunk's mean masses set rho (Eq. 3) and the type budgets (Eq. 2), which
-    become a row count for the evicting type (fewer rows are chosen among
-    those still kept, scored by the last obs_window query rows of each query
-    head over the current cache, and their logical indices composed) and a
-    (bits, group) configuration for the quantised type (a change re-quantises
-    its dequantised rows).  Eviction and re-quantisation are irreversible."""
+    per-segment log-sum-exps give the type masses, and scores over the whole
+    context from the step's query block select the kept rows of the evicting
+    type.  Later timesteps attend the compressed cache and record their type
+    masses; after every chunk of chunk_steps timesteps (if a timestep
+    follows) uc_budget_step turns the chunk's masses into the next
+    retention ratio (Eq. 3), type budgets (Eq. 2) and their translation on
+    the device: a row count for the evicting type (fewer rows are chosen
+    among those still kept, scored by the last obs_window query rows of each
+    query head over the current cache, and their logical indices composed)
+    and a (bits, group) configuration for the quantised type (a change
+    re-quantises its dequantised rows).  The host reads the decision once per
+    boundary, because the row count and the configuration size the next
+    launches.  Eviction and re-quantisation are irreversible."""
 
     def __init__(self, w, seg_k, seg_v, device="cuda"):
         """seg_k / seg_v: per segment, the request's rows [1, Hkv, n, D]."""
@@ -349,9 +353,6 @@ class DynamicRun:
         self.tdt = TORCH[segs[self.ev].dtype]
         self.n_ev, self.n_qt = segs[self.ev].n, segs[self.qt].n
         self.dense = [dense_segment(seg_k[i], seg_v[i]) for i in range(self.nseg)]
-        self.S = {a: Hkv * uc_dense_bytes(segs[a].n, D, NAME_DT[segs[a].dtype]) for a in self.cand}
-        self.S_total = float(sum(self.S.values()))
-        self.ng = int(math.log2(D // 32)) + 1
         q_dt = NAME_DT[w.q_dtype]
         # workspaces sized for the largest configuration: every row present,
         # the quantised type at the finest grouping
@@ -367,6 +368,7 @@ class DynamicRun:
         self.ws_sc = torch.empty(max(ws_sc, 256), dtype=torch.uint8, device=device)
         self.lse = torch.empty(1, Hq, M, device=device)
         self.seg_lse = torch.empty(1, Hq, M, self.nseg, device=device)
+        # raw per-segment masses of every timestep (uc_segment_mass)
         self.mass = torch.zeros(w.steps, 1, Hkv, self.nseg, device=device)
         self.scores = torch.empty(1, Hkv, self.n_ev, device=device)
         # the quantised type's current rows, dequantised: the source of a
@@ -375,15 +377,15 @@ class DynamicRun:
         self.deq_k = torch.empty(1, Hkv, self.n_qt, D, dtype=self.tdt, device=device)
         self.deq_v = torch.empty_like(self.deq_k)
         self.deq = dense_segment(self.deq_k, self.deq_v)
-        # state
+        # budget decisions on the device
+        self.params = uc_budget_params(Hq, Hkv, D, M, self.nseg, self.ev, self.qt, self.n_ev,
+                                       self.n_qt, self.dt, w.rho_init, w.rho_min)
+        self.state = budget_state_tensor(device)
+        # storage state
         self.compact = None     # dense segment of the kept rows of the evicting type
         self.idx = None         # [Hkv, k] int32 logical positions of those rows
         self.packed = None      # packed segment of the quantised type
         self.cfg = None         # (index, bits, group)
-        self.rho = w.rho_init
-        self.b_prev = dict(self.S)
-        self.M0 = None
-        self.chunk = []         # timesteps of the current chunk
         self.decisions: Dict[int, Dict] = {}
 
     # ---- helpers -----------------------------------------------------------
@@ -394,12 +396,6 @@ class DynamicRun:
         out[self.ev] = self.compact
         out[self.qt] = self.packed
         return out
-
-    def type_mass(self, rows):
-        """Mean over (query head, query row) of each type's probability, per
-        timestep in rows (Eq. 1 bracket); one host read."""
-        m = self.mass[rows].sum(dim=(1, 2)).double().cpu().numpy() / (self.w.Hq * self.w.M)
-        return m  # [len(rows), nseg]
 
     def _select(self, q_obs, W, k_new):
         """Scores of the evicting type's current rows from q_obs [1, Hq, W, D]
@@ -445,27 +441,19 @@ class DynamicRun:
         uc_dequantize_segment(self.shape, pk, self.deq_k, self.deq_v)
         self.packed, self.cfg = pk, cfg
 
-    def _decide(self, t, m, q_obs, W):
-        """Eq. 2 budgets and their translation at boundary t (m: per-type
-        chunk mass); the new state applies from the next timestep."""
-        w = self.w
-        B_next = self.rho * self.S_total
-        bud = uc_type_budget([m[a] for a in self.cand], [self.b_prev[a] for a in self.cand],
-                             B_next)
-        bud = {a: float(x) for a, x in zip(self.cand, bud)}
-        k_prev = self.n_ev if self.compact is None else self.compact.n_rows
-        k_new = min(k_prev, uc_evict_rows_for_budget(bud[self.ev] / w.Hkv, 0.0, self.n_ev, w.D,
-                                                     self.dt))
-        cfg = uc_quant_config(bud[self.qt], self.n_qt, w.D, self.dt, w.Hkv,
-                              0 if self.cfg is None else self.cfg[0])
-        if self.compact is None or k_new < k_prev:
-            self._select(q_obs, W, k_new)
-        if self.cfg is None or cfg[0] != self.cfg[0]:
-            self._quantize(cfg)
-        self.b_prev = bud
-        rec = {"rho": self.rho, "B": B_next, "m": {a: float(m[a]) for a in self.cand},
-               "b": bud, "k": k_new, "cfg": self.cfg[0], "bits": self.cfg[1],
-               "group": self.cfg[2]}
+    def _boundary(self, t, t0, n, q_obs, W):
+        """Boundary after timestep t over the chunk t0 .. t0+n-1: the device
+        decides (uc_budget_step), the host reads the decision and applies it
+        from the next timestep on."""
+        uc_budget_step(self.params, self.mass[t0:t0 + n], n, self.state)
+        st = budget_state_read(self.state)
+        if self.compact is None or st.k < st.k_prev:
+            self._select(q_obs, W, st.k)
+        if st.cfg != st.cfg_prev:
+            self._quantize((st.cfg, st.bits, st.group))
+        rec = {"rho": st.rho, "B": st.B, "m": {self.ev: st.m[0], self.qt: st.m[1]},
+               "b": {self.ev: st.b[0], self.qt: st.b[1]}, "k": st.k, "cfg": st.cfg,
+               "bits": st.bits, "group": st.group}
         self.decisions[t] = rec
         return rec
 
@@ -484,17 +472,11 @@ class DynamicRun:
         (a decision at a chunk boundary)."""
         w = self.w
         if t == 0:
-            m0 = self.type_mass([0])[0]
-            self.M0 = float(sum(m0[a] for a in self.cand))
-            return self._decide(0, m0, q, w.M)
-        self.chunk.append(t)
-        if t % w.chunk_steps == 0 and t < w.steps - 1:
-            m_c = self.type_mass(self.chunk).mean(axis=0)
-            self.rho = uc_retention_next(self.rho, w.rho_init, w.rho_min,
-                                         float(sum(m_c[a] for a in self.cand)), self.M0)
+            return self._boundary(0, 0, 1, q, w.M)
+        C = w.chunk_steps
+        if t % C == 0 and t < w.steps - 1:
             q_obs = q[:, :, w.M - w.obs_window:].contiguous()
-            self.chunk = []
-            return self._decide(t, m_c, q_obs, w.obs_window)
+            return self._boundary(t, t - C + 1, C, q_obs, w.obs_window)
         return None
 
 
@@ -517,15 +499,16 @@ def calibrate_policies(w, inp: Dict, examples: int, q_obs: Optional[torch.Tensor
     W = w.W if W is None else W
     scores = [torch.empty(B, Hkv, s.n, device=device) for s in w.segments]
     uc_score_importance(shape, full, q_obs, W, sm_scale(D), scores)
-    frac = torch.empty(B * Hkv, len(w.segments), device=device)
+    n = len(w.segments)
+    frac = torch.empty(B * Hkv, n, device=device)
     for i, s in enumerate(w.segments):
         k = int(math.ceil(top * s.n))
         col = torch.empty(B * Hkv, device=device)
         uc_topk_mass(scores[i].view(B * Hkv, s.n), k, col)
         frac[:, i] = col
-    f = frac[: examples * Hkv].double().cpu().numpy()
-    out = {}
-    for i, s in enumerate(w.segments):
-        c = float(f[:, i].mean())
-        out[s.name] = (c, "evict" if c >= threshold else "quant")
-    return out, f
+    conc = torch.empty(n, dtype=torch.float64, device=device)
+    evict = torch.empty(n, dtype=torch.int32, device=device)
+    uc_calibrate_policy(frac[: examples * Hkv].contiguous(), threshold, conc, evict)
+    c, e = conc.cpu().numpy(), evict.cpu().numpy()
+    out = {s.name: (float(c[i]), "evict" if e[i] else "quant") for i, s in enumerate(w.segments)}
+    return out, frac[: examples * Hkv].cpu().numpy()

@@ -212,3 +212,30 @@ def test_host_helpers_agree_with_oracle(uc, ref):
         assert uc.uc_quant_config(qb, rows, Dq, dt, nh, first) == \
             ref.quant_config(qb, rows, Dq, name, nh, first)
     assert uc.uc_packed_bytes(100, 128, 48, 4, 2) == -1
+
+
+def test_budget_structs_and_validation():
+    """uc_budget_params / uc_budget_state mirror the header's layouts, and
+    uc_budget_step / uc_calibrate_policy reject bad arguments on the host
+    (nothing is launched)."""
+    import paper_2609_32831_amd as uc
+    P, S = uc.uc_budget_params, uc.uc_budget_state
+    assert ctypes.sizeof(P) == 56 and P.rho_init.offset == 40 and P.rho_min.offset == 48
+    assert ctypes.sizeof(S) == 88 and S.m.offset == 24 and S.b.offset == 40
+    assert S.k.offset == 56 and S.n_boundaries.offset == 80
+    L, E = uc.lib, uc.UC_E_INVALID
+    FAKE = 4096
+    good = P(28, 4, 128, 16, 3, 1, 2, 4096, 4096, uc.UC_BF16, 0.3, 0.15)
+    assert L.uc_budget_step(ctypes.byref(good), None, 1, FAKE, None) == E
+    assert L.uc_budget_step(ctypes.byref(good), FAKE, 0, FAKE, None) == E
+    assert L.uc_budget_step(ctypes.byref(good), FAKE, 1, FAKE + 4, None) == E  # misaligned state
+    for field, bad in (("qt", 1), ("ev", 3), ("rho_min", 0.4), ("rho_min", 0.0), ("Hq", 30),
+                       ("D", 96), ("n_segs", 9), ("dtype", 7)):
+        p = P.from_buffer_copy(good)
+        setattr(p, field, bad)
+        assert L.uc_budget_step(ctypes.byref(p), FAKE, 1, FAKE, None) == E, field
+    assert "rho_min" in uc.uc_last_error() or uc.uc_last_error()
+    assert L.uc_calibrate_policy(FAKE, 0, 2, 0.5, FAKE, FAKE, None) == E
+    assert L.uc_calibrate_policy(FAKE, 4, 9, 0.5, FAKE, FAKE, None) == E
+    assert L.uc_calibrate_policy(None, 4, 2, 0.5, FAKE, FAKE, None) == E
+    assert L.uc_calibrate_policy(FAKE, 4, 2, float("nan"), FAKE, FAKE, None) == E

@@ -26,6 +26,12 @@ def _case(name, **kw):
     print("CASE", name, " ".join(f"{k}={v}" for k, v in kw.items()), flush=True)
 
 
+def _type_masses(run, w):
+    """Per timestep, the Mean over (query head, query row) of each segment's
+    probability (Eq. 1 bracket), from the raw per-KV-head masses."""
+    return run.mass.double().sum(dim=(1, 2)).cpu().numpy() / (w.Hq * w.M)
+
+
 def _run_request(w, inp, b, check):
     seg_k = [t[b:b + 1].contiguous() for t in inp["seg_k"]]
     seg_v = [t[b:b + 1].contiguous() for t in inp["seg_v"]]
@@ -42,7 +48,7 @@ def _run_request(w, inp, b, check):
             codes[t] = {n: run.packed.t[n].cpu().numpy().copy()
                         for n in ("codes_k", "codes_v", "scale_k", "min_k", "scale_v", "min_v")}
     torch.cuda.synchronize()
-    masses = run.type_mass(list(range(w.steps)))
+    masses = _type_masses(run, w)
     return run, outs, keeps, codes, masses
 
 
