@@ -6,24 +6,33 @@
 // Work item: 128 query rows of one (b, h_kv) -- the rows of its G query heads
 // are contiguous in q -- in one workgroup of four waves; each wave owns two
 // 16-row query tiles.  The workgroup walks every key tile (32 rows) of every
-// segment once: the four waves stage the K and V rows of tile i+2 through
-// registers into a three-deep ring of padded LDS tiles while the waves
-// compute tile i.  Per tile and wave:
-//   S^T = K Q^T    v_mfma_f32_16x16x32_bf16, K rows read from LDS as the A
-//                  operand (shared by both query tiles), Q^T in registers;
-//   softmax        base 2, lazy reference maximum (one ballot per tile and
-//                  query tile), running per-segment sums for seg_lse;
-//   O^T += V^T P   V^T by transposing LDS reads (shared by both query
-//                  tiles); fp16 P and V on v_mfma_f32_16x16x32_f16 when every
-//                  V value of the call fits fp16 (a range pass sets a flag the
-//                  kernel reads), else bf16 V with P as bf16 hi + lo parts.
+// segment once: the waves stage the K and V rows of tile i+2 through
+// registers into a four-deep ring of padded LDS tiles.  The loop is a
+// three-stage software pipeline: in iteration t a wave issues, interleaved,
+//   S^T(t+1) = K Q^T    v_mfma_f32_16x16x32_bf16, K rows read from LDS as the
+//                       A operand (shared by both query tiles), Q^T in
+//                       registers;
+//   O^T += V^T P(t-1)   V^T by transposing LDS reads (shared by both query
+//                       tiles); fp16 P and V on v_mfma_f32_16x16x32_f16 when
+//                       every V value of the call fits fp16 (a range pass sets
+//                       a flag the kernel reads), else bf16 V with P as bf16
+//                       hi + lo parts;
+//   softmax(t)          on the vector ALUs: base-2 exponentials against a
+//                       lazily raised reference maximum, running per-segment
+//                       sums for seg_lse;
+// none of which depends on another, so one wave keeps the matrix cores and
+// the vector ALUs busy at once.  The rare raise of the reference maximum runs
+// after the matrix instructions (it rescales the accumulators they update).
 // Outputs (normalised O, lse, per-segment lse) are written directly; no
 // split over keys.  Workgroups are mapped so that those of one (b, h_kv) run
 // on the same XCD and share its L2 copy of the head's rows.
 //
 // Packed segments first go through dequant_kernel: codes -> round_to_bf16(
-// fmaf(code, scale, min)) into a [B, Hkv, n_full, D] bf16 workspace; their
-// residual tails are read in place.
+// fmaf(code, scale, min)) into a [B, Hkv, n_full, D] bf16 workspace (once per
+// call, where the query blocks of a head would otherwise each decode every
+// packed tile again); their residual tails are read in place.
+#include <type_traits>
+
 #include "mfma_util.h"
 #include "uc_common.h"
 
@@ -33,7 +42,7 @@ namespace {
 using namespace mf;
 
 constexpr int QTW = 2;                     // query tiles per wave
-constexpr int STAGES = 3;                  // stages of 32-row tiles in LDS
+constexpr int STAGES = 4;                  // stages in LDS: t-1 .. t+1 in use, t+2 staged
 constexpr int SUBB = 2 * TILEB;            // one tile: K rows + V rows
 // Two layouts: W waves per workgroup and TPS tiles per stage (one barrier per
 // stage).  <4, 1>: 128 query rows, two workgroups per CU; <8, 2>: 256 query
@@ -140,64 +149,78 @@ __device__ inline char* tile_buf(char* lds, int t) {
   return lds + ((t / TPS) % STAGES) * (TPS * SUBB) + (t % TPS) * SUBB;
 }
 
-// softmax of one query tile's 8 logits per lane; returns the probability
-// operands: fp16 P (F16) or bf16 hi/lo parts.  n_valid < TILE masks the
-// tile's last rows.
-template <bool F16>
-__device__ inline void tile_softmax(QState& st, const f4& s0, const f4& s1, float scale_log2,
-                                    int n_valid, int g4, u4& phi, u4& plo) {
-  float p[8];
+// raw logits of one query tile (8 per lane).  Rows past a view's end were
+// staged as zeros (range-checked loads), so their logit is 0 and their V row
+// is 0: they add nothing to O, and tile_step removes what they add to the
+// row sums.
+__device__ inline void tile_logits(const f4& s0, const f4& s1, float (&p)[8]) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     p[j] = s0[j];
     p[4 + j] = s1[j];
   }
-  if (n_valid < TILE) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      if (g4 * 4 + j >= n_valid) p[j] = -INFINITY;
-      if (16 + g4 * 4 + j >= n_valid) p[4 + j] = -INFINITY;
-    }
-  }
-  // probabilities against the current reference first; a lane sum above
-  // 2^kLazy (every logit more than kLazy above the reference makes one, and
-  // a first tile's -inf reference makes inf or NaN) sends the wave through
-  // the rare path that raises the reference to the column maximum and
-  // recomputes them, so in the common path no maximum is taken
-  float e[8], psum = 0.0f;
+}
+
+// common path of the softmax of one query tile: probabilities against the
+// current reference; returns the lane's sum.  A lane sum above 2^kLazy
+// (every logit more than kLazy above the reference makes one, and a first
+// tile's -inf reference makes inf or NaN) sends the wave through tile_raise.
+__device__ inline float tile_exp(const QState& st, const f4& s0, const f4& s1, float scale_log2,
+                                 float (&e)[8]) {
+  float p[8];
+  tile_logits(s0, s1, p);
+  float psum = 0.0f;
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
     e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
     psum += e[j];
   }
-  if (__builtin_amdgcn_ballot_w64(!(psum <= kLazyExp))) {  // rare: raise the reference max
-    // the scale is positive, so the maximum of the raw logits gives the maximum
-    float mx = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])),
-                     fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7]))) * scale_log2;
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float m_new = fmaxf(st.m, mx);
-    const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
-    st.l *= alpha;
-    st.ls *= alpha;
+  return psum;
+}
+
+// rare path: raise the reference to the column maximum, rescale the running
+// state and recompute the probabilities (they stay below 2^kLazy, well inside
+// fp16)
+__device__ inline float tile_raise(QState& st, const f4& s0, const f4& s1, float scale_log2,
+                                   float (&e)[8]) {
+  float p[8];
+  tile_logits(s0, s1, p);
+  // the scale is positive, so the maximum of the raw logits gives the maximum
+  float mx = fmaxf(fmaxf(fmaxf(p[0], p[1]), fmaxf(p[2], p[3])),
+                   fmaxf(fmaxf(p[4], p[5]), fmaxf(p[6], p[7]))) * scale_log2;
+  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float m_new = fmaxf(st.m, mx);
+  const float alpha = __builtin_amdgcn_exp2f(st.m - m_new);
+  st.l *= alpha;
+  st.ls *= alpha;
 #pragma unroll
-    for (int d = 0; d < 8; ++d) st.acc[d] *= alpha;
-    st.m = m_new;
-    psum = 0.0f;
+  for (int d = 0; d < 8; ++d) st.acc[d] *= alpha;
+  st.m = m_new;
+  float psum = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
-      psum += e[j];
-    }
+  for (int j = 0; j < 8; ++j) {
+    e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
+    psum += e[j];
   }
-  st.l += psum;
-  st.ls += psum;
+  return psum;
+}
+
+// probability operands of one query tile: fp16 P (F16), else bf16 hi + lo
+struct POp {
+  u4 hi, lo;
+};
+
+template <bool F16>
+__device__ inline POp pack_p(const float (&e)[8]) {
+  POp r;
   if (F16) {
-    // probabilities stay below 2^kLazy, well inside fp16
-    phi = u4{h2(e[0], e[1]), h2(e[2], e[3]), h2(e[4], e[5]), h2(e[6], e[7])};
+    r.hi = u4{h2(e[0], e[1]), h2(e[2], e[3]), h2(e[4], e[5]), h2(e[6], e[7])};
+    r.lo = r.hi;
   } else {
-    split_p(e, phi, plo);
+    split_p(e, r.hi, r.lo);
   }
+  return r;
 }
 
 // sum of a lane-partial value over the four key-row lanes of a query column
@@ -216,26 +239,110 @@ __device__ inline void load_ka(const char* lk, int i16, int g4, u4 (&ka)[8]) {
   }
 }
 
-// S^T = K Q^T of one tile for every query tile of the wave
-__device__ inline void tile_scores(const u4 (&ka)[8], const u4 (&qop)[QTW][4], f4 (&s)[QTW][2]) {
+// S^T = K Q^T of one tile for one query tile
+__device__ inline void qt_scores(const u4 (&ka)[8], const u4 (&q)[4], f4& s0, f4& s1) {
+  s0 = f4{0.f, 0.f, 0.f, 0.f};
+  s1 = s0;
 #pragma unroll
-  for (int qt = 0; qt < QTW; ++qt) {
-    f4 s0 = f4{0.f, 0.f, 0.f, 0.f}, s1 = s0;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      s0 = mfma(ka[k], qop[qt][k], s0);
-      s1 = mfma(ka[4 + k], qop[qt][k], s1);
-    }
-    s[qt][0] = s0;
-    s[qt][1] = s1;
+  for (int k = 0; k < 4; ++k) {
+    s0 = mfma(ka[k], q[k], s0);
+    s1 = mfma(ka[4 + k], q[k], s1);
   }
 }
 
-// the key-tile loop of one workgroup (see the file comment), software
-// pipelined: while tile t's softmax runs on the vector ALUs, the scores of
-// tile t+1 run on the matrix cores (their K rows are in LDS one iteration
-// early: the three-deep ring holds tiles t, t+1 and the one being staged).
-// Returns the view of the last tile.
+// S^T = K Q^T of one tile for every query tile of the wave
+__device__ inline void tile_scores(const u4 (&ka)[8], const u4 (&qop)[QTW][4], f4 (&s)[QTW][2]) {
+#pragma unroll
+  for (int qt = 0; qt < QTW; ++qt) qt_scores(ka, qop[qt], s[qt][0], s[qt][1]);
+}
+
+// O^T += V^T P of one tile (V^T operands read from the tile's LDS V rows)
+template <bool F16>
+__device__ inline void tile_pv(const char* lv, const POp (&pp)[QTW], QState (&st)[QTW], int i16,
+                               int g4) {
+#pragma unroll
+  for (int d = 0; d < 8; ++d) {
+    const u4 vt = vt_operand(lv, d, i16, g4);
+#pragma unroll
+    for (int qt = 0; qt < QTW; ++qt) {
+      if (F16) {
+        st[qt].acc[d] = mfma_f16(vt, pp[qt].hi, st[qt].acc[d]);
+      } else {
+        st[qt].acc[d] = mfma(vt, pp[qt].hi, st[qt].acc[d]);
+        st[qt].acc[d] = mfma(vt, pp[qt].lo, st[qt].acc[d]);
+      }
+    }
+  }
+}
+
+// One iteration of the pipeline (tile t): scores of tile t+1 and, with PV,
+// O += V^T P of tile t-1 on the matrix cores, interleaved with the softmax
+// common path of tile t on the vector ALUs; then the rare reference raise
+// (which recomputes tile t's scores from its K rows, still in LDS, so the
+// scores need not stay in registers) and the running sums.  sc holds tile
+// t's scores on entry and tile t+1's on exit; pp holds tile t-1's
+// probability operands on entry and tile t's on exit.
+template <bool F16, int TPS, bool PV>
+__device__ __attribute__((always_inline)) inline void tile_step(
+    int t, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW], f4 (&sc)[QTW][2],
+    POp (&pp)[QTW], float scale_log2, int n_valid, int i16, int g4) {
+  float psum[QTW];
+  POp pn[QTW];
+#pragma unroll
+  for (int qt = 0; qt < QTW; ++qt) {
+    float e[8];
+    psum[qt] = tile_exp(st[qt], sc[qt][0], sc[qt][1], scale_log2, e);
+    pn[qt] = pack_p<F16>(e);
+  }
+  {
+    u4 ka[8];
+    load_ka(tile_buf<TPS>(lds, t + 1), i16, g4, ka);
+    tile_scores(ka, qop, sc);
+  }
+  if (PV) tile_pv<F16>(tile_buf<TPS>(lds, t - 1) + TILEB, pp, st, i16, g4);
+  // one matrix instruction, then vector instructions, in turn
+  constexpr int n_mfma = QTW * 8 + (PV ? QTW * 8 * (F16 ? 1 : 2) : 0);
+#pragma unroll
+  for (int i = 0; i < n_mfma; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
+  }
+  bool rare = false;
+#pragma unroll
+  for (int qt = 0; qt < QTW; ++qt) rare = rare || !(psum[qt] <= kLazyExp);
+  if (__builtin_amdgcn_ballot_w64(rare)) {  // rare: raise the reference max
+#pragma unroll
+    for (int qt = 0; qt < QTW; ++qt)
+      if (__builtin_amdgcn_ballot_w64(!(psum[qt] <= kLazyExp))) {
+        u4 ka[8];
+        load_ka(tile_buf<TPS>(lds, t), i16, g4, ka);
+        f4 s0, s1;
+        qt_scores(ka, qop[qt], s0, s1);
+        float e[8];
+        psum[qt] = tile_raise(st[qt], s0, s1, scale_log2, e);
+        pn[qt] = pack_p<F16>(e);
+      }
+  }
+  if (n_valid < TILE) {
+    // the TILE - n_valid rows past the view's end each added 2^-m to their
+    // column's sum (logit 0); a quarter of that comes off each of the
+    // column's four lanes.  The fp16 bound above counted them, so their
+    // probability operands stay in range too.
+    const float gone = 0.25f * (float)(TILE - n_valid);
+#pragma unroll
+    for (int qt = 0; qt < QTW; ++qt)
+      psum[qt] = fmaf(-gone, __builtin_amdgcn_exp2f(-st[qt].m), psum[qt]);
+  }
+#pragma unroll
+  for (int qt = 0; qt < QTW; ++qt) {
+    st[qt].l += psum[qt];
+    st[qt].ls += psum[qt];
+    pp[qt] = pn[qt];
+  }
+}
+
+// the key-tile loop of one workgroup (see the file comment).  Returns the
+// view of the last tile.
 template <bool F16, int W, int TPS>
 __device__ __attribute__((always_inline)) inline int tile_loop(
     const Views& vs, int bh, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW],
@@ -245,7 +352,8 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
   const int T = vs.tiles;
   // tiles go through LDS in stages of TPS: stage j holds tiles TPS*j ..
   // TPS*j + TPS - 1; during stage j the tiles of stage j + 2 are loaded and,
-  // after its last tile, stored, and one barrier per stage publishes them
+  // after its last tile, stored, and one barrier per stage publishes them.
+  // During stage j the pipeline reads stages j - 1 .. j + 1.
   constexpr int NT = W * 64;
   Cursor<F16> ct, cs;  // tile t (computed) and the next tile to stage
   {
@@ -270,9 +378,11 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     load_ka(tile_buf<TPS>(lds, 0), i16, g4, ka);
     tile_scores(ka, qop, sc);
   }
+  POp pp[QTW];
   Stage S;
   int n_pre = 0;  // tiles of the stage in flight
-  for (int t = 0; t < T; ++t) {
+  // one iteration; the first (no previous tile to multiply with V) is peeled
+  auto iter = [&](int t, auto pv) {
     if (t % TPS == 0 && t + 2 * TPS < T) {  // the tiles of stage t/TPS + 2
       if (TPS == 1) {
         stage_load<F16, NT>(cs, S, 0);
@@ -290,7 +400,6 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
         }
       }
     }
-    const char* lv = tile_buf<TPS>(lds, t) + TILEB;
     const int vi = ct.vi;
     const int n_valid = min(TILE, ct.n - ct.row0);
     if (seg_lse && vi != cur_view && cur_view >= 0 && ct.seg != cur_seg) {
@@ -308,30 +417,10 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     cur_view = vi;
     cur_seg = ct.seg;
     ct.next(vs, bh);
-    u4 phi[QTW], plo[QTW];
-#pragma unroll
-    for (int qt = 0; qt < QTW; ++qt)
-      tile_softmax<F16>(st[qt], sc[qt][0], sc[qt][1], scale_log2, n_valid, g4, phi[qt], plo[qt]);
-    // scores of the next tile (its stage is published; past the last tile:
-    // a stale buffer, unused)
-    {
-      u4 ka[8];
-      load_ka(tile_buf<TPS>(lds, t + 1), i16, g4, ka);
-      tile_scores(ka, qop, sc);
-    }
-#pragma unroll
-    for (int d = 0; d < 8; ++d) {
-      const u4 vt = vt_operand(lv, d, i16, g4);
-#pragma unroll
-      for (int qt = 0; qt < QTW; ++qt) {
-        if (F16) {
-          st[qt].acc[d] = mfma_f16(vt, phi[qt], st[qt].acc[d]);
-        } else {
-          st[qt].acc[d] = mfma(vt, phi[qt], st[qt].acc[d]);
-          st[qt].acc[d] = mfma(vt, plo[qt], st[qt].acc[d]);
-        }
-      }
-    }
+    // past the last tile the next scores come from a stale buffer and are
+    // never used
+    tile_step<F16, TPS, decltype(pv)::value>(t, lds, qop, st, sc, pp, scale_log2, n_valid, i16,
+                                             g4);
     if (t % TPS == TPS - 1 || t == T - 1) {  // the stage's last tile
       const int t0 = t - t % TPS + 2 * TPS;  // first tile of the staged stage
       if (TPS == 1) {
@@ -346,7 +435,11 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
       n_pre = 0;
       __syncthreads();
     }
-  }
+  };
+  iter(0, std::false_type{});
+  for (int t = 1; t < T; ++t) iter(t, std::true_type{});
+  // the last tile's O += V^T P
+  tile_pv<F16>(tile_buf<TPS>(lds, T - 1) + TILEB, pp, st, i16, g4);
   return cur_view;
 }
 
