@@ -644,6 +644,56 @@ int device_cus() {
 namespace {
 
 // workgroups per (b, h_kv): two resident workgroups per CU in one round
+// Merge of a decode call's partial records into O (and lse) when every
+// record belongs to one softmax (no per-segment outputs): one wave per query
+// row, four rows per workgroup, each lane owning two of the 128 dims.  A
+// record is (m, l, o[D]) with m the base-2 reference of its running sums;
+// eight records are loaded at a time, every load issued before any is used,
+// and merged online; an empty record (m = -inf, other fields undefined) is
+// dropped by selects.
+__global__ __launch_bounds__(256) void decode_merge_kernel(int Q, int C,
+                                                           const float* __restrict__ partial,
+                                                           float* __restrict__ o,
+                                                           float* __restrict__ lse) {
+  const int qi = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (qi >= Q) return;
+  const int lane = threadIdx.x & 63;
+  const int ps = D + 2;
+  const float* P = partial + (int64_t)qi * C * ps;
+  float M = -INFINITY, l = 0.0f;
+  f2 acc = f2{0.0f, 0.0f};
+  for (int c0 = 0; c0 < C; c0 += 8) {
+    f2 ml[8], oc[8];
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const int c = min(c0 + r, C - 1);
+      ml[r] = *reinterpret_cast<const f2*>(P + (int64_t)c * ps);
+      oc[r] = *reinterpret_cast<const f2*>(P + (int64_t)c * ps + 2 + 2 * lane);
+    }
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+      if (c0 + r >= C) ml[r][0] = -INFINITY;
+    float mx = M;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) mx = fmaxf(mx, ml[r][0]);
+    const float a = M == -INFINITY ? 0.0f : __builtin_amdgcn_exp2f(M - mx);
+    l *= a;
+    acc *= a;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) {
+      const bool live = ml[r][0] != -INFINITY;
+      const float b = live ? __builtin_amdgcn_exp2f(ml[r][0] - mx) : 0.0f;
+      l = fmaf(b, live ? ml[r][1] : 0.0f, l);
+      acc[0] = fmaf(b, live ? oc[r][0] : 0.0f, acc[0]);
+      acc[1] = fmaf(b, live ? oc[r][1] : 0.0f, acc[1]);
+    }
+    M = mx;
+  }
+  const float inv = 1.0f / l;
+  *reinterpret_cast<f2*>(o + (int64_t)qi * D + 2 * lane) = acc * inv;
+  if (lse && lane == 0) lse[qi] = (M + __log2f(l)) * kLn2;
+}
+
 int decode_w(const uc_shape& sh) {
   const int BH = sh.B * sh.Hkv;
   return max(1, (2 * device_cus()) / BH);
@@ -710,8 +760,13 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   e = hipGetLastError();
   if (e == hipSuccess) e = kernel_timer_end(st);
   if (e != hipSuccess) return e;
-  // per-segment records are segment-major (segment s owns slots [s*W, (s+1)*W));
-  // otherwise all W records are attributed to the first segment (no seg_lse)
+  if (!p.per_seg) {  // one softmax: the lean merge
+    const int Q = sh.B * sh.Hq * M;
+    hipLaunchKernelGGL(decode_merge_kernel, dim3((Q + 3) / 4), dim3(256), 0, st, Q, p.W, partial,
+                       o, lse);
+    return hipGetLastError();
+  }
+  // per-segment records are segment-major (segment s owns slots [s*W, (s+1)*W))
   ChunkPlan cp{};
   cp.n_chunks = p.per_seg ? segs.n * p.W : p.W;
   for (int i = 0; i <= kMaxSeg; ++i)
@@ -758,12 +813,10 @@ hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, 
   e = hipGetLastError();
   if (e == hipSuccess) e = kernel_timer_end(st);
   if (e != hipSuccess) return e;
-  KSegs none{};
-  none.n = 1;
-  ChunkPlan cp{};
-  cp.n_chunks = p.W;
-  for (int i = 0; i <= kMaxSeg; ++i) cp.first[i] = i == 0 ? 0 : p.W;
-  return launch_attend_combine(sh, none, cp, M, partial, o, lse, nullptr, st);
+  const int Q = sh.B * sh.Hq * M;
+  hipLaunchKernelGGL(decode_merge_kernel, dim3((Q + 3) / 4), dim3(256), 0, st, Q, p.W, partial, o,
+                     lse);
+  return hipGetLastError();
 }
 
 }  // namespace uc
