@@ -17,9 +17,10 @@
 //           their total is the chunk's probability mass (Eq. 1 bracket).
 // Both passes compute S^T = K Q^T with v_mfma_f32_16x16x32_bf16: a wave
 // takes 32-key tiles of the chunk (keys straight from HBM into the A-operand
-// layout, two register sets in flight) and runs them against every 16-row
-// query tile of the block, whose B operands it reads from the block staged
-// in LDS.  Logits are in base 2 (q.k times scale*log2(e)).
+// layout; packed rows decoded in registers to their stored bf16 values) and
+// runs them against every 16-row query tile of the block, whose B operands
+// it reads from the block staged in LDS.  Logits are in base 2 (q.k times
+// scale*log2(e)).
 // Column sums: a lane sums its key's probabilities over the query tiles in
 // fp32, the 16 query columns of a tile are added by a butterfly, and the
 // query blocks are accumulated in fp64 in LDS; chunk masses are fp64.
@@ -56,6 +57,109 @@ __device__ inline void k_issue(__amdgpu_buffer_rsrc_t rk, int row0, int lane, u4
   for (int t = 0; t < 4; ++t) {
     k[t] = bload(rk, ko, t * 64);
     k[4 + t] = bload(rk, ko, 16 * ROWB + t * 64);
+  }
+}
+
+// Where one (b, h_kv)'s key rows of a segment come from: dense rows, or
+// (packed) code rows 0 .. n_full-1 decoded in registers and residual-tail
+// rows n_full .. read as stored.  n_full is a multiple of the group G >= 32,
+// so a 32-row tile is all codes or all tail, and a code tile lies inside one
+// key group (one scale and minimum per channel).
+struct KSrc {
+  __amdgpu_buffer_rsrc_t rk;   // dense rows, or the tail rows of a packed segment
+  __amdgpu_buffer_rsrc_t rc;   // packed: this head's code rows
+  const float* sk;             // packed: this head's key scales [groups, D]
+  const float* mk;             // packed: this head's key minima
+  int n_full, bits, G;         // n_full = 0 for dense segments
+  bool bad;                    // packed head whose device-side layout is invalid
+};
+
+__device__ inline KSrc k_source(const KSeg& ks, int bh, int r1) {
+  KSrc src{};
+  if (ks.kind == UC_SEG_DENSE) {
+    const int64_t base = (int64_t)bh * ks.row_stride * D;
+    src.rk = rsrc((const uint16_t*)ks.k + base, (uint32_t)r1 * ROWB);
+    return src;
+  }
+  src.n_full = ks.n_full;
+  src.G = ks.group;
+  const int64_t tb = (int64_t)bh * ks.tail_stride * D;
+  src.rk = rsrc((const uint16_t*)ks.tail_k + tb, (uint32_t)max(0, r1 - ks.n_full) * ROWB);
+  int bits;
+  int64_t off;
+  src.bad = !head_codes(ks, bh, D, bits, off) || (off & 15);
+  src.bits = bits;
+  const uint32_t rb = (uint32_t)(D * bits / 8);
+  src.rc = rsrc(ks.codes_k + (src.bad ? 0 : off), src.bad ? 0u : (uint32_t)ks.n_full * rb);
+  src.sk = ks.scale_k + (int64_t)bh * ks.kgroups * D;
+  src.mk = ks.min_k + (int64_t)bh * ks.kgroups * D;
+  return src;
+}
+
+// 8 channels of one code word (BITS per channel, least significant first)
+// as bf16 A-operand bits: round_to_bf16(fmaf(code, scale, min)), the stored
+// value of each code
+template <int BITS>
+__device__ inline u4 k_decode8(uint64_t w, const float (&sc)[8], const float (&mn)[8]) {
+  constexpr uint32_t mask = (1u << BITS) - 1;
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float a = fmaf((float)(uint32_t)((w >> (2 * j * BITS)) & mask), sc[2 * j], mn[2 * j]);
+    const float b = fmaf((float)(uint32_t)((w >> ((2 * j + 1) * BITS)) & mask), sc[2 * j + 1],
+                         mn[2 * j + 1]);
+    o[j] = bf2(a, b);
+  }
+  return u4{o[0], o[1], o[2], o[3]};
+}
+
+// channels c0 .. c0+7 of code rows ra and ra + 16 (one key group: shared
+// scales and minima)
+template <int BITS>
+__device__ inline void k_decode_pair(const KSrc& src, int ra, int c0, u4& ka, u4& kb) {
+  const int rb = D * BITS / 8;
+  uint64_t wa, wb;
+  if (BITS == 4) {
+    wa = bload32(src.rc, ra * rb + c0 / 2, 0);
+    wb = bload32(src.rc, (ra + 16) * rb + c0 / 2, 0);
+  } else if (BITS == 2) {
+    wa = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(src.rc, ra * rb + c0 / 4, 0, 0);
+    wb = (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(src.rc, (ra + 16) * rb + c0 / 4, 0, 0);
+  } else {
+    wa = __builtin_bit_cast(uint64_t, __builtin_amdgcn_raw_buffer_load_b64(src.rc, ra * rb + c0, 0, 0));
+    wb = __builtin_bit_cast(uint64_t,
+                            __builtin_amdgcn_raw_buffer_load_b64(src.rc, (ra + 16) * rb + c0, 0, 0));
+  }
+  const int64_t g = (int64_t)(ra / src.G) * D + c0;
+  const f4 s0 = *reinterpret_cast<const f4*>(src.sk + g), s1 = *reinterpret_cast<const f4*>(src.sk + g + 4);
+  const f4 m0 = *reinterpret_cast<const f4*>(src.mk + g), m1 = *reinterpret_cast<const f4*>(src.mk + g + 4);
+  const float sc[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+  const float mn[8] = {m0[0], m0[1], m0[2], m0[3], m1[0], m1[1], m1[2], m1[3]};
+  ka = k_decode8<BITS>(wa, sc, mn);
+  kb = k_decode8<BITS>(wb, sc, mn);
+}
+
+// a wave's 32-row key tile at row0 as A operands (see KTiles); without
+// PACKED every segment of the call is dense
+template <bool PACKED>
+__device__ inline void k_load(const KSrc& src, int row0, int lane, u4 (&k)[8]) {
+  if (!PACKED || row0 >= src.n_full) {  // dense rows, or a packed segment's tail
+    k_issue(src.rk, row0 - src.n_full, lane, k);
+    return;
+  }
+  const int i16 = lane & 15, g4 = lane >> 4;
+  if (src.bad) {
+    const uint32_t nan2 = 0x7FC07FC0u;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) k[t] = u4{nan2, nan2, nan2, nan2};
+    return;
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const int c0 = t * 32 + g4 * 8;
+    if (src.bits == 4) k_decode_pair<4>(src, row0 + i16, c0, k[t], k[4 + t]);
+    else if (src.bits == 2) k_decode_pair<2>(src, row0 + i16, c0, k[t], k[4 + t]);
+    else k_decode_pair<8>(src, row0 + i16, c0, k[t], k[4 + t]);
   }
 }
 
@@ -218,6 +322,7 @@ __device__ inline void col_sub(const KTiles& K, const char* qs, const float* ls,
 
 // ---------------------------------------------------------------- pass 1
 // grid (chunks, query blocks, b*h_kv); one (m, l) record per (row, chunk)
+template <bool PACKED>
 __global__ __launch_bounds__(256, 2) void score_lse_kernel(KSegs segs, ChunkPlan plan,
                                                            const uint16_t* __restrict__ q, int Hq,
                                                            int Hkv, int W, float scale_log2,
@@ -240,13 +345,12 @@ __global__ __launch_bounds__(256, 2) void score_lse_kernel(KSegs segs, ChunkPlan
   }
   __syncthreads();
 
-  const int64_t base = (int64_t)bh * ks.row_stride * D;
-  const __amdgpu_buffer_rsrc_t rk = rsrc((const uint16_t*)ks.k + base, (uint32_t)r1 * ROWB);
+  const KSrc src = k_source(ks, bh, r1);
   for (int sc = r0; sc < r1; sc += SUB) {
     // the wave's tiles of this sub-chunk: rows sc + (wave + i*WAVES)*TILE
     KTiles K;
 #pragma unroll
-    for (int i = 0; i < TPW; ++i) k_issue(rk, sc + (wave + i * WAVES) * TILE, lane, K.k[i]);
+    for (int i = 0; i < TPW; ++i) k_load<PACKED>(src, sc + (wave + i * WAVES) * TILE, lane, K.k[i]);
     if (sc + SUB <= r1)
       lse_sub<false>(K, qs, red_m[wave], red_l[wave], nqt, sc, r1, wave, lane, scale_log2);
     else
@@ -278,6 +382,7 @@ struct ScoreOut {
 // [s*qbs, (s+1)*qbs) of the head.  With one group the scores and chunk mass
 // are written directly; with several, each group's column sums (double) go
 // to colpart and score_col_reduce_kernel adds them in group order.
+template <bool PACKED>
 __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan plan,
                                                            const uint16_t* __restrict__ q, int Hq,
                                                            int Hkv, int W, float scale_log2,
@@ -300,8 +405,7 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
   const float* lh = lse + ((int64_t)b * Hq + hkv * G) * W;
   for (int e = threadIdx.x; e < CHUNK; e += blockDim.x) colsum[e] = 0.0;
 
-  const int64_t base = (int64_t)bh * ks.row_stride * D;
-  const __amdgpu_buffer_rsrc_t rk = rsrc((const uint16_t*)ks.k + base, (uint32_t)r1 * ROWB);
+  const KSrc src = k_source(ks, bh, r1);
   const int q_end = min(nq, (sg + 1) * qbs * QB);
   for (int q0 = sg * qbs * QB; q0 < q_end; q0 += QB) {
     const int nqt = min(QT, (nq - q0 + 15) / 16);
@@ -313,7 +417,7 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
     for (int sc = r0; sc < r1; sc += SUB) {
       KTiles K;
 #pragma unroll
-      for (int i = 0; i < TPW; ++i) k_issue(rk, sc + (wave + i * WAVES) * TILE, lane, K.k[i]);
+      for (int i = 0; i < TPW; ++i) k_load<PACKED>(src, sc + (wave + i * WAVES) * TILE, lane, K.k[i]);
       float cs[TPW][8];
 #pragma unroll
       for (int i = 0; i < TPW; ++i)
@@ -400,12 +504,21 @@ __global__ __launch_bounds__(256) void score_col_reduce_kernel(KSegs segs, Chunk
 
 bool score_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt) {
   if (sh.D != D || q_dt != UC_BF16) return false;
-  for (int i = 0; i < segs.n; ++i)
-    if (segs.s[i].kind != UC_SEG_DENSE || segs.s[i].dtype != UC_BF16) return false;
+  for (int i = 0; i < segs.n; ++i) {
+    if (segs.s[i].dtype != UC_BF16) return false;
+    // packed: key groups of >= 32 rows, so a 32-row tile shares one scale set
+    if (segs.s[i].kind == UC_SEG_PACKED && segs.s[i].group < TILE) return false;
+  }
   return true;
 }
 
 int score_mfma_chunk_rows() { return CHUNK; }
+
+static bool has_packed(const KSegs& segs) {
+  for (int i = 0; i < segs.n; ++i)
+    if (segs.s[i].kind == UC_SEG_PACKED && segs.s[i].n_full > 0) return true;
+  return false;
+}
 
 int score_mfma_qblocks(int nq) { return (nq + QB - 1) / QB; }
 
@@ -423,8 +536,12 @@ hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const Ch
                                  hipStream_t st) {
   const int nq = (sh.Hq / sh.Hkv) * W;
   dim3 grid(plan.n_chunks, score_mfma_qblocks(nq), sh.B * sh.Hkv);
-  hipLaunchKernelGGL(score_lse_kernel, grid, dim3(256), 0, st, segs, plan, (const uint16_t*)q,
-                     sh.Hq, sh.Hkv, W, sm_scale * kLog2e, partial);
+  if (has_packed(segs))
+    hipLaunchKernelGGL(score_lse_kernel<true>, grid, dim3(256), 0, st, segs, plan,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, sm_scale * kLog2e, partial);
+  else
+    hipLaunchKernelGGL(score_lse_kernel<false>, grid, dim3(256), 0, st, segs, plan,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, sm_scale * kLog2e, partial);
   return hipGetLastError();
 }
 
@@ -439,9 +556,14 @@ hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const Ch
   const int qbs = (qblocks + groups - 1) / groups;
   const int n_groups = (qblocks + qbs - 1) / qbs;
   dim3 grid(plan.n_chunks, n_groups, sh.B * sh.Hkv);
-  hipLaunchKernelGGL(score_col_kernel, grid, dim3(256), 0, st, segs, plan, (const uint16_t*)q,
-                     sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so, mass_partial, qbs,
-                     n_groups > 1 ? colpart : nullptr);
+  if (has_packed(segs))
+    hipLaunchKernelGGL(score_col_kernel<true>, grid, dim3(256), 0, st, segs, plan,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so,
+                       mass_partial, qbs, n_groups > 1 ? colpart : nullptr);
+  else
+    hipLaunchKernelGGL(score_col_kernel<false>, grid, dim3(256), 0, st, segs, plan,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so,
+                       mass_partial, qbs, n_groups > 1 ? colpart : nullptr);
   if (n_groups > 1)
     hipLaunchKernelGGL(score_col_reduce_kernel, dim3(plan.n_chunks, sh.B * sh.Hkv), dim3(256), 0,
                        st, segs, plan, n_groups, (const double*)colpart, so, mass_partial);

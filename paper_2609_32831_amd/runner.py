@@ -371,12 +371,6 @@ class DynamicRun:
         # raw per-segment masses of every timestep (uc_segment_mass)
         self.mass = torch.zeros(w.steps, 1, Hkv, self.nseg, device=device)
         self.scores = torch.empty(1, Hkv, self.n_ev, device=device)
-        # the quantised type's current rows, dequantised: the source of a
-        # re-quantisation and, as a dense segment, what the re-scoring sees
-        # (the same values attention reads), so scoring runs on matrix cores
-        self.deq_k = torch.empty(1, Hkv, self.n_qt, D, dtype=self.tdt, device=device)
-        self.deq_v = torch.empty_like(self.deq_k)
-        self.deq = dense_segment(self.deq_k, self.deq_v)
         # budget decisions on the device
         self.params = uc_budget_params(Hq, Hkv, D, M, self.nseg, self.ev, self.qt, self.n_ev,
                                        self.n_qt, self.dt, w.rho_init, w.rho_min)
@@ -403,9 +397,7 @@ class DynamicRun:
         composed logical indices)."""
         w = self.w
         Hkv, D = w.Hkv, w.D
-        segs = self.segments()
-        if self.packed is not None:
-            segs[self.qt] = self.deq
+        segs = self.segments()  # the quantised type is scored in its packed form
         n_cur = segs[self.ev].n_rows
         sc = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)  # contiguous [1, Hkv, n_cur]
         outs = [None] * self.nseg
@@ -428,7 +420,9 @@ class DynamicRun:
 
     def _quantize(self, cfg):
         """(Re-)quantise the quantised type with configuration cfg, from its
-        original rows the first time, else from its dequantised rows."""
+        original rows the first time, else from its current rows decoded into
+        a buffer that lives only for this call (the packed segment is all that
+        stays resident)."""
         w = self.w
         _, bits, group = cfg
         pk = packed_segment(1, w.Hkv, self.n_qt, w.D, group, self.tdt, bits=bits,
@@ -436,9 +430,10 @@ class DynamicRun:
         if self.packed is None:
             src_k, src_v = self.dense[self.qt].t["k"], self.dense[self.qt].t["v"]
         else:
-            src_k, src_v = self.deq_k, self.deq_v  # the current rows, dequantised
+            src_k = torch.empty(1, w.Hkv, self.n_qt, w.D, dtype=self.tdt, device=self.device)
+            src_v = torch.empty_like(src_k)
+            uc_dequantize_segment(self.shape, self.packed, src_k, src_v)
         uc_quantize_segment(self.shape, src_k, src_v, self.n_qt, pk)
-        uc_dequantize_segment(self.shape, pk, self.deq_k, self.deq_v)
         self.packed, self.cfg = pk, cfg
 
     def _boundary(self, t, t0, n, q_obs, W):

@@ -303,6 +303,59 @@ def test_score_parity(B, Hq, Hkv, D, dtype, W, sizes):
         assert np.allclose(got.sum(axis=2), tot, rtol=1e-5), path
 
 
+SPCASES = [
+    # B, Hq, Hkv, W, G, bits, per_head, (text, packed rows); packed rows past
+    # n_full form the tail
+    (1, 28, 4, 32, 64, 4, False, (300, 4096 + 17)),
+    (2, 14, 2, 40, 32, 2, True, (0, 2000 + 5)),     # int2/int4 per head, two query blocks
+    (1, 28, 4, 5, 128, 8, False, (64, 1030)),
+    (1, 14, 2, 8, 16, 4, False, (100, 333)),        # groups below 32: the VALU scorer
+]
+
+
+@pytest.mark.parametrize("case", SPCASES, ids=[f"sp{i}" for i in range(len(SPCASES))])
+def test_score_parity_packed(case):
+    """Scoring over a cache holding a packed segment: the matrix-core passes
+    decode its code rows in registers (keys only) and read its tail rows as
+    stored; scores and masses match the oracle over the dequantised keys."""
+    B, Hq, Hkv, W, G, bits, per_head, (n_text, n_pack) = case
+    D = 128
+    _print_case(test="score_packed", B=B, Hq=Hq, Hkv=Hkv, W=W, G=G, bits=bits, sizes=(n_text, n_pack))
+    BH = B * Hkv
+    kt = rand_rows(61, BH, n_text, D, "bf16", outliers=(3,))
+    vt = rand_rows(62, BH, n_text, D, "bf16")
+    kp = rand_rows(63, BH, n_pack, D, "bf16", 2.0, outliers=(3, 77))
+    vp = rand_rows(64, BH, n_pack, D, "bf16")
+    hb = [bits] * BH if not per_head else [4 if (i % 3) else 2 for i in range(BH)]
+    pk = ref.quantize(kp, vp, "bf16", G, hb)
+    segs = [uc.dense_segment(dev(kt, "bf16").reshape(B, Hkv, n_text, D),
+                             dev(vt, "bf16").reshape(B, Hkv, n_text, D)),
+            packed_from_oracle(B, Hkv, n_pack, D, G, "bf16", pk, per_head=per_head)]
+    khp, _ = ref.dequant(pk, n_pack, D, G, "bf16")
+    K = np.concatenate([ref.widen(kt, "bf16"), khp], axis=1).reshape(B, Hkv, -1, D)
+    seg_id = np.asarray([0] * n_text + [1] * n_pack, np.int32)
+    q = rand_rows(65, B * Hq, W, D, "bf16").reshape(B, Hq, W, D)
+    sc_ref, ms_ref = ref.score64(ref.widen(q, "bf16"), K, seg_id, 2, sm_scale(D))
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    tot = Hq // Hkv * W
+    want_kernel = "score_mfma" if G >= 32 else "score_valu"
+    for path, kernel in ((uc.UC_PATH_AUTO, want_kernel), (uc.UC_PATH_VALU, "score_valu")):
+        prev = uc.uc_set_path(path)
+        try:
+            outs = [torch.empty(B, Hkv, n, device="cuda") for n in (n_text, n_pack)]
+            mass = torch.empty(B, Hkv, 2, device="cuda")
+            uc.uc_score_importance(shape, segs, dev(q, "bf16"), W, sm_scale(D), outs, mass)
+            assert uc.uc_last_kernel() == kernel, (path, uc.uc_last_kernel())
+            torch.cuda.synchronize()
+        finally:
+            uc.uc_set_path(prev)
+        got = np.concatenate([o.cpu().numpy().reshape(B, Hkv, -1) for o in outs],
+                             axis=2).astype(np.float64)
+        assert np.all(np.abs(got - sc_ref) <= 2e-5 * sc_ref + 1e-7 * tot), (kernel, np.max(
+            np.abs(got - sc_ref) / np.maximum(sc_ref, 1e-12)))
+        assert np.allclose(mass.cpu().numpy(), ms_ref, rtol=2e-5, atol=1e-6 * tot), kernel
+
+
 def test_segment_mass_from_attention():
     B, Hq, Hkv, D, M = 2, 28, 4, 128, 9
     segs, K, V, seg_id = _mixed_case(B, Hq, Hkv, D, "bf16", (64, 400, 100, 256, 3, 8), seed=3)
