@@ -22,7 +22,7 @@ from typing import Dict, List, Optional, Sequence, Tuple
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(HERE, "libucref.so")
+_LIB_PATH = os.environ.get("UCREF_LIB") or os.path.join(HERE, "libucref.so")  # override: sanitized builds
 _lib = None
 
 DT = {"f32": 0, "f16": 1, "bf16": 2}

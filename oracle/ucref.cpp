@@ -280,7 +280,7 @@ int ucref_select(int BH, int N, const float* scores, int k, int n_recent,
     std::vector<int32_t> kept(order.begin(), order.begin() + (k - n_recent));
     for (int i = N - n_recent; i < N; ++i) kept.push_back(i);
     std::sort(kept.begin(), kept.end());
-    std::memcpy(keep_idx + (int64_t)bh * k, kept.data(), sizeof(int32_t) * k);
+    if (k > 0) std::memcpy(keep_idx + (int64_t)bh * k, kept.data(), sizeof(int32_t) * k);
   }
   return 0;
 }

@@ -15,7 +15,9 @@ from typing import List, Optional, Sequence
 import torch
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libunicache.so")
+# UNICACHE_LIB: another build of the same library (the host-sanitized one
+# the CPU tests can run against)
+LIB_PATH = os.environ.get("UNICACHE_LIB") or os.path.join(HERE, "libunicache.so")
 
 UC_OK, UC_E_INVALID, UC_E_UNSUPPORTED, UC_E_WORKSPACE, UC_E_DEVICE = range(5)
 UC_F32, UC_F16, UC_BF16 = 0, 1, 2

@@ -37,9 +37,15 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def _compile(src: str, verbose: bool) -> str:
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC] + FLAGS + ["-c", src, "-o", obj]
+# host code only: the device code of a sanitized build is the ordinary one
+SAN_HOST = ["-Xarch_host", "-fsanitize=address,undefined", "-Xarch_host",
+            "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+SAN_DIR = os.path.join(BUILD, "sanitize")
+
+
+def _compile(src: str, verbose: bool, sanitize: bool = False) -> str:
+    obj = os.path.join(SAN_DIR if sanitize else BUILD, os.path.basename(src) + ".o")
+    cmd = [HIPCC] + FLAGS + (SAN_HOST if sanitize else []) + ["-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -50,19 +56,24 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, sanitize: bool = False) -> str:
+    """sanitize: AddressSanitizer + UndefinedBehaviorSanitizer on the host
+    code (argument validation, planning), into _build/sanitize/ (for the CPU
+    tests under oracle/sanitize.py; never run on a GPU)."""
+    os.makedirs(SAN_DIR if sanitize else BUILD, exist_ok=True)
+    lib = os.path.join(SAN_DIR, "libunicache.so") if sanitize else LIB
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-o", LIB + ".tmp"] + objs
+        objs = list(ex.map(lambda s: _compile(s, verbose, sanitize), srcs))
+    link = ["-shared-libsan", "-Xarch_host", "-fsanitize=address,undefined"] if sanitize else []
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC"] + link + ["-o", lib + ".tmp"] + objs
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(lib + ".tmp", lib)
+    return lib
 
 
 if __name__ == "__main__":
-    build(verbose="-v" in sys.argv)
+    build(verbose="-v" in sys.argv, sanitize="--sanitize" in sys.argv)
     print("built", LIB)

@@ -26,7 +26,7 @@ from typing import Dict, List, Optional, Tuple
 import numpy as np
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-_LIB_PATH = os.path.join(HERE, "libucgen.so")
+_LIB_PATH = os.environ.get("UCGEN_LIB") or os.path.join(HERE, "libucgen.so")  # override: sanitized builds
 _lib = None
 
 DTYPE_CODE = {"f32": 0, "f16": 1, "bf16": 2}
