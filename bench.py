@@ -675,8 +675,13 @@ def dynamic_bench(args):
     from paper_2609_32831_amd.runner import DynamicRun
     from workloads.device import device_inputs
 
+    from paper_2609_32831_amd.calibrate import calibrate_rho_min, realized_compression
+
     w = gen.IMAGE_EDITING_DYNAMIC
     inp = device_inputs(w, "cuda")
+    # rho_min calibrated to the workload's target average compression (App. B)
+    cal = calibrate_rho_min(w, inp, w.target_compression, requests=list(range(w.B)))
+    w = gen.scaled(w, rho_min=cal["rho_min"])
     qs = [inp["q_pre"](t) for t in range(w.steps)]
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
@@ -710,9 +715,15 @@ def dynamic_bench(args):
     att = sum(sum(r["att"][1:]) for r in res)
     bnd = sum(sum(r["bnd"][1:]) for r in res)
     last = res[0]["dec"][max(res[0]["dec"])]
+    realized = sum(realized_compression(w, r["dec"]) for r in res) / len(res)
     print(json.dumps({"metric": "dynamic budget overhead (Eq. 1-3 at chunk boundaries)",
                       "workload": w.name, "requests": w.B, "timesteps": w.steps,
                       "chunk_steps": w.chunk_steps,
+                      "compression": {"target": w.target_compression,
+                                      "realized": round(realized, 5),
+                                      "rho_init": w.rho_init,
+                                      "rho_min_calibrated": round(w.rho_min, 6),
+                                      "calibration_probes": len(cal["probes"])},
                       "full_kv_step_ms": round(att0 / w.B, 4),
                       "initial_compression_ms": round(init / w.B, 4),
                       "compressed_step_ms": round(att / w.B / (w.steps - 1), 4),

@@ -17,8 +17,8 @@ import numpy as np
 
 import workloads as gen
 
-from . import (assign_bits, attend, dense_bytes, dequant, evict_rows, packed_bytes, quant_config,
-               quantize, retention_next, score64, select, type_budget, widen)
+from . import (ELEM, assign_bits, attend, dense_bytes, dequant, evict_rows, packed_bytes,
+               quant_config, quantize, retention_next, score64, select, type_budget, widen)
 
 
 def sm_scale(D: int) -> float:
@@ -426,3 +426,65 @@ def budget_chain(w, b: int, steps: List[int], rows: Optional[np.ndarray] = None,
             acc = {a: 0.0 for a in range(nseg)}
             n_acc = 0
     return out
+
+
+def realized_compression(w, decisions: Dict[int, Dict]) -> float:
+    """Average KV compression a dynamic-budget run achieves (App. B,
+    "Compression Ratio": the realized ratio recorded against the target):
+    1 - the mean, over the timesteps that attend the compressed cache
+    (t = 1 .. steps-1), of stored / original bytes of the cached segments.
+    The state of timestep t is the decision of the last boundary before it.
+    Cached segments are the kept, eviction- and quantisation-managed ones;
+    protected segments (the current step's own tokens) are no part of the
+    cache.  Bytes per (b, h_kv): kept rows dense, kept evicted rows plus an
+    int32 index each, packed codes with float scales and minima and the
+    residual tail."""
+    D = w.D
+    cached = [s for s in w.segments if s.policy != "protect"]
+    orig = sum(dense_bytes(s.n, D, s.dtype) for s in cached)
+    bounds = sorted(decisions)
+    tot = 0.0
+    for t in range(1, w.steps):
+        d = decisions[max(b for b in bounds if b < t)]
+        stored = 0
+        for s in cached:
+            if s.policy == "keep":
+                stored += dense_bytes(s.n, D, s.dtype)
+            elif s.policy == "evict":
+                stored += d["k"] * (2 * D * ELEM[s.dtype] + 4)
+            else:
+                stored += packed_bytes(s.n, D, d["group"], d["bits"], s.dtype)
+        tot += stored / orig
+    return 1.0 - tot / (w.steps - 1)
+
+
+def calibrate_rho_min(w, target: float, requests: Optional[List[int]] = None,
+                      iters: int = 12) -> Dict:
+    """App. B, "Calibration Setting": the minimum retention ratio rho_min that
+    makes the average realized compression of the dynamic run (requests'
+    mean) match the target.  The realized compression does not increase
+    with rho_min (a higher floor keeps at least as many bytes at every
+    boundary), so it is found by bisection on [0, rho_init]: a probe whose
+    compression exceeds the target raises the lower end.  Returns the last
+    probe and every probe's (rho_min, compression)."""
+    import workloads as gen
+    requests = [0] if requests is None else requests
+
+    def f(x):
+        wx = gen.scaled(w, rho_min=x)
+        return sum(realized_compression(wx, budget_chain(wx, b, [])["decisions"])
+                   for b in requests) / len(requests)
+
+    lo, hi = 0.0, w.rho_init
+    probes = []
+    x = hi
+    for _ in range(iters):
+        x = 0.5 * (lo + hi)
+        c = f(x)
+        probes.append((x, c))
+        if c > target:
+            lo = x
+        else:
+            hi = x
+    best = min(probes, key=lambda p: abs(p[1] - target))
+    return {"rho_min": best[0], "compression": best[1], "probes": probes}

@@ -58,3 +58,29 @@ def test_calibration_long_context_64k():
             want = ref.topk_mass(part, int(math.ceil(0.1 * s.n)))[0]
             got = f[b * w.Hkv + h, i]
             assert abs(got - want) <= 1e-5 * want + 1e-6, (b, h, s.name, got, want)
+
+
+def test_rho_min_calibration_against_oracle():
+    """rho_min calibration (App. B) on the editing workload with 128-row query
+    blocks: at two of the GPU bisection's probes the oracle's own chain gives
+    the same realized compression."""
+    from paper_2609_32831_amd.calibrate import calibrate_rho_min
+    w = gen.scaled(gen.IMAGE_EDITING_DYNAMIC, M=128, W=128)
+    inp = device_inputs(w, "cuda")
+    res = calibrate_rho_min(w, inp, w.target_compression, requests=[0], iters=8)
+    print("CASE rho_min calibration M=128", res["rho_min"], res["compression"], flush=True)
+    for x, c in (res["probes"][0], res["probes"][-1]):
+        wx = gen.scaled(w, rho_min=x)
+        want = op.realized_compression(wx, op.budget_chain(wx, 0, [])["decisions"])
+        assert abs(c - want) <= 1e-12, (x, c, want)
+
+
+def test_rho_min_calibration_full_size():
+    """Full size, both requests: the calibrated rho_min gives an average
+    realized compression within 0.5 percentage points of the 80 % target."""
+    from paper_2609_32831_amd.calibrate import calibrate_rho_min
+    w = gen.IMAGE_EDITING_DYNAMIC
+    inp = device_inputs(w, "cuda")
+    res = calibrate_rho_min(w, inp, w.target_compression, requests=list(range(w.B)), iters=12)
+    print("CASE rho_min calibration full", res, flush=True)
+    assert abs(res["compression"] - w.target_compression) <= 0.005, res

@@ -35,7 +35,7 @@ ELEM_BYTES = {"f32": 4, "f16": 2, "bf16": 2}
 
 # tensor ids used in stream keys
 T_K, T_V, T_QOBS, T_QDEC, T_KDEC, T_VDEC, T_QPRE = 1, 2, 3, 4, 5, 6, 7
-T_OUTLIER, T_UDIR, T_TAU, T_DRIFT_Q, T_DRIFT_K = 8, 9, 10, 11, 12
+T_OUTLIER, T_UDIR, T_TAU, T_DRIFT_Q, T_DRIFT_K, T_SELFDIR = 8, 9, 10, 11, 12, 13
 
 
 def lib():
@@ -121,6 +121,7 @@ class SegSpec:
     bits: Optional[int] = None          # fixed code width, None = per-head by budget
     group: Optional[int] = None
     heavy_tail: bool = False            # Student-t heavy hitters on its keys
+    self_align: float = 0.0             # keys += self_align * (the head's self direction)
 
 
 @dataclass(frozen=True)
@@ -151,6 +152,14 @@ class Workload:
     rho_init: float = 0.0
     rho_min: float = 0.0
     obs_window: int = 0
+    # prefill queries of timestep t are pulled along their KV head's self
+    # direction by self_pull * min(1, t / self_ramp) (attention moving to the
+    # current latent's own tokens as denoising proceeds)
+    self_pull: float = 0.0
+    self_ramp: int = 1
+    # target average compression (1 - stored / original bytes of the cached
+    # segments) that the minimum retention ratio is calibrated to
+    target_compression: Optional[float] = None
     seed: int = 0
     notes: str = ""
 
@@ -214,11 +223,16 @@ IMAGE_EDITING_DYNAMIC = Workload(
        "name": "image_editing_dynamic",
        "segments": (SegSpec("text", 1024, "keep", "bf16"),
                     SegSpec("vit", 4096, "evict", "bf16"),
-                    SegSpec("vae", 4096, "quant", "bf16", bits=None, group=None)),
+                    SegSpec("vae", 4096, "quant", "bf16", bits=None, group=None),
+                    SegSpec("self", 1024, "protect", "bf16", self_align=6.0)),
        "budget_ratio": None, "chunk_steps": 5, "rho_init": 0.30, "rho_min": 0.15,
-       "obs_window": 32,
-       "notes": "editing with Eq. 1-3: chunks of 5 timesteps, rho from 0.30 down to "
-                "at least 0.15 with the candidate mass, Eq. 2 type budgets"})
+       "obs_window": 32, "self_pull": 10.0, "self_ramp": 10, "target_compression": 0.75,
+       "notes": "editing with Eq. 1-3: chunks of 5 timesteps, rho from 0.30 down to at "
+                "least rho_min with the candidate mass, Eq. 2 type budgets; a protected "
+                "self segment (the current latent's own tokens) draws attention away "
+                "from the cached conditioning as the timesteps advance; rho_min "
+                "calibrated to 75 % average compression (the first chunk at rho_init "
+                "and the kept text bound what this cache can reach)"})
 
 # The 64k decode workload with a streaming residual tail: each decode step's
 # K/V row enters the int4 text segment's bf16 tail, and every 64 rows form a
@@ -312,17 +326,36 @@ def segment_kv(w: Workload, seg_index: int, which: str, bh0: int = 0,
     if seg.heavy_tail:
         ad = heavy_dir(w, bh0, nbh)
         rc = heavy_coef(w, seg_index, bh0, nbh, row0, n)
+    elif seg.self_align:
+        ad = seg.self_align * self_dir(w, bh0, nbh)
     return _rows(base, bh0, nbh, n, w.D, row0, seg.dtype, cs, ad, rc, master=master)
 
 
-def _query_dir(w: Workload, bh0q: int, nbhq: int) -> Optional[np.ndarray]:
-    if not any(s.heavy_tail for s in w.segments):
+def self_dir(w: Workload, bh0: int, nbh: int) -> np.ndarray:
+    """Unit direction per KV row-block shared by a self segment's keys and
+    the pulled prefill queries of that KV head."""
+    u = np.empty((nbh, w.D))
+    for i in range(nbh):
+        z = normal(stream(w.seed, w.recipe_id, T_SELFDIR, bh0 + i), 0, w.D)
+        u[i] = z / np.sqrt(np.sum(z * z))
+    return u
+
+
+def _query_dir(w: Workload, bh0q: int, nbhq: int, tensor: int = 0,
+               step: int = 0) -> Optional[np.ndarray]:
+    heavy = any(s.heavy_tail for s in w.segments)
+    pull = w.self_pull * min(1.0, step / w.self_ramp) if tensor == T_QPRE else 0.0
+    if not heavy and pull == 0.0:
         return None
-    out = np.empty((nbhq, w.D))
+    out = np.zeros((nbhq, w.D))
     for i in range(nbhq):
         bq = bh0q + i
         b, h = divmod(bq, w.Hq)
-        out[i] = 2.0 * heavy_dir(w, b * w.Hkv + h // w.group_size, 1)[0]
+        bh = b * w.Hkv + h // w.group_size
+        if heavy:
+            out[i] += 2.0 * heavy_dir(w, bh, 1)[0]
+        if pull:
+            out[i] += pull * self_dir(w, bh, 1)[0]
     return out
 
 
@@ -334,7 +367,7 @@ def queries(w: Workload, tensor: int, n: int, row0: int = 0, bh0: int = 0,
     nbh = w.B * w.Hq if nbh is None else nbh
     base = stream(w.seed, w.recipe_id, tensor, step)
     return _rows(base, bh0, nbh, n, w.D, row0, w.q_dtype,
-                 add_dir=_query_dir(w, bh0, nbh), master=master)
+                 add_dir=_query_dir(w, bh0, nbh, tensor, step), master=master)
 
 
 def decode_kv(w: Workload, which: str, row0: int, n: int, bh0: int = 0,
