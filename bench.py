@@ -421,6 +421,25 @@ def cpu_prefill_baseline(w, stride: int = 16):
                        f"{w.B * w.Hkv} KV heads")}
 
 
+def t2i_stored_per_head(w, bits) -> float:
+    """Mean stored bytes per KV head of the text-to-image cache: kept text plus
+    the latent at each head's width."""
+    from paper_2609_32831_amd import NAME_DT, uc_dense_bytes, uc_packed_bytes
+    text, lat = w.segments
+    per = [uc_dense_bytes(text.n, w.D, NAME_DT[text.dtype])
+           + uc_packed_bytes(lat.n, w.D, lat.group, b, NAME_DT[lat.dtype]) for b in bits]
+    return sum(per) / len(per)
+
+
+def static_compression(w, stored_per_head: float) -> dict:
+    """Target and realized compression of a workload's cache (original bytes
+    at the I/O element type over stored bytes per KV head; protected decode
+    tails are no part of either)."""
+    from paper_2609_32831_amd import NAME_DT, uc_dense_bytes
+    orig = sum(uc_dense_bytes(s.n, w.D, NAME_DT[w.q_dtype]) for s in w.segments)
+    return {"target_x": w.budget_ratio, "realized_x": round(orig / stored_per_head, 5)}
+
+
 def prefill_bench(args):
     """Multi-query attention steps of the editing (4096-query blocks against
     text + compacted ViT + int4 VAE, fixed cache, fresh queries) and
@@ -477,6 +496,7 @@ def prefill_bench(args):
                       "kernel_ms": round(t_k, 4),
                       "kernel_frac_of_bf16_peak": round(fl / t_k / 1e9 / BF16_PEAK_TFLOPS, 4),
                       "gflop_per_step": round(fl / 1e9, 1), "attended_rows": n_att,
+                      "compression": static_compression(w, run.stored_bytes_per_head()),
                       "compress_ms": round(t_c, 3), "steps": n,
                       "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)}),
           flush=True)
@@ -502,6 +522,7 @@ def prefill_bench(args):
                       "kernel_frac_of_bf16_peak": round(fl / t_k / 1e9 / BF16_PEAK_TFLOPS, 4),
                       "gflop_per_step": round(fl / 1e9, 1), "attended_rows": w.n_context,
                       "step_with_requantise_ms": round(t_s, 4), "bits": run.bits[:8],
+                      "compression": static_compression(w, t2i_stored_per_head(w, run.bits)),
                       "steps": n,
                       "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)}),
           flush=True)
@@ -1004,7 +1025,11 @@ def main():
                      "traffic": traffic,
                      "kernel": "decode_mfma_kernel",
                      "avg_launch_us": round(kern_us, 2),
-                     "algorithmic_bytes_per_launch": int(avg_bytes)},
+                     "algorithmic_bytes_per_launch": int(avg_bytes),
+                     # the whole attention call: the kernel and the merge of
+                     # its partial records
+                     "call_frac": round(call_bytes / (att_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4)},
+        "compression": static_compression(w, run.stored_bytes_per_head()),
         "attend_call_us": round(att_us, 2),
         "attend_call_frac": round(call_bytes / (att_us * 1e-6) / 1e9 / HBM_PEAK_GBPS, 4),
         "decode_step_us": round(decode_ms / T * 1e3, 2),
