@@ -373,11 +373,28 @@ struct DecodePlan {
   int n_seg;
   int per_seg;  // 1: one record per segment and workgroup
   int split;    // segment taken around the others (see above), or -1
+  int skew;     // share weights of a head's early / late workgroups, see share_row_skewed
 };
 
 // tile-aligned share w of n rows among W workgroups
 __device__ inline int share_row(int n, int w, int W) {
   const int64_t r = ((int64_t)n * w + W - 1) / W;
+  const int64_t rt = (r + TILE - 1) / TILE * TILE;
+  return (int)(rt < n ? rt : n);
+}
+
+// Share boundaries when the first W/2 workgroups of a head are dispatched in
+// the launch's first half and the others in its second half: weights
+// 1000 + skew for the first, 1000 - skew for the second (integer sums, so
+// the last share ends exactly at n).  With two workgroups per CU the one
+// dispatched first wins the issue arbitration: with equal shares it finished
+// far ahead of its partner and the launch ended with one workgroup per CU.
+__device__ inline int share_row_skewed(int n, int w, int W, int skew) {
+  const int h = W / 2;
+  auto cum = [&](int x) {
+    return (int64_t)min(x, h) * (1000 + skew) + (int64_t)max(x - h, 0) * (1000 - skew);
+  };
+  const int64_t r = ((int64_t)n * cum(w) + cum(W) - 1) / cum(W);
   const int64_t rt = (r + TILE - 1) / TILE * TILE;
   return (int)(rt < n ? rt : n);
 }
@@ -573,8 +590,9 @@ __device__ __attribute__((always_inline)) inline void decode_body(
     // shares of the other segments are the remainders; workgroup 0 already
     // holds the start of the protected segment
     const int ws = (!BATCH && ap.n_new > 0 && si == n_seg - 1) ? Wr - 1 - w : w;
-    int r0 = share_row(ks.n_rows, ws, Wr);
-    int r1 = share_row(ks.n_rows, ws + 1, Wr);
+    int r0 = BATCH ? share_row(ks.n_rows, ws, Wr) : share_row_skewed(ks.n_rows, ws, Wr, pl.skew);
+    int r1 = BATCH ? share_row(ks.n_rows, ws + 1, Wr)
+                   : share_row_skewed(ks.n_rows, ws + 1, Wr, pl.skew);
     if (split >= 0 && si == split) {
       // r0 is tile-aligned, so both parts start on a tile boundary and only
       // the second can end in a partial tile
@@ -598,8 +616,23 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
                                                              int Hq, int Hkv, int M,
                                                              float scale_log2,
                                                              float* __restrict__ partial) {
-  decode_body<false>(segs, nullptr, nullptr, pl, ap, blockIdx.x, blockIdx.y, q, Hq, Hkv, M,
-                     scale_log2, partial);
+  // one-dimensional grid of W * BH workgroups, dispatched in order: the first
+  // half of the launch holds workgroups 0 .. W/2-1 of every head, the second
+  // half the others, so every head has workgroups of both halves
+  const int BH = gridDim.x / pl.W, h = pl.W / 2, L = blockIdx.x;
+  int w, bh;
+  if (h == 0) {
+    w = 0;
+    bh = L;
+  } else if (L < h * BH) {
+    bh = L / h;
+    w = L % h;
+  } else {
+    const int L2 = L - h * BH, hh = pl.W - h;
+    bh = L2 / hh;
+    w = h + L2 % hh;
+  }
+  decode_body<false>(segs, nullptr, nullptr, pl, ap, w, bh, q, Hq, Hkv, M, scale_log2, partial);
 }
 
 __global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* __restrict__ table,
@@ -738,6 +771,10 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   }
   p.n_seg = segs.n;
   p.per_seg = seg_lse != nullptr;
+  // a grid of exactly two workgroups per CU pairs every early workgroup with
+  // a late one: the early ones take 1.6 / 2 of a pair's share (the best of
+  // weights 0 .. 900 per mille measured on the 64k context)
+  p.skew = p.W * sh.B * sh.Hkv == 2 * device_cus() ? 600 : 0;
   // split the largest dense segment around the others when packed rows are
   // present (staggered packed phases, see DecodePlan)
   p.split = -1;
@@ -754,7 +791,7 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   float* partial = (float*)ws;
   hipError_t e = kernel_timer_begin(st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(decode_mfma_kernel, dim3(p.W, sh.B * sh.Hkv), dim3(256), 0, st, segs, p,
+  hipLaunchKernelGGL(decode_mfma_kernel, dim3(p.W * sh.B * sh.Hkv), dim3(256), 0, st, segs, p,
                      ap ? *ap : none, (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e,
                      partial);
   e = hipGetLastError();
