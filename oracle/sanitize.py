@@ -32,7 +32,8 @@ def main(argv):
     env["UNICACHE_LIB"] = lbuild.build(sanitize=True)
     rt = subprocess.run([obuild.CLANG, "-print-file-name=libclang_rt.asan-x86_64.so"],
                         capture_output=True, text=True, check=True).stdout.strip()
-    env["LD_PRELOAD"] = rt
+    # the sanitizer runtime must come first; anything already preloaded stays
+    env["LD_PRELOAD"] = ":".join(p for p in (rt, env.get("LD_PRELOAD", "")) if p)
     # the interpreter itself is not instrumented: leak checking would report
     # its own allocations
     env["ASAN_OPTIONS"] = "detect_leaks=0:halt_on_error=1:abort_on_error=1"
