@@ -41,14 +41,16 @@ namespace {
 
 using namespace mf;
 
-constexpr int QTW = 2;                     // query tiles per wave
 constexpr int STAGES = 4;                  // stages in LDS: t-1 .. t+1 in use, t+2 staged
 constexpr int SUBB = 2 * TILEB;            // one tile: K rows + V rows
-// Two layouts: W waves per workgroup and TPS tiles per stage (one barrier per
-// stage).  <4, 1>: 128 query rows, two workgroups per CU; <8, 2>: 256 query
-// rows, one workgroup per CU, half the barriers and staging per query row.
-template <int W>
-constexpr int qrows() { return W * QTW * 16; }
+// Layouts: W waves per workgroup, TPS tiles per stage (one barrier per
+// stage) and QT 16-row query tiles per wave.  <4, 1, 2>: 128 query rows, two
+// workgroups per CU; <8, 2, 2>: 256 query rows, one workgroup per CU, half
+// the barriers and staging per query row; <4, 1, 4>: 256 query rows, one
+// wave per SIMD with 64 query rows, so every K and V operand read from LDS
+// serves twice the products.
+template <int W, int QT>
+constexpr int qrows() { return W * QT * 16; }
 constexpr float kLazy = 8.0f;
 constexpr float kLazyExp = 256.0f;  // 2^kLazy
 constexpr int kMaxViews = 2 * kMaxSeg;
@@ -169,13 +171,9 @@ __device__ inline float tile_exp(const QState& st, const f4& s0, const f4& s1, f
                                  float (&e)[8]) {
   float p[8];
   tile_logits(s0, s1, p);
-  float psum = 0.0f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
-    psum += e[j];
-  }
-  return psum;
+  for (int j = 0; j < 8; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
+  return ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
 }
 
 // rare path: raise the reference to the column maximum, rescale the running
@@ -197,13 +195,9 @@ __device__ inline float tile_raise(QState& st, const f4& s0, const f4& s1, float
 #pragma unroll
   for (int d = 0; d < 8; ++d) st.acc[d] *= alpha;
   st.m = m_new;
-  float psum = 0.0f;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
-    psum += e[j];
-  }
-  return psum;
+  for (int j = 0; j < 8; ++j) e[j] = __builtin_amdgcn_exp2f(fmaf(p[j], scale_log2, -st.m));
+  return ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
 }
 
 // probability operands of one query tile: fp16 P (F16), else bf16 hi + lo
@@ -251,20 +245,22 @@ __device__ inline void qt_scores(const u4 (&ka)[8], const u4 (&q)[4], f4& s0, f4
 }
 
 // S^T = K Q^T of one tile for every query tile of the wave
-__device__ inline void tile_scores(const u4 (&ka)[8], const u4 (&qop)[QTW][4], f4 (&s)[QTW][2]) {
+template <int QT>
+__device__ inline void tile_scores(const u4 (&ka)[8], const u4 (&qop)[QT][4], f4 (&s)[QT][2]) {
 #pragma unroll
-  for (int qt = 0; qt < QTW; ++qt) qt_scores(ka, qop[qt], s[qt][0], s[qt][1]);
+  for (int qt = 0; qt < QT; ++qt) qt_scores(ka, qop[qt], s[qt][0], s[qt][1]);
 }
 
 // O^T += V^T P of one tile (V^T operands read from the tile's LDS V rows)
-template <bool F16>
-__device__ inline void tile_pv(const char* lv, const POp (&pp)[QTW], QState (&st)[QTW], int i16,
+template <bool F16, int QT>
+__device__ inline void tile_pv(const char* lv, const POp (&pp)[QT], QState (&st)[QT], int i16,
                                int g4) {
+  const char* vb = vt_base(lv, i16, g4);
 #pragma unroll
   for (int d = 0; d < 8; ++d) {
-    const u4 vt = vt_operand(lv, d, i16, g4);
+    const u4 vt = vt_operand_at(vb, d);
 #pragma unroll
-    for (int qt = 0; qt < QTW; ++qt) {
+    for (int qt = 0; qt < QT; ++qt) {
       if (F16) {
         st[qt].acc[d] = mfma_f16(vt, pp[qt].hi, st[qt].acc[d]);
       } else {
@@ -275,21 +271,33 @@ __device__ inline void tile_pv(const char* lv, const POp (&pp)[QTW], QState (&st
   }
 }
 
+// Scheduling of one pipeline iteration: N matrix instructions, each followed
+// by its even share of about NV vector instructions.
+template <int N, int NV, int I = 0>
+__device__ inline void interleave() {
+  if constexpr (I < N) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+    constexpr int v = (I + 1) * NV / N - I * NV / N;
+    if constexpr (v > 0) __builtin_amdgcn_sched_group_barrier(0x002, v, 0);  // VALU
+    interleave<N, NV, I + 1>();
+  }
+}
+
 // One iteration of the pipeline (tile t): scores of tile t+1 and, with PV,
-// O += V^T P of tile t-1 on the matrix cores, interleaved with the softmax
-// common path of tile t on the vector ALUs; then the rare reference raise
-// (which recomputes tile t's scores from its K rows, still in LDS, so the
-// scores need not stay in registers) and the running sums.  sc holds tile
-// t's scores on entry and tile t+1's on exit; pp holds tile t-1's
-// probability operands on entry and tile t's on exit.
-template <bool F16, int TPS, bool PV>
+// O += V^T P of tile t-1 (operands pp) on the matrix cores, interleaved with
+// the softmax common path of tile t on the vector ALUs; then the rare
+// reference raise (which recomputes tile t's scores from its K rows, still in
+// LDS, so the scores need not stay in registers) and the running sums.  sc
+// holds tile t's scores on entry and tile t+1's on exit; tile t's
+// probability operands go to pn (the caller alternates two sets, so they
+// are never copied).
+template <bool F16, int TPS, bool PV, int QT>
 __device__ __attribute__((always_inline)) inline void tile_step(
-    int t, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW], f4 (&sc)[QTW][2],
-    POp (&pp)[QTW], float scale_log2, int n_valid, int i16, int g4) {
-  float psum[QTW];
-  POp pn[QTW];
+    int t, char* lds, const u4 (&qop)[QT][4], QState (&st)[QT], f4 (&sc)[QT][2],
+    const POp (&pp)[QT], POp (&pn)[QT], float scale_log2, int n_valid, int i16, int g4) {
+  float psum[QT];
 #pragma unroll
-  for (int qt = 0; qt < QTW; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     float e[8];
     psum[qt] = tile_exp(st[qt], sc[qt][0], sc[qt][1], scale_log2, e);
     pn[qt] = pack_p<F16>(e);
@@ -299,20 +307,16 @@ __device__ __attribute__((always_inline)) inline void tile_step(
     load_ka(tile_buf<TPS>(lds, t + 1), i16, g4, ka);
     tile_scores(ka, qop, sc);
   }
-  if (PV) tile_pv<F16>(tile_buf<TPS>(lds, t - 1) + TILEB, pp, st, i16, g4);
-  // one matrix instruction, then vector instructions, in turn
-  constexpr int n_mfma = QTW * 8 + (PV ? QTW * 8 * (F16 ? 1 : 2) : 0);
-#pragma unroll
-  for (int i = 0; i < n_mfma; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // VALU
-  }
+  if (PV) tile_pv<F16, QT>(tile_buf<TPS>(lds, t - 1) + TILEB, pp, st, i16, g4);
+  // matrix and vector instructions in turn (the softmax takes about 26
+  // vector instructions per query tile, 30 with the bf16 split)
+  interleave<QT * 8 + (PV ? QT * 8 * (F16 ? 1 : 2) : 0), QT * (F16 ? 26 : 30)>();
   bool rare = false;
 #pragma unroll
-  for (int qt = 0; qt < QTW; ++qt) rare = rare || !(psum[qt] <= kLazyExp);
+  for (int qt = 0; qt < QT; ++qt) rare = rare || !(psum[qt] <= kLazyExp);
   if (__builtin_amdgcn_ballot_w64(rare)) {  // rare: raise the reference max
 #pragma unroll
-    for (int qt = 0; qt < QTW; ++qt)
+    for (int qt = 0; qt < QT; ++qt)
       if (__builtin_amdgcn_ballot_w64(!(psum[qt] <= kLazyExp))) {
         u4 ka[8];
         load_ka(tile_buf<TPS>(lds, t), i16, g4, ka);
@@ -330,22 +334,21 @@ __device__ __attribute__((always_inline)) inline void tile_step(
     // probability operands stay in range too.
     const float gone = 0.25f * (float)(TILE - n_valid);
 #pragma unroll
-    for (int qt = 0; qt < QTW; ++qt)
+    for (int qt = 0; qt < QT; ++qt)
       psum[qt] = fmaf(-gone, __builtin_amdgcn_exp2f(-st[qt].m), psum[qt]);
   }
 #pragma unroll
-  for (int qt = 0; qt < QTW; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     st[qt].l += psum[qt];
     st[qt].ls += psum[qt];
-    pp[qt] = pn[qt];
   }
 }
 
 // the key-tile loop of one workgroup (see the file comment).  Returns the
 // view of the last tile.
-template <bool F16, int W, int TPS>
+template <bool F16, int W, int TPS, int QT>
 __device__ __attribute__((always_inline)) inline int tile_loop(
-    const Views& vs, int bh, char* lds, const u4 (&qop)[QTW][4], QState (&st)[QTW],
+    const Views& vs, int bh, char* lds, const u4 (&qop)[QT][4], QState (&st)[QT],
     float scale_log2, int r_wave, int nq, int64_t qbase, int nseg, float* seg_lse, int i16,
     int g4) {
   int cur_view = -1, cur_seg = -1;
@@ -372,17 +375,18 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     }
   }
   __syncthreads();
-  f4 sc[QTW][2];
+  f4 sc[QT][2];
   {
     u4 ka[8];
     load_ka(tile_buf<TPS>(lds, 0), i16, g4, ka);
     tile_scores(ka, qop, sc);
   }
-  POp pp[QTW];
+  POp pa[QT], pb[QT];  // probability operands of alternate tiles
   Stage S;
   int n_pre = 0;  // tiles of the stage in flight
-  // one iteration; the first (no previous tile to multiply with V) is peeled
-  auto iter = [&](int t, auto pv) {
+  // one iteration (PV of tile t-1 from pp, P of tile t into pn); the first
+  // (no previous tile to multiply with V) is peeled
+  auto iter = [&](int t, auto pv, const POp (&pp)[QT], POp (&pn)[QT]) {
     if (t % TPS == 0 && t + 2 * TPS < T) {  // the tiles of stage t/TPS + 2
       if (TPS == 1) {
         stage_load<F16, NT>(cs, S, 0);
@@ -405,7 +409,7 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     if (seg_lse && vi != cur_view && cur_view >= 0 && ct.seg != cur_seg) {
       // the previous logical segment ended: its log-sum-exp per query row
 #pragma unroll
-      for (int qt = 0; qt < QTW; ++qt) {
+      for (int qt = 0; qt < QT; ++qt) {
         const float ls = col_sum(st[qt].ls);
         const int r = r_wave + qt * 16 + i16;
         if (g4 == 0 && r < nq)
@@ -419,8 +423,8 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     ct.next(vs, bh);
     // past the last tile the next scores come from a stale buffer and are
     // never used
-    tile_step<F16, TPS, decltype(pv)::value>(t, lds, qop, st, sc, pp, scale_log2, n_valid, i16,
-                                             g4);
+    tile_step<F16, TPS, decltype(pv)::value, QT>(t, lds, qop, st, sc, pp, pn, scale_log2,
+                                                 n_valid, i16, g4);
     if (t % TPS == TPS - 1 || t == T - 1) {  // the stage's last tile
       const int t0 = t - t % TPS + 2 * TPS;  // first tile of the staged stage
       if (TPS == 1) {
@@ -436,15 +440,24 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
       __syncthreads();
     }
   };
-  iter(0, std::false_type{});
-  for (int t = 1; t < T; ++t) iter(t, std::true_type{});
+  iter(0, std::false_type{}, pb, pa);
+  int t = 1;
+  for (; t + 1 < T; t += 2) {
+    iter(t, std::true_type{}, pa, pb);
+    iter(t + 1, std::true_type{}, pb, pa);
+  }
   // the last tile's O += V^T P
-  tile_pv<F16>(tile_buf<TPS>(lds, T - 1) + TILEB, pp, st, i16, g4);
+  if (t < T) {
+    iter(t, std::true_type{}, pa, pb);
+    tile_pv<F16, QT>(tile_buf<TPS>(lds, T - 1) + TILEB, pb, st, i16, g4);
+  } else {
+    tile_pv<F16, QT>(tile_buf<TPS>(lds, T - 1) + TILEB, pa, st, i16, g4);
+  }
   return cur_view;
 }
 
-template <int W, int TPS>
-__global__ __launch_bounds__(W * 64, W == 4 ? 2 : 1) void prefill_mfma_kernel(Views vs, const uint16_t* __restrict__ q,
+template <int W, int TPS, int QT>
+__global__ __launch_bounds__(W * 64, W == 4 && QT == 2 ? 2 : 1) void prefill_mfma_kernel(Views vs, const uint16_t* __restrict__ q,
                                                               int Hq, int Hkv, int M, int nseg,
                                                               int n_qblocks, int n_work,
                                                               float scale_log2, float* __restrict__ o,
@@ -462,12 +475,12 @@ __global__ __launch_bounds__(W * 64, W == 4 ? 2 : 1) void prefill_mfma_kernel(Vi
   const int i16 = lane & 15, g4 = lane >> 4;
   const int G = Hq / Hkv, nq = G * M, b = bh / Hkv, hkv = bh % Hkv;
   const int64_t qbase = ((int64_t)b * Hq + hkv * G) * M;  // first query row of the head
-  const int r_wave = qb * qrows<W>() + wave * QTW * 16;   // first row of the wave
+  const int r_wave = qb * qrows<W, QT>() + wave * QT * 16;  // first row of the wave
 
-  u4 qop[QTW][4];
-  QState st[QTW];
+  u4 qop[QT][4];
+  QState st[QT];
 #pragma unroll
-  for (int t = 0; t < QTW; ++t) {
+  for (int t = 0; t < QT; ++t) {
     const int r = r_wave + t * 16 + i16;
 #pragma unroll
     for (int k = 0; k < 4; ++k)
@@ -483,20 +496,20 @@ __global__ __launch_bounds__(W * 64, W == 4 ? 2 : 1) void prefill_mfma_kernel(Vi
   // segments without rows never see a tile: their log-sum-exp stays -inf
   if (seg_lse && g4 == 0) {
 #pragma unroll
-    for (int t = 0; t < QTW; ++t) {
+    for (int t = 0; t < QT; ++t) {
       const int r = r_wave + t * 16 + i16;
       if (r < nq)
         for (int a = 0; a < nseg; ++a) seg_lse[(qbase + r) * nseg + a] = -INFINITY;
     }
   }
   const bool f16 = *v_unsafe == 0;
-  const int cur_view = f16 ? tile_loop<true, W, TPS>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
+  const int cur_view = f16 ? tile_loop<true, W, TPS, QT>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
                                              nseg, seg_lse, i16, g4)
-                           : tile_loop<false, W, TPS>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
+                           : tile_loop<false, W, TPS, QT>(vs, bh, lds, qop, st, scale_log2, r_wave, nq, qbase,
                                               nseg, seg_lse, i16, g4);
   // outputs
 #pragma unroll
-  for (int qt = 0; qt < QTW; ++qt) {
+  for (int qt = 0; qt < QT; ++qt) {
     const int r = r_wave + qt * 16 + i16;
     const float l = col_sum(st[qt].l);
     const float ls = col_sum(st[qt].ls);
@@ -600,6 +613,10 @@ __global__ void flag_clear_kernel(int* flag) { *flag = 0; }
 
 }  // namespace
 
+#ifndef PREFILL_LAYOUT
+#define PREFILL_LAYOUT -1
+#endif
+
 bool prefill_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M) {
   if (sh.D != D || q_dt != UC_BF16) return false;
   if ((sh.Hq / sh.Hkv) * M <= 16) return false;  // the decode kernel's range
@@ -685,21 +702,25 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   // or runs many rounds; otherwise the 4-wave one (two per CU), whose last
   // round leaves fewer CUs idle
   const int cus = device_cus();
-  const int n8 = (nq + qrows<8>() - 1) / qrows<8>() * BH;
-  const bool wide = n8 % cus == 0 || n8 >= 8 * cus;
-  const int W = wide ? 8 : 4, qr = wide ? qrows<8>() : qrows<4>();
+  const int n8 = (nq + qrows<8, 2>() - 1) / qrows<8, 2>() * BH;
+  const int layout = PREFILL_LAYOUT >= 0 ? PREFILL_LAYOUT
+                     : (n8 % cus == 0 || n8 >= 8 * cus) ? 1 : 0;
+  const int qr = layout == 0 ? qrows<4, 2>() : layout == 1 ? qrows<8, 2>() : qrows<4, 4>();
   const int n_qblocks = (nq + qr - 1) / qr;
   const int n_work = n_qblocks * BH;
   const int grid = (n_work + 7) / 8 * 8;
+  const float sl2 = sm_scale * kLog2e;
+  const uint16_t* qp = (const uint16_t*)q;
   if ((e = kernel_timer_begin(st)) != hipSuccess) return e;
-  if (wide)
-    hipLaunchKernelGGL((prefill_mfma_kernel<8, 2>), dim3(grid), dim3(W * 64), 0, st, vs,
-                       (const uint16_t*)q, sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work,
-                       sm_scale * kLog2e, o, lse, seg_lse, v_unsafe);
+  if (layout == 1)
+    hipLaunchKernelGGL((prefill_mfma_kernel<8, 2, 2>), dim3(grid), dim3(8 * 64), 0, st, vs, qp,
+                       sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
+  else if (layout == 2)
+    hipLaunchKernelGGL((prefill_mfma_kernel<4, 1, 4>), dim3(grid), dim3(4 * 64), 0, st, vs, qp,
+                       sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
   else
-    hipLaunchKernelGGL((prefill_mfma_kernel<4, 1>), dim3(grid), dim3(W * 64), 0, st, vs,
-                       (const uint16_t*)q, sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work,
-                       sm_scale * kLog2e, o, lse, seg_lse, v_unsafe);
+    hipLaunchKernelGGL((prefill_mfma_kernel<4, 1, 2>), dim3(grid), dim3(4 * 64), 0, st, vs, qp,
+                       sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
   e = hipGetLastError();
   return e == hipSuccess ? kernel_timer_end(st) : e;
 }

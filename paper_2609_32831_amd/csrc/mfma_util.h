@@ -88,6 +88,15 @@ __device__ inline u4 vt_operand(const char* lv, int d, int i16, int g4) {
   return ds_tr(lv + toff(rr, 2 * d + cb) + hb8, lv + toff(rr + 16, 2 * d + cb) + hb8);
 }
 
+// the same operands from a lane base computed once per tile (vt_base), so
+// the dim tiles differ only in the reads' immediate offsets
+__device__ inline const char* vt_base(const char* lv, int i16, int g4) {
+  return lv + toff(g4 * 4 + (i16 >> 2), (i16 & 3) >> 1) + (i16 & 1) * 8;
+}
+__device__ inline u4 vt_operand_at(const char* vb, int d) {
+  return ds_tr(vb + d * 32, vb + 16 * LROW + d * 32);
+}
+
 // probabilities as bf16 hi + lo parts (16 significant bits between them)
 __device__ inline void split_p(const float (&e)[8], u4& phi, u4& plo) {
   uint32_t hi[4], lo[4];
