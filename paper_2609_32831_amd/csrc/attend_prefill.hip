@@ -354,11 +354,15 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
   int cur_view = -1, cur_seg = -1;
   const int T = vs.tiles;
   // tiles go through LDS in stages of TPS: stage j holds tiles TPS*j ..
-  // TPS*j + TPS - 1; during stage j the tiles of stage j + 2 are loaded and,
-  // after its last tile, stored, and one barrier per stage publishes them.
-  // During stage j the pipeline reads stages j - 1 .. j + 1.
+  // TPS*j + TPS - 1; after the last tile of stage j the tiles of stage j + 2
+  // are stored, and one barrier per stage publishes them.  During stage j
+  // the pipeline reads stages j - 1 .. j + 1.  With two tiles per stage the
+  // tiles of stage j + 2 are loaded at the start of stage j; with one, tile
+  // t + 3 is loaded at the start of iteration t into the other of two
+  // register sets, so a load has two iterations to arrive.
   constexpr int NT = W * 64;
   Cursor<F16> ct, cs;  // tile t (computed) and the next tile to stage
+  Stage SA, SB;
   {
     Stage S;
     ct.start(vs, bh, 0);
@@ -373,6 +377,11 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
         if (TPS == 1 || i == 0) stage_store<NT>(tile_buf<TPS>(lds, u), S, i);
       cs.next(vs, bh);
     }
+    if (TPS == 1 && T > 2) {
+      stage_load<F16, NT>(cs, SA, 0);
+      stage_load<F16, NT>(cs, SA, 1);
+      cs.next(vs, bh);
+    }
   }
   __syncthreads();
   f4 sc[QT][2];
@@ -382,18 +391,20 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     tile_scores(ka, qop, sc);
   }
   POp pa[QT], pb[QT];  // probability operands of alternate tiles
-  Stage S;
-  int n_pre = 0;  // tiles of the stage in flight
-  // one iteration (PV of tile t-1 from pp, P of tile t into pn); the first
-  // (no previous tile to multiply with V) is peeled
-  auto iter = [&](int t, auto pv, const POp (&pp)[QT], POp (&pn)[QT]) {
-    if (t % TPS == 0 && t + 2 * TPS < T) {  // the tiles of stage t/TPS + 2
-      if (TPS == 1) {
-        stage_load<F16, NT>(cs, S, 0);
-        stage_load<F16, NT>(cs, S, 1);
+  int n_pre = 0;  // tiles of the stage in flight (two tiles per stage)
+  // one iteration (PV of tile t-1 from pp, P of tile t into pn; with one
+  // tile per stage, tile t+2 stored from Sc and tile t+3 loaded into Sn);
+  // the first (no previous tile to multiply with V) is peeled
+  auto iter = [&](int t, auto pv, const POp (&pp)[QT], POp (&pn)[QT], Stage& Sc, Stage& Sn) {
+    Stage& S = Sn;
+    if (TPS == 1) {
+      if (t + 3 < T) {
+        stage_load<F16, NT>(cs, Sn, 0);
+        stage_load<F16, NT>(cs, Sn, 1);
         cs.next(vs, bh);
-        n_pre = 1;
-      } else {
+      }
+    } else if (t % TPS == 0 && t + 2 * TPS < T) {  // the tiles of stage t/TPS + 2
+      {
         stage_load<F16, NT>(cs, S, 0);
         cs.next(vs, bh);
         n_pre = 1;
@@ -428,9 +439,9 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
     if (t % TPS == TPS - 1 || t == T - 1) {  // the stage's last tile
       const int t0 = t - t % TPS + 2 * TPS;  // first tile of the staged stage
       if (TPS == 1) {
-        if (n_pre) {
-          stage_store<NT>(tile_buf<TPS>(lds, t0), S, 0);
-          stage_store<NT>(tile_buf<TPS>(lds, t0), S, 1);
+        if (t0 < T) {
+          stage_store<NT>(tile_buf<TPS>(lds, t0), Sc, 0);
+          stage_store<NT>(tile_buf<TPS>(lds, t0), Sc, 1);
         }
       } else {
         if (n_pre >= 1) stage_store<NT>(tile_buf<TPS>(lds, t0), S, 0);
@@ -440,15 +451,17 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
       __syncthreads();
     }
   };
-  iter(0, std::false_type{}, pb, pa);
+  // with two tiles per stage both register-set roles are SA
+  Stage& S1 = TPS == 1 ? SB : SA;
+  iter(0, std::false_type{}, pb, pa, SA, S1);
   int t = 1;
   for (; t + 1 < T; t += 2) {
-    iter(t, std::true_type{}, pa, pb);
-    iter(t + 1, std::true_type{}, pb, pa);
+    iter(t, std::true_type{}, pa, pb, S1, SA);
+    iter(t + 1, std::true_type{}, pb, pa, SA, S1);
   }
   // the last tile's O += V^T P
   if (t < T) {
-    iter(t, std::true_type{}, pa, pb);
+    iter(t, std::true_type{}, pa, pb, S1, SA);
     tile_pv<F16, QT>(tile_buf<TPS>(lds, T - 1) + TILEB, pb, st, i16, g4);
   } else {
     tile_pv<F16, QT>(tile_buf<TPS>(lds, T - 1) + TILEB, pa, st, i16, g4);
