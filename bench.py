@@ -717,6 +717,7 @@ def dynamic_bench(args):
             run = DynamicRun(w, seg_k, seg_v)
             ev = HipEvents(3 * w.steps)
             torch.cuda.synchronize()
+            bsteps = []
             for t in range(w.steps):
                 ev.record(3 * t, stream)
                 # the attention and the per-step type masses
@@ -724,11 +725,15 @@ def dynamic_bench(args):
                                 run.seg_lse, ws=run.ws_att)
                 uc_segment_mass(run.shape, w.M, run.nseg, run.lse, run.seg_lse, run.mass[t])
                 ev.record(3 * t + 1, stream)
-                run.after_step(t, q_b[t])
-                ev.record(3 * t + 2, stream)
+                if run.after_step(t, q_b[t]) is not None:
+                    # a boundary: its work is bracketed by one more event (the
+                    # other steps have none: an event costs the GPU a few us)
+                    ev.record(3 * t + 2, stream)
+                    bsteps.append(t)
             torch.cuda.synchronize()
         att = [ev.elapsed_ms(3 * t, 3 * t + 1) for t in range(w.steps)]
-        bnd = [ev.elapsed_ms(3 * t + 1, 3 * t + 2) for t in range(w.steps)]
+        bnd = [ev.elapsed_ms(3 * t + 1, 3 * t + 2) if t in bsteps else 0.0
+               for t in range(w.steps)]
         ev.close()
         d = run.decisions
         res.append({"att": att, "bnd": bnd, "dec": d})

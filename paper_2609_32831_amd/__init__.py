@@ -189,11 +189,14 @@ def packed_layout(BH: int, N: int, D: int, G: int, head_bits: Sequence[int]):
 
 def packed_segment(B: int, Hkv: int, N: int, D: int, G: int, dtype: torch.dtype,
                    bits: int = 4, head_bits: Optional[Sequence[int]] = None,
-                   device="cuda", capacity: int = 0) -> Segment:
+                   device="cuda", capacity: int = 0, zero: bool = True) -> Segment:
     """Allocate the buffers of a packed segment of N rows (to be filled by
     uc_quantize_segment).  head_bits: optional per-(b, h_kv) code widths.
     capacity > 0: room for that many rows per head (a segment that grows by
-    uc_stream_append; strides follow the capacity)."""
+    uc_stream_append; strides follow the capacity).  zero=False leaves the
+    buffers uninitialised (for a segment that uc_quantize_segment fills
+    whole before anything reads it)."""
+    alloc = torch.zeros if zero else torch.empty
     BH = B * Hkv
     n_full = G * (N // G)
     tail = N - n_full
@@ -206,14 +209,14 @@ def packed_segment(B: int, Hkv: int, N: int, D: int, G: int, dtype: torch.dtype,
         t["code_off"] = torch.tensor(off, dtype=torch.int64, device=device)
     else:
         total = BH * cap_full * D * bits // 8
-    t["codes_k"] = torch.zeros(max(total, 16), dtype=torch.uint8, device=device)
-    t["codes_v"] = torch.zeros(max(total, 16), dtype=torch.uint8, device=device)
-    t["scale_k"] = torch.zeros(B, Hkv, cap_full // G, D, dtype=torch.float32, device=device)
-    t["min_k"] = torch.zeros_like(t["scale_k"])
-    t["scale_v"] = torch.zeros(B, Hkv, cap_full, D // G, dtype=torch.float32, device=device)
-    t["min_v"] = torch.zeros_like(t["scale_v"])
-    t["tail_k"] = torch.zeros(B, Hkv, tail_rows, D, dtype=dtype, device=device)
-    t["tail_v"] = torch.zeros_like(t["tail_k"])
+    t["codes_k"] = alloc(max(total, 16), dtype=torch.uint8, device=device)
+    t["codes_v"] = alloc(max(total, 16), dtype=torch.uint8, device=device)
+    t["scale_k"] = alloc(B, Hkv, cap_full // G, D, dtype=torch.float32, device=device)
+    t["min_k"] = alloc(B, Hkv, cap_full // G, D, dtype=torch.float32, device=device)
+    t["scale_v"] = alloc(B, Hkv, cap_full, D // G, dtype=torch.float32, device=device)
+    t["min_v"] = alloc(B, Hkv, cap_full, D // G, dtype=torch.float32, device=device)
+    t["tail_k"] = alloc(B, Hkv, tail_rows, D, dtype=dtype, device=device)
+    t["tail_v"] = alloc(B, Hkv, tail_rows, D, dtype=dtype, device=device)
     d = uc_segment(kind=UC_SEG_PACKED, dtype=TORCH_DT[dtype], n_rows=N, row_stride=capacity,
                    group=G, bits=bits if head_bits is None else int(max(head_bits)),
                    head_bits=_ptr(t.get("head_bits")), code_off=_ptr(t.get("code_off")),
@@ -475,9 +478,17 @@ def budget_state_tensor(device="cuda") -> torch.Tensor:
     return torch.zeros(ctypes.sizeof(uc_budget_state), dtype=torch.uint8, device=device)
 
 
-def budget_state_read(state: torch.Tensor) -> uc_budget_state:
-    """Copy a device uc_budget_state to the host (waits for the stream)."""
-    return uc_budget_state.from_buffer_copy(bytes(state.cpu().numpy()))
+def budget_state_read(state: torch.Tensor, host: Optional[torch.Tensor] = None,
+                      stream=None) -> uc_budget_state:
+    """Copy a device uc_budget_state to the host (waits for the stream);
+    host: an optional pinned uint8 buffer of the same size to copy through."""
+    if host is None:
+        return uc_budget_state.from_buffer_copy(bytes(state.cpu().numpy()))
+    s = torch.cuda.current_stream() if stream is None else stream
+    with torch.cuda.stream(s):
+        host.copy_(state, non_blocking=True)
+    s.synchronize()
+    return uc_budget_state.from_buffer_copy(host.numpy().tobytes())
 
 
 def uc_budget_step(params: uc_budget_params, mass: torch.Tensor, n_steps: int,

@@ -375,6 +375,17 @@ class DynamicRun:
         self.params = uc_budget_params(Hq, Hkv, D, M, self.nseg, self.ev, self.qt, self.n_ev,
                                        self.n_qt, self.dt, w.rho_init, w.rho_min)
         self.state = budget_state_tensor(device)
+        self.state_host = torch.empty(self.state.numel(), dtype=torch.uint8, pin_memory=True)
+        # the kept rows of the evicting type, their logical indices and the
+        # selection's local indices: two sets of buffers sized for every row,
+        # alternating (a boundary gathers from one set into the other)
+        self.kept_k = [torch.empty(Hkv * self.n_ev * D, dtype=self.tdt, device=device)
+                       for _ in range(2)]
+        self.kept_v = [torch.empty_like(self.kept_k[0]) for _ in range(2)]
+        self.kept_idx = [torch.empty(Hkv * self.n_ev, dtype=torch.int32, device=device)
+                         for _ in range(2)]
+        self.local = torch.empty(Hkv * self.n_ev, dtype=torch.int32, device=device)
+        self.set = 0
         # storage state
         self.compact = None     # dense segment of the kept rows of the evicting type
         self.idx = None         # [Hkv, k] int32 logical positions of those rows
@@ -403,17 +414,19 @@ class DynamicRun:
         outs = [None] * self.nseg
         outs[self.ev] = sc
         uc_score_importance(self.shape, segs, q_obs, W, self.sm, outs, None, ws=self.ws_sc)
-        local = torch.empty(Hkv, k_new, dtype=torch.int32, device=self.device)
+        s = self.set = 1 - self.set
+        n = Hkv * k_new
+        local = self.local[:n].view(Hkv, k_new)
         src = segs[self.ev].t
-        kd = torch.empty(1, Hkv, k_new, D, dtype=self.tdt, device=self.device)
-        vd = torch.empty_like(kd)
+        kd = self.kept_k[s][: n * D].view(1, Hkv, k_new, D)
+        vd = self.kept_v[s][: n * D].view(1, Hkv, k_new, D)
         uc_select_keep(sc.reshape(Hkv, n_cur), k_new, 0, local, src["k"].reshape(Hkv, -1, D),
                        src["v"].reshape(Hkv, -1, D), kd.view(Hkv, k_new, D),
                        vd.view(Hkv, k_new, D))
+        idx = self.kept_idx[s][:n].view(Hkv, k_new)
         if self.idx is None:
-            idx = local
+            idx.copy_(local)
         else:
-            idx = torch.empty(Hkv, k_new, dtype=torch.int32, device=self.device)
             uc_compose_index(self.idx, local, idx)
         self.compact = dense_segment(kd, vd, idx=idx)
         self.idx = idx
@@ -426,7 +439,7 @@ class DynamicRun:
         w = self.w
         _, bits, group = cfg
         pk = packed_segment(1, w.Hkv, self.n_qt, w.D, group, self.tdt, bits=bits,
-                            device=self.device)
+                            device=self.device, zero=False)
         if self.packed is None:
             src_k, src_v = self.dense[self.qt].t["k"], self.dense[self.qt].t["v"]
         else:
@@ -441,7 +454,7 @@ class DynamicRun:
         decides (uc_budget_step), the host reads the decision and applies it
         from the next timestep on."""
         uc_budget_step(self.params, self.mass[t0:t0 + n], n, self.state)
-        st = budget_state_read(self.state)
+        st = budget_state_read(self.state, self.state_host)
         if self.compact is None or st.k < st.k_prev:
             self._select(q_obs, W, st.k)
         if st.cfg != st.cfg_prev:
