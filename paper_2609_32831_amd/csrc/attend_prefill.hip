@@ -46,9 +46,8 @@ constexpr int SUBB = 2 * TILEB;            // one tile: K rows + V rows
 // Layouts: W waves per workgroup, TPS tiles per stage (one barrier per
 // stage) and QT 16-row query tiles per wave.  <4, 1, 2>: 128 query rows, two
 // workgroups per CU; <8, 2, 2>: 256 query rows, one workgroup per CU, half
-// the barriers and staging per query row; <4, 1, 4>: 256 query rows, one
-// wave per SIMD with 64 query rows, so every K and V operand read from LDS
-// serves twice the products.
+// the barriers and staging per query row.  (Four query tiles per wave, one
+// wave per SIMD, measured slower than two waves per SIMD with two.)
 template <int W, int QT>
 constexpr int qrows() { return W * QT * 16; }
 constexpr float kLazy = 8.0f;
@@ -626,10 +625,6 @@ __global__ void flag_clear_kernel(int* flag) { *flag = 0; }
 
 }  // namespace
 
-#ifndef PREFILL_LAYOUT
-#define PREFILL_LAYOUT -1
-#endif
-
 bool prefill_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt, int M) {
   if (sh.D != D || q_dt != UC_BF16) return false;
   if ((sh.Hq / sh.Hkv) * M <= 16) return false;  // the decode kernel's range
@@ -716,20 +711,16 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   // round leaves fewer CUs idle
   const int cus = device_cus();
   const int n8 = (nq + qrows<8, 2>() - 1) / qrows<8, 2>() * BH;
-  const int layout = PREFILL_LAYOUT >= 0 ? PREFILL_LAYOUT
-                     : (n8 % cus == 0 || n8 >= 8 * cus) ? 1 : 0;
-  const int qr = layout == 0 ? qrows<4, 2>() : layout == 1 ? qrows<8, 2>() : qrows<4, 4>();
+  const bool wide = n8 % cus == 0 || n8 >= 8 * cus;
+  const int qr = wide ? qrows<8, 2>() : qrows<4, 2>();
   const int n_qblocks = (nq + qr - 1) / qr;
   const int n_work = n_qblocks * BH;
   const int grid = (n_work + 7) / 8 * 8;
   const float sl2 = sm_scale * kLog2e;
   const uint16_t* qp = (const uint16_t*)q;
   if ((e = kernel_timer_begin(st)) != hipSuccess) return e;
-  if (layout == 1)
+  if (wide)
     hipLaunchKernelGGL((prefill_mfma_kernel<8, 2, 2>), dim3(grid), dim3(8 * 64), 0, st, vs, qp,
-                       sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
-  else if (layout == 2)
-    hipLaunchKernelGGL((prefill_mfma_kernel<4, 1, 4>), dim3(grid), dim3(4 * 64), 0, st, vs, qp,
                        sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
   else
     hipLaunchKernelGGL((prefill_mfma_kernel<4, 1, 2>), dim3(grid), dim3(4 * 64), 0, st, vs, qp,
