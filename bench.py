@@ -632,6 +632,22 @@ def understanding_bench(args):
         run.compress()
         steps()
 
+    # the same steps through an execution plan of the frozen layout: created
+    # once per job after compression, then each step passes only pointers
+    # (App. E, "Cached metadata and execution plans")
+    step_ptrs = [(x.data_ptr(), x.stride(0) * x.element_size())
+                 for x in (inp["k_dec"], inp["v_dec"], inp["q_dec"], o)]
+    ws_plan = None
+
+    def plan_steps():
+        plan = uc.AttendPlan(run.shape, run.mixed, len(run.mixed) - 1, inp["q_dec"].dtype, 1,
+                             run.sm, ws=ws_plan)
+        step = plan.attend_append
+        (kb, ks), (vb, vs), (qb, qs), (ob, os_) = step_ptrs
+        for t in range(T):
+            step(kb + t * ks, vb + t * vs, 1, qb + t * qs, ob + t * os_)
+        plan.close()
+
     stream = torch.cuda.current_stream()
     ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
     for _ in range(max(1, args.warmup)):
@@ -651,6 +667,25 @@ def understanding_bench(args):
     job_ms /= n
     step_ms /= n
     o_eager = o.clone()
+    run.compress()
+    p0 = uc.AttendPlan(run.shape, run.mixed, len(run.mixed) - 1, inp["q_dec"].dtype, 1, run.sm)
+    ws_plan = p0.ws
+    p0.close()
+    plan_ms, plan_job_ms, plan_ok = 0.0, 0.0, True
+    for _ in range(n):
+        o.zero_()
+        torch.cuda.synchronize()
+        ev[0].record(stream)
+        run.compress()
+        ev[1].record(stream)
+        plan_steps()
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        plan_job_ms += ev[0].elapsed_time(ev[2])
+        plan_ms += ev[1].elapsed_time(ev[2])
+        plan_ok = plan_ok and bool(torch.equal(o, o_eager))
+    plan_ms /= n
+    plan_job_ms /= n
     # the same 256 steps as one graph: the tail restarts at row 0, and each
     # replay appends and attends exactly as the steps above did
     run.tail.n_rows = 0
@@ -677,6 +712,9 @@ def understanding_bench(args):
                       "tokens_per_s": round(tokens / (job_ms / 1e3), 1), "ms_per_job": round(job_ms, 3),
                       "compress_ms": round(job_ms - step_ms, 3),
                       "decode_step_us": round(step_ms / T * 1e3, 2),
+                      "decode_step_us_plan": round(plan_ms / T * 1e3, 2),
+                      "tokens_per_s_plan": round(tokens / (plan_job_ms / 1e3), 1),
+                      "plan_matches_steps": plan_ok,
                       "decode_step_us_graph": round(graph_ms / T * 1e3, 2),
                       "decode_tokens_per_s_graph": round(tokens / (graph_ms / 1e3), 1),
                       "bytes_per_step": int(nbytes), "graph_matches_steps": ok, "jobs": n}),

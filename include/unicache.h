@@ -22,6 +22,8 @@
  *                        dense segment (Sec. 3.1, protected objects)
  *   uc_attend_append     one decode step: the append and the attention in
  *                        one launch (Sec. 3.1 and App. E)
+ *   uc_plan_*            decode steps on a frozen, validated layout
+ *                        (App. E "Cached metadata and execution plans")
  *   host helpers         byte accounting and budget -> policy configuration
  *                        (Sec. 3.3 Eq. 2 and Eq. 3, Sec. 3.4)
  *
@@ -310,6 +312,42 @@ uc_status uc_attend_append(const uc_shape* shape, const uc_segment* segs,
                            uc_dtype q_dt, int M, float sm_scale, float* o,
                            float* lse, float* seg_lse, void* ws,
                            size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Execution plans (App. E, "Cached metadata and execution plans": once a
+ * physical layout is frozen, attention reuses its segment boundaries and type
+ * identifiers instead of matching segments and preparing operators again).
+ * A plan holds a copy of the segment descriptors and the device layout
+ * derived from them, validated once; its decode steps then check only their
+ * own pointers.  The layout is frozen except for segs[tail], a dense segment
+ * with a row capacity whose row count the plan advances by every step's
+ * n_new (the caller's descriptors are not written; uc_plan_tail_rows reports
+ * the count).  Host memory only; a plan is used by one thread at a time, and
+ * the segment buffers it points into must outlive it.
+ *   uc_plan_create   validates as uc_attend_append would (shape, segments,
+ *                    q_dt, M, sm_scale; segs[tail] dense with row_stride >=
+ *                    1; at most UC_MAX_SEGMENTS - 1 segments) and writes the
+ *                    new plan to *out (NULL on error). */
+typedef struct uc_plan_s* uc_plan;
+uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs,
+                         int n_segs, int tail, uc_dtype q_dt, int M,
+                         float sm_scale, uc_plan* out);
+/* Workspace bytes that serve every step of the plan up to the tail's
+ * capacity (0 for a NULL plan). */
+size_t uc_plan_workspace_size(uc_plan plan);
+/* The tail's current row count (-1 for a NULL plan). */
+int uc_plan_tail_rows(uc_plan plan);
+/* One decode step on the plan: exactly uc_attend_append(shape, segs, n_segs,
+ * tail, k_new, v_new, n_new, q, q_dt, M, sm_scale, o, lse, NULL, ws,
+ * ws_bytes, stream) with the plan's arguments and the tail at its current row
+ * count, which then advances by n_new.  ws: at least uc_plan_workspace_size
+ * bytes.  On error nothing is enqueued and the row count stays. */
+uc_status uc_plan_attend_append(uc_plan plan, const void* k_new,
+                                const void* v_new, int n_new, const void* q,
+                                float* o, float* lse, void* ws,
+                                size_t ws_bytes, void* stream);
+/* Frees the plan (NULL is allowed). */
+uc_status uc_plan_destroy(uc_plan plan);
 
 /* ------------------------------------------------------------------------ */
 /* Host helpers: storage accounting and budget -> policy configuration

@@ -117,6 +117,12 @@ def _load():
         "uc_quant_config": (i32, [dbl, i64, i32, i32, i32, i32, vp, vp]),
         "uc_budget_step": (i32, [ctypes.POINTER(uc_budget_params), vp, i32, vp, vp]),
         "uc_calibrate_policy": (i32, [vp, i32, i32, dbl, vp, vp, vp]),
+        "uc_plan_create": (i32, [shp, segp, i32, i32, i32, i32, ctypes.c_float,
+                                 ctypes.POINTER(vp)]),
+        "uc_plan_workspace_size": (sz, [vp]),
+        "uc_plan_tail_rows": (i32, [vp]),
+        "uc_plan_attend_append": (i32, [vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]),
+        "uc_plan_destroy": (i32, [vp]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -260,6 +266,59 @@ def uc_attend_mixed(shape: uc_shape, segs: Sequence[Segment], q: torch.Tensor, M
                                ctypes.c_float(sm_scale), o.data_ptr(), _ptr(lse), _ptr(seg_lse),
                                ws.data_ptr(), ws.numel(), _stream(stream)), "uc_attend_mixed")
     return o
+
+
+class AttendPlan:
+    """A decode-step execution plan over a frozen layout (uc_plan_create):
+    the segments are validated once and every step passes only pointers.
+    segs[tail] is the dense segment the steps append to; its Segment's
+    n_rows is kept in step with the plan.  Pointers may be given as tensors
+    or as raw device addresses (ints); the stream is the current one at
+    creation unless a call names another."""
+
+    def __init__(self, shape: uc_shape, segs: Sequence[Segment], tail: int, q_dtype: torch.dtype,
+                 M: int, sm_scale: float, ws: Optional[torch.Tensor] = None, stream=None,
+                 device="cuda"):
+        h = ctypes.c_void_p()
+        _check(lib.uc_plan_create(ctypes.byref(shape), _seg_array(segs), len(segs), tail,
+                                  TORCH_DT[q_dtype], M, ctypes.c_float(sm_scale),
+                                  ctypes.byref(h)), "uc_plan_create")
+        self._h = h
+        self.segs, self.tail = segs, tail
+        need = int(lib.uc_plan_workspace_size(h))
+        if ws is None:
+            ws = _ws(need, device)
+        assert ws.numel() >= need, f"workspace {ws.numel()} < {need} bytes"
+        self.ws = ws
+        self._ws_ptr, self._ws_n = ws.data_ptr(), ws.numel()
+        self._stream = _stream(stream)
+        self._fn = lib.uc_plan_attend_append
+
+    @property
+    def tail_rows(self) -> int:
+        return int(lib.uc_plan_tail_rows(self._h))
+
+    def attend_append(self, k_new, v_new, n_new: int, q, o, lse=None, stream=None):
+        """One decode step: k_new / v_new [B, Hkv, n_new, D] join the tail and
+        q [B, Hq, M, D] attends over every segment into o (and lse)."""
+        a = [t if t is None or isinstance(t, int) else t.data_ptr()
+             for t in (k_new, v_new, q, o, lse)]
+        _check(self._fn(self._h, a[0], a[1], n_new, a[2], a[3], a[4], self._ws_ptr, self._ws_n,
+                        self._stream if stream is None else _stream(stream)),
+               "uc_plan_attend_append")
+        self.segs[self.tail].n_rows += n_new
+        return o
+
+    def close(self):
+        if self._h:
+            lib.uc_plan_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 UC_SCRATCH_BYTES = 16 << 20

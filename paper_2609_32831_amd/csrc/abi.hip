@@ -10,6 +10,7 @@
 #include <algorithm>
 #include <atomic>
 #include <mutex>
+#include <new>
 #include <vector>
 
 #include "budget_rules.h"
@@ -435,6 +436,118 @@ uc_status uc_attend_append(const uc_shape* shape, const uc_segment* segs, int n_
               n_new, ks.s[tail].row_stride, pos, shape->D * dtype_bytes(nk.dtype)};
   g_last_kernel = "decode_mfma_append";
   return launched(launch_decode_mfma(*shape, ks, q, M, sm_scale, o, lse, nullptr, ws, s, &ap));
+}
+
+// ---------------------------------------------------------------- execution plans
+}  // extern "C"
+
+struct uc_plan_s {
+  uc_shape shape;
+  uc_segment segs[kMaxSeg];  // the frozen layout; segs[tail].n_rows advances
+  KSegs ks;                  // its derived device layout, kept in step
+  int n_segs, tail, M;
+  uc_dtype q_dt;
+  float sm_scale;
+  size_t ws_need;            // enough for every call up to the tail's capacity
+};
+
+extern "C" {
+
+uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs, int n_segs, int tail,
+                         uc_dtype q_dt, int M, float sm_scale, uc_plan* out) {
+  if (!out) return fail(UC_E_INVALID, "out is NULL");
+  *out = nullptr;
+  KSegs ks;
+  uc_status st = check_segments(shape, segs, n_segs, ks);
+  if (st) return st;
+  if (tail < 0 || tail >= n_segs) return fail(UC_E_INVALID, "tail %d not in [0,%d)", tail, n_segs);
+  if (segs[tail].kind != UC_SEG_DENSE || segs[tail].row_stride < 1)
+    return fail(UC_E_INVALID, "segment %d (tail) is not a dense segment with a row capacity", tail);
+  if (n_segs >= kMaxSeg)
+    return fail(UC_E_UNSUPPORTED, "a plan takes at most %d segments", kMaxSeg - 1);
+  if (!dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad q dtype %d", q_dt);
+  if (M < 1) return fail(UC_E_INVALID, "M must be >= 1 (got %d)", M);
+  if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
+  if ((int64_t)shape->B * shape->Hq * M > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
+  uc_plan p = new (std::nothrow) uc_plan_s;
+  if (!p) return fail(UC_E_INVALID, "out of host memory");
+  p->shape = *shape;
+  memcpy(p->segs, segs, (size_t)n_segs * sizeof(uc_segment));
+  p->ks = ks;
+  p->n_segs = n_segs;
+  p->tail = tail;
+  p->M = M;
+  p->q_dt = q_dt;
+  p->sm_scale = sm_scale;
+  // workspace: every path, at the tail's capacity (the sizes only grow with
+  // the row counts)
+  uc_segment full[kMaxSeg];
+  memcpy(full, segs, (size_t)n_segs * sizeof(uc_segment));
+  full[tail].n_rows = full[tail].row_stride;
+  KSegs kf;
+  check_segments(shape, full, n_segs, kf);
+  size_t need = generic_ws(*shape, kf, kAttRows, kAttMaxChunks, M, true);
+  if (decode_mfma_eligible(*shape, kf, q_dt, M)) need = std::max(need, decode_mfma_workspace(*shape, kf, M));
+  if (prefill_mfma_eligible(*shape, kf, q_dt, M)) need = std::max(need, prefill_mfma_workspace(*shape, kf));
+  p->ws_need = need;
+  *out = p;
+  return ok();
+}
+
+size_t uc_plan_workspace_size(uc_plan plan) { return plan ? plan->ws_need : 0; }
+
+int uc_plan_tail_rows(uc_plan plan) { return plan ? plan->segs[plan->tail].n_rows : -1; }
+
+uc_status uc_plan_attend_append(uc_plan plan, const void* k_new, const void* v_new, int n_new,
+                                const void* q, float* o, float* lse, void* ws, size_t ws_bytes,
+                                void* stream) {
+  TimerScope timer;
+  if (!plan) return fail(UC_E_INVALID, "plan is NULL");
+  const int tail = plan->tail, pos = plan->segs[tail].n_rows;
+  if (n_new < 0) return fail(UC_E_INVALID, "n_new must be >= 0 (got %d)", n_new);
+  if (n_new > 0) {
+    if ((int64_t)pos + n_new > plan->segs[tail].row_stride)
+      return fail(UC_E_INVALID, "tail rows %lld after the append exceed row_stride %d",
+                  (long long)pos + n_new, plan->segs[tail].row_stride);
+    if (!k_new || !v_new) return fail(UC_E_INVALID, "k_new or v_new is NULL");
+    if (!aligned16(k_new) || !aligned16(v_new))
+      return fail(UC_E_INVALID, "k_new/v_new not 16-byte aligned");
+  }
+  if (!q || !o) return fail(UC_E_INVALID, "q or o is NULL");
+  if (ws_bytes < plan->ws_need || (plan->ws_need && !ws))
+    return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, plan->ws_need);
+  const uc_shape& sh = plan->shape;
+  uc_status st;
+  if (n_new > 0 && g_path.load() == UC_PATH_AUTO && decode_mfma_eligible(sh, plan->ks, plan->q_dt, plan->M)) {
+    // the fused step of uc_attend_append, on the layout derived at creation
+    KSegs ks = plan->ks;
+    KSeg& nk = ks.s[ks.n++];
+    memset(&nk, 0, sizeof nk);
+    nk.kind = UC_SEG_DENSE;
+    nk.dtype = ks.s[tail].dtype;
+    nk.n_rows = n_new;
+    nk.row_stride = n_new;
+    nk.k = k_new;
+    nk.v = v_new;
+    AppendOp ap{(const char*)k_new, (const char*)v_new, (char*)ks.s[tail].k, (char*)ks.s[tail].v,
+                n_new, ks.s[tail].row_stride, pos, sh.D * dtype_bytes(nk.dtype)};
+    g_last_kernel = "decode_mfma_append";
+    st = launched(launch_decode_mfma(sh, ks, q, plan->M, plan->sm_scale, o, lse, nullptr, ws,
+                                     (hipStream_t)stream, &ap));
+  } else {
+    st = uc_attend_append(&sh, plan->segs, plan->n_segs, tail, k_new, v_new, n_new, q,
+                          plan->q_dt, plan->M, plan->sm_scale, o, lse, nullptr, ws, ws_bytes, stream);
+  }
+  if (st == UC_OK) {
+    plan->segs[tail].n_rows += n_new;
+    plan->ks.s[tail].n_rows += n_new;
+  }
+  return st;
+}
+
+uc_status uc_plan_destroy(uc_plan plan) {
+  delete plan;
+  return ok();
 }
 
 // ---------------------------------------------------------------- batched requests

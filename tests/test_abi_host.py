@@ -145,6 +145,64 @@ def test_attend_append_validation(uc):
     assert _attend_append(uc, sh, [_dense(uc, 0, stride=4)], 0, 0) == E
 
 
+def test_plan_validation(uc):
+    """uc_plan_create validates as uc_attend_append does; a plan's step checks
+    its own pointers, capacity and workspace before any launch, and a
+    rejected step leaves the tail's row count alone."""
+    sh = uc.uc_shape(1, 4, 1, 128)
+    E = uc.UC_E_INVALID
+    L = uc.lib
+
+    def create(segs, tail, M=1, scale=0.1, q_dt=None):
+        h = ctypes.c_void_p()
+        arr = (uc.uc_segment * len(segs))(*segs)
+        st = L.uc_plan_create(ctypes.byref(sh), arr, len(segs), tail,
+                              uc.UC_BF16 if q_dt is None else q_dt, M, ctypes.c_float(scale),
+                              ctypes.byref(h))
+        return st, h
+
+    segs = [_dense(uc, 64), _dense(uc, 7, stride=8)]
+    assert create(segs, 2)[0] == E  # tail out of range
+    assert create(segs, 0)[0] == E  # tail without a row capacity
+    assert create([_dense(uc, 64), _packed(uc, 128)], 1)[0] == E  # tail not dense
+    assert create(segs, 1, M=0)[0] == E
+    assert create(segs, 1, scale=-1.0)[0] == E
+    assert create(segs, 1, q_dt=99)[0] == E
+    st, h = create([_dense(uc, 64, stride=64)] * uc.UC_MAX_SEGMENTS, 1)
+    assert st == uc.UC_E_UNSUPPORTED and not h
+    assert L.uc_plan_create(ctypes.byref(sh), (uc.uc_segment * 2)(*segs), 2, 1, uc.UC_BF16, 1,
+                            ctypes.c_float(0.1), None) == E
+    st, h = create(segs, 1)
+    assert st == uc.UC_OK and h
+    try:
+        assert L.uc_plan_tail_rows(h) == 7
+        need = L.uc_plan_workspace_size(h)
+        assert need > 0
+        # the workspace covers the tail at its capacity: the same as
+        # uc_attend_workspace_size with 8 tail rows
+        full = (uc.uc_segment * 2)(_dense(uc, 64), _dense(uc, 8, stride=8))
+        assert need >= L.uc_attend_workspace_size(ctypes.byref(sh), full, 2, uc.UC_BF16, 1)
+
+        def step(n_new, kn=FAKE, vn=FAKE, q=FAKE, o=FAKE, ws_bytes=1 << 40):
+            return L.uc_plan_attend_append(h, kn, vn, n_new, q, o, None, FAKE, ws_bytes, None)
+
+        assert step(2) == E  # 7 + 2 rows > capacity 8
+        assert "exceed row_stride" in uc.uc_last_error()
+        assert step(-1) == E
+        assert step(1, kn=None) == E
+        assert step(1, vn=FAKE + 4) == E  # misaligned
+        assert step(1, q=None) == E
+        assert step(1, o=None) == E
+        assert step(1, ws_bytes=need - 1) == uc.UC_E_WORKSPACE
+        assert L.uc_plan_tail_rows(h) == 7  # no rejected step moved the tail
+        assert L.uc_plan_attend_append(None, FAKE, FAKE, 1, FAKE, FAKE, None, FAKE, 1 << 40,
+                                       None) == E
+    finally:
+        assert L.uc_plan_destroy(h) == uc.UC_OK
+    assert L.uc_plan_destroy(None) == uc.UC_OK
+    assert L.uc_plan_tail_rows(None) == -1 and L.uc_plan_workspace_size(None) == 0
+
+
 def test_dynamic_budget_entry_validation(uc):
     sh = uc.uc_shape(1, 4, 2, 128)
     dense = _dense(uc, 64)

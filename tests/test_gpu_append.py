@@ -189,3 +189,55 @@ def test_attend_append_kernel_events():
     call_ms, kern_ms = ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
     assert 0.0 < kern_ms <= call_ms
     assert torch.equal(outs[0], outs[1])
+
+
+@pytest.mark.parametrize("case", CASES[:3], ids=[f"p{i}" for i in range(3)])
+@pytest.mark.parametrize("path", ["auto", "valu"])
+def test_plan_steps_match_attend_append(case, path):
+    """Decode steps through an execution plan (uc_plan_create /
+    uc_plan_attend_append, App. E "Cached metadata and execution plans")
+    equal the same steps through uc_attend_append bit for bit -- outputs,
+    lse and the stored tail rows -- on the matrix-core path and on the VALU
+    path (which runs the two-call route), and match the oracle."""
+    B, Hq, Hkv, M, parts, cap, n0, n_new, steps = case
+    _case(test="plan_steps", B=B, Hq=Hq, Hkv=Hkv, M=M, parts=parts, cap=cap, n0=n0,
+          n_new=n_new, steps=steps, path=path)
+    BH = B * Hkv
+    shape = uc.make_shape(B, Hq, Hkv, D)
+    sm = sm_scale(D)
+    seed = len(parts) + cap
+    segs, kh, vh, sid, tk, tv = _build(B, Hkv, parts, cap, n0, seed=seed)
+    segs2, _, _, _, _, _ = _build(B, Hkv, parts, cap, n0, seed=seed)
+    ns = len(segs)
+    prev = uc.uc_set_path(uc.UC_PATH_VALU if path == "valu" else uc.UC_PATH_AUTO)
+    try:
+        plan = uc.AttendPlan(shape, segs, ns - 1, torch.bfloat16, M, sm)
+        assert plan.tail_rows == n0
+        ws2 = torch.empty(uc.uc_attend_workspace_size(
+            shape, segs2[:-1] + [uc.dense_segment(segs2[-1].t["k"], segs2[-1].t["v"])],
+            uc.UC_BF16, M), dtype=torch.uint8, device="cuda")
+        for step in range(steps):
+            kn = rand_rows(700 + step, BH, n_new, D, "bf16")
+            vn = rand_rows(800 + step, BH, n_new, D, "bf16")
+            q = rand_rows(900 + step, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+            kd = dev(kn, "bf16").reshape(B, Hkv, n_new, D)
+            vd = dev(vn, "bf16").reshape(B, Hkv, n_new, D)
+            qd = dev(q, "bf16")
+            o, o2 = (torch.empty(B, Hq, M, D, device="cuda") for _ in range(2))
+            lse, lse2 = (torch.empty(B, Hq, M, device="cuda") for _ in range(2))
+            # the plan takes raw device addresses as well as tensors
+            plan.attend_append(kd.data_ptr(), vd, n_new, qd, o, lse)
+            uc.uc_attend_append(shape, segs2, ns - 1, kd, vd, n_new, qd, M, sm, o2, lse2, ws=ws2)
+            torch.cuda.synchronize()
+            assert plan.tail_rows == segs[-1].n_rows == segs2[-1].n_rows == n0 + (step + 1) * n_new
+            assert torch.equal(o, o2) and torch.equal(lse, lse2), step
+            n = segs[-1].n_rows
+            assert torch.equal(segs[-1].t["k"][:, :, :n], segs2[-1].t["k"][:, :, :n]), step
+            assert torch.equal(segs[-1].t["v"][:, :, :n], segs2[-1].t["v"][:, :, :n]), step
+            tk = np.concatenate([tk, kn], axis=1)
+            tv = np.concatenate([tv, vn], axis=1)
+            o_ref, lse_ref, _, _ = _oracle(q, B, Hkv, kh, vh, sid, tk, tv, ns, sm)
+            check_attention(o.cpu().numpy(), o_ref, f"step {step}")
+        plan.close()
+    finally:
+        uc.uc_set_path(prev)
