@@ -318,16 +318,18 @@ uc_status uc_attend_append(const uc_shape* shape, const uc_segment* segs,
  * physical layout is frozen, attention reuses its segment boundaries and type
  * identifiers instead of matching segments and preparing operators again).
  * A plan holds a copy of the segment descriptors and the device layout
- * derived from them, validated once; its decode steps then check only their
- * own pointers.  The layout is frozen except for segs[tail], a dense segment
- * with a row capacity whose row count the plan advances by every step's
- * n_new (the caller's descriptors are not written; uc_plan_tail_rows reports
- * the count).  Host memory only; a plan is used by one thread at a time, and
- * the segment buffers it points into must outlive it.
+ * derived from them, validated once; its calls then check only their own
+ * pointers.  The layout is frozen except for segs[tail] (tail >= 0), a dense
+ * segment with a row capacity whose row count the plan advances by every
+ * decode step's n_new (the caller's descriptors are not written;
+ * uc_plan_tail_rows reports the count); tail = -1 freezes every segment.
+ * Host memory only; a plan is used by one thread at a time, and the segment
+ * buffers it points into must outlive it.
  *   uc_plan_create   validates as uc_attend_append would (shape, segments,
  *                    q_dt, M, sm_scale; segs[tail] dense with row_stride >=
- *                    1; at most UC_MAX_SEGMENTS - 1 segments) and writes the
- *                    new plan to *out (NULL on error). */
+ *                    1 unless tail = -1; at most UC_MAX_SEGMENTS - 1
+ *                    segments) and writes the new plan to *out (NULL on
+ *                    error). */
 typedef struct uc_plan_s* uc_plan;
 uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs,
                          int n_segs, int tail, uc_dtype q_dt, int M,
@@ -335,13 +337,30 @@ uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs,
 /* Workspace bytes that serve every step of the plan up to the tail's
  * capacity (0 for a NULL plan). */
 size_t uc_plan_workspace_size(uc_plan plan);
-/* The tail's current row count (-1 for a NULL plan). */
+/* The tail's current row count (-1 for a NULL plan or one without a tail). */
 int uc_plan_tail_rows(uc_plan plan);
+/* Attention over the plan's segments as they stand: the result of
+ * uc_attend_mixed(shape, segs, n_segs, q, q_dt, M, sm_scale, o, lse, seg_lse,
+ * ws, ws_bytes, stream).  On the multi-query matrix-core path ((Hq/Hkv)*M >
+ * 16) the first call with a given ws also prepares it -- packed rows
+ * dequantised, V converted to fp16, the range flag -- and later calls with
+ * the same ws reuse that preparation (App. E: packed KV dequantised into a
+ * reusable workspace), so between them the segments' contents and ws must
+ * not change: after writing to a segment (re-quantisation, appended rows
+ * outside the plan) or using ws for other calls, call uc_plan_invalidate.
+ * ws: at least uc_plan_workspace_size bytes. */
+uc_status uc_plan_attend(uc_plan plan, const void* q, float* o, float* lse,
+                         float* seg_lse, void* ws, size_t ws_bytes,
+                         void* stream);
+/* Drops the plan's prepared workspace; the next uc_plan_attend prepares it
+ * again. */
+uc_status uc_plan_invalidate(uc_plan plan);
 /* One decode step on the plan: exactly uc_attend_append(shape, segs, n_segs,
  * tail, k_new, v_new, n_new, q, q_dt, M, sm_scale, o, lse, NULL, ws,
  * ws_bytes, stream) with the plan's arguments and the tail at its current row
- * count, which then advances by n_new.  ws: at least uc_plan_workspace_size
- * bytes.  On error nothing is enqueued and the row count stays. */
+ * count, which then advances by n_new (and a prepared workspace is dropped).
+ * ws: at least uc_plan_workspace_size bytes.  A plan without a tail refuses
+ * it.  On error nothing is enqueued and the row count stays. */
 uc_status uc_plan_attend_append(uc_plan plan, const void* k_new,
                                 const void* v_new, int n_new, const void* q,
                                 float* o, float* lse, void* ws,

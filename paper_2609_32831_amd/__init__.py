@@ -123,6 +123,8 @@ def _load():
         "uc_plan_tail_rows": (i32, [vp]),
         "uc_plan_attend_append": (i32, [vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]),
         "uc_plan_destroy": (i32, [vp]),
+        "uc_plan_attend": (i32, [vp, vp, vp, vp, vp, vp, sz, vp]),
+        "uc_plan_invalidate": (i32, [vp]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -269,17 +271,21 @@ def uc_attend_mixed(shape: uc_shape, segs: Sequence[Segment], q: torch.Tensor, M
 
 
 class AttendPlan:
-    """A decode-step execution plan over a frozen layout (uc_plan_create):
-    the segments are validated once and every step passes only pointers.
-    segs[tail] is the dense segment the steps append to; its Segment's
-    n_rows is kept in step with the plan.  Pointers may be given as tensors
-    or as raw device addresses (ints); the stream is the current one at
-    creation unless a call names another."""
+    """An execution plan over a frozen layout (uc_plan_create): the segments
+    are validated once and every call passes only pointers.  segs[tail] is
+    the dense segment decode steps append to (its Segment's n_rows is kept
+    in step with the plan); tail=None freezes every segment, and attend()
+    then reuses its workspace preparation across calls (see
+    uc_plan_attend).  Pointers may be given as tensors or as raw device
+    addresses (ints); the stream is the current one at creation unless a
+    call names another."""
 
-    def __init__(self, shape: uc_shape, segs: Sequence[Segment], tail: int, q_dtype: torch.dtype,
+    def __init__(self, shape: uc_shape, segs: Sequence[Segment], tail: Optional[int],
+                 q_dtype: torch.dtype,
                  M: int, sm_scale: float, ws: Optional[torch.Tensor] = None, stream=None,
                  device="cuda"):
         h = ctypes.c_void_p()
+        tail = -1 if tail is None else tail
         _check(lib.uc_plan_create(ctypes.byref(shape), _seg_array(segs), len(segs), tail,
                                   TORCH_DT[q_dtype], M, ctypes.c_float(sm_scale),
                                   ctypes.byref(h)), "uc_plan_create")
@@ -308,6 +314,19 @@ class AttendPlan:
                "uc_plan_attend_append")
         self.segs[self.tail].n_rows += n_new
         return o
+
+    def attend(self, q, o, lse=None, seg_lse=None, stream=None):
+        """Attention of q [B, Hq, M, D] over the plan's segments into o (and
+        lse, seg_lse)."""
+        a = [t if t is None or isinstance(t, int) else t.data_ptr() for t in (q, o, lse, seg_lse)]
+        _check(lib.uc_plan_attend(self._h, a[0], a[1], a[2], a[3], self._ws_ptr, self._ws_n,
+                                  self._stream if stream is None else _stream(stream)),
+               "uc_plan_attend")
+        return o
+
+    def invalidate(self):
+        """The segments' contents changed: prepare the workspace again."""
+        _check(lib.uc_plan_invalidate(self._h), "uc_plan_invalidate")
 
     def close(self):
         if self._h:

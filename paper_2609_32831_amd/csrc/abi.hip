@@ -26,6 +26,11 @@ size_t prefill_mfma_workspace(const uc_shape& sh, const KSegs& segs);
 hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
                                float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
                                hipStream_t st);
+hipError_t launch_prefill_prepare(const uc_shape& sh, const KSegs& segs, void* ws, hipStream_t st,
+                                  void* views_out);
+hipError_t launch_prefill_run(const uc_shape& sh, int n_segs, const void* views, const void* q,
+                              int M, float sm_scale, float* o, float* lse, float* seg_lse,
+                              void* ws, hipStream_t st);
 int score_mfma_chunk_rows();
 hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
                                  const void* q, int W, float sm_scale, float* partial,
@@ -449,6 +454,11 @@ struct uc_plan_s {
   uc_dtype q_dt;
   float sm_scale;
   size_t ws_need;            // enough for every call up to the tail's capacity
+  // multi-query attention: the workspace prepared by the last call (packed
+  // rows dequantised, V converted) and the views over it, reused while the
+  // segments stay as they are
+  void* prepared_ws;
+  alignas(16) char views[kPrefillViewBytes];
 };
 
 extern "C" {
@@ -460,8 +470,8 @@ uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs, int n_se
   KSegs ks;
   uc_status st = check_segments(shape, segs, n_segs, ks);
   if (st) return st;
-  if (tail < 0 || tail >= n_segs) return fail(UC_E_INVALID, "tail %d not in [0,%d)", tail, n_segs);
-  if (segs[tail].kind != UC_SEG_DENSE || segs[tail].row_stride < 1)
+  if (tail < -1 || tail >= n_segs) return fail(UC_E_INVALID, "tail %d not in [-1,%d)", tail, n_segs);
+  if (tail >= 0 && (segs[tail].kind != UC_SEG_DENSE || segs[tail].row_stride < 1))
     return fail(UC_E_INVALID, "segment %d (tail) is not a dense segment with a row capacity", tail);
   if (n_segs >= kMaxSeg)
     return fail(UC_E_UNSUPPORTED, "a plan takes at most %d segments", kMaxSeg - 1);
@@ -479,11 +489,12 @@ uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs, int n_se
   p->M = M;
   p->q_dt = q_dt;
   p->sm_scale = sm_scale;
+  p->prepared_ws = nullptr;
   // workspace: every path, at the tail's capacity (the sizes only grow with
   // the row counts)
   uc_segment full[kMaxSeg];
   memcpy(full, segs, (size_t)n_segs * sizeof(uc_segment));
-  full[tail].n_rows = full[tail].row_stride;
+  if (tail >= 0) full[tail].n_rows = full[tail].row_stride;
   KSegs kf;
   check_segments(shape, full, n_segs, kf);
   size_t need = generic_ws(*shape, kf, kAttRows, kAttMaxChunks, M, true);
@@ -496,13 +507,46 @@ uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs, int n_se
 
 size_t uc_plan_workspace_size(uc_plan plan) { return plan ? plan->ws_need : 0; }
 
-int uc_plan_tail_rows(uc_plan plan) { return plan ? plan->segs[plan->tail].n_rows : -1; }
+int uc_plan_tail_rows(uc_plan plan) {
+  return plan && plan->tail >= 0 ? plan->segs[plan->tail].n_rows : -1;
+}
+
+uc_status uc_plan_invalidate(uc_plan plan) {
+  if (!plan) return fail(UC_E_INVALID, "plan is NULL");
+  plan->prepared_ws = nullptr;
+  return ok();
+}
+
+uc_status uc_plan_attend(uc_plan plan, const void* q, float* o, float* lse, float* seg_lse,
+                         void* ws, size_t ws_bytes, void* stream) {
+  TimerScope timer;
+  if (!plan) return fail(UC_E_INVALID, "plan is NULL");
+  if (!q || !o) return fail(UC_E_INVALID, "q or o is NULL");
+  if (ws_bytes < plan->ws_need || (plan->ws_need && !ws))
+    return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, plan->ws_need);
+  const uc_shape& sh = plan->shape;
+  if (g_path.load() != UC_PATH_AUTO || !prefill_mfma_eligible(sh, plan->ks, plan->q_dt, plan->M)) {
+    plan->prepared_ws = nullptr;
+    return uc_attend_mixed(&sh, plan->segs, plan->n_segs, q, plan->q_dt, plan->M, plan->sm_scale,
+                           o, lse, seg_lse, ws, ws_bytes, stream);
+  }
+  hipStream_t s = (hipStream_t)stream;
+  if (plan->prepared_ws != ws) {
+    const hipError_t e = launch_prefill_prepare(sh, plan->ks, ws, s, plan->views);
+    if (e != hipSuccess) return launched(e);
+    plan->prepared_ws = ws;
+  }
+  g_last_kernel = "prefill_mfma";
+  return launched(launch_prefill_run(sh, plan->n_segs, plan->views, q, plan->M, plan->sm_scale, o,
+                                     lse, seg_lse, ws, s));
+}
 
 uc_status uc_plan_attend_append(uc_plan plan, const void* k_new, const void* v_new, int n_new,
                                 const void* q, float* o, float* lse, void* ws, size_t ws_bytes,
                                 void* stream) {
   TimerScope timer;
   if (!plan) return fail(UC_E_INVALID, "plan is NULL");
+  if (plan->tail < 0) return fail(UC_E_INVALID, "the plan has no tail segment to append to");
   const int tail = plan->tail, pos = plan->segs[tail].n_rows;
   if (n_new < 0) return fail(UC_E_INVALID, "n_new must be >= 0 (got %d)", n_new);
   if (n_new > 0) {
@@ -538,9 +582,10 @@ uc_status uc_plan_attend_append(uc_plan plan, const void* k_new, const void* v_n
     st = uc_attend_append(&sh, plan->segs, plan->n_segs, tail, k_new, v_new, n_new, q,
                           plan->q_dt, plan->M, plan->sm_scale, o, lse, nullptr, ws, ws_bytes, stream);
   }
-  if (st == UC_OK) {
+  if (st == UC_OK && n_new > 0) {
     plan->segs[tail].n_rows += n_new;
     plan->ks.s[tail].n_rows += n_new;
+    plan->prepared_ws = nullptr;  // the tail's rows changed
   }
   return st;
 }

@@ -31,6 +31,8 @@
 // fmaf(code, scale, min)) into a [B, Hkv, n_full, D] bf16 workspace (once per
 // call, where the query blocks of a head would otherwise each decode every
 // packed tile again); their residual tails are read in place.
+#include <string.h>
+
 #include <type_traits>
 
 #include "mfma_util.h"
@@ -652,9 +654,15 @@ size_t prefill_mfma_workspace(const uc_shape& sh, const KSegs& segs) {
   return bytes;
 }
 
-hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
-                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
-                               hipStream_t st) {
+static_assert(sizeof(Views) <= kPrefillViewBytes, "prepared views do not fit their slot");
+
+// Preparation of a call: the range flag, the dequantised rows of every
+// packed segment and the fp16 V copies, all in ws; the views the attention
+// kernel walks go to views_out (kPrefillViewBytes).  The result depends only
+// on the segments' contents and ws, so calls over unchanged segments can
+// reuse it (execution plans).
+hipError_t launch_prefill_prepare(const uc_shape& sh, const KSegs& segs, void* ws, hipStream_t st,
+                                  void* views_out) {
   const int BH = sh.B * sh.Hkv;
   Views vs{};
   int* v_unsafe = (int*)ws;
@@ -703,8 +711,20 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
                        vs.v[i].v, vs.v[i].bh_stride, vs.v[i].n, (uint16_t*)vs.v[i].vh, v_unsafe);
   }
   vs.tiles = tiles;
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  memcpy(views_out, &vs, sizeof vs);
+  return hipGetLastError();
+}
+
+// The attention kernel over prepared views (launch_prefill_prepare on the
+// same ws).
+hipError_t launch_prefill_run(const uc_shape& sh, int n_segs, const void* views, const void* q,
+                              int M, float sm_scale, float* o, float* lse, float* seg_lse,
+                              void* ws, hipStream_t st) {
+  Views vs;
+  memcpy(&vs, views, sizeof vs);
+  const int BH = sh.B * sh.Hkv;
+  const int* v_unsafe = (const int*)ws;
+  hipError_t e;
   const int nq = (sh.Hq / sh.Hkv) * M;
   // the 8-wave layout (one workgroup per CU) when its grid fills every round
   // or runs many rounds; otherwise the 4-wave one (two per CU), whose last
@@ -721,12 +741,21 @@ hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void
   if ((e = kernel_timer_begin(st)) != hipSuccess) return e;
   if (wide)
     hipLaunchKernelGGL((prefill_mfma_kernel<8, 2, 2>), dim3(grid), dim3(8 * 64), 0, st, vs, qp,
-                       sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
+                       sh.Hq, sh.Hkv, M, n_segs, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
   else
     hipLaunchKernelGGL((prefill_mfma_kernel<4, 1, 2>), dim3(grid), dim3(4 * 64), 0, st, vs, qp,
-                       sh.Hq, sh.Hkv, M, segs.n, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
+                       sh.Hq, sh.Hkv, M, n_segs, n_qblocks, n_work, sl2, o, lse, seg_lse, v_unsafe);
   e = hipGetLastError();
   return e == hipSuccess ? kernel_timer_end(st) : e;
+}
+
+hipError_t launch_prefill_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
+                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
+                               hipStream_t st) {
+  alignas(16) char views[kPrefillViewBytes];
+  const hipError_t e = launch_prefill_prepare(sh, segs, ws, st, views);
+  if (e != hipSuccess) return e;
+  return launch_prefill_run(sh, segs.n, views, q, M, sm_scale, o, lse, seg_lse, ws, st);
 }
 
 }  // namespace uc

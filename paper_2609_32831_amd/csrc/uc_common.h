@@ -10,6 +10,8 @@
 namespace uc {
 
 constexpr int kMaxSeg = UC_MAX_SEGMENTS;
+// bytes that hold the prepared views of one multi-query attention call
+constexpr size_t kPrefillViewBytes = 1024;
 
 // compute units of the current device (cached after the first call)
 int device_cus();

@@ -201,6 +201,26 @@ def test_plan_validation(uc):
         assert L.uc_plan_destroy(h) == uc.UC_OK
     assert L.uc_plan_destroy(None) == uc.UC_OK
     assert L.uc_plan_tail_rows(None) == -1 and L.uc_plan_workspace_size(None) == 0
+    assert L.uc_plan_invalidate(None) == E
+    assert L.uc_plan_attend(None, FAKE, FAKE, None, None, FAKE, 1 << 40, None) == E
+    # a plan without a tail: attention only
+    st, h = create(segs, -1, M=64)
+    assert st == uc.UC_OK and h
+    try:
+        assert L.uc_plan_tail_rows(h) == -1
+        need = L.uc_plan_workspace_size(h)
+        assert need >= L.uc_attend_workspace_size(ctypes.byref(sh), (uc.uc_segment * 2)(*segs),
+                                                  2, uc.UC_BF16, 64)
+        assert L.uc_plan_attend_append(h, FAKE, FAKE, 1, FAKE, FAKE, None, FAKE, 1 << 40,
+                                       None) == E
+        assert "no tail" in uc.uc_last_error()
+        assert L.uc_plan_attend(h, None, FAKE, None, None, FAKE, 1 << 40, None) == E
+        assert L.uc_plan_attend(h, FAKE, FAKE, None, None, FAKE, need - 1,
+                                None) == uc.UC_E_WORKSPACE
+        assert L.uc_plan_invalidate(h) == uc.UC_OK
+    finally:
+        L.uc_plan_destroy(h)
+    assert create(segs, -2)[0] == E
 
 
 def test_dynamic_budget_entry_validation(uc):
