@@ -397,7 +397,6 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
   // tile per stage, tile t+2 stored from Sc and tile t+3 loaded into Sn);
   // the first (no previous tile to multiply with V) is peeled
   auto iter = [&](int t, auto pv, const POp (&pp)[QT], POp (&pn)[QT], Stage& Sc, Stage& Sn) {
-    Stage& S = Sn;
     if (TPS == 1) {
       if (t + 3 < T) {
         stage_load<F16, NT>(cs, Sn, 0);
@@ -405,15 +404,13 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
         cs.next(vs, bh);
       }
     } else if (t % TPS == 0 && t + 2 * TPS < T) {  // the tiles of stage t/TPS + 2
-      {
-        stage_load<F16, NT>(cs, S, 0);
+      stage_load<F16, NT>(cs, Sn, 0);
+      cs.next(vs, bh);
+      n_pre = 1;
+      if (t + 2 * TPS + 1 < T) {
+        stage_load<F16, NT>(cs, Sn, 1);
         cs.next(vs, bh);
-        n_pre = 1;
-        if (t + 2 * TPS + 1 < T) {
-          stage_load<F16, NT>(cs, S, 1);
-          cs.next(vs, bh);
-          n_pre = 2;
-        }
+        n_pre = 2;
       }
     }
     const int vi = ct.vi;
@@ -444,9 +441,9 @@ __device__ __attribute__((always_inline)) inline int tile_loop(
           stage_store<NT>(tile_buf<TPS>(lds, t0), Sc, 0);
           stage_store<NT>(tile_buf<TPS>(lds, t0), Sc, 1);
         }
-      } else {
-        if (n_pre >= 1) stage_store<NT>(tile_buf<TPS>(lds, t0), S, 0);
-        if (n_pre >= 2) stage_store<NT>(tile_buf<TPS>(lds, t0 + 1), S, 1);
+      } else {  // Sc and Sn are the same set
+        if (n_pre >= 1) stage_store<NT>(tile_buf<TPS>(lds, t0), Sc, 0);
+        if (n_pre >= 2) stage_store<NT>(tile_buf<TPS>(lds, t0 + 1), Sc, 1);
       }
       n_pre = 0;
       __syncthreads();
