@@ -325,10 +325,15 @@ def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
     K = np.concatenate([ref.widen(kt, "bf16"), ref.widen(kv_, "bf16")], axis=1).reshape(nb, w.Hkv, -1, D)
     seg = np.concatenate([np.zeros(n_t, np.int32), np.ones(n_v, np.int32)])
     sc, _ = ref.score(ref.widen(q_obs, "bf16").reshape(nb, w.Hq, w.W, D), K, seg, 2, sm)
+    t1 = time.perf_counter()
     keep = ref.select(sc.reshape(BHs, -1)[:, n_t:], pols[vit]["k"], 0)
+    t2 = time.perf_counter()
     pk = ref.quantize(kt, vt, "bf16", pols[text]["group"], [pols[text]["bits"]] * BHs)
     kh, vh = ref.dequant(pk, n_t, D, pols[text]["group"], "bf16")
-    t_compress = time.perf_counter() - t0
+    t3 = time.perf_counter()
+    t_compress = t3 - t0
+    stages = {"score_s": round(t1 - t0, 3), "select_s": round(t2 - t1, 3),
+              "quantize_s": round(t3 - t2, 3)}
 
     present = np.zeros((BHs, n_v), np.uint8)
     for i in range(BHs):
@@ -347,6 +352,20 @@ def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
         t0 = time.perf_counter()
         ref.attend(q, Kt, Vt, pr, segs, 3, sm)
         t_att += time.perf_counter() - t0
+    stages["attend_s_per_step"] = round(t_att / n_steps, 4)
+    # one representative step (decode step 0's attention over the sampled
+    # heads) again on a single thread
+    Kt = np.concatenate([Kl, ref.widen(kd[:, :1], "bf16")], axis=1).reshape(nb, w.Hkv, -1, D)
+    Vt = np.concatenate([Vl, ref.widen(vd[:, :1], "bf16")], axis=1).reshape(nb, w.Hkv, -1, D)
+    pr = np.concatenate([np.ones((BHs, n_t), np.uint8), present, np.ones((BHs, 1), np.uint8)],
+                        axis=1).reshape(nb, w.Hkv, -1)
+    segs = np.concatenate([seg, np.full(1, 2, np.int32)])
+    q = ref.widen(qd[:, 0:1], "bf16").reshape(nb, w.Hq, 1, D)
+    ref.set_threads(1)
+    t0 = time.perf_counter()
+    ref.attend(q, Kt, Vt, pr, segs, 3, sm)
+    t_one = time.perf_counter() - t0
+    ref.set_threads(cores)
     scale = (w.B * w.Hkv) / BHs
     t_job = (t_compress + t_att / n_steps * T) * scale
     return {
@@ -359,6 +378,9 @@ def cpu_baseline(w, n_heads: int, n_steps: int, T: int):
                    f"scoring + selection + quantization ({t_compress:.2f} s) and "
                    f"{n_steps} of {T} decode steps ({t_att:.2f} s), extrapolated "
                    f"linearly to all heads and steps"),
+        "stages": stages,
+        "single_thread": {"step": f"decode step 0 attention over {BHs} KV heads",
+                          "s": round(t_one, 4), "threads": 1},
     }
 
 
