@@ -6,9 +6,11 @@
 // Work item: 128 query rows of one (b, h_kv) -- the rows of its G query heads
 // are contiguous in q -- in one workgroup of four waves; each wave owns two
 // 16-row query tiles.  The workgroup walks every key tile (32 rows) of every
-// segment once: the waves stage the K and V rows of tile i+2 through
-// registers into a four-deep ring of padded LDS tiles.  The loop is a
-// three-stage software pipeline: in iteration t a wave issues, interleaved,
+// segment once: the waves stage the K and V rows of later tiles through
+// registers (two register sets, so a tile's loads have two iterations to
+// arrive) into a four-deep ring of padded LDS tiles.  The loop is a
+// three-stage software pipeline: in iteration t a wave issues, interleaved
+// (each matrix instruction followed by its share of the softmax),
 //   S^T(t+1) = K Q^T    v_mfma_f32_16x16x32_bf16, K rows read from LDS as the
 //                       A operand (shared by both query tiles), Q^T in
 //                       registers;
@@ -21,7 +23,9 @@
 //                       lazily raised reference maximum, running per-segment
 //                       sums for seg_lse;
 // none of which depends on another, so one wave keeps the matrix cores and
-// the vector ALUs busy at once.  The rare raise of the reference maximum runs
+// the vector ALUs busy at once; the probability operands of consecutive
+// tiles alternate between two register sets.  The rare raise of the reference
+// maximum runs
 // after the matrix instructions (it rescales the accumulators they update).
 // Outputs (normalised O, lse, per-segment lse) are written directly; no
 // split over keys.  Workgroups are mapped so that those of one (b, h_kv) run
@@ -30,7 +34,9 @@
 // Packed segments first go through dequant_kernel: codes -> round_to_bf16(
 // fmaf(code, scale, min)) into a [B, Hkv, n_full, D] bf16 workspace (once per
 // call, where the query blocks of a head would otherwise each decode every
-// packed tile again); their residual tails are read in place.
+// packed tile again); their residual tails are read in place.  This
+// preparation (with the fp16 V copies and the range flag) is a stage of its
+// own, so an execution plan over an unchanged cache runs it once.
 #include <string.h>
 
 #include <type_traits>
