@@ -179,25 +179,33 @@ def summarize_prefill(d: str, command: str):
         grids[((qb * w.B * w.Hkv + 7) // 8 * 8) * 256] = w
     pm = glob.glob(os.path.join(d, "ppmc", "**", "*counter_collection.csv"), recursive=True)
     if pm:
-        lines += ["", "Counters per dispatch of prefill_mfma_kernel (one counter pass; "
-                      "dispatches run serialised under counter collection):", "",
-                  "| workload | MFMA busy cycles | x 1024 flop | algorithmic flop | "
-                  "GRBM_GUI_ACTIVE / XCD | MFMA utilisation | VALU insts | LDS insts | "
-                  "LDS conflict cycles |", "|---|---|---|---|---|---|---|---|---|"]
+        lines += ["", "Counters of prefill_mfma_kernel per workload (one counter pass; "
+                      "dispatches run serialised under counter collection; per-dispatch "
+                      "counts, utilisation as mean and range over the dispatches):", "",
+                  "| workload | dispatches | MFMA busy cycles | x 1024 flop | algorithmic flop | "
+                  "MFMA utilisation | VALU insts | LDS insts | LDS conflict cycles |",
+                  "|---|---|---|---|---|---|---|---|---|"]
+        rows = {}
         for e in _counters(pm[0], "prefill_mfma_kernel", per_dispatch=True):
-            w = grids.get(e["_grid"])
-            busy = e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
-            act = e.get("GRBM_GUI_ACTIVE", 0.0) / XCDS
+            rows.setdefault(e["_grid"], []).append(e)
+        for grid, es in rows.items():
+            w = grids.get(grid)
             alg = float("nan")
             if w is not None:  # attended rows: fixed-fraction evictions keep floor(ratio * n)
                 n_att = sum(int(sg.n * sg.keep_ratio) if sg.policy == "evict" else sg.n
                             for sg in w.segments)
                 alg = 4.0 * w.M * n_att * w.D * w.Hq * w.B
-            util = busy / (4 * CUS * act) if act else float("nan")
-            lines.append(f"| {w.name if w else e['_grid']} | {busy:.4g} | {busy * 1024:.4g} | "
-                         f"{alg:.4g} | {act:.4g} | {util:.3f} | "
-                         f"{e.get('SQ_INSTS_VALU', 0):.4g} | {e.get('SQ_INSTS_LDS', 0):.4g} | "
-                         f"{e.get('SQ_LDS_BANK_CONFLICT', 0):.4g} |")
+            utils = []
+            for e in es:
+                act = e.get("GRBM_GUI_ACTIVE", 0.0) / XCDS
+                utils.append(e.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0) / (4 * CUS * act)
+                             if act else float("nan"))
+            mean = lambda k: sum(e.get(k, 0.0) for e in es) / len(es)  # noqa: E731
+            busy = mean("SQ_VALU_MFMA_BUSY_CYCLES")
+            lines.append(f"| {w.name if w else grid} | {len(es)} | {busy:.4g} | "
+                         f"{busy * 1024:.4g} | {alg:.4g} | {sum(utils) / len(utils):.3f} "
+                         f"({min(utils):.3f}-{max(utils):.3f}) | {mean('SQ_INSTS_VALU'):.4g} | "
+                         f"{mean('SQ_INSTS_LDS'):.4g} | {mean('SQ_LDS_BANK_CONFLICT'):.4g} |")
         lines += ["", "The busy-cycle count times 1024 matches the algorithmic flop count "
                       "4 M N D Hq B of each step (one 16x16x32 product = 16384 flop = 16 busy "
                       "cycles) to within 1 %: no padded products; the extra work is the one tile "
