@@ -16,13 +16,13 @@ from typing import Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (NAME_DT, TORCH_DT, budget_state_read, budget_state_tensor, dense_segment,
+from . import (NAME_DT, TORCH_DT, budget_state_tensor, dense_segment,
                make_shape, packed_layout, packed_segment, uc_assign_bits, uc_attend_append,
                uc_attend_mixed, uc_attend_workspace_size, uc_budget_params, uc_budget_step,
                uc_calibrate_policy, uc_compose_index, uc_dense_bytes, uc_dequantize_segment,
                uc_evict_rows_for_budget, uc_evicted_bytes, uc_packed_bytes, uc_quantize_segment,
                uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep,
-               uc_stream_append, uc_topk_mass)
+               uc_stream_append, uc_topk_mass, uc_budget_state)
 
 TORCH = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -376,6 +376,8 @@ class DynamicRun:
                                        self.n_qt, self.dt, w.rho_init, w.rho_min)
         self.state = budget_state_tensor(device)
         self.state_host = torch.empty(self.state.numel(), dtype=torch.uint8, pin_memory=True)
+        self.state_ready = torch.cuda.Event()
+        self.falling = True
         # the kept rows of the evicting type, their logical indices and the
         # selection's local indices: two sets of buffers sized for every row,
         # alternating (a boundary gathers from one set into the other)
@@ -402,18 +404,24 @@ class DynamicRun:
         out[self.qt] = self.packed
         return out
 
-    def _select(self, q_obs, W, k_new):
+    def _score(self, q_obs, W):
         """Scores of the evicting type's current rows from q_obs [1, Hq, W, D]
-        over the current cache; keep the best k_new of them (compacted, with
-        composed logical indices)."""
+        over the current cache (the quantised type in its packed form)."""
+        Hkv = self.w.Hkv
+        segs = self.segments()
+        n_cur = segs[self.ev].n_rows
+        outs = [None] * self.nseg
+        outs[self.ev] = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)
+        uc_score_importance(self.shape, segs, q_obs, W, self.sm, outs, None, ws=self.ws_sc)
+
+    def _select(self, k_new):
+        """Keep the best k_new of the evicting type's current rows by the
+        scores _score left (compacted, with composed logical indices)."""
         w = self.w
         Hkv, D = w.Hkv, w.D
-        segs = self.segments()  # the quantised type is scored in its packed form
+        segs = self.segments()
         n_cur = segs[self.ev].n_rows
-        sc = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)  # contiguous [1, Hkv, n_cur]
-        outs = [None] * self.nseg
-        outs[self.ev] = sc
-        uc_score_importance(self.shape, segs, q_obs, W, self.sm, outs, None, ws=self.ws_sc)
+        sc = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)
         s = self.set = 1 - self.set
         n = Hkv * k_new
         local = self.local[:n].view(Hkv, k_new)
@@ -452,13 +460,29 @@ class DynamicRun:
     def _boundary(self, t, t0, n, q_obs, W):
         """Boundary after timestep t over the chunk t0 .. t0+n-1: the device
         decides (uc_budget_step), the host reads the decision and applies it
-        from the next timestep on."""
+        from the next timestep on.  While the host waits for the decision,
+        the device already scores the current cache when the retention ratio
+        was still above its floor at the last boundary, so that the budget is
+        likely to shrink again (the scores are only used if the evicting type
+        shrinks; they depend on nothing the decision changes)."""
+        stream = torch.cuda.current_stream()
         uc_budget_step(self.params, self.mass[t0:t0 + n], n, self.state)
-        st = budget_state_read(self.state, self.state_host)
-        if self.compact is None or st.k < st.k_prev:
-            self._select(q_obs, W, st.k)
+        self.state_host.copy_(self.state, non_blocking=True)
+        self.state_ready.record(stream)
+        first = self.compact is None
+        ahead = first or self.falling
+        if ahead:
+            self._score(q_obs, W)
+        self.state_ready.synchronize()
+        st = uc_budget_state.from_buffer_copy(self.state_host.numpy().tobytes())
+        shrink = first or st.k < st.k_prev
+        if shrink:
+            if not ahead:
+                self._score(q_obs, W)
+            self._select(st.k)
         if st.cfg != st.cfg_prev:
             self._quantize((st.cfg, st.bits, st.group))
+        self.falling = st.rho > self.w.rho_min
         rec = {"rho": st.rho, "B": st.B, "m": {self.ev: st.m[0], self.qt: st.m[1]},
                "b": {self.ev: st.b[0], self.qt: st.b[1]}, "k": st.k, "cfg": st.cfg,
                "bits": st.bits, "group": st.group}
