@@ -770,7 +770,6 @@ def dynamic_bench(args):
     import torch
 
     import workloads as gen
-    from paper_2609_32831_amd import uc_attend_mixed, uc_segment_mass
     from paper_2609_32831_amd.runner import DynamicRun
     from workloads.device import device_inputs
 
@@ -797,10 +796,9 @@ def dynamic_bench(args):
             bsteps = []
             for t in range(w.steps):
                 ev.record(3 * t, stream)
-                # the attention and the per-step type masses
-                uc_attend_mixed(run.shape, run.segments(), q_b[t], w.M, run.sm, o, run.lse,
-                                run.seg_lse, ws=run.ws_att)
-                uc_segment_mass(run.shape, w.M, run.nseg, run.lse, run.seg_lse, run.mass[t])
+                # the attention (on the layout's execution plan) and the
+                # per-step type masses
+                run.attend(t, q_b[t], o)
                 ev.record(3 * t + 1, stream)
                 if run.after_step(t, q_b[t]) is not None:
                     # a boundary: its work is bracketed by one more event (the

@@ -11,7 +11,10 @@
  *   uc_score_importance  attention-probability importance per cached token and
  *                        attention mass per segment (Sec. 3.3, Eq. 1;
  *                        App. E "Efficient attention-guided allocation")
+ *   uc_score_columns     the same scores from the row normalisers of an
+ *                        attention pass already run (its second pass only)
  *   uc_select_keep       per-KV-head top-k token eviction with compaction
+ *   uc_evict_step        the same with the row count read on the device
  *                        (App. E "Batched GQA token selection")
  *   uc_quantize_segment  group-wise asymmetric low-bit quantization
  *                        (App. E "Physical, type-aware KV storage")
@@ -183,6 +186,35 @@ uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs,
 size_t uc_score_workspace_size(const uc_shape* shape, const uc_segment* segs,
                                int n_segs, int W);
 
+/* Importance scores from the row log-sum-exps of an attention pass already
+ * run over the same segments (Sec. 3.3 Eq. 1: P is the softmax whose
+ * normaliser that pass computed; App. E "Efficient attention-guided
+ * allocation": attention statistics gathered next to attention).  The result
+ * is that of uc_score_importance with its first pass (each row's
+ * log-sum-exp over every segment) replaced by the caller's values:
+ *   q_obs, q_ld  observation row (b, h, w) at q_obs + ((b*Hq + h)*q_ld + w)*D
+ *                (q_ld >= W; q_ld = W is the contiguous [B, Hq, W, D] block,
+ *                and the last W rows of a [B, Hq, M, D] query block are
+ *                q + (M - W)*D with q_ld = M);
+ *   row_lse      device float; observation row (b, h, w) has its natural-log
+ *                normaliser at row_lse[(b*Hq + h)*lse_ld + w], e.g. the lse
+ *                output of uc_attend_mixed for the same query rows over the
+ *                same segments (pass lse + (M - W) with lse_ld = M to score
+ *                the last W of its M rows);
+ *   lse_ld       >= W.
+ * Every other argument, the outputs and the workspace
+ * (uc_score_workspace_size) are as for uc_score_importance.  With mass_out
+ * NULL only the segments whose scores_out entry is set are read; with
+ * neither, nothing is enqueued.  The probabilities are exp(s - lse) with the
+ * caller's lse: a normaliser that is not the log-sum-exp of the row gives
+ * scores scaled by the ratio (rows of one head need not sum to G*W). */
+uc_status uc_score_columns(const uc_shape* shape, const uc_segment* segs,
+                           int n_segs, const void* q_obs, int64_t q_ld,
+                           uc_dtype q_dt, int W, float sm_scale,
+                           const float* row_lse, int64_t lse_ld,
+                           float* const* scores_out, float* mass_out, void* ws,
+                           size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Top-k token selection and physical compaction for one eviction-managed
  * segment (App. E "Batched GQA token selection" and "Physical, type-aware KV
@@ -204,6 +236,32 @@ uc_status uc_select_keep(const float* scores, int BH, int N, int k,
                          void* stream);
 
 size_t uc_select_workspace_size(int BH, int N);
+
+/* One eviction step whose row count is decided on the device (Sec. 3.3
+ * dynamic budget with the Sec. 3.4 translation: an eviction-managed type
+ * keeps k rows per KV head; App. E "Batched GQA token selection" and
+ * "Physical, type-aware KV storage").  With N = cur->n_rows and
+ * k = max(*k_dev, 0), read by the kernels:
+ *   k >= N  nothing is written (the caller keeps cur);
+ *   k <  N  for each (b, h_kv) the rows of uc_select_keep(scores, BH, N, k,
+ *           0, ...) -- the k largest (score, -index), ascending -- are
+ *           copied to rows 0..k-1 of out, and out->idx[bh, j] receives
+ *           cur->idx[bh, i] for the j-th kept row i (i itself when cur->idx
+ *           is NULL, i.e. cur holds the segment's original rows).
+ *   scores  device float [B*Hkv, N] (uc_score_importance / uc_score_columns
+ *           output for cur);
+ *   cur     dense segment; idx, when given, int32 with the rows' row_stride
+ *           ([B, Hkv, row_stride]);
+ *   out     dense segment of cur's dtype with row_stride >= N and k, v, idx
+ *           non-NULL (idx int32 [B, Hkv, row_stride]); its n_rows is not
+ *           read: after the call it holds k rows.  out must not overlap cur;
+ *   k_dev   device int32, e.g. the k field of a uc_budget_state that
+ *           uc_budget_step writes earlier on the same stream.
+ * The host does not learn k from this call: it reads the decision back to
+ * size the calls that follow.  Three launches; no workspace. */
+uc_status uc_evict_step(const uc_shape* shape, const float* scores,
+                        const uc_segment* cur, const int32_t* k_dev,
+                        const uc_segment* out, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Group-wise asymmetric min/max quantization of one segment (App. E
@@ -335,7 +393,10 @@ uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs,
                          int n_segs, int tail, uc_dtype q_dt, int M,
                          float sm_scale, uc_plan* out);
 /* Workspace bytes that serve every step of the plan up to the tail's
- * capacity (0 for a NULL plan). */
+ * capacity on the kernel path selected when the plan was created
+ * (uc_set_path); a call made after the path was switched needs that path's
+ * uc_attend_workspace_size and fails with UC_E_WORKSPACE without it (0 for
+ * a NULL plan). */
 size_t uc_plan_workspace_size(uc_plan plan);
 /* The tail's current row count (-1 for a NULL plan or one without a tail). */
 int uc_plan_tail_rows(uc_plan plan);

@@ -9,6 +9,7 @@ and a call raises ``UcError`` when the library returns an error status.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from typing import List, Optional, Sequence
 
@@ -82,9 +83,12 @@ def _load():
         "uc_score_importance": (i32, [shp, segp, i32, vp, i32, i32, ctypes.c_float, vp, vp, vp,
                                       sz, vp]),
         "uc_score_workspace_size": (sz, [shp, segp, i32, i32]),
+        "uc_score_columns": (i32, [shp, segp, i32, vp, i64, i32, i32, ctypes.c_float, vp, i64,
+                                   vp, vp, vp, sz, vp]),
         "uc_select_keep": (i32, [vp, i32, i32, i32, i32, vp, vp, vp, vp, vp, i32, i32, vp, sz,
                                  vp]),
         "uc_select_workspace_size": (sz, [i32, i32]),
+        "uc_evict_step": (i32, [shp, vp, segp, vp, segp, vp]),
         "uc_quantize_segment": (i32, [shp, vp, vp, i32, i32, segp, vp]),
         "uc_attend_mixed": (i32, [shp, segp, i32, vp, i32, i32, ctypes.c_float, vp, vp, vp, vp,
                                   sz, vp]),
@@ -195,16 +199,37 @@ def packed_layout(BH: int, N: int, D: int, G: int, head_bits: Sequence[int]):
     return off, pos
 
 
+def packed_storage(B: int, Hkv: int, N: int, D: int, dtype: torch.dtype, device="cuda") -> dict:
+    """Flat buffers that hold a packed segment of N rows in any uniform
+    configuration (codes up to 8 bits, groups down to 8 rows), for
+    packed_segment(..., storage=...)."""
+    BH = B * Hkv
+    return {"codes_k": torch.empty(max(BH * N * D, 16), dtype=torch.uint8, device=device),
+            "codes_v": torch.empty(max(BH * N * D, 16), dtype=torch.uint8, device=device),
+            "scale_k": torch.empty(BH * (N // 8) * D, dtype=torch.float32, device=device),
+            "min_k": torch.empty(BH * (N // 8) * D, dtype=torch.float32, device=device),
+            "scale_v": torch.empty(BH * N * (D // 8), dtype=torch.float32, device=device),
+            "min_v": torch.empty(BH * N * (D // 8), dtype=torch.float32, device=device),
+            "tail_k": torch.empty(BH * 127 * D, dtype=dtype, device=device),
+            "tail_v": torch.empty(BH * 127 * D, dtype=dtype, device=device)}
+
+
 def packed_segment(B: int, Hkv: int, N: int, D: int, G: int, dtype: torch.dtype,
                    bits: int = 4, head_bits: Optional[Sequence[int]] = None,
-                   device="cuda", capacity: int = 0, zero: bool = True) -> Segment:
+                   device="cuda", capacity: int = 0, zero: bool = True,
+                   storage: Optional[dict] = None) -> Segment:
     """Allocate the buffers of a packed segment of N rows (to be filled by
     uc_quantize_segment).  head_bits: optional per-(b, h_kv) code widths.
     capacity > 0: room for that many rows per head (a segment that grows by
     uc_stream_append; strides follow the capacity).  zero=False leaves the
     buffers uninitialised (for a segment that uc_quantize_segment fills
-    whole before anything reads it)."""
-    alloc = torch.zeros if zero else torch.empty
+    whole before anything reads it).  storage: buffers from packed_storage
+    to lay the segment out in instead of allocating (uniform widths, no
+    capacity; contents left as they are)."""
+    def take(name, shape, dt):
+        if storage is None:
+            return (torch.zeros if zero else torch.empty)(*shape, dtype=dt, device=device)
+        return storage[name][:math.prod(shape)].view(*shape)
     BH = B * Hkv
     n_full = G * (N // G)
     tail = N - n_full
@@ -217,14 +242,15 @@ def packed_segment(B: int, Hkv: int, N: int, D: int, G: int, dtype: torch.dtype,
         t["code_off"] = torch.tensor(off, dtype=torch.int64, device=device)
     else:
         total = BH * cap_full * D * bits // 8
-    t["codes_k"] = alloc(max(total, 16), dtype=torch.uint8, device=device)
-    t["codes_v"] = alloc(max(total, 16), dtype=torch.uint8, device=device)
-    t["scale_k"] = alloc(B, Hkv, cap_full // G, D, dtype=torch.float32, device=device)
-    t["min_k"] = alloc(B, Hkv, cap_full // G, D, dtype=torch.float32, device=device)
-    t["scale_v"] = alloc(B, Hkv, cap_full, D // G, dtype=torch.float32, device=device)
-    t["min_v"] = alloc(B, Hkv, cap_full, D // G, dtype=torch.float32, device=device)
-    t["tail_k"] = alloc(B, Hkv, tail_rows, D, dtype=dtype, device=device)
-    t["tail_v"] = alloc(B, Hkv, tail_rows, D, dtype=dtype, device=device)
+    assert storage is None or (head_bits is None and not capacity)
+    shapes = {"codes_k": (max(total, 16),), "codes_v": (max(total, 16),),
+              "scale_k": (B, Hkv, cap_full // G, D), "min_k": (B, Hkv, cap_full // G, D),
+              "scale_v": (B, Hkv, cap_full, D // G), "min_v": (B, Hkv, cap_full, D // G),
+              "tail_k": (B, Hkv, tail_rows, D), "tail_v": (B, Hkv, tail_rows, D)}
+    for name, shp in shapes.items():
+        dt = torch.uint8 if name.startswith("codes") else dtype if name.startswith("tail") \
+            else torch.float32
+        t[name] = take(name, shp, dt)
     d = uc_segment(kind=UC_SEG_PACKED, dtype=TORCH_DT[dtype], n_rows=N, row_stride=capacity,
                    group=G, bits=bits if head_bits is None else int(max(head_bits)),
                    head_bits=_ptr(t.get("head_bits")), code_off=_ptr(t.get("code_off")),
@@ -376,6 +402,31 @@ def uc_score_importance(shape: uc_shape, segs: Sequence[Segment], q_obs: torch.T
            "uc_score_importance")
 
 
+def uc_score_columns(shape: uc_shape, segs: Sequence[Segment], q_obs: torch.Tensor, W: int,
+                     sm_scale: float, row_lse, lse_ld: int,
+                     scores_out: Sequence[Optional[torch.Tensor]],
+                     mass_out: Optional[torch.Tensor] = None,
+                     ws: Optional[torch.Tensor] = None, stream=None, q_ld: Optional[int] = None):
+    """uc_score_importance with the row log-sum-exps given: row_lse is a
+    float tensor (or a raw device address) whose element (b*Hq + h)*lse_ld + w
+    is observation row (b, h, w)'s normaliser.  q_obs [B, Hq, W, D], or with
+    q_ld the window starting at q_obs's first element with q_ld rows between
+    query heads (q_obs then may be the whole [B, Hq, M, D] block and W its
+    last rows: pass q_obs[:, :, M - W:] as a view)."""
+    arr = _seg_array(segs)
+    if ws is None:
+        ws = _ws(lib.uc_score_workspace_size(ctypes.byref(shape), arr, len(segs), W),
+                 q_obs.device)
+    ptrs = (ctypes.c_void_p * len(segs))(*[_ptr(t) for t in scores_out])
+    lp = row_lse if isinstance(row_lse, int) else row_lse.data_ptr()
+    _check(lib.uc_score_columns(ctypes.byref(shape), arr, len(segs), q_obs.data_ptr(),
+                                W if q_ld is None else q_ld, TORCH_DT[q_obs.dtype], W,
+                                ctypes.c_float(sm_scale), lp, lse_ld,
+                                ctypes.cast(ptrs, ctypes.c_void_p), _ptr(mass_out),
+                                ws.data_ptr(), ws.numel(), _stream(stream)),
+           "uc_score_columns")
+
+
 def uc_select_keep(scores: torch.Tensor, k: int, n_recent: int, keep_idx: torch.Tensor,
                    k_src: Optional[torch.Tensor] = None, v_src: Optional[torch.Tensor] = None,
                    k_dst: Optional[torch.Tensor] = None, v_dst: Optional[torch.Tensor] = None,
@@ -389,6 +440,16 @@ def uc_select_keep(scores: torch.Tensor, k: int, n_recent: int, keep_idx: torch.
                               _ptr(k_src), _ptr(v_src), _ptr(k_dst), _ptr(v_dst), dt, D,
                               ws.data_ptr(), ws.numel(), _stream(stream)), "uc_select_keep")
     return keep_idx
+
+
+def uc_evict_step(shape: uc_shape, scores, cur: Segment, k_dev, out: Segment, stream=None):
+    """Keep the best k = *k_dev rows of cur (scores [B*Hkv, cur.n_rows]) in
+    out, composing logical indices; k >= cur.n_rows writes nothing.  scores
+    and k_dev: tensors or raw device addresses."""
+    sp = scores if isinstance(scores, int) else scores.data_ptr()
+    kp = k_dev if isinstance(k_dev, int) else k_dev.data_ptr()
+    _check(lib.uc_evict_step(ctypes.byref(shape), sp, ctypes.byref(cur.desc), kp,
+                             ctypes.byref(out.desc), _stream(stream)), "uc_evict_step")
 
 
 def uc_quantize_segment(shape: uc_shape, k: torch.Tensor, v: torch.Tensor, N: int,

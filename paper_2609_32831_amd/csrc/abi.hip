@@ -36,7 +36,7 @@ hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const Ch
                                  const void* q, int W, float sm_scale, float* partial,
                                  hipStream_t st);
 hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
-                                 const void* q, int W, float sm_scale, const float* lse,
+                                 const void* q, int W, int q_ld, float sm_scale, const float* lse,
                                  float* const* scores, double* mass_partial, double* colpart,
                                  hipStream_t st);
 int score_mfma_qblocks(int nq);
@@ -490,16 +490,23 @@ uc_status uc_plan_create(const uc_shape* shape, const uc_segment* segs, int n_se
   p->q_dt = q_dt;
   p->sm_scale = sm_scale;
   p->prepared_ws = nullptr;
-  // workspace: every path, at the tail's capacity (the sizes only grow with
-  // the row counts)
+  // workspace: the path selected now (uc_set_path), at the tail's capacity
+  // (the sizes only grow with the row counts).  A call after the path was
+  // switched goes through uc_attend_mixed / uc_attend_append, which check
+  // the workspace against that path's own need.
   uc_segment full[kMaxSeg];
   memcpy(full, segs, (size_t)n_segs * sizeof(uc_segment));
   if (tail >= 0) full[tail].n_rows = full[tail].row_stride;
   KSegs kf;
   check_segments(shape, full, n_segs, kf);
-  size_t need = generic_ws(*shape, kf, kAttRows, kAttMaxChunks, M, true);
-  if (decode_mfma_eligible(*shape, kf, q_dt, M)) need = std::max(need, decode_mfma_workspace(*shape, kf, M));
-  if (prefill_mfma_eligible(*shape, kf, q_dt, M)) need = std::max(need, prefill_mfma_workspace(*shape, kf));
+  size_t need;
+  if (g_path.load() == UC_PATH_AUTO && prefill_mfma_eligible(*shape, kf, q_dt, M)) {
+    need = prefill_mfma_workspace(*shape, kf);
+  } else {
+    need = generic_ws(*shape, kf, kAttRows, kAttMaxChunks, M, true);
+    if (g_path.load() == UC_PATH_AUTO && decode_mfma_eligible(*shape, kf, q_dt, M))
+      need = std::max(need, decode_mfma_workspace(*shape, kf, M));
+  }
   p->ws_need = need;
   *out = p;
   return ok();
@@ -782,7 +789,7 @@ uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int
     e = launch_score_lse_mfma(*shape, ks, p, q_obs, W, sm_scale, partial, s);
     if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p, W, partial, nullptr, lse, nullptr, s);
     if (e == hipSuccess)
-      e = launch_score_col_mfma(*shape, ks, p, q_obs, W, sm_scale, lse, sp, mpart, colpart, s);
+      e = launch_score_col_mfma(*shape, ks, p, q_obs, W, W, sm_scale, lse, sp, mpart, colpart, s);
     p2 = p;
   } else {
     const ChunkPlan p1 = score_lse_plan(ks);
@@ -790,7 +797,61 @@ uc_status uc_score_importance(const uc_shape* shape, const uc_segment* segs, int
     e = launch_attend_generic(*shape, ks, p1, q_obs, q_dt, W, sm_scale, partial, false, s);
     if (e == hipSuccess) e = launch_attend_combine(*shape, ks, p1, W, partial, nullptr, lse, nullptr, s);
     if (e == hipSuccess)
-      e = launch_score_colsum(*shape, ks, p2, q_obs, q_dt, W, sm_scale, lse, sp, mpart, s);
+      e = launch_score_colsum(*shape, ks, p2, q_obs, q_dt, W, W, sm_scale, lse, sp, mpart, s);
+  }
+  if (e == hipSuccess && mass_out)
+    e = launch_mass_finalize(p2, shape->B * shape->Hkv, n_segs, mpart, mass_out, s);
+  return launched(e);
+}
+
+uc_status uc_score_columns(const uc_shape* shape, const uc_segment* segs, int n_segs,
+                           const void* q_obs, int64_t q_ld, uc_dtype q_dt, int W, float sm_scale,
+                           const float* row_lse, int64_t lse_ld, float* const* scores_out,
+                           float* mass_out, void* ws, size_t ws_bytes, void* stream) {
+  KSegs ks;
+  uc_status st = check_segments(shape, segs, n_segs, ks);
+  if (st) return st;
+  if (!q_obs) return fail(UC_E_INVALID, "q_obs is NULL");
+  if (!dtype_ok(q_dt)) return fail(UC_E_INVALID, "bad q dtype %d", q_dt);
+  if (W < 1) return fail(UC_E_INVALID, "W must be >= 1 (got %d)", W);
+  if (!(sm_scale > 0.0f) || !isfinite(sm_scale)) return fail(UC_E_INVALID, "sm_scale must be finite and > 0");
+  if ((int64_t)shape->B * shape->Hq * W > INT32_MAX) return fail(UC_E_UNSUPPORTED, "too many query rows");
+  if (!row_lse) return fail(UC_E_INVALID, "row_lse is NULL");
+  if (lse_ld < W) return fail(UC_E_INVALID, "lse_ld=%lld < W=%d", (long long)lse_ld, W);
+  if (q_ld < W || q_ld > INT32_MAX) return fail(UC_E_INVALID, "q_ld=%lld < W=%d", (long long)q_ld, W);
+  const bool fast = score_fast(*shape, ks, q_dt);
+  size_t a, b, c, d;
+  score_ws_parts(*shape, ks, W, fast, a, b, c, d);
+  if (!ws || ws_bytes < a + b + c + d)
+    return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, a + b + c + d);
+  float* sp[kMaxSeg] = {};
+  bool any = false;
+  if (scores_out)
+    for (int i = 0; i < n_segs; ++i) {
+      sp[i] = scores_out[i];
+      any = any || sp[i] != nullptr;
+    }
+  g_last_kernel = fast ? "score_mfma" : "score_valu";
+  if (!any && !mass_out) return ok();
+  // without masses, the chunks of segments whose scores are not wanted are
+  // left out of the plan (the kernels read the row counts from ks)
+  KSegs kp = ks;
+  if (!mass_out)
+    for (int i = 0; i < n_segs; ++i)
+      if (!sp[i]) kp.s[i].n_rows = 0;
+  hipStream_t s = (hipStream_t)stream;
+  float* lse = (float*)((char*)ws + a);
+  double* mpart = mass_out ? (double*)((char*)ws + a + b) : nullptr;
+  double* colpart = d ? (double*)((char*)ws + a + b + c) : nullptr;
+  const ChunkPlan p2 = fast ? score_mfma_plan(kp) : score_col_plan(kp);
+  hipError_t e = hipSuccess;
+  if (p2.n_chunks > 0) {
+    e = launch_lse_rows(row_lse, lse_ld, W, shape->B * shape->Hq, lse, s);
+    if (e == hipSuccess)
+      e = fast ? launch_score_col_mfma(*shape, ks, p2, q_obs, W, (int)q_ld, sm_scale, lse, sp,
+                                       mpart, colpart, s)
+               : launch_score_colsum(*shape, ks, p2, q_obs, q_dt, W, (int)q_ld, sm_scale, lse, sp,
+                                     mpart, s);
   }
   if (e == hipSuccess && mass_out)
     e = launch_mass_finalize(p2, shape->B * shape->Hkv, n_segs, mpart, mass_out, s);
@@ -837,6 +898,49 @@ uc_status uc_select_keep(const float* scores, int BH, int N, int k, int n_recent
   if (e == hipSuccess && k_src)
     e = launch_gather(keep_idx, BH, N, k, k_src, v_src, k_dst, v_dst, dtype_bytes(dt), D, s);
   return launched(e);
+}
+
+// ---------------------------------------------------------------- device-sized eviction
+uc_status uc_evict_step(const uc_shape* shape, const float* scores, const uc_segment* cur,
+                        const int32_t* k_dev, const uc_segment* out, void* stream) {
+  uc_status st = check_shape(shape);
+  if (st) return st;
+  if (!cur || !out) return fail(UC_E_INVALID, "cur or out is NULL");
+  if (cur->kind != UC_SEG_DENSE || out->kind != UC_SEG_DENSE)
+    return fail(UC_E_INVALID, "cur and out must be dense segments");
+  KSeg kc, ko;
+  st = check_segment(*shape, *cur, 0, kc, false);
+  if (st) return st;
+  uc_segment o = *out;
+  o.n_rows = 0;  // not read
+  st = check_segment(*shape, o, 1, ko, false);
+  if (st) return st;
+  if (cur->dtype != out->dtype) return fail(UC_E_INVALID, "cur and out differ in dtype");
+  const int N = kc.n_rows;
+  if (ko.row_stride < N)
+    return fail(UC_E_INVALID, "out row_stride %d < cur n_rows %d", ko.row_stride, N);
+  if (N == 0) return ok();
+  if (!scores || !k_dev) return fail(UC_E_INVALID, "scores or k_dev is NULL");
+  if (!out->k || !out->v || !out->idx) return fail(UC_E_INVALID, "out k/v/idx NULL");
+  const int64_t BH = (int64_t)shape->B * shape->Hkv;
+  const size_t row_bytes = (size_t)shape->D * dtype_bytes(cur->dtype);
+  auto overlap = [&](const void* a, size_t na, const void* b, size_t nb) {
+    const char* x = (const char*)a;
+    const char* y = (const char*)b;
+    return x < y + nb && y < x + na;
+  };
+  const size_t cur_rows = (size_t)BH * kc.row_stride * row_bytes;
+  const size_t out_rows = (size_t)BH * ko.row_stride * row_bytes;
+  if (overlap(out->k, out_rows, cur->k, cur_rows) || overlap(out->k, out_rows, cur->v, cur_rows) ||
+      overlap(out->v, out_rows, cur->k, cur_rows) || overlap(out->v, out_rows, cur->v, cur_rows) ||
+      overlap(out->k, out_rows, out->v, out_rows))
+    return fail(UC_E_INVALID, "out rows overlap cur rows or each other");
+  if (cur->idx &&
+      overlap(out->idx, (size_t)BH * ko.row_stride * 4, cur->idx, (size_t)BH * kc.row_stride * 4))
+    return fail(UC_E_INVALID, "out idx overlaps cur idx");
+  return launched(launch_evict_step((int)BH, N, scores, k_dev, cur->k, cur->v, kc.row_stride,
+                                    (const int32_t*)cur->idx, out->k, out->v, (int32_t*)out->idx,
+                                    ko.row_stride, (int)row_bytes, (hipStream_t)stream));
 }
 
 // ---------------------------------------------------------------- quantize

@@ -243,7 +243,7 @@ struct ScorePtrs {
 template <int D>
 __global__ __launch_bounds__(256) void score_colsum_kernel(KSegs segs, ChunkPlan plan,
                                                            const void* __restrict__ q, int q_dt,
-                                                           int Hq, int Hkv, int W,
+                                                           int Hq, int Hkv, int W, int q_ld,
                                                            float scale_log2,
                                                            const float* __restrict__ lse,
                                                            ScorePtrs scores,
@@ -299,7 +299,7 @@ __global__ __launch_bounds__(256) void score_colsum_kernel(KSegs segs, ChunkPlan
       float val = 0.0f;
       if (qr < nq) {
         const int g = qr / W, w = qr % W;
-        val = load_elem(q, q_dt, (((int64_t)b * Hq + hkv * G + g) * W + w) * D + d) * scale_log2;
+        val = load_elem(q, q_dt, (((int64_t)b * Hq + hkv * G + g) * q_ld + w) * D + d) * scale_log2;
       }
       qs[j][d] = val;
     }
@@ -348,7 +348,11 @@ __global__ void mass_finalize_kernel(ChunkPlan plan, int nseg, const double* __r
 // head and the query rows of P mass per segment = exp(seg_lse - lse).  One
 // 1024-thread workgroup per (b, h_kv); each term is exp of the exact
 // double-precision difference evaluated in binary32 (relative error below
-// 1e-6), and the terms are summed in double.
+// 1e-6), and the terms are summed in double.  A thread takes rows tid,
+// tid + 1024, ... and issues the loads of kMassRows of them before summing,
+// so the row loop waits on memory once per kMassRows rows instead of once
+// per row.
+constexpr int kMassRows = 8;
 __global__ __launch_bounds__(1024) void segment_mass_kernel(int Hq, int Hkv, int M, int nseg,
                                                             const float* __restrict__ lse,
                                                             const float* __restrict__ seg_lse,
@@ -360,12 +364,21 @@ __global__ __launch_bounds__(1024) void segment_mass_kernel(int Hq, int Hkv, int
   const int n = G * M;
   // the G*M rows of one KV head are contiguous in lse / seg_lse
   const int64_t q0 = ((int64_t)b * Hq + hkv * G) * M;
-  for (int i = threadIdx.x; i < n; i += blockDim.x) {
-    const double L = lse[q0 + i];
-    for (int a = 0; a < nseg; ++a) {
-      const float sl = seg_lse[(q0 + i) * nseg + a];
-      if (sl != -INFINITY) acc[a] += (double)expf((float)((double)sl - L));
+  for (int i0 = threadIdx.x; i0 < n; i0 += kMassRows * blockDim.x) {
+    float L[kMassRows], sl[kMassRows][kMaxSeg];
+#pragma unroll
+    for (int u = 0; u < kMassRows; ++u) {
+      const int i = i0 + u * blockDim.x;
+      L[u] = i < n ? lse[q0 + i] : 0.0f;
+#pragma unroll
+      for (int a = 0; a < kMaxSeg; ++a)
+        sl[u][a] = i < n && a < nseg ? seg_lse[(q0 + i) * nseg + a] : -INFINITY;
     }
+#pragma unroll
+    for (int u = 0; u < kMassRows; ++u)
+#pragma unroll
+      for (int a = 0; a < kMaxSeg; ++a)
+        if (sl[u][a] != -INFINITY) acc[a] += (double)expf((float)((double)sl[u][a] - (double)L[u]));
   }
   for (int a = 0; a < nseg; ++a) {
     double v = wave_sum_d(acc[a]);
@@ -378,6 +391,14 @@ __global__ __launch_bounds__(1024) void segment_mass_kernel(int Hq, int Hkv, int
     for (int w = 0; w < (int)(blockDim.x >> 6); ++w) t += red[w][a];
     mass[(int64_t)bh * nseg + a] = (float)t;
   }
+}
+
+// Row log-sum-exps of the observation rows taken from a caller's array with
+// a leading dimension: dst[r * W + w] = src[r * ld + w] for r = b * Hq + h.
+__global__ void lse_rows_kernel(const float* __restrict__ src, int64_t ld, int W,
+                                float* __restrict__ dst) {
+  const int64_t r = blockIdx.x;
+  for (int w = threadIdx.x; w < W; w += blockDim.x) dst[r * W + w] = src[r * ld + w];
 }
 
 }  // namespace
@@ -412,7 +433,8 @@ hipError_t launch_attend_combine(const uc_shape& sh, const KSegs& segs, const Ch
 }
 
 hipError_t launch_score_colsum(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
-                               const void* q, int q_dt, int W, float sm_scale, const float* lse,
+                               const void* q, int q_dt, int W, int q_ld, float sm_scale,
+                               const float* lse,
                                float* const* scores, double* mass_partial, hipStream_t st) {
   ScorePtrs sp{};
   for (int i = 0; i < segs.n; ++i) sp.p[i] = scores ? scores[i] : nullptr;
@@ -420,10 +442,10 @@ hipError_t launch_score_colsum(const uc_shape& sh, const KSegs& segs, const Chun
   const float sl2 = sm_scale * kLog2e;
   if (sh.D == 64)
     hipLaunchKernelGGL(score_colsum_kernel<64>, grid, dim3(256), 0, st, segs, plan, q, q_dt, sh.Hq,
-                       sh.Hkv, W, sl2, lse, sp, mass_partial);
+                       sh.Hkv, W, q_ld, sl2, lse, sp, mass_partial);
   else
     hipLaunchKernelGGL(score_colsum_kernel<128>, grid, dim3(256), 0, st, segs, plan, q, q_dt,
-                       sh.Hq, sh.Hkv, W, sl2, lse, sp, mass_partial);
+                       sh.Hq, sh.Hkv, W, q_ld, sl2, lse, sp, mass_partial);
   return hipGetLastError();
 }
 
@@ -431,6 +453,12 @@ hipError_t launch_mass_finalize(const ChunkPlan& plan, int BH, int n_segs,
                                 const double* mass_partial, float* mass, hipStream_t st) {
   hipLaunchKernelGGL(mass_finalize_kernel, dim3(BH), dim3(64), 0, st, plan, n_segs, mass_partial,
                      mass);
+  return hipGetLastError();
+}
+
+hipError_t launch_lse_rows(const float* src, int64_t ld, int W, int rows, float* dst,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(lse_rows_kernel, dim3(rows), dim3(256), 0, st, src, ld, W, dst);
   return hipGetLastError();
 }
 

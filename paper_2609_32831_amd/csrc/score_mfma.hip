@@ -184,12 +184,16 @@ __device__ inline void s_tile(const u4 (&k)[8], const u4 (&qb)[4], f4& s0, f4& s
 }
 
 // stage query rows [q0, q0 + QB) of the head's observation block (rows past nq
-// are zero) into LDS
-__device__ inline void stage_q(char* qs, const uint16_t* qh, int q0, int nq) {
+// are zero) into LDS; row g*W + w of the block is window row w of the
+// group's query head g, which starts ld rows after head g - 1
+__device__ inline void stage_q(char* qs, const uint16_t* qh, int q0, int nq, int W, int ld) {
   for (int e = threadIdx.x; e < QB * (D / 8); e += blockDim.x) {
     const int r = e / (D / 8), c = e % (D / 8);
     u4 v = u4{0, 0, 0, 0};
-    if (q0 + r < nq) v = *reinterpret_cast<const u4*>(qh + (int64_t)(q0 + r) * D + c * 8);
+    if (q0 + r < nq) {
+      const int g = (q0 + r) / W, w = q0 + r - g * W;
+      v = *reinterpret_cast<const u4*>(qh + ((int64_t)g * ld + w) * D + c * 8);
+    }
     *reinterpret_cast<u4*>(qs + r * QROW + c * 16) = v;
   }
 }
@@ -338,7 +342,7 @@ __global__ __launch_bounds__(256, 2) void score_lse_kernel(KSegs segs, ChunkPlan
   const uint16_t* qh = q + ((int64_t)b * Hq + hkv * G) * W * D;
   const int q0 = qb * QB;
   const int nqt = min(QT, (nq - q0 + 15) / 16);
-  stage_q(qs, qh, q0, nq);
+  stage_q(qs, qh, q0, nq, W, W);
   for (int e = threadIdx.x; e < WAVES * QB; e += blockDim.x) {
     red_m[e / QB][e % QB] = -INFINITY;
     red_l[e / QB][e % QB] = 0.0f;
@@ -385,7 +389,8 @@ struct ScoreOut {
 template <bool PACKED>
 __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan plan,
                                                            const uint16_t* __restrict__ q, int Hq,
-                                                           int Hkv, int W, float scale_log2,
+                                                           int Hkv, int W, int q_ld,
+                                                           float scale_log2,
                                                            const float* __restrict__ lse,
                                                            ScoreOut out,
                                                            double* __restrict__ mass_partial,
@@ -401,7 +406,7 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
   int r0, r1;
   const int si = chunk_rows(plan, segs, c, r0, r1);
   const KSeg& ks = segs.s[si];
-  const uint16_t* qh = q + ((int64_t)b * Hq + hkv * G) * W * D;
+  const uint16_t* qh = q + ((int64_t)b * Hq + hkv * G) * q_ld * D;
   const float* lh = lse + ((int64_t)b * Hq + hkv * G) * W;
   for (int e = threadIdx.x; e < CHUNK; e += blockDim.x) colsum[e] = 0.0;
 
@@ -410,7 +415,7 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
   for (int q0 = sg * qbs * QB; q0 < q_end; q0 += QB) {
     const int nqt = min(QT, (nq - q0 + 15) / 16);
     __syncthreads();  // the previous block's readers are done
-    stage_q(qs, qh, q0, nq);
+    stage_q(qs, qh, q0, nq, W, q_ld);
     for (int r = threadIdx.x; r < QB; r += blockDim.x)
       ls[r] = q0 + r < nq ? lh[q0 + r] * kLog2e : INFINITY;  // padded rows: p = 0
     __syncthreads();
@@ -514,9 +519,12 @@ bool score_mfma_eligible(const uc_shape& sh, const KSegs& segs, int q_dt) {
 
 int score_mfma_chunk_rows() { return CHUNK; }
 
-static bool has_packed(const KSegs& segs) {
+// a packed segment with code rows among the plan's chunks (the plan may
+// leave segments out)
+static bool has_packed(const KSegs& segs, const ChunkPlan& plan) {
   for (int i = 0; i < segs.n; ++i)
-    if (segs.s[i].kind == UC_SEG_PACKED && segs.s[i].n_full > 0) return true;
+    if (segs.s[i].kind == UC_SEG_PACKED && segs.s[i].n_full > 0 && plan.first[i + 1] > plan.first[i])
+      return true;
   return false;
 }
 
@@ -536,7 +544,7 @@ hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const Ch
                                  hipStream_t st) {
   const int nq = (sh.Hq / sh.Hkv) * W;
   dim3 grid(plan.n_chunks, score_mfma_qblocks(nq), sh.B * sh.Hkv);
-  if (has_packed(segs))
+  if (has_packed(segs, plan))
     hipLaunchKernelGGL(score_lse_kernel<true>, grid, dim3(256), 0, st, segs, plan,
                        (const uint16_t*)q, sh.Hq, sh.Hkv, W, sm_scale * kLog2e, partial);
   else
@@ -546,7 +554,7 @@ hipError_t launch_score_lse_mfma(const uc_shape& sh, const KSegs& segs, const Ch
 }
 
 hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
-                                 const void* q, int W, float sm_scale, const float* lse,
+                                 const void* q, int W, int q_ld, float sm_scale, const float* lse,
                                  float* const* scores, double* mass_partial, double* colpart,
                                  hipStream_t st) {
   ScoreOut so{};
@@ -556,13 +564,13 @@ hipError_t launch_score_col_mfma(const uc_shape& sh, const KSegs& segs, const Ch
   const int qbs = (qblocks + groups - 1) / groups;
   const int n_groups = (qblocks + qbs - 1) / qbs;
   dim3 grid(plan.n_chunks, n_groups, sh.B * sh.Hkv);
-  if (has_packed(segs))
+  if (has_packed(segs, plan))
     hipLaunchKernelGGL(score_col_kernel<true>, grid, dim3(256), 0, st, segs, plan,
-                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, q_ld, sm_scale * kLog2e, lse, so,
                        mass_partial, qbs, n_groups > 1 ? colpart : nullptr);
   else
     hipLaunchKernelGGL(score_col_kernel<false>, grid, dim3(256), 0, st, segs, plan,
-                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, sm_scale * kLog2e, lse, so,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, W, q_ld, sm_scale * kLog2e, lse, so,
                        mass_partial, qbs, n_groups > 1 ? colpart : nullptr);
   if (n_groups > 1)
     hipLaunchKernelGGL(score_col_reduce_kernel, dim3(plan.n_chunks, sh.B * sh.Hkv), dim3(256), 0,

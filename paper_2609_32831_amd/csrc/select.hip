@@ -53,17 +53,25 @@ __device__ inline uint32_t wave_exclusive(uint32_t x, uint32_t* wave_tot) {
 // keys at a time; a kept key's output slot is the number of kept keys before
 // it: (keys above tau before it) + min(keys equal to tau before it, need),
 // from ballots within the wave and exclusive sums over the waves.
+// With k_dev the row count is read from device memory (k = max(*k_dev, 0));
+// k >= N then writes nothing.  Output row stride: keep_ld.
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __restrict__ scores, int N,
                                                              int k, int n_recent,
-                                                             int32_t* __restrict__ keep) {
+                                                             int32_t* __restrict__ keep,
+                                                             const int32_t* __restrict__ k_dev,
+                                                             int64_t keep_ld) {
   __shared__ uint32_t whist[kSelWaves][256];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t wave_tot[kSelWaves];
   __shared__ uint32_t sh_digit, sh_need;
   const int bh = blockIdx.x, tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
+  if (k_dev) {
+    k = max(*k_dev, 0);
+    if (k >= N) return;  // nothing evicted: the caller keeps its rows
+  }
   const float* s = scores + (int64_t)bh * N;
-  int32_t* out = keep + (int64_t)bh * k;
+  int32_t* out = keep + (int64_t)bh * keep_ld;
   const int Nc = N - n_recent, kc = k - n_recent;
 
   uint32_t prefix = 0, need = (uint32_t)kc;
@@ -147,18 +155,25 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const float* __rest
   for (int j = tid; j < n_recent; j += kSelThreads) out[kc + j] = Nc + j;
 }
 
-// Copy kept rows: 16 bytes per lane; grid.y = (b, h_kv).
+// Copy kept rows: 16 bytes per lane; grid.y = (b, h_kv).  Row strides:
+// keep_ld (indices), src_ld and dst_ld (rows); with k_dev as in select_kernel.
 __global__ void gather_kernel(const int32_t* __restrict__ keep, int N, int k, const char* ksrc,
-                              const char* vsrc, char* kdst, char* vdst, int row_bytes) {
+                              const char* vsrc, char* kdst, char* vdst, int row_bytes,
+                              const int32_t* __restrict__ k_dev, int64_t keep_ld, int64_t src_ld,
+                              int64_t dst_ld) {
   const int bh = blockIdx.y;
+  if (k_dev) {
+    k = max(*k_dev, 0);
+    if (k >= N) return;
+  }
   const int lanes_per_row = row_bytes / 16;
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= (int64_t)k * lanes_per_row) return;
   const int j = (int)(e / lanes_per_row), piece = (int)(e % lanes_per_row);
-  const int src_row = keep[(int64_t)bh * k + j];
+  const int src_row = keep[(int64_t)bh * keep_ld + j];
   if (src_row < 0 || src_row >= N) return;
-  const int64_t so = ((int64_t)bh * N + src_row) * row_bytes + piece * 16;
-  const int64_t dof = ((int64_t)bh * k + j) * row_bytes + piece * 16;
+  const int64_t so = ((int64_t)bh * src_ld + src_row) * row_bytes + piece * 16;
+  const int64_t dof = ((int64_t)bh * dst_ld + j) * row_bytes + piece * 16;
   *reinterpret_cast<uint4*>(kdst + dof) = *reinterpret_cast<const uint4*>(ksrc + so);
   *reinterpret_cast<uint4*>(vdst + dof) = *reinterpret_cast<const uint4*>(vsrc + so);
 }
@@ -198,15 +213,24 @@ __global__ void blob_store_kernel(Blob b, int n, uint32_t* __restrict__ dst) {
   for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = b.w[i];
 }
 
-// out[bh, j] = outer[bh, inner[bh, j]] (-1 for an inner value out of range).
-__global__ void compose_index_kernel(const int32_t* __restrict__ outer, int n_outer,
-                                     const int32_t* __restrict__ inner, int k,
-                                     int32_t* __restrict__ out) {
+// out[bh, j] = outer[bh, inner[bh, j]] (-1 for an inner value out of range);
+// rows of outer, inner and out are outer_ld, inner_ld and out_ld apart.  An
+// element is read before it is written, so out may be inner (in place).
+// outer NULL: out = inner (the inner indices are already logical).  With
+// k_dev as in select_kernel (n_outer playing N).
+__global__ void compose_index_kernel(const int32_t* outer, int n_outer, const int32_t* inner,
+                                     int k, int32_t* out, const int32_t* __restrict__ k_dev,
+                                     int64_t outer_ld, int64_t inner_ld, int64_t out_ld) {
   const int bh = blockIdx.y;
+  if (k_dev) {
+    k = max(*k_dev, 0);
+    if (k >= n_outer) return;
+  }
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= k) return;
-  const int i = inner[(int64_t)bh * k + j];
-  out[(int64_t)bh * k + j] = (i >= 0 && i < n_outer) ? outer[(int64_t)bh * n_outer + i] : -1;
+  const int i = inner[(int64_t)bh * inner_ld + j];
+  const int r = !outer ? i : (i >= 0 && i < n_outer) ? outer[(int64_t)bh * outer_ld + i] : -1;
+  out[(int64_t)bh * out_ld + j] = r;
 }
 
 // Decode append: rows pos..pos+n_new-1 of a dense segment.
@@ -227,7 +251,7 @@ __global__ void append_kernel(const char* knew, const char* vnew, int n_new, cha
 hipError_t launch_select(const float* scores, int BH, int N, int k, int n_recent, int32_t* keep,
                          hipStream_t st) {
   hipLaunchKernelGGL(select_kernel, dim3(BH), dim3(kSelThreads), 0, st, scores, N, k, n_recent,
-                     keep);
+                     keep, nullptr, (int64_t)k);
   return hipGetLastError();
 }
 
@@ -239,7 +263,7 @@ hipError_t launch_gather(const int32_t* keep, int BH, int N, int k, const void* 
   if (lanes == 0) return hipSuccess;
   hipLaunchKernelGGL(gather_kernel, dim3((unsigned)((lanes + 255) / 256), BH), dim3(256), 0, st,
                      keep, N, k, (const char*)ksrc, (const char*)vsrc, (char*)kdst, (char*)vdst,
-                     row_bytes);
+                     row_bytes, nullptr, (int64_t)k, (int64_t)N, (int64_t)k);
   return hipGetLastError();
 }
 
@@ -270,7 +294,24 @@ hipError_t launch_compose_index(const int32_t* outer, int n_outer, const int32_t
                                 int k, int32_t* out, hipStream_t st) {
   if (k == 0 || BH == 0) return hipSuccess;
   hipLaunchKernelGGL(compose_index_kernel, dim3((k + 255) / 256, BH), dim3(256), 0, st, outer,
-                     n_outer, inner, k, out);
+                     n_outer, inner, k, out, nullptr, (int64_t)n_outer, (int64_t)k, (int64_t)k);
+  return hipGetLastError();
+}
+
+hipError_t launch_evict_step(int BH, int N, const float* scores, const int32_t* k_dev,
+                             const void* ksrc, const void* vsrc, int64_t src_ld,
+                             const int32_t* idx_src, void* kdst, void* vdst, int32_t* idx_dst,
+                             int64_t dst_ld, int row_bytes, hipStream_t st) {
+  if (N == 0) return hipSuccess;  // k >= N whatever k is
+  hipLaunchKernelGGL(select_kernel, dim3(BH), dim3(kSelThreads), 0, st, scores, N, 0, 0, idx_dst,
+                     k_dev, dst_ld);
+  const int64_t lanes = (int64_t)N * (row_bytes / 16);  // grid for k = N - 1 at most
+  hipLaunchKernelGGL(gather_kernel, dim3((unsigned)((lanes + 255) / 256), BH), dim3(256), 0, st,
+                     (const int32_t*)idx_dst, N, 0, (const char*)ksrc, (const char*)vsrc,
+                     (char*)kdst, (char*)vdst, row_bytes, k_dev, dst_ld, src_ld, dst_ld);
+  // local positions -> logical indices, in place
+  hipLaunchKernelGGL(compose_index_kernel, dim3((N + 255) / 256, BH), dim3(256), 0, st, idx_src, N,
+                     (const int32_t*)idx_dst, 0, idx_dst, k_dev, src_ld, dst_ld, dst_ld);
   return hipGetLastError();
 }
 

@@ -176,7 +176,8 @@ hipError_t launch_attend_combine(const uc_shape& sh, const KSegs& segs, const Ch
                                  int M, const float* partial, float* o, float* lse, float* seg_lse,
                                  hipStream_t st);
 hipError_t launch_score_colsum(const uc_shape& sh, const KSegs& segs, const ChunkPlan& plan,
-                               const void* q, int q_dt, int W, float sm_scale, const float* lse,
+                               const void* q, int q_dt, int W, int q_ld, float sm_scale,
+                               const float* lse,
                                float* const* scores, double* mass_partial, hipStream_t st);
 hipError_t launch_mass_finalize(const ChunkPlan& plan, int BH, int n_segs,
                                 const double* mass_partial, float* mass, hipStream_t st);
@@ -191,6 +192,12 @@ hipError_t launch_budget_step(const uc_budget_params& p, const float* mass, int 
                               uc_budget_state* state, hipStream_t st);
 hipError_t launch_calibrate_policy(const float* frac, int rows, int n_types, double threshold,
                                    double* conc, int32_t* evict, hipStream_t st);
+hipError_t launch_evict_step(int BH, int N, const float* scores, const int32_t* k_dev,
+                             const void* ksrc, const void* vsrc, int64_t src_ld,
+                             const int32_t* idx_src, void* kdst, void* vdst, int32_t* idx_dst,
+                             int64_t dst_ld, int row_bytes, hipStream_t st);
+hipError_t launch_lse_rows(const float* src, int64_t ld, int W, int rows, float* dst,
+                          hipStream_t st);
 hipError_t launch_segment_mass(const uc_shape& sh, int M, int n_segs, const float* lse,
                                const float* seg_lse, float* mass, hipStream_t st);
 }  // namespace uc

@@ -19,10 +19,11 @@ import torch
 from . import (NAME_DT, TORCH_DT, budget_state_tensor, dense_segment,
                make_shape, packed_layout, packed_segment, uc_assign_bits, uc_attend_append,
                uc_attend_mixed, uc_attend_workspace_size, uc_budget_params, uc_budget_step,
-               uc_calibrate_policy, uc_compose_index, uc_dense_bytes, uc_dequantize_segment,
+               uc_calibrate_policy, uc_dense_bytes, uc_dequantize_segment,
                uc_evict_rows_for_budget, uc_evicted_bytes, uc_packed_bytes, uc_quantize_segment,
-               uc_score_importance, uc_score_workspace_size, uc_segment_mass, uc_select_keep,
-               uc_stream_append, uc_topk_mass, uc_budget_state)
+               uc_score_columns, uc_score_importance, uc_score_workspace_size, uc_segment_mass,
+               uc_select_keep, uc_stream_append, uc_topk_mass, uc_budget_state, AttendPlan,
+               packed_storage, uc_evict_step)
 
 TORCH = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}
 
@@ -336,7 +337,14 @@ class DynamicRun:
     and a (bits, group) configuration for the quantised type (a change
     re-quantises its dequantised rows).  The host reads the decision once per
     boundary, because the row count and the configuration size the next
-    launches.  Eviction and re-quantisation are irreversible."""
+    launches.  Eviction and re-quantisation are irreversible.
+
+    Scores come from the row normalisers of the timestep's own attention
+    pass (uc_score_columns): the observation rows are rows of that query
+    block over the same cache, so its log-sum-exps are the softmax
+    normalisers of Eq. 1's P.  Between boundaries the layout is frozen, so
+    the timesteps run on an execution plan (App. E, cached metadata and
+    execution plans) that prepares the packed rows once per layout."""
 
     def __init__(self, w, seg_k, seg_v, device="cuda"):
         """seg_k / seg_v: per segment, the request's rows [1, Hkv, n, D]."""
@@ -354,6 +362,7 @@ class DynamicRun:
         self.n_ev, self.n_qt = segs[self.ev].n, segs[self.qt].n
         self.dense = [dense_segment(seg_k[i], seg_v[i]) for i in range(self.nseg)]
         q_dt = NAME_DT[w.q_dtype]
+        self.q_torch_dt = TORCH[w.q_dtype]
         # workspaces sized for the largest configuration: every row present,
         # the quantised type at the finest grouping
         biggest = packed_segment(1, Hkv, self.n_qt, D, 32, self.tdt, bits=8, device=device)
@@ -367,6 +376,7 @@ class DynamicRun:
         self.ws_att = torch.empty(max(ws_att, 256), dtype=torch.uint8, device=device)
         self.ws_sc = torch.empty(max(ws_sc, 256), dtype=torch.uint8, device=device)
         self.lse = torch.empty(1, Hq, M, device=device)
+        self.lse_ptr = self.lse.data_ptr()
         self.seg_lse = torch.empty(1, Hq, M, self.nseg, device=device)
         # raw per-segment masses of every timestep (uc_segment_mass)
         self.mass = torch.zeros(w.steps, 1, Hkv, self.nseg, device=device)
@@ -378,24 +388,41 @@ class DynamicRun:
         self.state_host = torch.empty(self.state.numel(), dtype=torch.uint8, pin_memory=True)
         self.state_ready = torch.cuda.Event()
         self.falling = True
-        # the kept rows of the evicting type, their logical indices and the
-        # selection's local indices: two sets of buffers sized for every row,
-        # alternating (a boundary gathers from one set into the other)
-        self.kept_k = [torch.empty(Hkv * self.n_ev * D, dtype=self.tdt, device=device)
-                       for _ in range(2)]
-        self.kept_v = [torch.empty_like(self.kept_k[0]) for _ in range(2)]
-        self.kept_idx = [torch.empty(Hkv * self.n_ev, dtype=torch.int32, device=device)
-                         for _ in range(2)]
-        self.local = torch.empty(Hkv * self.n_ev, dtype=torch.int32, device=device)
-        self.set = 0
+        # the kept rows of the evicting type and their logical indices: two
+        # sets of buffers with a row capacity of every row, alternating (a
+        # boundary keeps rows of one set in the other)
+        cap = self.n_ev
+        self.kept = [dense_segment(torch.empty(1, Hkv, cap, D, dtype=self.tdt, device=device),
+                                   torch.empty(1, Hkv, cap, D, dtype=self.tdt, device=device),
+                                   n_rows=0,
+                                   idx=torch.empty(1, Hkv, cap, dtype=torch.int32, device=device))
+                     for _ in range(2)]
+        self.set = 1  # the set the first boundary fills is 0
+        self.k_dev = self.state.data_ptr() + uc_budget_state.k.offset
+        # the quantised type: two storage sets for its packed form (a
+        # re-quantisation reads one and writes the other) and a buffer for
+        # its decoded rows
+        self.pstore = [packed_storage(1, Hkv, self.n_qt, D, self.tdt, device) for _ in range(2)]
+        self.pset = 1
+        self.deq_k = torch.empty(1, Hkv, self.n_qt, D, dtype=self.tdt, device=device)
+        self.deq_v = torch.empty_like(self.deq_k)
+        self.plan: Optional[AttendPlan] = None  # plan of the current layout
         # storage state
         self.compact = None     # dense segment of the kept rows of the evicting type
-        self.idx = None         # [Hkv, k] int32 logical positions of those rows
         self.packed = None      # packed segment of the quantised type
         self.cfg = None         # (index, bits, group)
         self.decisions: Dict[int, Dict] = {}
 
     # ---- helpers -----------------------------------------------------------
+    @property
+    def idx(self) -> torch.Tensor:
+        """[Hkv, k] int32 logical positions of the evicting type's kept rows."""
+        c = self.compact
+        if c is None or c.t.get("idx") is None:
+            n = self.n_ev
+            return torch.arange(n, dtype=torch.int32, device=self.device).expand(self.w.Hkv, n)
+        return c.t["idx"][0, :, :c.n_rows]
+
     def segments(self):
         if self.compact is None:
             return list(self.dense)
@@ -404,84 +431,88 @@ class DynamicRun:
         out[self.qt] = self.packed
         return out
 
-    def _score(self, q_obs, W):
-        """Scores of the evicting type's current rows from q_obs [1, Hq, W, D]
-        over the current cache (the quantised type in its packed form)."""
-        Hkv = self.w.Hkv
+    def _score(self, q, W):
+        """Scores of the evicting type's current rows from the last W rows of
+        q [1, Hq, M, D], the query block the last attention pass ran, over
+        the current cache (the quantised type in its packed form); the
+        normalisers are that pass's row log-sum-exps."""
+        Hkv, M = self.w.Hkv, self.w.M
         segs = self.segments()
         n_cur = segs[self.ev].n_rows
         outs = [None] * self.nseg
         outs[self.ev] = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)
-        uc_score_importance(self.shape, segs, q_obs, W, self.sm, outs, None, ws=self.ws_sc)
+        uc_score_columns(self.shape, segs, q[:, :, M - W:], W, self.sm, self.lse_ptr + 4 * (M - W),
+                         M, outs, None, ws=self.ws_sc, q_ld=M)
 
-    def _select(self, k_new):
-        """Keep the best k_new of the evicting type's current rows by the
-        scores _score left (compacted, with composed logical indices)."""
-        w = self.w
-        Hkv, D = w.Hkv, w.D
-        segs = self.segments()
-        n_cur = segs[self.ev].n_rows
-        sc = self.scores.view(-1)[: Hkv * n_cur].view(1, Hkv, n_cur)
-        s = self.set = 1 - self.set
-        n = Hkv * k_new
-        local = self.local[:n].view(Hkv, k_new)
-        src = segs[self.ev].t
-        kd = self.kept_k[s][: n * D].view(1, Hkv, k_new, D)
-        vd = self.kept_v[s][: n * D].view(1, Hkv, k_new, D)
-        uc_select_keep(sc.reshape(Hkv, n_cur), k_new, 0, local, src["k"].reshape(Hkv, -1, D),
-                       src["v"].reshape(Hkv, -1, D), kd.view(Hkv, k_new, D),
-                       vd.view(Hkv, k_new, D))
-        idx = self.kept_idx[s][:n].view(Hkv, k_new)
-        if self.idx is None:
-            idx.copy_(local)
-        else:
-            uc_compose_index(self.idx, local, idx)
-        self.compact = dense_segment(kd, vd, idx=idx)
-        self.idx = idx
+    def _evict(self):
+        """Keep the best k rows of the evicting type's current rows in the
+        other buffer set, k read from the budget state on the device (nothing
+        is written when k is not below the current count)."""
+        cur = self.segments()[self.ev]
+        uc_evict_step(self.shape, self.scores, cur, self.k_dev, self.kept[1 - self.set])
 
-    def _quantize(self, cfg):
-        """(Re-)quantise the quantised type with configuration cfg, from its
-        original rows the first time, else from its current rows decoded into
-        a buffer that lives only for this call (the packed segment is all that
-        stays resident)."""
+    def _decode(self):
+        """The quantised type's current rows, decoded into deq_k / deq_v."""
+        uc_dequantize_segment(self.shape, self.packed, self.deq_k, self.deq_v)
+
+    def _quantize(self, cfg, decoded: bool):
+        """(Re-)quantise the quantised type with configuration cfg into the
+        other storage set, from its original rows the first time, else from
+        its current rows decoded into deq_k / deq_v (decoded: already done).
+        The packed segment is all that stays resident."""
         w = self.w
         _, bits, group = cfg
+        self.pset = 1 - self.pset
         pk = packed_segment(1, w.Hkv, self.n_qt, w.D, group, self.tdt, bits=bits,
-                            device=self.device, zero=False)
+                            device=self.device, storage=self.pstore[self.pset])
         if self.packed is None:
             src_k, src_v = self.dense[self.qt].t["k"], self.dense[self.qt].t["v"]
         else:
-            src_k = torch.empty(1, w.Hkv, self.n_qt, w.D, dtype=self.tdt, device=self.device)
-            src_v = torch.empty_like(src_k)
-            uc_dequantize_segment(self.shape, self.packed, src_k, src_v)
+            if not decoded:
+                self._decode()
+            src_k, src_v = self.deq_k, self.deq_v
         uc_quantize_segment(self.shape, src_k, src_v, self.n_qt, pk)
         self.packed, self.cfg = pk, cfg
 
-    def _boundary(self, t, t0, n, q_obs, W):
+    def _boundary(self, t, t0, n, q, W):
         """Boundary after timestep t over the chunk t0 .. t0+n-1: the device
         decides (uc_budget_step), the host reads the decision and applies it
-        from the next timestep on.  While the host waits for the decision,
-        the device already scores the current cache when the retention ratio
-        was still above its floor at the last boundary, so that the budget is
-        likely to shrink again (the scores are only used if the evicting type
-        shrinks; they depend on nothing the decision changes)."""
-        stream = torch.cuda.current_stream()
+        from the next timestep on.  When the retention ratio was still above
+        its floor at the last boundary (so the budget is likely to shrink
+        again), the work that does not depend on the host knowing the
+        decision is queued before the host waits for it: scoring the current
+        cache, the eviction step (its row count is read on the device, and
+        it writes nothing if the count did not fall) and decoding the
+        quantised type's rows for a re-quantisation."""
         uc_budget_step(self.params, self.mass[t0:t0 + n], n, self.state)
         self.state_host.copy_(self.state, non_blocking=True)
-        self.state_ready.record(stream)
+        self.state_ready.record()
         first = self.compact is None
         ahead = first or self.falling
         if ahead:
-            self._score(q_obs, W)
-        self.state_ready.synchronize()
+            self._score(q, W)
+            self._evict()
+            if self.packed is not None:
+                self._decode()
+        while not self.state_ready.query():  # the decision is tiny: poll for it
+            pass
         st = uc_budget_state.from_buffer_copy(self.state_host.numpy().tobytes())
-        shrink = first or st.k < st.k_prev
-        if shrink:
+        n_cur = self.n_ev if first else self.compact.n_rows
+        if st.k < n_cur:
             if not ahead:
-                self._score(q_obs, W)
-            self._select(st.k)
-        if st.cfg != st.cfg_prev:
-            self._quantize((st.cfg, st.bits, st.group))
+                self._score(q, W)
+                self._evict()
+            self.set = 1 - self.set
+            self.compact = self.kept[self.set]
+            self.compact.n_rows = st.k
+            self.plan = None
+        elif first:  # nothing evicted: the original rows stay
+            self.compact = self.dense[self.ev]
+        if st.cfg != st.cfg_prev or self.packed is None:
+            self._quantize((st.cfg, st.bits, st.group), decoded=ahead)
+            self.plan = None
+        if self.plan is None:  # the new layout's execution plan
+            self._make_plan()
         self.falling = st.rho > self.w.rho_min
         rec = {"rho": st.rho, "B": st.B, "m": {self.ev: st.m[0], self.qt: st.m[1]},
                "b": {self.ev: st.b[0], self.qt: st.b[1]}, "k": st.k, "cfg": st.cfg,
@@ -489,14 +520,24 @@ class DynamicRun:
         self.decisions[t] = rec
         return rec
 
+    def _make_plan(self):
+        self.plan = AttendPlan(self.shape, self.segments(), None, self.q_torch_dt, self.w.M,
+                               self.sm, ws=self.ws_att)
+
     # ---- one timestep --------------------------------------------------------
+    def attend(self, t: int, q: torch.Tensor, o: torch.Tensor):
+        """Timestep t's attention over the current cache (on the layout's
+        execution plan) and its type masses."""
+        w = self.w
+        if self.plan is None:
+            self._make_plan()
+        self.plan.attend(q, o, self.lse, self.seg_lse)
+        uc_segment_mass(self.shape, w.M, self.nseg, self.lse, self.seg_lse, self.mass[t])
+
     def step(self, t: int, q: torch.Tensor, o: torch.Tensor):
         """Timestep t with query block q [1, Hq, M, D]; returns the boundary
         decision taken after it, if any."""
-        w = self.w
-        uc_attend_mixed(self.shape, self.segments(), q, w.M, self.sm, o, self.lse, self.seg_lse,
-                        ws=self.ws_att)
-        uc_segment_mass(self.shape, w.M, self.nseg, self.lse, self.seg_lse, self.mass[t])
+        self.attend(t, q, o)
         return self.after_step(t, q)
 
     def after_step(self, t: int, q: torch.Tensor):
@@ -507,8 +548,7 @@ class DynamicRun:
             return self._boundary(0, 0, 1, q, w.M)
         C = w.chunk_steps
         if t % C == 0 and t < w.steps - 1:
-            q_obs = q[:, :, w.M - w.obs_window:].contiguous()
-            return self._boundary(t, t - C + 1, C, q_obs, w.obs_window)
+            return self._boundary(t, t - C + 1, C, q, w.obs_window)
         return None
 
 

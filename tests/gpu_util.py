@@ -68,3 +68,48 @@ def check_attention(o_gpu: np.ndarray, o_ref: np.ndarray, what=""):
 
 def sm_scale(D: int) -> float:
     return float(np.float32(1.0 / math.sqrt(D)))
+
+
+def mixed_case(B, Hq, Hkv, D, dtype, sizes, seed=0, G=64, bits=4, per_head=False):
+    """Segments: dense 'text', compacted 'vit' (rows chosen at random, with
+    their logical positions), packed 'vae' with tail, dense tail segment with
+    spare capacity.  Returns GPU segments and the oracle's logical K/V."""
+    n_text, n_vit_full, n_vit_keep, n_pack, n_tail, cap = sizes
+    BH = B * Hkv
+    segs, kh, vh, seg_id = [], [], [], []
+    # text (dense)
+    kt = rand_rows(seed + 1, BH, n_text, D, dtype, outliers=(5,))
+    vt = rand_rows(seed + 2, BH, n_text, D, dtype)
+    segs.append(uc.dense_segment(dev(kt, dtype).reshape(B, Hkv, n_text, D),
+                                 dev(vt, dtype).reshape(B, Hkv, n_text, D)))
+    kh.append(ref.widen(kt, dtype)); vh.append(ref.widen(vt, dtype))
+    # compacted eviction survivors
+    kv_full = rand_rows(seed + 3, BH, n_vit_full, D, dtype, outliers=(5,))
+    vv_full = rand_rows(seed + 4, BH, n_vit_full, D, dtype)
+    rng = np.random.default_rng(seed)
+    idx = np.sort(np.stack([rng.choice(n_vit_full, n_vit_keep, replace=False) for _ in range(BH)]), 1)
+    kc = np.stack([kv_full[i][idx[i]] for i in range(BH)])
+    vc = np.stack([vv_full[i][idx[i]] for i in range(BH)])
+    segs.append(uc.dense_segment(dev(kc, dtype).reshape(B, Hkv, n_vit_keep, D),
+                                 dev(vc, dtype).reshape(B, Hkv, n_vit_keep, D),
+                                 idx=torch.from_numpy(idx.astype(np.int32)).cuda()))
+    kh.append(ref.widen(kc, dtype)); vh.append(ref.widen(vc, dtype))
+    # packed
+    kp = rand_rows(seed + 5, BH, n_pack, D, dtype, 2.0, outliers=(5,))
+    vp = rand_rows(seed + 6, BH, n_pack, D, dtype)
+    hb = [bits] * BH if not per_head else [4 if (i % 3) else 2 for i in range(BH)]
+    pk = ref.quantize(kp, vp, dtype, G, hb)
+    segs.append(packed_from_oracle(B, Hkv, n_pack, D, G, dtype, pk, per_head=per_head))
+    khp, vhp = ref.dequant(pk, n_pack, D, G, dtype)
+    kh.append(khp); vh.append(vhp)
+    # dense tail with spare capacity
+    ktl = rand_rows(seed + 7, BH, cap, D, dtype)
+    vtl = rand_rows(seed + 8, BH, cap, D, dtype)
+    segs.append(uc.dense_segment(dev(ktl, dtype).reshape(B, Hkv, cap, D),
+                                 dev(vtl, dtype).reshape(B, Hkv, cap, D), n_rows=n_tail))
+    kh.append(ref.widen(ktl[:, :n_tail], dtype)); vh.append(ref.widen(vtl[:, :n_tail], dtype))
+    for a, n in enumerate([n_text, n_vit_keep, n_pack, n_tail]):
+        seg_id += [a] * n
+    K = np.concatenate(kh, axis=1).reshape(B, Hkv, -1, D)
+    V = np.concatenate(vh, axis=1).reshape(B, Hkv, -1, D)
+    return segs, K, V, np.asarray(seg_id, np.int32)

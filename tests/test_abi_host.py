@@ -116,6 +116,60 @@ def test_select_quantize_append_validation(uc):
     assert L.uc_segment_mass(ctypes.byref(sh), 0, 1, FAKE, FAKE, FAKE, None) == E
 
 
+def test_score_columns_validation(uc):
+    """uc_score_columns checks its row normalisers and workspace before any
+    launch, and enqueues nothing when neither scores nor masses are asked for
+    (so the last call runs without a GPU)."""
+    L, E = uc.lib, uc.UC_E_INVALID
+    sh = uc.uc_shape(1, 28, 4, 128)
+    segs = (uc.uc_segment * 2)(_dense(uc, 100), _packed(uc, 256, BH=4))
+    need = L.uc_score_workspace_size(ctypes.byref(sh), segs, 2, 32)
+    assert need > 0
+    outs = (ctypes.c_void_p * 2)(FAKE, None)
+
+    def f(lse=FAKE, ld=64, W=32, out=outs, mass=None, ws_bytes=need, q_ld=32):
+        return L.uc_score_columns(ctypes.byref(sh), segs, 2, FAKE, q_ld, uc.UC_BF16, W,
+                                  ctypes.c_float(0.1), lse, ld, out, mass, FAKE, ws_bytes, None)
+    assert f(lse=None) == E
+    assert "row_lse" in uc.uc_last_error()
+    assert f(ld=31) == E
+    assert f(q_ld=31) == E
+    assert f(W=0) == E
+    assert f(ws_bytes=need - 1) == uc.UC_E_WORKSPACE
+    assert f(out=None, mass=None) == uc.UC_OK  # nothing asked for: no work
+
+
+def test_evict_step_validation(uc):
+    """uc_evict_step rejects bad segments before any launch; an empty
+    current segment is a valid no-op (no launch, so it runs without a GPU)."""
+    L, E = uc.lib, uc.UC_E_INVALID
+    sh = uc.uc_shape(1, 28, 4, 128)
+    BUF = 1 << 30  # far from FAKE: no overlap
+
+    def f(cur, out, scores=FAKE, k_dev=FAKE):
+        return L.uc_evict_step(ctypes.byref(sh), scores, ctypes.byref(cur), k_dev,
+                               ctypes.byref(out), None)
+    cur = _dense(uc, 100, stride=128)
+    out = _dense(uc, 0, k=BUF, v=BUF + (1 << 24), stride=128)
+    out.idx = BUF + (1 << 25)
+    assert f(cur, _dense(uc, 0, k=BUF, v=BUF + (1 << 24), stride=99)) == E  # stride < N
+    assert "row_stride" in uc.uc_last_error()
+    assert f(cur, _packed(uc, 128)) == E
+    assert f(_packed(uc, 128), out) == E
+    o2 = _dense(uc, 0, dt=1, k=BUF, v=BUF + (1 << 24), stride=128)
+    o2.idx = BUF + (1 << 25)
+    assert f(cur, o2) == E  # dtype
+    assert f(cur, out, scores=None) == E
+    assert f(cur, out, k_dev=None) == E
+    o3 = _dense(uc, 0, k=BUF, v=BUF + (1 << 24), stride=128)
+    assert f(cur, o3) == E  # out idx NULL
+    o4 = _dense(uc, 0, k=FAKE, v=BUF + (1 << 24), stride=128)
+    o4.idx = BUF + (1 << 25)
+    assert f(cur, o4) == E  # out rows overlap cur rows
+    assert "overlap" in uc.uc_last_error()
+    assert f(_dense(uc, 0, stride=8), out) == uc.UC_OK  # no rows: nothing to do
+
+
 def _attend_append(uc, shape, segs, tail, n_new, kn=FAKE, vn=FAKE, q=FAKE, M=1, ws_bytes=1 << 40):
     arr = (uc.uc_segment * len(segs))(*segs)
     return uc.lib.uc_attend_append(ctypes.byref(shape), arr, len(segs), tail, kn, vn, n_new, q,

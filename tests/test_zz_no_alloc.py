@@ -16,7 +16,7 @@ if not torch.cuda.is_available():
 import oracle as ref  # noqa: E402
 import paper_2609_32831_amd as uc  # noqa: E402
 from gpu_util import check_attention, dev, rand_rows, sm_scale  # noqa: E402
-from test_gpu_kernels import _mixed_case  # noqa: E402
+from gpu_util import mixed_case as _mixed_case  # noqa: E402
 
 
 def _run(segs, B, Hq, Hkv, M, q, noalloc, stats=True):
