@@ -71,6 +71,9 @@ def parse():
                     help="the 7B-shaped understanding workload (4 requests, 4608-row context, "
                          "256 decode steps): whole job, and the decode steps issued one by one "
                          "and replayed as one HIP graph (one JSON line)")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="default run only: skip the secondary measurements (prefill, dynamic "
+                         "budget, understanding workload) reported under 'secondary'")
     ap.add_argument("--dynamic", action="store_true",
                     help="instead of the decode job: the editing workload under the dynamic "
                          "budget (Eq. 1-3), reporting the chunk-boundary overhead (one JSON line)")
@@ -481,6 +484,7 @@ def prefill_bench(args):
 
     import workloads as gen
     import paper_2609_32831_amd as uc
+    results = []
     from paper_2609_32831_amd import uc_attend_mixed, uc_set_kernel_events
     from paper_2609_32831_amd.runner import DenoiseRun, Run
     from workloads.device import DenoiseInputs, device_inputs
@@ -528,7 +532,7 @@ def prefill_bench(args):
     plan.close()
     n_att = sum(p.k if p.kind == "evict" else s.n for s, p in zip(w.segments, run.pol))
     fl = 4.0 * w.M * n_att * w.D * w.Hq * w.B
-    print(json.dumps({"metric": "prefill attention step (matrix cores)", "workload": w.name,
+    results.append({"metric": "prefill attention step (matrix cores)", "workload": w.name,
                       "ms_per_step": round(t_p, 4), "tflops": round(fl / t_p / 1e9, 1),
                       "frac_of_bf16_peak": round(fl / t_p / 1e9 / BF16_PEAK_TFLOPS, 4),
                       "kernel_ms": round(t_k, 4),
@@ -538,8 +542,7 @@ def prefill_bench(args):
                       "gflop_per_step": round(fl / 1e9, 1), "attended_rows": n_att,
                       "compression": static_compression(w, run.stored_bytes_per_head()),
                       "compress_ms": round(t_c, 3), "steps": n,
-                      "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)}),
-          flush=True)
+                      "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)})
     del run, inp, qs, o
     torch.cuda.empty_cache()
     # text-to-image: widths from the first (dense) step, then requantise + attend
@@ -555,7 +558,7 @@ def prefill_bench(args):
     t_k = timed_kernel(lambda i: uc_attend_mixed(run.shape, segs, di.q, w.M, run.sm, o,
                                                  ws=run.ws), n)
     fl = 4.0 * w.M * w.n_context * w.D * w.Hq * w.B
-    print(json.dumps({"metric": "prefill attention step (matrix cores)", "workload": w.name,
+    results.append({"metric": "prefill attention step (matrix cores)", "workload": w.name,
                       "ms_per_step": round(t_a, 4), "tflops": round(fl / t_a / 1e9, 1),
                       "frac_of_bf16_peak": round(fl / t_a / 1e9 / BF16_PEAK_TFLOPS, 4),
                       "kernel_ms": round(t_k, 4),
@@ -564,8 +567,10 @@ def prefill_bench(args):
                       "step_with_requantise_ms": round(t_s, 4), "bits": run.bits[:8],
                       "compression": static_compression(w, t2i_stored_per_head(w, run.bits)),
                       "steps": n,
-                      "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)}),
-          flush=True)
+                      "cpu_baseline": None if args.no_cpu_baseline else cpu_prefill_baseline(w)})
+    del run, di, o
+    torch.cuda.empty_cache()
+    return results
 
 
 def _clone_segment(seg):
@@ -747,7 +752,7 @@ def understanding_bench(args):
     graph_ms /= n
     nbytes = sum(run.attended_bytes(t + 1) for t in range(T)) / T
     tokens = w.B * T
-    print(json.dumps({"metric": "understanding decode", "workload": w.name,
+    return ({"metric": "understanding decode", "workload": w.name,
                       "tokens_per_s": round(tokens / (job_ms / 1e3), 1), "ms_per_job": round(job_ms, 3),
                       "compress_ms": round(job_ms - step_ms, 3),
                       "decode_step_us": round(step_ms / T * 1e3, 2),
@@ -756,8 +761,7 @@ def understanding_bench(args):
                       "plan_matches_steps": plan_ok,
                       "decode_step_us_graph": round(graph_ms / T * 1e3, 2),
                       "decode_tokens_per_s_graph": round(tokens / (graph_ms / 1e3), 1),
-                      "bytes_per_step": int(nbytes), "graph_matches_steps": ok, "jobs": n}),
-          flush=True)
+                      "bytes_per_step": int(nbytes), "graph_matches_steps": ok, "jobs": n})
 
 
 def dynamic_bench(args):
@@ -818,7 +822,7 @@ def dynamic_bench(args):
     bnd = sum(sum(r["bnd"][1:]) for r in res)
     last = res[0]["dec"][max(res[0]["dec"])]
     realized = sum(realized_compression(w, r["dec"]) for r in res) / len(res)
-    print(json.dumps({"metric": "dynamic budget overhead (Eq. 1-3 at chunk boundaries)",
+    return ({"metric": "dynamic budget overhead (Eq. 1-3 at chunk boundaries)",
                       "workload": w.name, "requests": w.B, "timesteps": w.steps,
                       "chunk_steps": w.chunk_steps,
                       "compression": {"target": w.target_compression,
@@ -835,7 +839,7 @@ def dynamic_bench(args):
                                                       "bits": x["bits"], "group": x["group"]}
                                              for t, x in res[0]["dec"].items()},
                       "final_k": last["k"], "final_bits": last["bits"],
-                      "final_group": last["group"]}), flush=True)
+                      "final_group": last["group"]})
 
 
 def batch_bench(args):
@@ -943,6 +947,29 @@ def batch_bench(args):
           flush=True)
 
 
+def secondary(args) -> dict:
+    """The other workloads' figures, measured in the same run as the headline
+    line (no CPU baselines): the two prefill workloads, the dynamic budget's
+    boundary overhead and the understanding workload's decode.  A part that
+    fails is reported with its error instead of its figures."""
+    import copy
+    import traceback
+    a = copy.copy(args)
+    a.no_cpu_baseline = True
+    res = {}
+    for name, fn in (("prefill", prefill_bench), ("dynamic", dynamic_bench),
+                     ("understanding", understanding_bench)):
+        t0 = time.perf_counter()
+        try:
+            res[name] = fn(a)
+        except Exception as e:  # keep the headline line whatever happens here
+            traceback.print_exc()
+            res[name] = {"error": f"{type(e).__name__}: {e}"}
+        print(f"# secondary {name} took {time.perf_counter() - t0:.1f} s", file=sys.stderr,
+              flush=True)
+    return res
+
+
 def main():
     args = parse()
     if args.summarize_profiles:
@@ -954,12 +981,13 @@ def main():
     if args.prefill:
         if args.gpus != 1:
             sys.exit(2)
-        prefill_bench(args)
+        for r in prefill_bench(args):
+            print(json.dumps(r), flush=True)
         return
     if args.dynamic:
         if args.gpus != 1:
             sys.exit(2)
-        dynamic_bench(args)
+        print(json.dumps(dynamic_bench(args)), flush=True)
         return
     if args.mall_check:
         if args.gpus != 1:
@@ -969,7 +997,7 @@ def main():
     if args.understanding:
         if args.gpus != 1:
             sys.exit(2)
-        understanding_bench(args)
+        print(json.dumps(understanding_bench(args)), flush=True)
         return
     if args.batch:
         if args.gpus != 1:
@@ -1125,6 +1153,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if not args.no_secondary and not args.streaming:
+        del run, inp, o, ev
+        torch.cuda.empty_cache()
+        out["secondary"] = secondary(args)
     if not args.no_cpu_baseline and not args.streaming:  # the baseline models the headline job
         t0 = time.perf_counter()
         out["cpu_baseline"] = cpu_baseline(w, args.cpu_sample_heads, args.cpu_sample_steps, T)
