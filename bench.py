@@ -280,20 +280,51 @@ def summarize_profiles(d: str, command: str):
         lines.append(f"- {kn}: read {fb / 1e6:.2f} MB, written {wb / 1e6:.2f} MB "
                      f"({out[f'{kn}_dispatches']} dispatches)")
     lines.append(f"- per call (both kernels): {out['traffic_bytes_per_call'] / 1e6:.2f} MB")
-    dp = glob.glob(os.path.join(d, "dpmc", "**", "*counter_collection.csv"), recursive=True)
-    if dp:
-        c = _counters(dp[0], DECODE_KERNELS[0])
+    # counter passes dpmc, dpmc2, ...: one rocprofv3 --pmc run each (the
+    # hardware takes at most 8 SQ, 4 TCC, 4 TCP, 2 TA and 2 GRBM counters
+    # per run); their per-dispatch averages are merged
+    dps = sorted(glob.glob(os.path.join(d, "dpmc*", "**", "*counter_collection.csv"),
+                           recursive=True))
+    if dps:
+        c, n_disp = {}, []
+        for path in dps:
+            ci = _counters(path, DECODE_KERNELS[0])
+            n_disp.append(ci.pop("_dispatches"))
+            c.update(ci)
         hit, miss = c.get("TCC_HIT_sum"), c.get("TCC_MISS_sum")
-        lines += ["", f"Counters of {DECODE_KERNELS[0]} (average per dispatch, "
-                      f"{c['_dispatches']} dispatches, one counter pass):", ""]
-        for k in sorted(x for x in c if not x.startswith("_")):
+        lines += ["", f"Counters of {DECODE_KERNELS[0]} (average per dispatch over "
+                      f"{'/'.join(str(x) for x in n_disp)} dispatches, {len(dps)} counter "
+                      f"passes):", ""]
+        for k in sorted(c):
             lines.append(f"- {k}: {c[k]:.4g}")
+        lines += ["", "Derived:"]
         if hit is not None and miss is not None:
             lines.append(f"- L2 hit fraction: {hit / (hit + miss):.3f} "
                          f"(misses x 128 B = {miss * 128 / 1e6:.1f} MB)")
         if c.get("SQ_INSTS_LDS"):
             lines.append(f"- LDS bank-conflict cycles per LDS instruction: "
                          f"{c.get('SQ_LDS_BANK_CONFLICT', 0.0) / c['SQ_INSTS_LDS']:.3f}")
+        if c.get("TCC_EA0_RDREQ_sum") and c.get("TCC_EA0_RDREQ_LEVEL_sum"):
+            lines.append(f"- memory read latency at the L2 (EA read requests in flight summed "
+                         f"per cycle / requests): "
+                         f"{c['TCC_EA0_RDREQ_LEVEL_sum'] / c['TCC_EA0_RDREQ_sum']:.0f} cycles")
+        if c.get("TCP_TCC_READ_REQ_sum") and c.get("TCP_TCC_READ_REQ_LATENCY_sum"):
+            lines.append(f"- L1-to-L2 read latency (TCP_TCC_READ_REQ_LATENCY / "
+                         f"TCP_TCC_READ_REQ): "
+                         f"{c['TCP_TCC_READ_REQ_LATENCY_sum'] / c['TCP_TCC_READ_REQ_sum']:.0f} "
+                         f"cycles")
+        if c.get("SQ_WAVE_CYCLES"):
+            for k, what in (("SQ_WAIT_INST_ANY", "waiting for an issued instruction's result"),
+                            ("SQ_WAIT_ANY", "waiting for anything"),
+                            ("SQ_ACTIVE_INST_VALU", "issuing vector ALU instructions"),
+                            ("SQ_ACTIVE_INST_VMEM", "issuing memory instructions")):
+                if c.get(k) is not None:
+                    lines.append(f"- {k} / SQ_WAVE_CYCLES ({what}): "
+                                 f"{c[k] / c['SQ_WAVE_CYCLES']:.3f}")
+        if c.get("SQ_INST_LEVEL_VMEM") and c.get("SQ_INSTS_VMEM_RD"):
+            lines.append(f"- vector memory instructions in flight per issued one "
+                         f"(SQ_INST_LEVEL_VMEM / SQ_INSTS_VMEM): "
+                         f"{c['SQ_INST_LEVEL_VMEM'] / c.get('SQ_INSTS_VMEM', c['SQ_INSTS_VMEM_RD']):.0f}")
     os.makedirs(os.path.join(ROOT, "profiles"), exist_ok=True)
     with open(os.path.join(ROOT, "profiles", "decode_attend_64k_traffic.json"), "w") as f:
         json.dump(out, f, indent=1)

@@ -65,17 +65,24 @@
 extern "C" {
 #endif
 
+/* Every enum below also names the ends of the 32-bit range, so that any
+ * int32 a caller passes is a value of the type (out-of-range values are then
+ * rejected by the checks, not undefined); these two are never valid
+ * arguments. */
+#define UC_ENUM_RANGE(p) p##_RANGE_MIN_ = -2147483647 - 1, p##_RANGE_MAX_ = 2147483647
+
 typedef enum {
   UC_OK = 0,
   UC_E_INVALID = 1,
   UC_E_UNSUPPORTED = 2,
   UC_E_WORKSPACE = 3,
-  UC_E_DEVICE = 4
+  UC_E_DEVICE = 4,
+  UC_ENUM_RANGE(UC_STATUS)
 } uc_status;
 
 /* Element type of dense rows, residual-tail rows, queries and of the value a
  * dequantised code is rounded to (round-to-nearest-even). */
-typedef enum { UC_F32 = 0, UC_F16 = 1, UC_BF16 = 2 } uc_dtype;
+typedef enum { UC_F32 = 0, UC_F16 = 1, UC_BF16 = 2, UC_ENUM_RANGE(UC_DTYPE) } uc_dtype;
 
 /* Storage kind of one segment (App. E "Physical, type-aware KV storage"):
  * UC_SEG_DENSE  rows kept in their original representation -- protected
@@ -83,7 +90,7 @@ typedef enum { UC_F32 = 0, UC_F16 = 1, UC_BF16 = 2 } uc_dtype;
  *               survivors of an eviction policy (ascending token order);
  * UC_SEG_PACKED low-bit codes with per-group scales and minima plus a short
  *               residual tail of rows held in `dtype`. */
-typedef enum { UC_SEG_DENSE = 0, UC_SEG_PACKED = 1 } uc_seg_kind;
+typedef enum { UC_SEG_DENSE = 0, UC_SEG_PACKED = 1, UC_ENUM_RANGE(UC_SEG_KIND) } uc_seg_kind;
 
 /* Batch B, query heads Hq, KV heads Hkv (Hq % Hkv == 0), head dim D. */
 typedef struct {
