@@ -399,7 +399,10 @@ __global__ __launch_bounds__(256, 2) void score_col_kernel(KSegs segs, ChunkPlan
   __shared__ float ls[QB];
   __shared__ double colsum[CHUNK];
   __shared__ double red[WAVES];
-  const int c = blockIdx.x, sg = blockIdx.y, bh = blockIdx.z;
+  // the first pass walks heads and chunks in grid order, so this one walks
+  // them backwards: the keys it reads first are those the first pass read
+  // last, which the last-level cache may still hold
+  const int c = gridDim.x - 1 - blockIdx.x, sg = blockIdx.y, bh = gridDim.z - 1 - blockIdx.z;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i16 = lane & 15, g4 = lane >> 4;
   const int G = Hq / Hkv, nq = G * W, b = bh / Hkv, hkv = bh % Hkv;
