@@ -47,9 +47,12 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
 int decode_batch_wgs(const uc_shape& sh);
 size_t decode_batch_desc_bytes(int n_req, int n_segs_total);
 size_t decode_batch_workspace(const uc_shape& sh, int M, int n_segs_total);
+int decode_split_segment(const KSegs& segs);
+size_t decode_batch_table_bytes(int n_req);
+size_t decode_batch_grid_bytes(int n_req);
 hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, int n_wgs,
-                               const void* q, int M, float sm_scale, float* o, float* lse,
-                               void* ws, hipStream_t st);
+                               int n_grid, int skew, const void* q, int M, float sm_scale,
+                               float* o, float* lse, void* ws, hipStream_t st);
 }  // namespace uc
 
 namespace {
@@ -603,6 +606,13 @@ uc_status uc_plan_destroy(uc_plan plan) {
 }
 
 // ---------------------------------------------------------------- batched requests
+// Time of a packed row relative to a dense one in the batched decode kernel
+// (a third of the bytes, more vector-ALU work), for sharing rows among
+// workgroups.  Measured on one MI355X with 16 requests of int4 text and
+// dense rows: 0.33 (bytes) 63.1 us, 0.6 60.0 us, 1.0 (rows) 61.7 us.
+constexpr double kPackedRowCost = 0.6;
+
+
 // Validates every request against a one-request shape; true if all of them
 // can run in the batched decode kernel.
 static uc_status batch_check(const uc_shape* shape, const uc_segment* const* segs,
@@ -660,35 +670,57 @@ uc_status uc_attend_batch(const uc_shape* shape, const uc_segment* const* segs, 
     for (int r = 0; r < shape->B; ++r) total += n_segs[r];
     const size_t need = decode_batch_workspace(*shape, M, total);
     if (ws_bytes < need || !ws) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
-    // request table and flat descriptors, in the workspace's layout, sent to
-    // the GPU inside small kernels' arguments (no staging, no host wait)
-    const size_t tbytes = (((size_t)shape->B * sizeof(BatchDesc)) + 255) & ~(size_t)255;
-    std::vector<char> desc(decode_batch_desc_bytes(shape->B, total), 0);
+    // request table, grid runs and flat descriptors, in the workspace's
+    // layout, sent to the GPU inside small kernels' arguments (no staging, no
+    // host wait)
+    const int B = shape->B, Hkv = shape->Hkv;
+    const size_t tbytes = decode_batch_table_bytes(B), gbytes = decode_batch_grid_bytes(B);
+    std::vector<char> desc(decode_batch_desc_bytes(B, total), 0);
     BatchDesc* table = (BatchDesc*)desc.data();
-    KSeg* flat = (KSeg*)(desc.data() + tbytes);
-    // workgroups per KV head in proportion to each request's rows
+    BatchGrid* grid = (BatchGrid*)(desc.data() + tbytes);
+    KSeg* flat = (KSeg*)(desc.data() + tbytes + gbytes);
+    // workgroups per KV head: one unit each, then a unit at a time to the
+    // request with the most weighted rows per workgroup until the budget (a
+    // round of resident workgroups) is spent, which minimises the largest
+    // share (packed rows weighted by kPackedRowCost).
+    // Workgroups go in pairs when the budget gives every request one (an
+    // early and a late workgroup per pair, so the launch's two halves hold
+    // the same number and every CU pairs one of each).
     const int budget = decode_batch_wgs(*shape);
-    double all_rows = 0.0;
-    std::vector<double> rows(shape->B, 0.0);
-    for (int r = 0; r < shape->B; ++r) {
-      for (int i = 0; i < n_segs[r]; ++i) rows[r] += ks[r].s[i].n_rows;
-      all_rows += rows[r];
+    const int unit = budget >= 2 * B ? 2 : 1;
+    std::vector<double> rows(B, 0.0);
+    for (int r = 0; r < B; ++r)
+      for (int i = 0; i < n_segs[r]; ++i)
+        rows[r] += ks[r].s[i].n_rows * (ks[r].s[i].kind == UC_SEG_PACKED ? kPackedRowCost : 1.0);
+    std::vector<int> W(B, unit);
+    for (int left = budget - unit * B; left >= unit; left -= unit) {
+      int best = 0;
+      for (int r = 1; r < B; ++r)
+        if (rows[r] * W[best] > rows[best] * W[r]) best = r;  // rows/W largest, lower r on ties
+      W[best] += unit;
     }
-    // (the minimum of one per request is taken out of the budget first, so
-    // the grid stays within one round of resident workgroups)
-    const int spare = std::max(0, budget - shape->B);
-    int pos = 0, W_max = 1, n_wgs = 0;
-    for (int r = 0; r < shape->B; ++r) {
-      const int Wr = std::min(budget, 1 + (int)(spare * rows[r] / all_rows));
-      W_max = std::max(W_max, Wr);
-      table[r] = BatchDesc{pos, n_segs[r], Wr, n_wgs};
-      n_wgs += Wr * shape->Hkv;
+    int pos = 0, W_max = 1, n_wgs = 0, n_grid = 0;
+    for (int r = 0; r < B; ++r) {
+      W_max = std::max(W_max, W[r]);
+      table[r] = BatchDesc{pos, n_segs[r], W[r], decode_split_segment(ks[r])};
       for (int i = 0; i < n_segs[r]; ++i) flat[pos++] = ks[r].s[i];
     }
+    // grid runs: workgroups 0 .. W/2 - 1 of every request (the early ones,
+    // dispatched in the launch's first half), then the others
+    for (int half = 0; half < 2; ++half)
+      for (int r = 0; r < B; ++r) {
+        const int w0 = half ? W[r] / 2 : 0, nw = half ? W[r] - W[r] / 2 : W[r] / 2;
+        if (nw == 0) continue;
+        grid[n_grid++] = BatchGrid{n_wgs, r, w0, nw};
+        n_wgs += nw * Hkv;
+      }
+    // early workgroups take the larger share when the grid is two per CU
+    const int skew = n_wgs == 2 * device_cus() ? 600 : 0;
     g_last_kernel = "decode_batch";
     hipError_t e = launch_blob_upload(desc.data(), desc.size(), ws, s);
     if (e == hipSuccess)
-      e = launch_decode_batch(*shape, total, W_max, n_wgs, q, M, sm_scale, o, lse, ws, s);
+      e = launch_decode_batch(*shape, total, W_max, n_wgs, n_grid, skew, q, M, sm_scale, o, lse,
+                              ws, s);
     return launched(e);
   }
   // one call per request (the timing hook is not applied here)

@@ -578,9 +578,9 @@ __device__ __attribute__((always_inline)) inline void decode_body(
   }
   const int sbh = BATCH ? hkv : bh;  // (b, h_kv) within the segments' own layout
   // items: the segments in order, or with a split segment (never with
-  // per-segment records or batched requests) its first part, the others in
-  // order, then its second part
-  const int split = BATCH ? -1 : pl.split;
+  // per-segment records) its first part, the others in order, then its
+  // second part
+  const int split = BATCH ? table[b].split : pl.split;
   const int n_items = split >= 0 ? n_seg + 1 : n_seg;
   for (int it = 0; it < n_items; ++it) {
     int si = it;
@@ -590,9 +590,8 @@ __device__ __attribute__((always_inline)) inline void decode_body(
     // shares of the other segments are the remainders; workgroup 0 already
     // holds the start of the protected segment
     const int ws = (!BATCH && ap.n_new > 0 && si == n_seg - 1) ? Wr - 1 - w : w;
-    int r0 = BATCH ? share_row(ks.n_rows, ws, Wr) : share_row_skewed(ks.n_rows, ws, Wr, pl.skew);
-    int r1 = BATCH ? share_row(ks.n_rows, ws + 1, Wr)
-                   : share_row_skewed(ks.n_rows, ws + 1, Wr, pl.skew);
+    int r0 = share_row_skewed(ks.n_rows, ws, Wr, pl.skew);
+    int r1 = share_row_skewed(ks.n_rows, ws + 1, Wr, pl.skew);
     if (split >= 0 && si == split) {
       // r0 is tile-aligned, so both parts start on a tile boundary and only
       // the second can end in a partial tile
@@ -636,27 +635,30 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
 }
 
 __global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* __restrict__ table,
+                                                              const BatchGrid* __restrict__ grid,
+                                                              int n_grid,
                                                               const KSeg* __restrict__ flat,
                                                               DecodePlan pl,
                                                               const uint16_t* __restrict__ q,
                                                               int Hq, int Hkv, int M,
                                                               float scale_log2,
                                                               float* __restrict__ partial) {
-  // the request of this workgroup: the last table entry starting at or
-  // before it (starts ascend); then its KV head and share
+  // the grid run of this workgroup: the last entry starting at or before it
+  // (starts ascend); then its request, KV head and share
   const int g = blockIdx.x;
-  int lo = 0, hi = pl.n_seg - 1;  // n_seg holds the number of requests here
+  int lo = 0, hi = n_grid - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (table[mid].start <= g) lo = mid;
+    if (grid[mid].start <= g) lo = mid;
     else hi = mid - 1;
   }
-  const int local = g - table[lo].start, Wr = table[lo].W;
+  const BatchGrid e = grid[lo];
+  const int local = g - e.start;
   KSegs none;
   none.n = 0;
   const AppendOp no_append{};
-  decode_body<true>(none, table, flat, pl, no_append, local % Wr, lo * Hkv + local / Wr, q, Hq,
-                    Hkv, M, scale_log2, partial);
+  decode_body<true>(none, table, flat, pl, no_append, e.w0 + local % e.nw,
+                    e.req * Hkv + local / e.nw, q, Hq, Hkv, M, scale_log2, partial);
 }
 
 }  // namespace
@@ -756,6 +758,20 @@ size_t decode_mfma_workspace(const uc_shape& sh, const KSegs& segs, int M) {
   return (bytes + 255) & ~(size_t)255;
 }
 
+// the segment a workgroup takes around the others: the largest dense one,
+// when there is another segment and some packed code rows (else -1)
+int decode_split_segment(const KSegs& segs) {
+  if (segs.n < 2) return -1;
+  bool packed = false;
+  int best = -1;
+  for (int i = 0; i < segs.n; ++i) {
+    const KSeg& s = segs.s[i];
+    if (s.kind == UC_SEG_PACKED && s.n_full > 0) packed = true;
+    if (s.kind == UC_SEG_DENSE && (best < 0 || s.n_rows > segs.s[best].n_rows)) best = i;
+  }
+  return packed && best >= 0 && segs.s[best].n_rows > 0 ? best : -1;
+}
+
 hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void* q, int M,
                               float sm_scale, float* o, float* lse, float* seg_lse, void* ws,
                               hipStream_t st, const AppendOp* ap) {
@@ -777,17 +793,7 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   p.skew = p.W * sh.B * sh.Hkv == 2 * device_cus() ? 600 : 0;
   // split the largest dense segment around the others when packed rows are
   // present (staggered packed phases, see DecodePlan)
-  p.split = -1;
-  if (!p.per_seg && segs.n > 1) {
-    bool packed = false;
-    int best = -1;
-    for (int i = 0; i < segs.n; ++i) {
-      const KSeg& s = segs.s[i];
-      if (s.kind == UC_SEG_PACKED && s.n_full > 0) packed = true;
-      if (s.kind == UC_SEG_DENSE && (best < 0 || s.n_rows > segs.s[best].n_rows)) best = i;
-    }
-    if (packed && best >= 0 && segs.s[best].n_rows > 0) p.split = best;
-  }
+  p.split = p.per_seg ? -1 : decode_split_segment(segs);
   float* partial = (float*)ws;
   hipError_t e = kernel_timer_begin(st);
   if (e != hipSuccess) return e;
@@ -821,9 +827,16 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
 // depend on row counts).
 int decode_batch_wgs(const uc_shape& sh) { return max(1, (2 * device_cus()) / sh.Hkv); }
 
+// descriptor area: request table | grid runs (two per request) | flat segments
+size_t decode_batch_table_bytes(int n_req) {
+  return (((size_t)n_req * sizeof(BatchDesc)) + 255) & ~(size_t)255;
+}
+size_t decode_batch_grid_bytes(int n_req) {
+  return (((size_t)2 * n_req * sizeof(BatchGrid)) + 255) & ~(size_t)255;
+}
 size_t decode_batch_desc_bytes(int n_req, int n_segs_total) {
-  const size_t t = (((size_t)n_req * sizeof(BatchDesc)) + 255) & ~(size_t)255;
-  return t + ((((size_t)n_segs_total * sizeof(KSeg)) + 255) & ~(size_t)255);
+  return decode_batch_table_bytes(n_req) + decode_batch_grid_bytes(n_req) +
+         ((((size_t)n_segs_total * sizeof(KSeg)) + 255) & ~(size_t)255);
 }
 
 size_t decode_batch_workspace(const uc_shape& sh, int M, int n_segs_total) {
@@ -832,21 +845,23 @@ size_t decode_batch_workspace(const uc_shape& sh, int M, int n_segs_total) {
 }
 
 hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, int n_wgs,
-                               const void* q, int M, float sm_scale, float* o, float* lse,
-                               void* ws, hipStream_t st) {
+                               int n_grid, int skew, const void* q, int M, float sm_scale,
+                               float* o, float* lse, void* ws, hipStream_t st) {
   DecodePlan p{};
   p.W = W_max;
-  p.n_seg = sh.B;  // the batched kernel reads the number of requests from here
+  p.n_seg = sh.B;
   p.per_seg = 0;
-  p.split = -1;
+  p.split = -1;  // per request, in the table
+  p.skew = skew;
   const BatchDesc* table = (const BatchDesc*)ws;
-  const KSeg* flat =
-      (const KSeg*)((char*)ws + ((((size_t)sh.B * sizeof(BatchDesc)) + 255) & ~(size_t)255));
+  const BatchGrid* grid = (const BatchGrid*)((char*)ws + decode_batch_table_bytes(sh.B));
+  const KSeg* flat = (const KSeg*)((char*)ws + decode_batch_table_bytes(sh.B) +
+                                   decode_batch_grid_bytes(sh.B));
   float* partial = (float*)((char*)ws + decode_batch_desc_bytes(sh.B, n_segs_total));
   hipError_t e = kernel_timer_begin(st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(decode_batch_kernel, dim3(n_wgs), dim3(256), 0, st, table, flat, p,
-                     (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
+  hipLaunchKernelGGL(decode_batch_kernel, dim3(n_wgs), dim3(256), 0, st, table, grid, n_grid,
+                     flat, p, (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
   e = hipGetLastError();
   if (e == hipSuccess) e = kernel_timer_end(st);
   if (e != hipSuccess) return e;

@@ -57,11 +57,19 @@ struct AppendOp {
 };
 
 // Batched requests: request r's segments are flat[first .. first + n - 1]
-// (one-request layouts); table and flat live in the workspace.
+// (one-request layouts); table, grid entries and flat live in the workspace.
 struct BatchDesc {
   int first, n;
-  int W;      // the request's workgroups per KV head (by its share of the rows)
-  int start;  // its first workgroup in the one-dimensional grid
+  int W;      // the request's workgroups per KV head (by its share of the bytes)
+  int split;  // segment taken around the others (staggered packed phases), or -1
+};
+
+// A run of the one-dimensional grid: workgroups start .. start + Hkv*nw - 1
+// are workgroups w0 .. w0 + nw - 1 of every KV head of request req.  With
+// two runs per request the first holds its early half (dispatched in the
+// launch's first half), the second its late half.
+struct BatchGrid {
+  int start, req, w0, nw;
 };
 
 // Split of every segment's rows into chunks (work items of the split-K

@@ -79,6 +79,7 @@ def test_attend_batch_matches_each_request(M):
     lse = torch.empty(B, Hq, M, device="cuda")
     sm = sm_scale(D)
     uc.uc_attend_batch(shape, reqs, dev(q, "bf16"), M, sm, o, lse)
+    assert uc.uc_last_kernel() == "decode_batch"
     torch.cuda.synchronize()
     og, lg = o.cpu().numpy(), lse.cpu().numpy()
     for r, (K, V, seg_id, ns) in enumerate(refs):
@@ -90,6 +91,30 @@ def test_attend_batch_matches_each_request(M):
         uc.uc_attend_mixed(uc.make_shape(1, Hq, Hkv, D), reqs[r], dev(q[r:r + 1], "bf16"), M, sm, o1)
         torch.cuda.synchronize()
         assert np.abs(o1.cpu().numpy() - og[r:r + 1]).max() < 5e-4, r
+
+
+def test_attend_batch_many_requests():
+    """More requests than the launch can give a pair of workgroups per KV
+    head (70 > 2 * 256 / 4 / 2): each gets single workgroups by its share of
+    the bytes; every request still matches the oracle."""
+    print("CASE attend_batch 70 requests", flush=True)
+    reqs, refs = [], []
+    for r in range(70):
+        parts = [("dense", 20 + 37 * (r % 9))] + ([("packed", 64, 64, 4)] if r % 3 == 0 else [])
+        segs, K, V, seg_id = _request(200 + r, parts)
+        reqs.append(segs)
+        refs.append((K, V, seg_id, len(parts)))
+    B, M = len(reqs), 1
+    q = rand_rows(98, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+    o = torch.empty(B, Hq, M, D, device="cuda")
+    sm = sm_scale(D)
+    uc.uc_attend_batch(uc.make_shape(B, Hq, Hkv, D), reqs, dev(q, "bf16"), M, sm, o)
+    assert uc.uc_last_kernel() == "decode_batch"
+    torch.cuda.synchronize()
+    og = o.cpu().numpy()
+    for r, (K, V, seg_id, ns) in enumerate(refs):
+        o_ref, _, _, _ = ref.attend(ref.widen(q[r:r + 1], "bf16"), K, V, None, seg_id, ns, sm)
+        check_attention(og[r:r + 1], o_ref, f"request {r}")
 
 
 def test_attend_batch_falls_back_per_request():
