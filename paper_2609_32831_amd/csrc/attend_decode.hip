@@ -118,37 +118,45 @@ __device__ inline u4 q_operand(const char* lq, int t, int lane) {
 }
 
 // ---------------------------------------------------------------- dense rows
+// K and V rows are both loaded as whole lines: load i covers rows 4i .. 4i+3
+// of the tile, 256 contiguous bytes each (lane = row lane/16, 16-byte chunk
+// lane%16).  Loading K straight into the matrix-core operand layout instead
+// (16 rows x 64 bytes per load, half of each 128-byte line) streams about 15 %
+// slower on this chip, so K takes the way through the wave's LDS tile that
+// dequantised packed rows take.
 struct DenseSet {
-  u4 k[8];  // A operands: k[blk*4 + t] = row blk*16 + i16, dims t*32 + g4*8 .. +7
-  u4 v[8];  // v[i] = row lane/16 + 4*i, 16-byte chunk lane%16
+  u4 k[8];  // k[i] = row lane/16 + 4*i, 16-byte chunk lane%16
+  u4 v[8];  // likewise for V
 };
 
 __device__ inline void dense_issue(__amdgpu_buffer_rsrc_t rk, __amdgpu_buffer_rsrc_t rv, int row0,
                                    int lane, DenseSet& S) {
   const int i16 = lane & 15, g4 = lane >> 4;
-  const int ko = (row0 + i16) * ROWB + g4 * 16;
+  const int o = (row0 + g4) * ROWB + i16 * 16;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    S.k[t] = bload<kNT>(rk, ko, t * 64);
-    S.k[4 + t] = bload<kNT>(rk, ko, 16 * ROWB + t * 64);
-  }
-  const int vo = (row0 + g4) * ROWB + i16 * 16;
+  for (int i = 0; i < 8; ++i) S.k[i] = bload<kNT>(rk, o, i * 4 * ROWB);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) S.v[i] = bload<kNT>(rv, vo, i * 4 * ROWB);
+  for (int i = 0; i < 8; ++i) S.v[i] = bload<kNT>(rv, o, i * 4 * ROWB);
 }
 
-__device__ inline void dense_head(const DenseSet& S, char* lv, const char* lq, int lane,
+__device__ inline void dense_head(const DenseSet& S, char* lk, char* lv, const char* lq, int lane,
                                   f4& s0, f4& s1) {
   const int i16 = lane & 15, g4 = lane >> 4;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) *reinterpret_cast<u4*>(lv + toff(g4 + 4 * i, i16)) = S.v[i];
+  for (int i = 0; i < 8; ++i) {
+    *reinterpret_cast<u4*>(lk + toff(g4 + 4 * i, i16)) = S.k[i];
+    *reinterpret_cast<u4*>(lv + toff(g4 + 4 * i, i16)) = S.v[i];
+  }
   s0 = f4{0.f, 0.f, 0.f, 0.f};
   s1 = s0;
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
+    // A operands: rows blk*16 + i16, dims t*32 + g4*8 .. +7
+    const u4 k0 = *reinterpret_cast<const u4*>(lk + toff(i16, t * 4 + g4));
+    const u4 k1 = *reinterpret_cast<const u4*>(lk + toff(16 + i16, t * 4 + g4));
     const u4 qb = q_operand(lq, t, lane);
-    s0 = mfma(S.k[t], qb, s0);
-    s1 = mfma(S.k[4 + t], qb, s1);
+    s0 = mfma(k0, qb, s0);
+    s1 = mfma(k1, qb, s1);
   }
 }
 
@@ -157,7 +165,7 @@ __device__ inline void dense_head(const DenseSet& S, char* lv, const char* lq, i
 // range can be partial, and it is always one of the epilogue tiles.
 __device__ __attribute__((always_inline)) inline void dense_loop(State& st, const uint16_t* kb, const uint16_t* vb, int r0, int r1,
                                   int wave, int lane, const char* lq, float scale_log2,
-                                  char* lv) {
+                                  char* lk, char* lv) {
   const int n_tiles = (r1 - r0 + TILE - 1) / TILE;
   const int n_mine = n_tiles > wave ? (n_tiles - wave + WAVES - 1) / WAVES : 0;
   if (n_mine == 0) return;
@@ -176,23 +184,23 @@ __device__ __attribute__((always_inline)) inline void dense_loop(State& st, cons
   // steady state without branches, so the compiler's wait counts keep the
   // other set's loads in flight: consume A, refill A, consume B, refill B
   for (; k + 3 < n_mine; k += 2) {
-    dense_head(A, lv, lq, lane, s0, s1);
+    dense_head(A, lk, lv, lq, lane, s0, s1);
     dense_issue(rk, rv, row_of(k + 2), lane, A);
     softmax_pv<false>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
-    dense_head(B, lv, lq, lane, s0, s1);
+    dense_head(B, lk, lv, lq, lane, s0, s1);
     dense_issue(rk, rv, row_of(k + 3), lane, B);
     softmax_pv<false>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
   const int left = n_mine - k;  // 1..3 tiles; A holds tile k, B tile k+1
-  dense_head(A, lv, lq, lane, s0, s1);
+  dense_head(A, lk, lv, lq, lane, s0, s1);
   if (left == 3) dense_issue(rk, rv, row_of(k + 2), lane, A);
   softmax_pv<true>(st, s0, s1, scale_log2, row_of(k), r1, lv, i16, g4);
   if (left >= 2) {
-    dense_head(B, lv, lq, lane, s0, s1);
+    dense_head(B, lk, lv, lq, lane, s0, s1);
     softmax_pv<true>(st, s0, s1, scale_log2, row_of(k + 1), r1, lv, i16, g4);
   }
   if (left == 3) {
-    dense_head(A, lv, lq, lane, s0, s1);
+    dense_head(A, lk, lv, lq, lane, s0, s1);
     softmax_pv<true>(st, s0, s1, scale_log2, row_of(k + 2), r1, lv, i16, g4);
   }
 }
@@ -461,7 +469,7 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
   if (ks.kind == UC_SEG_DENSE) {
     const int64_t base = (int64_t)bh * ks.row_stride * D;
     dense_loop(st, (const uint16_t*)ks.k + base, (const uint16_t*)ks.v + base, r0, r1,
-               (wave - rot) & (WAVES - 1), lane, lq, scale_log2, lv);
+               (wave - rot) & (WAVES - 1), lane, lq, scale_log2, lk, lv);
     rot += (r1 - r0 + TILE - 1) / TILE;
     return true;
   }
@@ -500,7 +508,7 @@ __device__ __attribute__((always_inline)) inline bool segment_share(State& st, c
     const int64_t base = (int64_t)bh * ks.tail_stride * D;
     dense_loop(st, (const uint16_t*)ks.tail_k + base, (const uint16_t*)ks.tail_v + base,
                t0 - ks.n_full, r1 - ks.n_full, (wave - rot) & (WAVES - 1), lane, lq, scale_log2,
-               lv);
+               lk, lv);
     rot += (r1 - t0 + TILE - 1) / TILE;
   }
   return true;

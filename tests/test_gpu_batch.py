@@ -117,6 +117,34 @@ def test_attend_batch_many_requests():
         check_attention(og[r:r + 1], o_ref, f"request {r}")
 
 
+@pytest.mark.parametrize("M", [1, 2])
+def test_attend_batch_short_line(M):
+    """A batch with a few tiles in all: requests shorter than a tile (most
+    of their workgroups get empty shares), a packed segment with residual
+    rows, M = 2 query rows per head."""
+    print("CASE attend_batch short line M", M, flush=True)
+    parts = [[("dense", 5)], [("dense", 40), ("tail", 2, 4)], [("packed", 70, 32, 2), ("dense", 70)],
+             [("tail", 1, 1)]]
+    reqs, refs = [], []
+    for r, pr in enumerate(parts):
+        segs, K, V, seg_id = _request(300 + r, pr)
+        reqs.append(segs)
+        refs.append((K, V, seg_id, len(pr)))
+    B = len(reqs)
+    q = rand_rows(97, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+    o = torch.empty(B, Hq, M, D, device="cuda")
+    lse = torch.empty(B, Hq, M, device="cuda")
+    sm = sm_scale(D)
+    uc.uc_attend_batch(uc.make_shape(B, Hq, Hkv, D), reqs, dev(q, "bf16"), M, sm, o, lse)
+    assert uc.uc_last_kernel() == "decode_batch"
+    torch.cuda.synchronize()
+    og, lg = o.cpu().numpy(), lse.cpu().numpy()
+    for r, (K, V, seg_id, ns) in enumerate(refs):
+        o_ref, lse_ref, _, _ = ref.attend(ref.widen(q[r:r + 1], "bf16"), K, V, None, seg_id, ns, sm)
+        check_attention(og[r:r + 1], o_ref, f"request {r}")
+        assert np.allclose(lg[r:r + 1], lse_ref, rtol=1e-5, atol=1e-4), r
+
+
 def test_attend_batch_falls_back_per_request():
     """A request outside the batched kernel's range (fp32 rows) sends every
     request through its own call; results are the same as each call's."""
