@@ -51,8 +51,8 @@ int decode_split_segment(const KSegs& segs);
 size_t decode_batch_table_bytes(int n_req);
 size_t decode_batch_grid_bytes(int n_req);
 hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, int n_wgs,
-                               int n_grid, int skew, const void* q, int M, float sm_scale,
-                               float* o, float* lse, void* ws, hipStream_t st);
+                               int n_grid, int skew, const BatchArgs* args, const void* q, int M,
+                               float sm_scale, float* o, float* lse, void* ws, hipStream_t st);
 }  // namespace uc
 
 namespace {
@@ -671,8 +671,9 @@ uc_status uc_attend_batch(const uc_shape* shape, const uc_segment* const* segs, 
     const size_t need = decode_batch_workspace(*shape, M, total);
     if (ws_bytes < need || !ws) return fail(UC_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
     // request table, grid runs and flat descriptors, in the workspace's
-    // layout, sent to the GPU inside small kernels' arguments (no staging, no
-    // host wait)
+    // layout; a small batch passes them in the attention kernel's arguments,
+    // a larger one sends them to the workspace inside small kernels'
+    // arguments first (no staging, no host wait)
     const int B = shape->B, Hkv = shape->Hkv;
     const size_t tbytes = decode_batch_table_bytes(B), gbytes = decode_batch_grid_bytes(B);
     std::vector<char> desc(decode_batch_desc_bytes(B, total), 0);
@@ -717,10 +718,21 @@ uc_status uc_attend_batch(const uc_shape* shape, const uc_segment* const* segs, 
     // early workgroups take the larger share when the grid is two per CU
     const int skew = n_wgs == 2 * device_cus() ? 600 : 0;
     g_last_kernel = "decode_batch";
-    hipError_t e = launch_blob_upload(desc.data(), desc.size(), ws, s);
-    if (e == hipSuccess)
-      e = launch_decode_batch(*shape, total, W_max, n_wgs, n_grid, skew, q, M, sm_scale, o, lse,
-                              ws, s);
+    hipError_t e = hipSuccess;
+    if (B <= kArgReq && total <= kArgSeg) {
+      static thread_local BatchArgs args;  // 11.8 KB: not on the stack
+      memset(&args, 0, sizeof args);
+      memcpy(args.table, table, sizeof(BatchDesc) * B);
+      memcpy(args.grid, grid, sizeof(BatchGrid) * n_grid);
+      memcpy(args.flat, flat, sizeof(KSeg) * total);
+      e = launch_decode_batch(*shape, total, W_max, n_wgs, n_grid, skew, &args, q, M, sm_scale, o,
+                              lse, ws, s);
+    } else {
+      e = launch_blob_upload(desc.data(), desc.size(), ws, s);
+      if (e == hipSuccess)
+        e = launch_decode_batch(*shape, total, W_max, n_wgs, n_grid, skew, nullptr, q, M,
+                                sm_scale, o, lse, ws, s);
+    }
     return launched(e);
   }
   // one call per request (the timing hook is not applied here)

@@ -642,17 +642,12 @@ __global__ __launch_bounds__(256, 2) void decode_mfma_kernel(KSegs segs, DecodeP
   decode_body<false>(segs, nullptr, nullptr, pl, ap, w, bh, q, Hq, Hkv, M, scale_log2, partial);
 }
 
-__global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* __restrict__ table,
-                                                              const BatchGrid* __restrict__ grid,
-                                                              int n_grid,
-                                                              const KSeg* __restrict__ flat,
-                                                              DecodePlan pl,
-                                                              const uint16_t* __restrict__ q,
-                                                              int Hq, int Hkv, int M,
-                                                              float scale_log2,
-                                                              float* __restrict__ partial) {
-  // the grid run of this workgroup: the last entry starting at or before it
-  // (starts ascend); then its request, KV head and share
+// a batched workgroup: its grid run is the last entry starting at or before
+// it (starts ascend); then its request, KV head and share
+__device__ __attribute__((always_inline)) inline void batch_entry(
+    const BatchDesc* __restrict__ table, const BatchGrid* __restrict__ grid, int n_grid,
+    const KSeg* __restrict__ flat, const DecodePlan& pl, const uint16_t* __restrict__ q, int Hq,
+    int Hkv, int M, float scale_log2, float* __restrict__ partial) {
   const int g = blockIdx.x;
   int lo = 0, hi = n_grid - 1;
   while (lo < hi) {
@@ -667,6 +662,29 @@ __global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* _
   const AppendOp no_append{};
   decode_body<true>(none, table, flat, pl, no_append, e.w0 + local % e.nw,
                     e.req * Hkv + local / e.nw, q, Hq, Hkv, M, scale_log2, partial);
+}
+
+// descriptors stored in the workspace
+__global__ __launch_bounds__(256, 2) void decode_batch_kernel(const BatchDesc* __restrict__ table,
+                                                              const BatchGrid* __restrict__ grid,
+                                                              int n_grid,
+                                                              const KSeg* __restrict__ flat,
+                                                              DecodePlan pl,
+                                                              const uint16_t* __restrict__ q,
+                                                              int Hq, int Hkv, int M,
+                                                              float scale_log2,
+                                                              float* __restrict__ partial) {
+  batch_entry(table, grid, n_grid, flat, pl, q, Hq, Hkv, M, scale_log2, partial);
+}
+
+// descriptors in the kernel arguments
+__global__ __launch_bounds__(256, 2) void decode_batch_args_kernel(BatchArgs a, int n_grid,
+                                                                   DecodePlan pl,
+                                                                   const uint16_t* __restrict__ q,
+                                                                   int Hq, int Hkv, int M,
+                                                                   float scale_log2,
+                                                                   float* __restrict__ partial) {
+  batch_entry(a.table, a.grid, n_grid, a.flat, pl, q, Hq, Hkv, M, scale_log2, partial);
 }
 
 }  // namespace
@@ -825,9 +843,11 @@ hipError_t launch_decode_mfma(const uc_shape& sh, const KSegs& segs, const void*
   return launch_attend_combine(sh, segs, cp, M, partial, o, lse, seg_lse, st);
 }
 
-// Requests of different layouts: sh.B = number of requests; the workspace
-// holds the request table and the flat segment descriptors (written by the
-// caller through launch_blob_upload), then the partial records; q / o / lse
+// Requests of different layouts: sh.B = number of requests; the request
+// table, grid runs and flat segment descriptors come in args (a batch within
+// kArgReq / kArgSeg) or, when args is null, from the workspace (written by
+// the caller through launch_blob_upload); the workspace then holds the
+// partial records after the descriptor area; q / o / lse
 // are laid out as for sh.B batch elements.  Each request gets workgroups per
 // KV head in proportion to its rows (at least one), all of them in one
 // one-dimensional grid; the record stride per query row is the largest share
@@ -853,8 +873,8 @@ size_t decode_batch_workspace(const uc_shape& sh, int M, int n_segs_total) {
 }
 
 hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, int n_wgs,
-                               int n_grid, int skew, const void* q, int M, float sm_scale,
-                               float* o, float* lse, void* ws, hipStream_t st) {
+                               int n_grid, int skew, const BatchArgs* args, const void* q, int M,
+                               float sm_scale, float* o, float* lse, void* ws, hipStream_t st) {
   DecodePlan p{};
   p.W = W_max;
   p.n_seg = sh.B;
@@ -868,8 +888,12 @@ hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, 
   float* partial = (float*)((char*)ws + decode_batch_desc_bytes(sh.B, n_segs_total));
   hipError_t e = kernel_timer_begin(st);
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(decode_batch_kernel, dim3(n_wgs), dim3(256), 0, st, table, grid, n_grid,
-                     flat, p, (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
+  if (args)
+    hipLaunchKernelGGL(decode_batch_args_kernel, dim3(n_wgs), dim3(256), 0, st, *args, n_grid, p,
+                       (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
+  else
+    hipLaunchKernelGGL(decode_batch_kernel, dim3(n_wgs), dim3(256), 0, st, table, grid, n_grid,
+                       flat, p, (const uint16_t*)q, sh.Hq, sh.Hkv, M, sm_scale * kLog2e, partial);
   e = hipGetLastError();
   if (e == hipSuccess) e = kernel_timer_end(st);
   if (e != hipSuccess) return e;

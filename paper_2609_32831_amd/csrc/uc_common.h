@@ -72,6 +72,16 @@ struct BatchGrid {
   int start, req, w0, nw;
 };
 
+// A batch of at most kArgReq requests and kArgSeg segments in all travels
+// in the attention kernel's arguments (11.8 KB) instead of being stored
+// into the workspace by separate launches first.
+constexpr int kArgReq = 32, kArgSeg = 64;
+struct BatchArgs {
+  BatchDesc table[kArgReq];
+  BatchGrid grid[2 * kArgReq];
+  KSeg flat[kArgSeg];
+};
+
 // Split of every segment's rows into chunks (work items of the split-K
 // attention and of the scoring passes); chunks never straddle segments.
 struct ChunkPlan {
