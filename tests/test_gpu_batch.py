@@ -145,6 +145,31 @@ def test_attend_batch_short_line(M):
         assert np.allclose(lg[r:r + 1], lse_ref, rtol=1e-5, atol=1e-4), r
 
 
+@pytest.mark.parametrize("n_req", [32, 33])
+def test_attend_batch_descriptor_capacity(n_req):
+    """32 requests of two segments fill the descriptors that travel in the
+    attention kernel's arguments exactly (32 requests, 64 segments); 33 go
+    through the workspace instead.  Both match the oracle."""
+    print("CASE attend_batch capacity", n_req, flush=True)
+    reqs, refs = [], []
+    for r in range(n_req):
+        parts = [("dense", 40 + 29 * (r % 7)), ("packed", 64, 32, 2 if r % 2 else 4)]
+        segs, K, V, seg_id = _request(400 + r, parts)
+        reqs.append(segs)
+        refs.append((K, V, seg_id, len(parts)))
+    B, M = len(reqs), 1
+    q = rand_rows(96, B * Hq, M, D, "bf16").reshape(B, Hq, M, D)
+    o = torch.empty(B, Hq, M, D, device="cuda")
+    sm = sm_scale(D)
+    uc.uc_attend_batch(uc.make_shape(B, Hq, Hkv, D), reqs, dev(q, "bf16"), M, sm, o)
+    assert uc.uc_last_kernel() == "decode_batch"
+    torch.cuda.synchronize()
+    og = o.cpu().numpy()
+    for r, (K, V, seg_id, ns) in enumerate(refs):
+        o_ref, _, _, _ = ref.attend(ref.widen(q[r:r + 1], "bf16"), K, V, None, seg_id, ns, sm)
+        check_attention(og[r:r + 1], o_ref, f"request {r}")
+
+
 def test_attend_batch_falls_back_per_request():
     """A request outside the batched kernel's range (fp32 rows) sends every
     request through its own call; results are the same as each call's."""
