@@ -67,6 +67,9 @@ def parse():
                     help="decode kernel time on one copy of the compressed 64k cache vs "
                          "alternating between two copies (reuse distance above the 256 MB "
                          "last-level cache)")
+    ap.add_argument("--read-ceiling", action="store_true",
+                    help="streaming-read rate of HBM in the decode kernel's launch shape: "
+                         "whole-line loads and the matrix-core operand pattern (one JSON line)")
     ap.add_argument("--understanding", action="store_true",
                     help="the 7B-shaped understanding workload (4 requests, 4608-row context, "
                          "256 decode steps): whole job, and the decode steps issued one by one "
@@ -978,10 +981,47 @@ def batch_bench(args):
           flush=True)
 
 
+def read_ceiling(args) -> dict:
+    """The streaming-read probe (uc_read_probe) over a 2 GiB buffer, both load
+    patterns, 20 timed calls each after 3 warm-up calls (fence-free events
+    around each call): the rate a plain read of HBM reaches in the decode
+    kernel's launch shape, which the decode kernel's achieved bandwidth is
+    compared with."""
+    import torch
+
+    import paper_2609_32831_amd as uc
+
+    unit = uc.uc_read_probe_unit()
+    nbytes = (2 << 30) // unit * unit
+    buf = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.empty(uc.uc_read_probe_sink_bytes(), dtype=torch.uint8, device="cuda")
+    n = 20
+    res = {"metric": "streaming read of HBM (probe)", "bytes": nbytes,
+           "launch": "2 x 256-thread workgroups per CU, non-temporal 16-byte loads"}
+    for name, pat in (("lines", uc.UC_PROBE_LINES), ("operand_pattern", uc.UC_PROBE_OPERAND)):
+        for _ in range(3):
+            uc.uc_read_probe(buf, pat, sink)
+        ev = HipEvents(2 * n)
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        for i in range(n):
+            ev.record(2 * i, stream)
+            uc.uc_read_probe(buf, pat, sink)
+            ev.record(2 * i + 1, stream)
+        torch.cuda.synchronize()
+        ts = sorted(ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(n))
+        ev.close()
+        res[name + "_tbs"] = round(nbytes / (ts[n // 2] * 1e-3) / 1e12, 3)
+        res[name + "_best_tbs"] = round(nbytes / (ts[0] * 1e-3) / 1e12, 3)
+    del buf
+    return res
+
+
 def secondary(args) -> dict:
     """The other workloads' figures, measured in the same run as the headline
     line (no CPU baselines): the two prefill workloads, the dynamic budget's
-    boundary overhead and the understanding workload's decode.  A part that
+    boundary overhead, the understanding workload's decode and the
+    streaming-read ceiling of HBM.  A part that
     fails is reported with its error instead of its figures."""
     import copy
     import traceback
@@ -989,7 +1029,7 @@ def secondary(args) -> dict:
     a.no_cpu_baseline = True
     res = {}
     for name, fn in (("prefill", prefill_bench), ("dynamic", dynamic_bench),
-                     ("understanding", understanding_bench)):
+                     ("understanding", understanding_bench), ("read_ceiling", read_ceiling)):
         t0 = time.perf_counter()
         try:
             res[name] = fn(a)
@@ -1024,6 +1064,11 @@ def main():
         if args.gpus != 1:
             sys.exit(2)
         mall_check(args)
+        return
+    if args.read_ceiling:
+        if args.gpus != 1:
+            sys.exit(2)
+        print(json.dumps(read_ceiling(args)), flush=True)
         return
     if args.understanding:
         if args.gpus != 1:

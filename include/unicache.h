@@ -648,6 +648,27 @@ int uc_quant_config(double budget_bytes, int64_t N, int D, uc_dtype dt, int n_he
  * An event-record failure makes that call return UC_E_DEVICE. */
 uc_status uc_set_kernel_events(void* start, void* stop);
 
+/* Streaming-read probe (instrumentation: the rate at which a plain read of
+ * HBM proceeds on this device, for the attention kernels' roofline fractions
+ * to be read against).  Reads the device buffer buf[0 .. bytes) once with
+ * non-temporal 16-byte loads in the decode kernel's launch shape: two
+ * 256-thread workgroups per CU, workgroup g streaming the g-th of
+ * 2*CUs equal contiguous regions, its four waves taking 4 KB pieces (16 rows
+ * of 256 bytes) in turn.  UC_PROBE_LINES loads each piece as whole 128-byte
+ * lines (four rows per load); UC_PROBE_OPERAND in the A-operand layout of a
+ * 16x16x32 matrix instruction (16 rows x 64 bytes per load, half of each
+ * line), the pattern of loading keys straight into operand registers.  Wave
+ * w of workgroup g stores the XOR of the 16-byte words it read into
+ * sink[(4g + w) * 16 .. +16) (uc_read_probe_sink_bytes() bytes in all, device
+ * memory owned by the caller).  UC_E_INVALID for NULL pointers, an unknown
+ * pattern, or bytes not a positive multiple of uc_read_probe_unit(). */
+#define UC_PROBE_LINES 0
+#define UC_PROBE_OPERAND 1
+size_t uc_read_probe_unit(void);
+size_t uc_read_probe_sink_bytes(void);
+uc_status uc_read_probe(const void* buf, size_t bytes, int pattern, void* sink,
+                        void* stream);
+
 /* ------------------------------------------------------------------------ */
 const char* uc_status_string(uc_status s);
 /* Thread-local description of the calling thread's last error ("" if none). */

@@ -129,6 +129,9 @@ def _load():
         "uc_plan_destroy": (i32, [vp]),
         "uc_plan_attend": (i32, [vp, vp, vp, vp, vp, vp, sz, vp]),
         "uc_plan_invalidate": (i32, [vp]),
+        "uc_read_probe_unit": (sz, []),
+        "uc_read_probe_sink_bytes": (sz, []),
+        "uc_read_probe": (i32, [vp, sz, i32, vp, vp]),
     }
     for name, (res, args) in sigs.items():
         f = getattr(L, name)
@@ -674,6 +677,27 @@ def uc_set_kernel_events(start, stop) -> None:
             return None
         return ctypes.c_void_p(ev.cuda_event if hasattr(ev, "cuda_event") else int(ev))
     _check(lib.uc_set_kernel_events(handle(start), handle(stop)), "uc_set_kernel_events")
+
+
+UC_PROBE_LINES = 0
+UC_PROBE_OPERAND = 1
+
+
+def uc_read_probe_unit() -> int:
+    """Byte granularity of uc_read_probe's buffer (4 KB per workgroup)."""
+    return lib.uc_read_probe_unit()
+
+
+def uc_read_probe_sink_bytes() -> int:
+    return lib.uc_read_probe_sink_bytes()
+
+
+def uc_read_probe(buf: torch.Tensor, pattern: int, sink: torch.Tensor, stream=None) -> None:
+    """Stream buf once (instrumentation; see the header): whole-line loads
+    (UC_PROBE_LINES) or the matrix-core operand pattern (UC_PROBE_OPERAND);
+    sink receives each wave's XOR of the words it read."""
+    _check(lib.uc_read_probe(_ptr(buf), buf.numel() * buf.element_size(), pattern, _ptr(sink),
+                             _stream(stream)), "uc_read_probe")
 
 
 def uc_set_path(path: int) -> int:

@@ -53,6 +53,9 @@ size_t decode_batch_grid_bytes(int n_req);
 hipError_t launch_decode_batch(const uc_shape& sh, int n_segs_total, int W_max, int n_wgs,
                                int n_grid, int skew, const BatchArgs* args, const void* q, int M,
                                float sm_scale, float* o, float* lse, void* ws, hipStream_t st);
+int read_probe_wgs();
+hipError_t launch_read_probe(const void* buf, size_t bytes, int pattern, void* sink,
+                             hipStream_t st);
 }  // namespace uc
 
 namespace {
@@ -1176,3 +1179,17 @@ uc_status uc_calibrate_policy(const float* frac, int rows, int n_types, double t
 }
 
 }  // extern "C"
+
+// ---------------------------------------------------------------- read probe
+size_t uc_read_probe_unit(void) { return (size_t)4096 * read_probe_wgs(); }
+size_t uc_read_probe_sink_bytes(void) { return (size_t)16 * 4 * read_probe_wgs(); }
+
+uc_status uc_read_probe(const void* buf, size_t bytes, int pattern, void* sink, void* stream) {
+  if (!buf || !sink) return fail(UC_E_INVALID, "buf or sink is NULL");
+  if (pattern != UC_PROBE_LINES && pattern != UC_PROBE_OPERAND)
+    return fail(UC_E_INVALID, "unknown probe pattern %d", pattern);
+  const size_t unit = uc_read_probe_unit();
+  if (bytes == 0 || bytes % unit)
+    return fail(UC_E_INVALID, "bytes %zu is not a positive multiple of %zu", bytes, unit);
+  return launched(launch_read_probe(buf, bytes, pattern, sink, (hipStream_t)stream));
+}

@@ -371,3 +371,19 @@ def test_budget_structs_and_validation():
     assert L.uc_calibrate_policy(FAKE, 4, 9, 0.5, FAKE, FAKE, None) == E
     assert L.uc_calibrate_policy(None, 4, 2, 0.5, FAKE, FAKE, None) == E
     assert L.uc_calibrate_policy(FAKE, 4, 2, float("nan"), FAKE, FAKE, None) == E
+
+
+def test_read_probe_validation(uc):
+    """uc_read_probe rejects NULL pointers, unknown patterns and sizes that are
+    not whole 4 KB pieces per workgroup before anything is launched."""
+    L, E = uc.lib, uc.UC_E_INVALID
+    unit = uc.uc_read_probe_unit()
+    assert unit % 4096 == 0 and unit >= 4096
+    assert uc.uc_read_probe_sink_bytes() == unit // 4096 * 4 * 16
+    assert L.uc_read_probe(None, unit, 0, FAKE, None) == E
+    assert L.uc_read_probe(FAKE, unit, 0, None, None) == E
+    assert L.uc_read_probe(FAKE, unit, 2, FAKE, None) == E
+    assert L.uc_read_probe(FAKE, unit, -1, FAKE, None) == E
+    assert L.uc_read_probe(FAKE, 0, 0, FAKE, None) == E
+    assert L.uc_read_probe(FAKE, unit + 4096, 1, FAKE, None) == E
+    assert "multiple" in uc.uc_last_error()
