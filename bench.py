@@ -969,16 +969,15 @@ def batch_bench(args):
         ev.close()
         del g
     ach = n_bytes / (res["kernel"] * 1e-6) / 1e9
-    print(json.dumps({"metric": "batched decode over requests of different layouts",
-                      "requests": R, "bytes_per_step": n_bytes,
-                      "batched_call_us": round(res["batched"], 2),
-                      "per_request_calls_us": round(res["per_request"], 2),
-                      "speedup": round(res["per_request"] / res["batched"], 3),
-                      "roofline": {"bound": "hbm", "kernel": "decode_mfma_kernel (batched)",
-                                   "avg_launch_us": round(res["kernel"], 2),
-                                   "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
-                                   "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4)}}),
-          flush=True)
+    return {"metric": "batched decode over requests of different layouts",
+            "requests": R, "bytes_per_step": n_bytes,
+            "batched_call_us": round(res["batched"], 2),
+            "per_request_calls_us": round(res["per_request"], 2),
+            "speedup": round(res["per_request"] / res["batched"], 3),
+            "roofline": {"bound": "hbm", "kernel": "decode_batch_args_kernel",
+                         "avg_launch_us": round(res["kernel"], 2),
+                         "achieved": round(ach, 1), "peak": HBM_PEAK_GBPS,
+                         "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBPS, 4)}}
 
 
 def read_ceiling(args) -> dict:
@@ -1020,8 +1019,9 @@ def read_ceiling(args) -> dict:
 def secondary(args) -> dict:
     """The other workloads' figures, measured in the same run as the headline
     line (no CPU baselines): the two prefill workloads, the dynamic budget's
-    boundary overhead, the understanding workload's decode and the
-    streaming-read ceiling of HBM.  A part that
+    boundary overhead, the understanding workload's decode, the batched
+    decode of requests of different layouts and the streaming-read ceiling
+    of HBM.  A part that
     fails is reported with its error instead of its figures."""
     import copy
     import traceback
@@ -1029,7 +1029,8 @@ def secondary(args) -> dict:
     a.no_cpu_baseline = True
     res = {}
     for name, fn in (("prefill", prefill_bench), ("dynamic", dynamic_bench),
-                     ("understanding", understanding_bench), ("read_ceiling", read_ceiling)):
+                     ("understanding", understanding_bench), ("batch", batch_bench),
+                     ("read_ceiling", read_ceiling)):
         t0 = time.perf_counter()
         try:
             res[name] = fn(a)
@@ -1078,7 +1079,7 @@ def main():
     if args.batch:
         if args.gpus != 1:
             sys.exit(2)
-        batch_bench(args)
+        print(json.dumps(batch_bench(args)), flush=True)
         return
     if args.gpus != 1:
         print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
